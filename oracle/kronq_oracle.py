@@ -1,0 +1,321 @@
+"""Float64 reference of the KronQ per-layer quantisation path, written from the paper.
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
+``cpu_baseline`` leg, never by the product path. Plain numpy in float64; a matmul, a Cholesky or
+an inverse from numpy/LAPACK serves as a step where the paper's definition is that operation.
+
+Paper references (arxiv 2607.07964, "KronQ"):
+
+* layer objective, Sec. 3.1 eq. (ptq_obj); K-FAC factors, Sec. 4.1 eq. (kfac), objective eq.
+  (kron_obj);
+* OBS compensation, Sec. 3.1 eq. (obs_update) and Proposition 1 eq. (kronq_update);
+* BiIP rescaling, Sec. 4.2 eq. (rescale); rotations eq. (biip); Algorithm 1 (appendix B);
+* sensitivity score, Sec. 4.3 eq. (sensitivity);
+* quantisation loop, Algorithm 2 (appendix B);
+* LDL loss identity, appendix A.3 eq. (app-decomp).
+
+Readings taken where the paper is silent or garbled (each also listed in the design doc):
+
+R1  covariances are plain sums, H_X = X^T X, H_G = G^T G (token-major X, G).
+R3  the inverse-Cholesky factor is the UPPER U with inv(H~) = U^T U; the sweep uses rows of U
+    (Algorithm 2 prints rows of a lower L, which would be zero blocks).
+R5  no drift statistics: the P correction of Algorithm 2 is zero ("KronQ+GPTQ").
+R6  damping lambda = 0.01 of the mean diagonal, on the post-BiIP H_X.
+R7  asymmetric min-max grid per row and group (GPTQ convention): xmin = min(0, min w),
+    xmax = max(0, max w), (-1, 1) if both are 0; scale = float32((xmax - xmin) / (2^b - 1));
+    zero = rint(-xmin / scale); q = clamp(rint(w / scale) + zero, 0, 2^b - 1);
+    w_hat = scale * (q - zero). rint is round-half-to-even; divisions are float64 IEEE.
+    Group parameters are taken when the sweep reaches the group's first column.
+R8  natural column order.
+R10 a zero column/row norm or zero diagonal gives a scale of 1.
+R11 V = H_d diag(sigma) / sqrt(d) (Sylvester H), or (Q28 kron H_m / sqrt(m)) diag(sigma) for
+    d = 28 m, with the 28-point factor on the slow index.
+R12 H_G is rotated too (Algorithm 1 does so before releasing it).
+R13 traces are reported before and after BiIP; the sensitivity score uses post-BiIP traces.
+R14 bit allocation: exhaustive search minimising sum_l s_l (2^b_l - 1)^-2 under a
+    parameter-weighted average-bit budget, ties to the lexicographically smallest vector.
+R15 the reported loss is taken in the original space with undamped H_X, H_G.
+"""
+from __future__ import annotations
+
+import itertools
+
+import numpy as np
+
+__all__ = [
+    "widen_bf16", "as_f64", "covariance", "traces", "rescale_factors", "hadamard", "rht_matrix",
+    "biip_forward", "biip_revert", "damp", "inverse_cholesky_factor", "group_params",
+    "quantize", "obs_unblocked", "obs_blocked", "kfac_loss", "allocate_bits", "count_avg_bits",
+    "RESCALE_IN", "RESCALE_OUT", "ROT_IN", "ROT_OUT", "BIIP",
+]
+
+# BiIP switches (the ablation of Table "ablation" toggles these)
+RESCALE_IN, RESCALE_OUT, ROT_IN, ROT_OUT = 1, 2, 4, 8
+BIIP = RESCALE_IN | RESCALE_OUT | ROT_IN | ROT_OUT
+
+
+# ----------------------------------------------------------------------------------------------
+# input widening
+# ----------------------------------------------------------------------------------------------
+def widen_bf16(bits: np.ndarray) -> np.ndarray:
+    """bfloat16 bit patterns (uint16) -> exact float64 values (bits go to the high half of an
+    IEEE float32, which widens exactly)."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+def as_f64(a) -> np.ndarray:
+    """float16/32/64 numpy array -> float64 (exact)."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return widen_bf16(a)
+    return a.astype(np.float64)
+
+
+# ----------------------------------------------------------------------------------------------
+# O1: covariances  (Sec. 3.1: H_X = X X^T for column-stacked samples; Algorithm 1 first line;
+#                   Sec. 4.1 eq. kfac for H_G)
+# ----------------------------------------------------------------------------------------------
+def covariance(A, chunk: int = 8192) -> np.ndarray:
+    """H = A^T A for token-major A [N x d], summed over token chunks in float64 (reading R1)."""
+    A = np.asarray(A)
+    n, d = A.shape
+    H = np.zeros((d, d), dtype=np.float64)
+    for t0 in range(0, n, chunk):
+        C = as_f64(A[t0:t0 + chunk])
+        H += C.T @ C
+    return H
+
+
+# ----------------------------------------------------------------------------------------------
+# O2: traces and the sensitivity score  (Sec. 4.3 eq. sensitivity)
+# ----------------------------------------------------------------------------------------------
+def traces(HX: np.ndarray, HG: np.ndarray) -> tuple[float, float, float]:
+    """(tr H_X, tr H_G, s = tr H_G * tr H_X)."""
+    tx = float(np.sum(np.diag(HX)))
+    tg = float(np.sum(np.diag(HG)))
+    return tx, tg, tx * tg
+
+
+# ----------------------------------------------------------------------------------------------
+# O3: BiIP diagonal rescaling  (Sec. 4.2 eq. rescale; Algorithm 1 rescaling lines)
+# ----------------------------------------------------------------------------------------------
+def _quarter_ratio(h: np.ndarray, a: np.ndarray) -> np.ndarray:
+    ok = (h > 0) & (a > 0)
+    s = np.ones_like(h)
+    s[ok] = (h[ok] / a[ok]) ** 0.25
+    return s  # reading R10: 1 where a norm or a diagonal entry is zero
+
+
+def rescale_factors(W: np.ndarray, HX: np.ndarray, HG: np.ndarray | None, flags: int = BIIP):
+    """s^X_j = (H_X,jj / ||W_:,j||^2)^(1/4) and s^G_i = (H_G,ii / ||W_i,:||^2)^(1/4), both from
+    the original W (1 for a side whose rescale is off)."""
+    W = as_f64(W)
+    a = np.sum(W * W, axis=0)  # squared column norms (input side)
+    b = np.sum(W * W, axis=1)  # squared row norms (output side)
+    sx = _quarter_ratio(np.diag(HX).astype(np.float64), a) if flags & RESCALE_IN else np.ones(W.shape[1])
+    if flags & RESCALE_OUT:
+        if HG is None:
+            raise ValueError("output-side rescaling needs H_G")
+        sg = _quarter_ratio(np.diag(HG).astype(np.float64), b)
+    else:
+        sg = np.ones(W.shape[0])
+    return sx, sg
+
+
+# ----------------------------------------------------------------------------------------------
+# O4: randomised Hadamard rotations  (Sec. 4.2 eq. biip; reading R11)
+# ----------------------------------------------------------------------------------------------
+def hadamard(m: int) -> np.ndarray:
+    """Sylvester-ordered Hadamard matrix, entry (i, j) = (-1)^popcount(i & j)."""
+    if m <= 0 or m & (m - 1):
+        raise ValueError("Hadamard order must be a power of two")
+    i = np.arange(m)
+    x = i[:, None] & i[None, :]
+    par = np.zeros_like(x)
+    while np.any(x):
+        par ^= x & 1
+        x = x >> 1
+    return np.where(par == 1, -1.0, 1.0)
+
+
+def rht_matrix(d: int, sign, q28=None) -> np.ndarray:
+    """Dense orthogonal V = H_d diag(sigma) / sqrt(d), or (Q28 kron H_m / sqrt(m)) diag(sigma)
+    when d = 28 m (Q28 on the slow index: element index = a * m + b)."""
+    sign = np.asarray(sign, dtype=np.float64)
+    if q28 is None:
+        core = hadamard(d) / np.sqrt(d)
+    else:
+        m = d // 28
+        if 28 * m != d:
+            raise ValueError("d must be 28 * 2^k when a 28-point factor is given")
+        core = np.kron(np.asarray(q28, dtype=np.float64), hadamard(m) / np.sqrt(m))
+    return core * sign[None, :]
+
+
+def biip_forward(W, HX, HG, rot_in=None, rot_out=None, flags: int = BIIP):
+    """Algorithm 1 without the drift statistic (reading R5):
+    W' = S_G W S_X; H_X' = S_X^-1 H_X S_X^-1; H_G' = S_G^-1 H_G S_G^-1; then
+    W'' = U W' V^T, H_X'' = V H_X' V^T, H_G'' = U H_G' U^T.
+
+    ``rot_in`` / ``rot_out`` are (sign, q28-or-None). Returns a dict with W, HX, HG, sx, sg,
+    V, U (V, U are identities for a side whose rotation is off)."""
+    W = as_f64(W)
+    HX = np.asarray(HX, dtype=np.float64)
+    HG = None if HG is None else np.asarray(HG, dtype=np.float64)
+    d_out, d_in = W.shape
+    sx, sg = rescale_factors(W, HX, HG, flags)
+    W1 = sg[:, None] * W * sx[None, :]
+    HX1 = HX / np.outer(sx, sx)
+    HG1 = None if HG is None else HG / np.outer(sg, sg)
+    V = rht_matrix(d_in, *rot_in) if flags & ROT_IN else np.eye(d_in)
+    U = rht_matrix(d_out, *rot_out) if flags & ROT_OUT else np.eye(d_out)
+    return {
+        "W": U @ W1 @ V.T,
+        "HX": V @ HX1 @ V.T,
+        "HG": None if HG1 is None else U @ HG1 @ U.T,
+        "sx": sx, "sg": sg, "V": V, "U": U,
+    }
+
+
+def biip_revert(W_hat, sx, sg, V, U) -> np.ndarray:
+    """Algorithm 2's final line: W = S_G^-1 U^T W_hat V S_X^-1."""
+    W_hat = np.asarray(W_hat, dtype=np.float64)
+    return (U.T @ W_hat @ V) / sg[:, None] / sx[None, :]
+
+
+# ----------------------------------------------------------------------------------------------
+# O5, O6: damping and the inverse-Cholesky factor  (Algorithm 2 first two lines; Prop. 1)
+# ----------------------------------------------------------------------------------------------
+def damp(H, lam: float = 0.01) -> np.ndarray:
+    """H~ = H + lam * mean(diag H) * I (reading R6)."""
+    H = np.asarray(H, dtype=np.float64)
+    return H + lam * np.mean(np.diag(H)) * np.eye(H.shape[0])
+
+
+def inverse_cholesky_factor(Hd) -> np.ndarray:
+    """Upper-triangular U with inv(H~) = U^T U (reading R3), by the LAPACK route
+    U = cholesky(inv(H~))^T."""
+    Hinv = np.linalg.inv(np.asarray(Hd, dtype=np.float64))
+    Hinv = 0.5 * (Hinv + Hinv.T)
+    return np.linalg.cholesky(Hinv).T
+
+
+# ----------------------------------------------------------------------------------------------
+# O7: the asymmetric min-max quantiser  (reading R7)
+# ----------------------------------------------------------------------------------------------
+def group_params(wg: np.ndarray, bits: int):
+    """Per-row (scale, zero) of a [rows x g] group; scale rounded once to float32."""
+    wg = np.asarray(wg, dtype=np.float64)
+    maxq = float(2 ** bits - 1)
+    xmin = np.minimum(wg.min(axis=1), 0.0)
+    xmax = np.maximum(wg.max(axis=1), 0.0)
+    flat = xmax == xmin
+    xmin = np.where(flat, -1.0, xmin)
+    xmax = np.where(flat, 1.0, xmax)
+    scale = ((xmax - xmin) / maxq).astype(np.float32).astype(np.float64)
+    zero = np.rint(-xmin / scale)
+    return scale, zero
+
+
+def quantize(w: np.ndarray, scale: np.ndarray, zero: np.ndarray, bits: int):
+    """Codes q and dequantised values w_hat of one column w (per-row scale and zero)."""
+    maxq = float(2 ** bits - 1)
+    q = np.clip(np.rint(np.asarray(w, dtype=np.float64) / scale) + zero, 0.0, maxq)
+    return q.astype(np.int64), scale * (q - zero)
+
+
+# ----------------------------------------------------------------------------------------------
+# O8: the column-wise OBS sweep  (eq. obs_update; Prop. 1 with P = 0; Algorithm 2)
+# ----------------------------------------------------------------------------------------------
+def _outputs(d_out, d_in, group):
+    ng = d_in // group
+    return (np.zeros((d_out, d_in), np.int64), np.zeros((d_out, ng)), np.zeros((d_out, ng)),
+            np.zeros((d_out, d_in)), np.zeros((d_out, d_in)))
+
+
+def obs_unblocked(W, U, bits: int, group: int = 128):
+    """Sequential OBS: for each column p, quantise it (group parameters taken at the group's
+    first column from the current W), form the scaled error e_p = (w_p - w_hat_p) / U_pp and
+    subtract e_p U_{p, p:} from the columns p onward. Column p then holds w_hat_p.
+
+    Returns dict(codes, scales, zeros, err, w_hat, W) with W the final compensated matrix."""
+    W = as_f64(W).copy()
+    U = np.asarray(U, dtype=np.float64)
+    d_out, d_in = W.shape
+    if d_in % group:
+        raise ValueError("d_in must be a multiple of the group size")
+    codes, scales, zeros, err, w_hat = _outputs(d_out, d_in, group)
+    for p in range(d_in):
+        if p % group == 0:
+            s, z = group_params(W[:, p:p + group], bits)
+            scales[:, p // group], zeros[:, p // group] = s, z
+        q, wh = quantize(W[:, p], s, z, bits)
+        e = (W[:, p] - wh) / U[p, p]
+        W[:, p:] -= np.outer(e, U[p, p:])
+        codes[:, p], err[:, p], w_hat[:, p] = q, e, wh
+    return {"codes": codes, "scales": scales, "zeros": zeros, "err": err, "w_hat": w_hat, "W": W}
+
+
+def obs_blocked(W, U, bits: int, group: int = 128, block: int = 128):
+    """Algorithm 2 with P = 0: in-block sequential updates restricted to the block, then one
+    trailing update W[:, i+B:] -= E U[i:i+B, i+B:] per block (lazy batch)."""
+    W = as_f64(W).copy()
+    U = np.asarray(U, dtype=np.float64)
+    d_out, d_in = W.shape
+    if d_in % group:
+        raise ValueError("d_in must be a multiple of the group size")
+    codes, scales, zeros, err, w_hat = _outputs(d_out, d_in, group)
+    for i in range(0, d_in, block):
+        j_end = min(i + block, d_in)
+        E = np.zeros((d_out, j_end - i))
+        for j in range(i, j_end):
+            if j % group == 0:
+                s, z = group_params(W[:, j:j + group], bits)
+                scales[:, j // group], zeros[:, j // group] = s, z
+            q, wh = quantize(W[:, j], s, z, bits)
+            e = (W[:, j] - wh) / U[j, j]
+            W[:, j:j_end] -= np.outer(e, U[j, j:j_end])
+            E[:, j - i] = e
+            codes[:, j], err[:, j], w_hat[:, j] = q, e, wh
+        if j_end < d_in:
+            W[:, j_end:] -= E @ U[i:j_end, j_end:]
+    return {"codes": codes, "scales": scales, "zeros": zeros, "err": err, "w_hat": w_hat, "W": W}
+
+
+# ----------------------------------------------------------------------------------------------
+# O10: the K-FAC loss  (Sec. 4.1 eq. kron_obj)
+# ----------------------------------------------------------------------------------------------
+def kfac_loss(dW, HX, HG) -> float:
+    """tr(H_G dW H_X dW^T) = sum_ij (H_G dW)_ij (dW H_X)_ij."""
+    dW = np.asarray(dW, dtype=np.float64)
+    return float(np.sum((np.asarray(HG, np.float64) @ dW) * (dW @ np.asarray(HX, np.float64))))
+
+
+# ----------------------------------------------------------------------------------------------
+# O11: mixed-precision allocation  (Sec. 4.3; Sec. 5.5; reading R14)
+# ----------------------------------------------------------------------------------------------
+def allocate_bits(scores, weights, choices=(2, 3, 4), avg_bits: float = 3.0):
+    """Exhaustive search over every assignment (lexicographic order of ``choices``) of
+    sum_l s_l / (2^b_l - 1)^2 subject to sum_l w_l b_l <= avg_bits * sum_l w_l.
+    Returns (bits tuple, objective)."""
+    scores = [float(s) for s in scores]
+    weights = [int(w) for w in weights]
+    budget = avg_bits * float(sum(weights))
+    best, best_val = None, None
+    for bits in itertools.product(sorted(choices), repeat=len(scores)):
+        if float(sum(w * b for w, b in zip(weights, bits))) > budget:
+            continue
+        val = 0.0
+        for s, b in zip(scores, bits):
+            val += s / float((2 ** b - 1) ** 2)
+        if best_val is None or val < best_val:
+            best, best_val = bits, val
+    if best is None:
+        raise ValueError("no assignment meets the bit budget")
+    return best, best_val
+
+
+def count_avg_bits(bits) -> float:
+    """Count-weighted average bit width (the 'Avg bits' column of the mixed-precision table)."""
+    return float(np.mean(np.asarray(bits, dtype=np.float64)))
