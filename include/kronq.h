@@ -1,0 +1,190 @@
+/*
+ * kronq.h -- C ABI of the KronQ per-layer quantisation path for AMD MI355X (gfx950).
+ *
+ * KronQ (arxiv 2607.07964) quantises one linear layer W [d_out x d_in] with a
+ * Kronecker-factored Hessian H ~ H_X (x) H_G. The path is:
+ *   1. covariances H_X = X^T X and H_G = G^T G over N calibration tokens   (Sec. 4.1, eq. kfac);
+ *   2. traces and the sensitivity score s = tr(H_G) tr(H_X)                (Sec. 4.3, eq. sensitivity);
+ *   3. bidirectional incoherence processing: rescaling and randomised
+ *      Hadamard rotations on both sides                                   (Sec. 4.2, eqs. rescale, biip; Alg. 1);
+ *   4. damping and the inverse-Cholesky factor of H_X                      (Alg. 2, first lines);
+ *   5. the column-wise OBS sweep with group quantisation, in lazy blocks   (eq. obs_update, Prop. 1; Alg. 2).
+ *
+ * Conventions (all entry points):
+ *   - Matrices are row-major with an explicit leading dimension (elements). Pointers marked
+ *     "device" are device memory owned by the caller; the library never frees them.
+ *   - Every call is ordered on `stream` (a hipStream_t; NULL = the default stream), returns
+ *     after enqueueing, and keeps no state between calls apart from the optional profiler.
+ *   - Scratch memory comes from the caller: `ws` (device, 256-byte aligned) of `ws_bytes`
+ *     bytes, at least kronq_workspace_bytes() for that operation. ws may be NULL when that
+ *     size is 0.
+ *   - Scalar results (traces, loss, info) are written to device memory; synchronise the
+ *     stream before reading them.
+ *   - Return value: KRONQ_OK or a negative KRONQ_ERR_* code; kronq_last_error() then holds a
+ *     message (thread-local). Nothing is enqueued when an argument check fails.
+ *
+ * Readings of the paper that fix the semantics (the paper is silent or garbled there):
+ *   covariances are plain sums; the inverse-Cholesky factor is the upper U with
+ *   inv(H~) = U^T U and the sweep uses its rows; the drift correction P of Algorithm 2 is
+ *   zero; the quantiser is the asymmetric min-max grid per row and group of 128 columns,
+ *   with scale = float32((xmax - xmin) / (2^b - 1)), zero = rint(-xmin / scale),
+ *   q = clamp(rint(w / scale) + zero, 0, 2^b - 1), divisions in IEEE float64, rint half to even.
+ */
+#ifndef KRONQ_H
+#define KRONQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------------------------- */
+#define KRONQ_OK 0
+#define KRONQ_ERR_INVALID_ARG (-1) /* null pointer, non-positive size, bad leading dim, misalignment */
+#define KRONQ_ERR_SHAPE (-2)       /* sizes inconsistent with each other (e.g. d_in % group) */
+#define KRONQ_ERR_NOT_PD (-3)      /* reported by the host binding after reading *info */
+#define KRONQ_ERR_HIP (-4)         /* a HIP launch or runtime call failed */
+#define KRONQ_ERR_WORKSPACE (-5)   /* ws_bytes smaller than kronq_workspace_bytes() */
+#define KRONQ_ERR_UNSUPPORTED (-6) /* valid but not implemented: group != 128, bits not in 2..4,
+                                      rotated dimension not 2^k or 28 * 2^k */
+
+/* ---- element types --------------------------------------------------------------------- */
+#define KRONQ_BF16 1
+#define KRONQ_FP32 2
+
+/* ---- kronq_rotate flags ------------------------------------------------------------------ */
+#define KRONQ_RESCALE_IN 1   /* S_X = diag(H_X,jj / ||W_:,j||^2)^(1/4)        (eq. rescale) */
+#define KRONQ_RESCALE_OUT 2  /* S_G = diag(H_G,ii / ||W_i,:||^2)^(1/4)        (eq. rescale) */
+#define KRONQ_ROT_IN 4       /* V: W <- W V^T, H_X <- V H_X V^T              (eq. biip)    */
+#define KRONQ_ROT_OUT 8      /* U: W <- U W, H_G <- U H_G U^T                 (eq. biip)    */
+#define KRONQ_INVERSE 16     /* revert W only: W <- S_G^-1 U^T W V S_X^-1     (Alg. 2, last line) */
+#define KRONQ_BIIP (KRONQ_RESCALE_IN | KRONQ_RESCALE_OUT | KRONQ_ROT_IN | KRONQ_ROT_OUT)
+
+/* ---- workspace queries ------------------------------------------------------------------- */
+#define KRONQ_OP_COV 1
+#define KRONQ_OP_ROTATE 2
+#define KRONQ_OP_CHOL 3
+#define KRONQ_OP_OBS 4
+#define KRONQ_OP_LOSS 5
+
+/* Bytes of scratch the operation needs for these sizes. For KRONQ_OP_COV pass the covariance
+ * dimension d as d_in and the token count as n_rows (d_out ignored); for KRONQ_OP_CHOL pass
+ * the matrix order as d_in. Returns 0 for invalid sizes. Host only, never fails. */
+size_t kronq_workspace_bytes(int op, int64_t d_out, int64_t d_in, int64_t n_rows);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* kronq_last_error(void);
+
+/* Library version (major * 10000 + minor * 100 + patch). */
+int kronq_version(void);
+
+/* ---- 1. covariances (Sec. 4.1 eq. kfac; Alg. 1 first line; reading: plain sums) ----------
+ * H <- beta * H + alpha * A^T A, for token-major A [n_rows x d] (X with d = d_in, or G with
+ * d = d_out). The full symmetric d x d matrix is written. Calls can be chained over token
+ * chunks with beta = 1. beta = 0 never reads H (NaNs in it do not propagate).
+ *   A     device, dtype KRONQ_BF16 (products exact in fp32, fp32 accumulation on MFMA) or
+ *         KRONQ_FP32 (fp32 FMA); rows of lda elements; A and lda*elem_size 16-byte aligned.
+ *   H     device fp32 [d x ldh], ldh >= d.
+ *   n_rows may be 0 (then H <- beta * H). */
+int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
+                         float* H, int64_t ldh, float alpha, float beta, void* ws,
+                         size_t ws_bytes, void* stream);
+
+/* ---- 2. traces and sensitivity (Sec. 4.3 eq. sensitivity) --------------------------------
+ * out3[0] = tr H_X, out3[1] = tr H_G, out3[2] = tr H_X * tr H_G, accumulated in fp64.
+ * Call before and/or after kronq_rotate (the score of the paper uses post-BiIP traces).
+ *   HX device fp32 [d_in x ldx]; HG device fp32 [d_out x ldg]; out3 device double[3]. */
+int kronq_traces(const float* HX, int64_t d_in, int64_t ldx, const float* HG, int64_t d_out,
+                 int64_t ldg, double* out3, void* stream);
+
+/* ---- 3. bidirectional incoherence processing (Sec. 4.2 eqs. rescale, biip; Alg. 1) -------
+ * Forward (no KRONQ_INVERSE):
+ *   a_j = ||W_in[:, j]||^2, b_i = ||W_in[i, :]||^2 (original W), sx_j = (H_X,jj / a_j)^(1/4),
+ *   sg_i = (H_G,ii / b_i)^(1/4) (1 when a side is off or a norm/diagonal is 0);
+ *   W  <- U diag(sg) W_in diag(sx) V^T                 (written to W, fp32)
+ *   HX <- V diag(1/sx) HX diag(1/sx) V^T               (in place)
+ *   HG <- U diag(1/sg) HG diag(1/sg) U^T               (in place, skipped if HG is NULL)
+ * with V = H_{d_in} diag(sign_in) / sqrt(d_in) for d_in = 2^k, or
+ * (Q28_in (x) H_{d_in/28} / sqrt(d_in/28)) diag(sign_in) for d_in = 28 * 2^k (28-point factor
+ * on the slow index), and U likewise from sign_out / q28_out. H is the Sylvester Hadamard.
+ * Inverse (KRONQ_INVERSE, W only, sx and sg are inputs):
+ *   W <- diag(1/sg) U^T W_in V diag(1/sx).
+ *   W_in   device, w_dtype KRONQ_BF16 or KRONQ_FP32, [d_out x ldw_in]; may alias W when fp32.
+ *   W      device fp32 [d_out x ldw].
+ *   HX     device fp32 [d_in x ldx] (forward; may be NULL for INVERSE).
+ *   HG     device fp32 [d_out x ldg] or NULL; required by KRONQ_RESCALE_OUT.
+ *   sign_in/sign_out  device int8 (+1/-1) [d_in]/[d_out]; required when that side rotates.
+ *   q28_in/q28_out    device fp32 [28 x 28] row-major; required iff that dimension is
+ *                     28 * 2^k and rotates; ignored otherwise.
+ *   sx/sg  device fp32 [d_in]/[d_out]: outputs (forward), inputs (inverse).
+ * Rotated dimensions must be 2^k (k >= 1) or 28 * 2^k with 2^k <= 16384. */
+int kronq_rotate(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_t d_out,
+                 int64_t d_in, int64_t ldw, float* HX, int64_t ldx, float* HG, int64_t ldg,
+                 const int8_t* sign_in, const int8_t* sign_out, const float* q28_in,
+                 const float* q28_out, float* sx, float* sg, int flags, void* ws,
+                 size_t ws_bytes, void* stream);
+
+/* ---- 4. damping + inverse-Cholesky factor (Alg. 2 first two lines; Prop. 1) --------------
+ * H <- H + damp_rel * mean(diag H) * I (in place), then Uout = upper-triangular U with
+ * inv(H) = U^T U (zeros below the diagonal are written). U = R^-1 where H = R R^T, R upper
+ * (a Cholesky factorisation in reversed index order followed by a triangular inverse, fp32).
+ *   H    device fp32 [d x ldh], symmetric (both triangles read).
+ *   Uout device fp32 [d x ldu]; must not alias H.
+ *   info device int32: 0 on success, else the 1-based column of H (original order) whose
+ *        pivot was not positive; Uout is then undefined. The host reads it after a sync. */
+int kronq_cholesky_inv(float* H, int64_t d, int64_t ldh, float damp_rel, float* Uout,
+                       int64_t ldu, int* info, void* ws, size_t ws_bytes, void* stream);
+
+/* ---- 5. lazy-block column-wise OBS with group quantisation (Alg. 2 with P = 0) -----------
+ * For each block of `block` columns and each column p in it: group parameters per row are
+ * taken from the current W when p is a group start; q = quant(W[:, p]);
+ * e_p = (W[:, p] - w_hat_p) / U[p, p]; W[:, p:blk_end] -= e_p U[p, p:blk_end]; after the
+ * block W[:, blk_end:] -= E_blk U[blk, blk_end:]. Column p is left holding w_hat_p.
+ *   W      device fp32 [d_out x ldw], consumed (ends as the dequantised W_hat).
+ *   U      device fp32 upper [d_in x ldu] from kronq_cholesky_inv.
+ *   bits   2, 3 or 4; group must be 128; block must be 128.
+ *   codes  device uint8 [d_out x d_in] (ld = d_in), one code per byte.
+ *   scales, zeros  device fp32 [d_out x d_in/group] (zeros are integer-valued).
+ *   err    device fp32 [d_out x d_in] or NULL: the scaled errors e (ld = d_in).
+ *   W_hat  device fp32 [d_out x d_in] or NULL: a copy of the dequantised values (ld = d_in). */
+int kronq_obs_quantize_layer(float* W, int64_t d_out, int64_t d_in, int64_t ldw,
+                             const float* U, int64_t ldu, int bits, int group, int block,
+                             uint8_t* codes, float* scales, float* zeros, float* err,
+                             float* W_hat, void* ws, size_t ws_bytes, void* stream);
+
+/* ---- 6. K-FAC loss (Sec. 4.1 eq. kron_obj) -----------------------------------------------
+ * loss = tr(H_G dW H_X dW^T) = sum_ij (H_G dW)_ij (dW H_X)_ij with dW = W - W_hat (W_hat NULL:
+ * dW = W), fp32 products with fp32 accumulation and an fp64 final sum.
+ *   W     device [d_out x ldw], w_dtype KRONQ_BF16 or KRONQ_FP32.
+ *   W_hat device fp32 [d_out x ldwh] or NULL.
+ *   HX, HG device fp32 (ldx, ldg). loss device double[1]. */
+int kronq_layer_loss(const void* W, int w_dtype, int64_t ldw, const float* W_hat,
+                     int64_t ldwh, int64_t d_out, int64_t d_in, const float* HX, int64_t ldx,
+                     const float* HG, int64_t ldg, double* loss, void* ws, size_t ws_bytes,
+                     void* stream);
+
+/* ---- mixed-precision allocation (Sec. 4.3, Sec. 5.5) -------------------------------------
+ * Host only. Chooses bits_out[l] in `choices` minimising sum_l scores[l] / (2^b_l - 1)^2
+ * subject to sum_l weights[l] * b_l <= avg_bits * sum_l weights[l] (weights = parameter
+ * counts for a parameter-weighted budget, or 1 for a count-weighted one), by exhaustive
+ * search in lexicographic order of the sorted choices; ties keep the first (smallest) vector.
+ * n_layers <= 12, n_choices <= 8. objective_out (nullable) receives the minimum. */
+int kronq_allocate_bits(const double* scores, const int64_t* weights, int n_layers,
+                        const int* choices, int n_choices, double avg_bits, int* bits_out,
+                        double* objective_out);
+
+/* ---- profiler (hipEvent timing of every kernel launch, by kernel name) --------------------
+ * While enabled, each launch is bracketed by two events on its stream. kronq_profile_read
+ * synchronises the recorded events and returns the summed milliseconds and the launch count
+ * of the named kernel (0 if never launched). Not thread-safe; meant for benchmarks. */
+int kronq_profile_enable(int on);
+void kronq_profile_reset(void);
+int kronq_profile_read(const char* kernel, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KRONQ_H */

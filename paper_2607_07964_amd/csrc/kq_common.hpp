@@ -1,0 +1,140 @@
+// Internal helpers shared by the kernels and the C-ABI layer of libkronq (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "kronq.h"
+
+namespace kq {
+
+// ---- error state (thread-local message behind kronq_last_error) ----------------------------
+void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
+void clear_error();
+
+#define KQ_REQUIRE(cond, code, ...)      \
+  do {                                   \
+    if (!(cond)) {                       \
+      ::kq::set_error(__VA_ARGS__);      \
+      return (code);                     \
+    }                                    \
+  } while (0)
+
+#define KQ_HIP(call)                                                              \
+  do {                                                                            \
+    hipError_t kq_e_ = (call);                                                    \
+    if (kq_e_ != hipSuccess) {                                                    \
+      ::kq::set_error("%s failed: %s", #call, hipGetErrorString(kq_e_));          \
+      return KRONQ_ERR_HIP;                                                       \
+    }                                                                             \
+  } while (0)
+
+#define KQ_TRY(expr)            \
+  do {                          \
+    int kq_rc_ = (expr);        \
+    if (kq_rc_ != KRONQ_OK) {   \
+      return kq_rc_;            \
+    }                           \
+  } while (0)
+
+// ---- profiler: optional hipEvent pair around every launch ----------------------------------
+bool prof_on();
+void prof_begin(const char* name, hipStream_t s);
+void prof_end(const char* name, hipStream_t s);
+
+// Launch a kernel; checks the launch status and records profiler events when enabled.
+template <typename Kernel, typename... Args>
+int launch(const char* name, Kernel kernel, dim3 grid, dim3 block, size_t shmem, hipStream_t s,
+           Args... args) {
+  if (grid.x == 0 || grid.y == 0 || grid.z == 0) return KRONQ_OK;
+  if (shmem > 65536) {  // opt in to more than 64 KB of dynamic LDS (gfx950 has 160 KB per CU)
+    hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(shmem));
+    if (ea != hipSuccess) {
+      set_error("LDS request of %zu bytes for %s refused: %s", shmem, name, hipGetErrorString(ea));
+      return KRONQ_ERR_HIP;
+    }
+  }
+  const bool p = prof_on();
+  if (p) prof_begin(name, s);
+  hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error("launch of %s failed: %s", name, hipGetErrorString(e));
+    return KRONQ_ERR_HIP;
+  }
+  if (p) prof_end(name, s);
+  return KRONQ_OK;
+}
+
+// ---- workspace carving -----------------------------------------------------------------------
+struct Carver {
+  char* base;
+  size_t used = 0;
+  explicit Carver(void* p) : base(static_cast<char*>(p)) {}
+  template <typename T>
+  T* take(size_t count) {
+    used = (used + 255) & ~size_t(255);
+    T* r = reinterpret_cast<T*>(base ? base + used : nullptr);
+    used += count * sizeof(T);
+    return r;
+  }
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+__host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ---- shapes used by the rotation ---------------------------------------------------------------
+// d = 2^k (k >= 1) -> (pow2 = d, has28 = false); d = 28 * 2^k -> (pow2 = 2^k, has28 = true).
+struct RotDim {
+  bool ok = false;
+  bool has28 = false;
+  int64_t m = 0;  // Hadamard order
+};
+RotDim rot_dim(int64_t d);
+
+// ---- kernel-side entry points (defined in the per-step sources) ------------------------------
+// covariance
+size_t cov_ws_bytes(int dtype, int64_t n_rows, int64_t d);
+int cov_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda, float* H,
+               int64_t ldh, float alpha, float beta, void* ws, hipStream_t s);
+// traces
+int traces_launch(const float* HX, int64_t d_in, int64_t ldx, const float* HG, int64_t d_out,
+                  int64_t ldg, double* out3, hipStream_t s);
+// rotation
+size_t rotate_ws_bytes(int64_t d_out, int64_t d_in);
+int rotate_launch(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_t d_out,
+                  int64_t d_in, int64_t ldw, float* HX, int64_t ldx, float* HG, int64_t ldg,
+                  const int8_t* sign_in, const int8_t* sign_out, const float* q28_in,
+                  const float* q28_out, float* sx, float* sg, int flags, void* ws,
+                  hipStream_t s);
+// fp32 GEMM on MFMA: C = alpha * op(A) op(B) + beta * C
+enum GemmFlags : int {
+  GEMM_TA = 1,          // op(A) = A^T (A stored [K x M])
+  GEMM_TB = 2,          // op(B) = B^T (B stored [N x K])
+  GEMM_LOWER_C = 4,     // only output tiles that touch the lower triangle (i >= j)
+  GEMM_B_LOWER = 8,     // B is lower triangular: skip k < column-tile start
+  GEMM_A_LOWER = 16,    // A is lower triangular: skip k > row-tile end
+};
+int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
+             int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
+             hipStream_t s, const char* name = "gemm_f32_mfma");
+// Cholesky inverse factor
+size_t chol_ws_bytes(int64_t d);
+int chol_launch(float* H, int64_t d, int64_t ldh, float damp_rel, float* U, int64_t ldu,
+                int* info, void* ws, hipStream_t s);
+// OBS sweep
+size_t obs_ws_bytes(int64_t d_out, int64_t d_in);
+int obs_launch(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* U, int64_t ldu,
+               int bits, uint8_t* codes, float* scales, float* zeros, float* err, float* W_hat,
+               void* ws, hipStream_t s);
+// loss
+size_t loss_ws_bytes(int64_t d_out, int64_t d_in);
+int loss_launch(const void* W, int w_dtype, int64_t ldw, const float* W_hat, int64_t ldwh,
+                int64_t d_out, int64_t d_in, const float* HX, int64_t ldx, const float* HG,
+                int64_t ldg, double* loss, void* ws, hipStream_t s);
+
+}  // namespace kq

@@ -1,0 +1,194 @@
+// C-ABI entry points of libkronq: argument validation, workspace checks and dispatch to the
+// HIP kernels. Nothing is enqueued when a check fails.
+#include <hip/hip_runtime.h>
+
+#include "kq_common.hpp"
+
+namespace {
+
+using kq::aligned;
+
+bool valid_dtype(int t) { return t == KRONQ_BF16 || t == KRONQ_FP32; }
+
+int check_ws(void* ws, size_t ws_bytes, size_t need) {
+  KQ_REQUIRE(ws_bytes >= need, KRONQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given",
+             need, ws_bytes);
+  KQ_REQUIRE(need == 0 || (ws && aligned(ws, 256)), KRONQ_ERR_INVALID_ARG,
+             "workspace must be a 256-byte aligned device pointer");
+  return KRONQ_OK;
+}
+
+// fp32 matrix used with 16-byte vector accesses
+int check_f32_mat(const float* p, int64_t rows, int64_t cols, int64_t ld, const char* what) {
+  KQ_REQUIRE(p, KRONQ_ERR_INVALID_ARG, "%s is NULL", what);
+  KQ_REQUIRE(rows >= 1 && cols >= 1, KRONQ_ERR_INVALID_ARG, "%s has a non-positive size", what);
+  KQ_REQUIRE(ld >= cols, KRONQ_ERR_INVALID_ARG, "leading dimension of %s (%lld) < %lld", what,
+             (long long)ld, (long long)cols);
+  KQ_REQUIRE(ld % 4 == 0 && aligned(p, 16), KRONQ_ERR_INVALID_ARG,
+             "%s must be 16-byte aligned with a leading dimension divisible by 4", what);
+  return KRONQ_OK;
+}
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+constexpr int64_t kMaxRotDim = 32768;  // a transformed row must fit the 160 KB LDS
+
+int check_rot_side(int64_t d, const int8_t* sign, const float* q28, const char* side) {
+  const kq::RotDim r = kq::rot_dim(d);
+  KQ_REQUIRE(r.ok && d <= kMaxRotDim, KRONQ_ERR_UNSUPPORTED,
+             "%s dimension %lld is not 2^k or 28*2^k (<= %lld)", side, (long long)d,
+             (long long)kMaxRotDim);
+  KQ_REQUIRE(sign, KRONQ_ERR_INVALID_ARG, "%s rotation needs its sign vector", side);
+  KQ_REQUIRE(!r.has28 || (q28 && aligned(q28, 4)), KRONQ_ERR_INVALID_ARG,
+             "%s dimension %lld = 28 * 2^k needs the 28 x 28 factor", side, (long long)d);
+  return KRONQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t kronq_workspace_bytes(int op, int64_t d_out, int64_t d_in, int64_t n_rows) {
+  switch (op) {
+    case KRONQ_OP_COV:
+      return kq::cov_ws_bytes(KRONQ_BF16, n_rows, d_in);
+    case KRONQ_OP_ROTATE:
+      return kq::rotate_ws_bytes(d_out, d_in);
+    case KRONQ_OP_CHOL:
+      return kq::chol_ws_bytes(d_in);
+    case KRONQ_OP_OBS:
+      return kq::obs_ws_bytes(d_out, d_in);
+    case KRONQ_OP_LOSS:
+      return kq::loss_ws_bytes(d_out, d_in);
+    default:
+      return 0;
+  }
+}
+
+int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
+                         float* H, int64_t ldh, float alpha, float beta, void* ws,
+                         size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(valid_dtype(dtype), KRONQ_ERR_INVALID_ARG, "dtype must be KRONQ_BF16 or KRONQ_FP32");
+  KQ_REQUIRE(H, KRONQ_ERR_INVALID_ARG, "H is NULL");
+  KQ_REQUIRE(n_rows >= 0 && d >= 1 && d <= 65535, KRONQ_ERR_INVALID_ARG,
+             "need n_rows >= 0 and 1 <= d <= 65535");
+  KQ_REQUIRE(ldh >= d && aligned(H, 4), KRONQ_ERR_INVALID_ARG, "bad H leading dimension");
+  if (n_rows > 0) {
+    KQ_REQUIRE(A, KRONQ_ERR_INVALID_ARG, "A is NULL");
+    KQ_REQUIRE(lda >= d, KRONQ_ERR_INVALID_ARG, "lda < d");
+    if (dtype == KRONQ_BF16)
+      KQ_REQUIRE(aligned(A, 16) && lda % 8 == 0, KRONQ_ERR_INVALID_ARG,
+                 "bf16 A must be 16-byte aligned with lda divisible by 8");
+    else
+      KQ_REQUIRE(aligned(A, 4), KRONQ_ERR_INVALID_ARG, "fp32 A must be 4-byte aligned");
+    KQ_TRY(check_ws(ws, ws_bytes, kq::cov_ws_bytes(dtype, n_rows, d)));
+  }
+  return kq::cov_launch(A, dtype, n_rows, d, lda, H, ldh, alpha, beta, ws, as_stream(stream));
+}
+
+int kronq_traces(const float* HX, int64_t d_in, int64_t ldx, const float* HG, int64_t d_out,
+                 int64_t ldg, double* out3, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(HX && HG && out3, KRONQ_ERR_INVALID_ARG, "null pointer");
+  KQ_REQUIRE(d_in >= 1 && d_out >= 1 && ldx >= d_in && ldg >= d_out, KRONQ_ERR_INVALID_ARG,
+             "bad sizes");
+  KQ_REQUIRE(aligned(out3, 8), KRONQ_ERR_INVALID_ARG, "out3 must be 8-byte aligned");
+  return kq::traces_launch(HX, d_in, ldx, HG, d_out, ldg, out3, as_stream(stream));
+}
+
+int kronq_rotate(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_t d_out,
+                 int64_t d_in, int64_t ldw, float* HX, int64_t ldx, float* HG, int64_t ldg,
+                 const int8_t* sign_in, const int8_t* sign_out, const float* q28_in,
+                 const float* q28_out, float* sx, float* sg, int flags, void* ws,
+                 size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  const int known = KRONQ_BIIP | KRONQ_INVERSE;
+  KQ_REQUIRE((flags & ~known) == 0, KRONQ_ERR_INVALID_ARG, "unknown flag bits 0x%x",
+             flags & ~known);
+  KQ_REQUIRE(W_in && valid_dtype(w_dtype), KRONQ_ERR_INVALID_ARG, "bad W_in");
+  KQ_REQUIRE(ldw_in >= d_in, KRONQ_ERR_INVALID_ARG, "ldw_in < d_in");
+  KQ_REQUIRE(aligned(W_in, w_dtype == KRONQ_BF16 ? 2 : 4), KRONQ_ERR_INVALID_ARG,
+             "W_in misaligned");
+  KQ_TRY(check_f32_mat(W, d_out, d_in, ldw, "W"));
+  KQ_REQUIRE(sx && sg && aligned(sx, 4) && aligned(sg, 4), KRONQ_ERR_INVALID_ARG,
+             "sx and sg are required");
+  const bool inv = flags & KRONQ_INVERSE;
+  if (inv) {
+    KQ_REQUIRE(w_dtype == KRONQ_FP32, KRONQ_ERR_INVALID_ARG, "KRONQ_INVERSE needs fp32 W_in");
+    KQ_REQUIRE(ldw_in % 4 == 0 && aligned(W_in, 16), KRONQ_ERR_INVALID_ARG,
+               "W_in must be 16-byte aligned with ldw_in divisible by 4");
+  } else {
+    KQ_TRY(check_f32_mat(HX, d_in, d_in, ldx, "HX"));
+    if (HG) KQ_TRY(check_f32_mat(HG, d_out, d_out, ldg, "HG"));
+    KQ_REQUIRE(HG || !(flags & KRONQ_RESCALE_OUT), KRONQ_ERR_INVALID_ARG,
+               "KRONQ_RESCALE_OUT needs H_G");
+    KQ_REQUIRE(W_in != static_cast<const void*>(W) || w_dtype == KRONQ_FP32,
+               KRONQ_ERR_INVALID_ARG, "in-place rotation needs fp32 W");
+  }
+  if (flags & KRONQ_ROT_IN) KQ_TRY(check_rot_side(d_in, sign_in, q28_in, "input"));
+  if (flags & KRONQ_ROT_OUT) KQ_TRY(check_rot_side(d_out, sign_out, q28_out, "output"));
+  KQ_REQUIRE(d_in <= (int64_t(1) << 24) && d_out <= (int64_t(1) << 24), KRONQ_ERR_UNSUPPORTED,
+             "dimension too large");
+  KQ_TRY(check_ws(ws, ws_bytes, kq::rotate_ws_bytes(d_out, d_in)));
+  return kq::rotate_launch(W_in, w_dtype, ldw_in, W, d_out, d_in, ldw, HX, ldx, HG, ldg, sign_in,
+                           sign_out, q28_in, q28_out, sx, sg, flags, ws, as_stream(stream));
+}
+
+int kronq_cholesky_inv(float* H, int64_t d, int64_t ldh, float damp_rel, float* Uout,
+                       int64_t ldu, int* info, void* ws, size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(H && Uout && info, KRONQ_ERR_INVALID_ARG, "null pointer");
+  KQ_REQUIRE(d >= 1 && d <= 65535, KRONQ_ERR_INVALID_ARG, "need 1 <= d <= 65535");
+  KQ_REQUIRE(ldh >= d && ldu >= d, KRONQ_ERR_INVALID_ARG, "bad leading dimension");
+  KQ_REQUIRE(aligned(H, 4) && aligned(Uout, 4) && aligned(info, 4), KRONQ_ERR_INVALID_ARG,
+             "misaligned pointer");
+  KQ_REQUIRE(Uout != H, KRONQ_ERR_INVALID_ARG, "Uout must not alias H");
+  KQ_REQUIRE(damp_rel >= 0.f, KRONQ_ERR_INVALID_ARG, "damp_rel must be >= 0");
+  KQ_TRY(check_ws(ws, ws_bytes, kq::chol_ws_bytes(d)));
+  return kq::chol_launch(H, d, ldh, damp_rel, Uout, ldu, info, ws, as_stream(stream));
+}
+
+int kronq_obs_quantize_layer(float* W, int64_t d_out, int64_t d_in, int64_t ldw,
+                             const float* U, int64_t ldu, int bits, int group, int block,
+                             uint8_t* codes, float* scales, float* zeros, float* err,
+                             float* W_hat, void* ws, size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(bits >= 2 && bits <= 8, KRONQ_ERR_UNSUPPORTED, "bits must be in 2..8");
+  KQ_REQUIRE(group == 128, KRONQ_ERR_UNSUPPORTED, "only group size 128 is implemented");
+  KQ_REQUIRE(block == 128, KRONQ_ERR_UNSUPPORTED, "only block size 128 is implemented");
+  KQ_TRY(check_f32_mat(W, d_out, d_in, ldw, "W"));
+  KQ_REQUIRE(d_in % group == 0, KRONQ_ERR_SHAPE, "d_in (%lld) must be a multiple of the group",
+             (long long)d_in);
+  KQ_TRY(check_f32_mat(U, d_in, d_in, ldu, "U"));
+  KQ_REQUIRE(codes && aligned(codes, 4), KRONQ_ERR_INVALID_ARG, "codes must be 4-byte aligned");
+  KQ_REQUIRE(scales && zeros && aligned(scales, 4) && aligned(zeros, 4), KRONQ_ERR_INVALID_ARG,
+             "scales and zeros are required");
+  KQ_REQUIRE(!err || aligned(err, 16), KRONQ_ERR_INVALID_ARG, "err must be 16-byte aligned");
+  KQ_REQUIRE(!W_hat || aligned(W_hat, 16), KRONQ_ERR_INVALID_ARG,
+             "W_hat must be 16-byte aligned");
+  KQ_REQUIRE(static_cast<const float*>(W) != U, KRONQ_ERR_INVALID_ARG, "W must not alias U");
+  if (!err) KQ_TRY(check_ws(ws, ws_bytes, kq::obs_ws_bytes(d_out, d_in)));
+  return kq::obs_launch(W, d_out, d_in, ldw, U, ldu, bits, codes, scales, zeros, err, W_hat, ws,
+                        as_stream(stream));
+}
+
+int kronq_layer_loss(const void* W, int w_dtype, int64_t ldw, const float* W_hat,
+                     int64_t ldwh, int64_t d_out, int64_t d_in, const float* HX, int64_t ldx,
+                     const float* HG, int64_t ldg, double* loss, void* ws, size_t ws_bytes,
+                     void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(W && valid_dtype(w_dtype) && loss, KRONQ_ERR_INVALID_ARG, "bad W or loss");
+  KQ_REQUIRE(d_out >= 1 && d_in >= 1 && d_out <= 65535 && ldw >= d_in, KRONQ_ERR_INVALID_ARG,
+             "bad sizes");
+  KQ_REQUIRE(aligned(W, w_dtype == KRONQ_BF16 ? 2 : 4) && aligned(loss, 8), KRONQ_ERR_INVALID_ARG,
+             "misaligned pointer");
+  KQ_REQUIRE(!W_hat || (ldwh >= d_in && aligned(W_hat, 4)), KRONQ_ERR_INVALID_ARG, "bad W_hat");
+  KQ_TRY(check_f32_mat(HX, d_in, d_in, ldx, "HX"));
+  KQ_TRY(check_f32_mat(HG, d_out, d_out, ldg, "HG"));
+  KQ_TRY(check_ws(ws, ws_bytes, kq::loss_ws_bytes(d_out, d_in)));
+  return kq::loss_launch(W, w_dtype, ldw, W_hat, ldwh, d_out, d_in, HX, ldx, HG, ldg, loss, ws,
+                         as_stream(stream));
+}
+
+}  // extern "C"

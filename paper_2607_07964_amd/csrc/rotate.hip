@@ -1,0 +1,470 @@
+// Bidirectional incoherence processing (Sec. 4.2 eqs. rescale and biip; Alg. 1).
+//
+// The randomised Hadamard transform of a length-d vector is applied as sign flip, fast
+// Walsh-Hadamard butterflies (O(d log d) adds) and, when d = 28 * 2^k, a dense 28-point mix of
+// the slow index, instead of the dense d x d products the paper's implementation uses. All
+// transforms are HBM-bound passes over fp32 matrices:
+//   * norms:      one read of W_in -> squared row norms and per-block column partial sums (fp64);
+//   * factors:    s = (diag H / norm^2)^(1/4) per side, and the per-index multipliers that the
+//                 passes fold in (rescale x random sign);
+//   * row pass:   one workgroup per row, the row staged in LDS; multipliers, radix-8/4/2
+//                 butterflies in registers between LDS round trips, optional 28-point mix,
+//                 1/sqrt(m) and output multipliers, written once;
+//   * column pass: transform along the strided (row) axis for a strip of columns: L rows at a
+//                 fixed row stride are staged in LDS and transformed there. An order-m transform
+//                 is split into passes of length <= 512 (H_m = H_m1 (x) H_m2), plus a 28-point pass.
+// Forward: W <- U S_G W S_X V^T; H_X <- V S_X^-1 H_X S_X^-1 V^T; H_G <- U S_G^-1 H_G S_G^-1 U^T.
+// Inverse (W only): W <- S_G^-1 U^T W V S_X^-1 (column pass with Q28^T, then the row pass).
+#include <cmath>
+
+#include "kq_common.hpp"
+
+namespace kq {
+namespace {
+
+constexpr int RP_THREADS = 512;
+constexpr int CP_THREADS = 256;
+constexpr int CP_MAXL = 512;
+constexpr int NORM_ROWS = 32;
+
+// ----------------------------------------------------------------------------- norms
+template <typename T>
+__device__ __forceinline__ float ld_as_f32(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float ld_as_f32<float>(const float* p, int64_t i) { return p[i]; }
+template <>
+__device__ __forceinline__ float ld_as_f32<uint16_t>(const uint16_t* p, int64_t i) {
+  return __uint_as_float(uint32_t(p[i]) << 16);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void w_norms(const T* __restrict__ W, int64_t d_out,
+                                               int64_t d_in, int64_t ldw,
+                                               double* __restrict__ col_part,
+                                               double* __restrict__ rowsq) {
+  __shared__ double red[256];
+  const int tid = threadIdx.x;
+  const int64_t r0 = int64_t(blockIdx.x) * NORM_ROWS;
+  const int64_t r1 = min(d_out, r0 + NORM_ROWS);
+  for (int64_t c = tid; c < d_in; c += 256) {
+    double s = 0.0;
+    for (int64_t r = r0; r < r1; ++r) {
+      const double x = ld_as_f32(W, r * ldw + c);
+      s += x * x;
+    }
+    col_part[int64_t(blockIdx.x) * d_in + c] = s;
+  }
+  for (int64_t r = r0; r < r1; ++r) {
+    double s = 0.0;
+    for (int64_t c = tid; c < d_in; c += 256) {
+      const double x = ld_as_f32(W, r * ldw + c);
+      s += x * x;
+    }
+    red[tid] = s;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if (tid < w) red[tid] += red[tid + w];
+      __syncthreads();
+    }
+    if (tid == 0) rowsq[r] = red[0];
+    __syncthreads();
+  }
+}
+
+// s = (h / a)^(1/4), 1 when either is zero (or the side is off). Also the multipliers used by
+// the passes: mul_w = s * sign, mul_h = sign / s (sign = 1 when the side does not rotate).
+__global__ void side_factors(int64_t n, const float* __restrict__ H, int64_t ldh,
+                             const double* __restrict__ part, int64_t n_part,
+                             const double* __restrict__ direct, const int8_t* __restrict__ sign,
+                             int rescale, float* __restrict__ s_out, float* __restrict__ mul_w,
+                             float* __restrict__ mul_h) {
+  const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  float s = 1.f;
+  if (rescale) {
+    double a;
+    if (direct) {
+      a = direct[j];
+    } else {
+      a = 0.0;
+      for (int64_t p = 0; p < n_part; ++p) a += part[p * n + j];
+    }
+    const double h = H[j * ldh + j];
+    if (a > 0.0 && h > 0.0) s = float(sqrt(sqrt(h / a)));
+  }
+  const float sg = sign ? float(sign[j]) : 1.f;
+  s_out[j] = s;
+  mul_w[j] = s * sg;
+  mul_h[j] = sg / s;
+}
+
+// inverse multipliers: sign / s
+__global__ void inv_factors(int64_t n, const float* __restrict__ s, const int8_t* __restrict__ sign,
+                            float* __restrict__ mul) {
+  const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  mul[j] = (sign ? float(sign[j]) : 1.f) / s[j];
+}
+
+// ----------------------------------------------------------------------------- butterflies
+template <int R>
+__device__ __forceinline__ void hadamard_reg(float* x) {
+#pragma unroll
+  for (int s = 1; s < R; s <<= 1)
+#pragma unroll
+    for (int k = 0; k < R; ++k)
+      if (!(k & s)) {
+        const float a = x[k], b = x[k + s];
+        x[k] = a + b;
+        x[k + s] = a - b;
+      }
+}
+
+// One group of up to 3 butterfly stages (strides h, 2h, 4h) over a buffer of n floats in LDS,
+// segments of length m. `stride` is the LDS distance between consecutive vector elements.
+template <int R>
+__device__ __forceinline__ void fwht_stage_group(float* buf, int64_t n, int64_t h, int tid,
+                                                 int nthreads) {
+  const int64_t groups = n / R;
+  for (int64_t q = tid; q < groups; q += nthreads) {
+    const int64_t base = (q / h) * (R * h) + (q % h);
+    float x[R];
+#pragma unroll
+    for (int k = 0; k < R; ++k) x[k] = buf[base + k * h];
+    hadamard_reg<R>(x);
+#pragma unroll
+    for (int k = 0; k < R; ++k) buf[base + k * h] = x[k];
+  }
+}
+
+__device__ void fwht_lds(float* buf, int64_t n, int64_t m, int tid, int nthreads) {
+  int64_t h = 1;
+  while (h < m) {
+    const int64_t left = m / h;
+    if (left >= 8) {
+      fwht_stage_group<8>(buf, n, h, tid, nthreads);
+      h *= 8;
+    } else if (left == 4) {
+      fwht_stage_group<4>(buf, n, h, tid, nthreads);
+      h *= 4;
+    } else {
+      fwht_stage_group<2>(buf, n, h, tid, nthreads);
+      h *= 2;
+    }
+    __syncthreads();
+  }
+}
+
+// ----------------------------------------------------------------------------- row pass
+// dst[r][c] = post_row[r] * post_col[c] * T(x)[c] with x[c] = pre_row[r] * pre_col[c] * src[r][c]
+// and T = (Q (x) H_m) / sqrt(m) (Q = 28 x 28 or identity), or the identity when transform == 0.
+template <typename T>
+__global__ __launch_bounds__(RP_THREADS) void row_pass(
+    const T* __restrict__ src, int64_t lds_, float* __restrict__ dst, int64_t ldd, int64_t rows,
+    int64_t n, const float* __restrict__ pre_row, const float* __restrict__ pre_col,
+    const float* __restrict__ post_row, const float* __restrict__ post_col, int transform,
+    int64_t m, const float* __restrict__ q28, int q_trans, float norm) {
+  extern __shared__ float smem[];
+  float* buf = smem;       // n floats
+  float* qs = smem + n;    // 28 x 28
+  const int tid = threadIdx.x;
+  if (transform && q28) {
+    for (int i = tid; i < 28 * 28; i += RP_THREADS) {
+      const int a = i / 28, b = i % 28;
+      qs[i] = q_trans ? q28[b * 28 + a] : q28[i];
+    }
+  }
+  for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
+    const float pr = pre_row ? pre_row[r] : 1.f;
+    const float po = (post_row ? post_row[r] : 1.f) * norm;
+    const T* s = src + r * lds_;
+    float* o = dst + r * ldd;
+    if (!transform) {
+      for (int64_t c = tid; c < n; c += RP_THREADS) {
+        float x = ld_as_f32(s, c) * pr;
+        if (pre_col) x *= pre_col[c];
+        if (post_col) x *= post_col[c];
+        o[c] = x * po;
+      }
+      continue;
+    }
+    __syncthreads();  // previous row finished with buf
+    for (int64_t c = tid; c < n; c += RP_THREADS) {
+      float x = ld_as_f32(s, c) * pr;
+      if (pre_col) x *= pre_col[c];
+      buf[c] = x;
+    }
+    __syncthreads();
+    fwht_lds(buf, n, m, tid, RP_THREADS);
+    if (q28) {
+      const int64_t items = n;  // (a, b): output a * m + b
+      for (int64_t it = tid; it < items; it += RP_THREADS) {
+        const int64_t a = it / m, b = it % m;
+        float acc = 0.f;
+#pragma unroll 4
+        for (int k = 0; k < 28; ++k) acc = fmaf(qs[a * 28 + k], buf[k * m + b], acc);
+        const int64_t c = a * m + b;
+        float y = acc * po;
+        if (post_col) y *= post_col[c];
+        o[c] = y;
+      }
+    } else {
+      for (int64_t c = tid; c < n; c += RP_THREADS) {
+        float y = buf[c] * po;
+        if (post_col) y *= post_col[c];
+        o[c] = y;
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------- column pass
+// Transform along the row axis. Rows are indexed r = hi * (L * n_lo) + a * n_lo + lo; for each
+// (hi, lo) and a strip of CW columns the L rows a = 0..L-1 are transformed:
+//   kind 0: H_L / sqrt(L) (FWHT);  kind 1: the 28-point factor Q (or Q^T), L = 28.
+__global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__ src, int64_t lds_,
+                                                       float* __restrict__ dst, int64_t ldd,
+                                                       int64_t cols, int64_t L, int64_t n_lo,
+                                                       int64_t n_groups, int CW, int kind,
+                                                       const float* __restrict__ q28,
+                                                       int q_trans, float norm) {
+  extern __shared__ float smem[];
+  const int CWP = CW + 4;
+  float* tile = smem;                // L x CWP
+  float* qs = smem + L * CWP;        // 28 x 28
+  const int tid = threadIdx.x;
+  const int64_t strips = cdiv(cols, CW);
+  const int64_t g = blockIdx.x / strips;
+  const int64_t c0 = (blockIdx.x % strips) * CW;
+  if (g >= n_groups) return;
+  const int64_t hi = g / n_lo, lo = g % n_lo;
+  const int64_t row0 = hi * L * n_lo + lo;  // row of a = 0
+  if (kind == 1) {
+    for (int i = tid; i < 28 * 28; i += CP_THREADS) {
+      const int a = i / 28, b = i % 28;
+      qs[i] = q_trans ? q28[b * 28 + a] : q28[i];
+    }
+  }
+  const int cw4 = CW / 4;
+  for (int64_t it = tid; it < L * cw4; it += CP_THREADS) {
+    const int64_t a = it / cw4;
+    const int c = int(it % cw4) * 4;
+    const int64_t gr = row0 + a * n_lo;
+    const int64_t gc = c0 + c;
+    float4 x;
+    if (gc + 4 <= cols) {
+      x = *reinterpret_cast<const float4*>(src + gr * lds_ + gc);
+    } else {
+      const float* p = src + gr * lds_;
+      x.x = gc + 0 < cols ? p[gc + 0] : 0.f;
+      x.y = gc + 1 < cols ? p[gc + 1] : 0.f;
+      x.z = gc + 2 < cols ? p[gc + 2] : 0.f;
+      x.w = gc + 3 < cols ? p[gc + 3] : 0.f;
+    }
+    *reinterpret_cast<float4*>(tile + a * CWP + c) = x;
+  }
+  __syncthreads();
+  if (kind == 0) {
+    // butterflies along a, items (group q, column c)
+    int64_t h = 1;
+    while (h < L) {
+      const int64_t left = L / h;
+      const int R = left >= 8 ? 8 : (left == 4 ? 4 : 2);
+      const int64_t items = (L / R) * CW;
+      for (int64_t it = tid; it < items; it += CP_THREADS) {
+        const int64_t q = it / CW;
+        const int c = int(it % CW);
+        const int64_t base = (q / h) * (R * h) + (q % h);
+        float x[8];
+        if (R == 8) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) x[k] = tile[(base + k * h) * CWP + c];
+          hadamard_reg<8>(x);
+#pragma unroll
+          for (int k = 0; k < 8; ++k) tile[(base + k * h) * CWP + c] = x[k];
+        } else if (R == 4) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) x[k] = tile[(base + k * h) * CWP + c];
+          hadamard_reg<4>(x);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) tile[(base + k * h) * CWP + c] = x[k];
+        } else {
+          x[0] = tile[base * CWP + c];
+          x[1] = tile[(base + h) * CWP + c];
+          tile[base * CWP + c] = x[0] + x[1];
+          tile[(base + h) * CWP + c] = x[0] - x[1];
+        }
+      }
+      h *= R;
+      __syncthreads();
+    }
+    for (int64_t it = tid; it < L * cw4; it += CP_THREADS) {
+      const int64_t a = it / cw4;
+      const int c = int(it % cw4) * 4;
+      const int64_t gr = row0 + a * n_lo;
+      const int64_t gc = c0 + c;
+      float4 x = *reinterpret_cast<const float4*>(tile + a * CWP + c);
+      x.x *= norm;
+      x.y *= norm;
+      x.z *= norm;
+      x.w *= norm;
+      if (gc + 4 <= cols) {
+        *reinterpret_cast<float4*>(dst + gr * ldd + gc) = x;
+      } else {
+        float* p = dst + gr * ldd;
+        if (gc + 0 < cols) p[gc + 0] = x.x;
+        if (gc + 1 < cols) p[gc + 1] = x.y;
+        if (gc + 2 < cols) p[gc + 2] = x.z;
+      }
+    }
+  } else {
+    // 28-point mix: out[a][c] = sum_k Q[a][k] tile[k][c]
+    for (int64_t it = tid; it < 28 * CW; it += CP_THREADS) {
+      const int a = int(it / CW);
+      const int c = int(it % CW);
+      const int64_t gc = c0 + c;
+      float acc = 0.f;
+#pragma unroll 4
+      for (int k = 0; k < 28; ++k) acc = fmaf(qs[a * 28 + k], tile[k * CWP + c], acc);
+      if (gc < cols) dst[(row0 + a * n_lo) * ldd + gc] = acc * norm;
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------- host helpers
+int launch_row_pass(const void* src, int dtype, int64_t lds_, float* dst, int64_t ldd,
+                    int64_t rows, int64_t n, const float* pre_row, const float* pre_col,
+                    const float* post_row, const float* post_col, bool transform,
+                    const RotDim& rd, const float* q28, bool q_trans, hipStream_t s,
+                    const char* name) {
+  const size_t shmem = transform ? (size_t(n) + 28 * 28) * sizeof(float) : 0;
+  const unsigned grid = unsigned(rows < 4096 ? rows : 4096);
+  const float norm = transform ? float(1.0 / std::sqrt(double(rd.m))) : 1.f;
+  const float* q = (transform && rd.has28) ? q28 : nullptr;
+  if (dtype == KRONQ_BF16)
+    return launch(name, row_pass<uint16_t>, dim3(grid), dim3(RP_THREADS), shmem, s,
+                  static_cast<const uint16_t*>(src), lds_, dst, ldd, rows, n, pre_row, pre_col,
+                  post_row, post_col, int(transform), rd.m, q, int(q_trans), norm);
+  return launch(name, row_pass<float>, dim3(grid), dim3(RP_THREADS), shmem, s,
+                static_cast<const float*>(src), lds_, dst, ldd, rows, n, pre_row, pre_col,
+                post_row, post_col, int(transform), rd.m, q, int(q_trans), norm);
+}
+
+int launch_col_step(const float* src, int64_t lds_, float* dst, int64_t ldd, int64_t rows,
+                    int64_t cols, int64_t L, int64_t n_lo, int kind, const float* q28,
+                    bool q_trans, hipStream_t s) {
+  const int CW = L <= 128 ? 64 : (L <= 256 ? 64 : 32);
+  const int64_t n_groups = rows / L;
+  const int64_t strips = cdiv(cols, CW);
+  const size_t shmem = (size_t(L) * (CW + 4) + 28 * 28) * sizeof(float);
+  const float norm = kind == 0 ? float(1.0 / std::sqrt(double(L))) : 1.f;
+  return launch(kind == 0 ? "fwht_col" : "mix28_col", col_pass, dim3(unsigned(n_groups * strips)),
+                dim3(CP_THREADS), shmem, s, src, lds_, dst, ldd, cols, L, n_lo, n_groups, CW,
+                kind, q28, int(q_trans), norm);
+}
+
+// Full transform of every column (rows axis, length d): T = (Q (x) H_m) / sqrt(m).
+int col_transform(const float* src, int64_t lds_, float* dst, int64_t ldd, int64_t d,
+                  int64_t cols, const RotDim& rd, const float* q28, bool q_trans, hipStream_t s) {
+  // Hadamard factors, fast index first: m = m1 * m2 * ..., each <= CP_MAXL
+  int64_t n_lo = 1;
+  int64_t left = rd.m;
+  const float* cur = src;
+  int64_t ldc = lds_;
+  while (left > 1) {
+    const int64_t L = left > CP_MAXL ? CP_MAXL : left;
+    KQ_TRY(launch_col_step(cur, ldc, dst, ldd, d, cols, L, n_lo, 0, nullptr, false, s));
+    cur = dst;
+    ldc = ldd;
+    n_lo *= L;
+    left /= L;
+  }
+  if (rd.has28) {
+    KQ_TRY(launch_col_step(cur, ldc, dst, ldd, d, cols, 28, rd.m, 1, q28, q_trans, s));
+  }
+  return KRONQ_OK;
+}
+
+}  // namespace
+
+size_t rotate_ws_bytes(int64_t d_out, int64_t d_in) {
+  if (d_out <= 0 || d_in <= 0) return 0;
+  const int64_t nb = cdiv(d_out, NORM_ROWS);
+  size_t b = 0;
+  b += align256(size_t(nb) * d_in * sizeof(double));          // column partials
+  b += align256(size_t(d_out) * sizeof(double));               // row sums
+  b += 2 * align256(size_t(d_in) * sizeof(float));             // mul_w_in, mul_h_in
+  b += 2 * align256(size_t(d_out) * sizeof(float));            // mul_w_out, mul_h_out
+  return b + 256;
+}
+
+int rotate_launch(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_t d_out,
+                  int64_t d_in, int64_t ldw, float* HX, int64_t ldx, float* HG, int64_t ldg,
+                  const int8_t* sign_in, const int8_t* sign_out, const float* q28_in,
+                  const float* q28_out, float* sx, float* sg, int flags, void* ws,
+                  hipStream_t s) {
+  const bool rot_in = flags & KRONQ_ROT_IN, rot_out = flags & KRONQ_ROT_OUT;
+  const RotDim ri = rot_dim(d_in), ro = rot_dim(d_out);
+  Carver cv(ws);
+  const int64_t nb = cdiv(d_out, NORM_ROWS);
+  double* colp = cv.take<double>(size_t(nb) * d_in);
+  double* rows = cv.take<double>(d_out);
+  float* mw_in = cv.take<float>(d_in);
+  float* mh_in = cv.take<float>(d_in);
+  float* mw_out = cv.take<float>(d_out);
+  float* mh_out = cv.take<float>(d_out);
+
+  if (flags & KRONQ_INVERSE) {
+    // W <- diag(sign_out / sg) (Q^T (x) H) W_in (...)  V-side: rows of the result get
+    // diag(sign_in / sx) after the transposed row transform.
+    KQ_TRY(launch("rot_inv_factors", inv_factors, dim3(unsigned(cdiv(d_in, 256))), dim3(256), 0,
+                  s, d_in, static_cast<const float*>(sx), rot_in ? sign_in : nullptr, mw_in));
+    KQ_TRY(launch("rot_inv_factors", inv_factors, dim3(unsigned(cdiv(d_out, 256))), dim3(256), 0,
+                  s, d_out, static_cast<const float*>(sg), rot_out ? sign_out : nullptr, mw_out));
+    const float* src = static_cast<const float*>(W_in);
+    int64_t lsrc = ldw_in;
+    if (rot_out) {
+      KQ_TRY(col_transform(src, lsrc, W, ldw, d_out, d_in, ro, q28_out, true, s));
+      src = W;
+      lsrc = ldw;
+    }
+    return launch_row_pass(src, KRONQ_FP32, lsrc, W, ldw, d_out, d_in, nullptr, nullptr, mw_out,
+                           mw_in, rot_in, ri, q28_in, true, s, "rot_row_pass");
+  }
+
+  // ---- forward
+  const bool need_norms = flags & (KRONQ_RESCALE_IN | KRONQ_RESCALE_OUT);
+  if (need_norms) {
+    if (w_dtype == KRONQ_BF16)
+      KQ_TRY(launch("rot_w_norms", w_norms<uint16_t>, dim3(unsigned(nb)), dim3(256), 0, s,
+                    static_cast<const uint16_t*>(W_in), d_out, d_in, ldw_in, colp, rows));
+    else
+      KQ_TRY(launch("rot_w_norms", w_norms<float>, dim3(unsigned(nb)), dim3(256), 0, s,
+                    static_cast<const float*>(W_in), d_out, d_in, ldw_in, colp, rows));
+  }
+  KQ_TRY(launch("rot_factors", side_factors, dim3(unsigned(cdiv(d_in, 256))), dim3(256), 0, s,
+                d_in, static_cast<const float*>(HX), ldx, static_cast<const double*>(colp), nb,
+                static_cast<const double*>(nullptr), rot_in ? sign_in : nullptr,
+                int((flags & KRONQ_RESCALE_IN) != 0), sx, mw_in, mh_in));
+  KQ_TRY(launch("rot_factors", side_factors, dim3(unsigned(cdiv(d_out, 256))), dim3(256), 0, s,
+                d_out, static_cast<const float*>(HG), ldg, static_cast<const double*>(nullptr),
+                int64_t(0), static_cast<const double*>(rows), rot_out ? sign_out : nullptr,
+                int((flags & KRONQ_RESCALE_OUT) != 0), sg, mw_out, mh_out));
+  // W: rescale + signs + V side (row pass), then U side (column pass)
+  KQ_TRY(launch_row_pass(W_in, w_dtype, ldw_in, W, ldw, d_out, d_in, mw_out, mw_in, nullptr,
+                         nullptr, rot_in, ri, q28_in, false, s, "rot_row_pass"));
+  if (rot_out) KQ_TRY(col_transform(W, ldw, W, ldw, d_out, d_in, ro, q28_out, false, s));
+  // H_X <- V S^-1 H_X S^-1 V^T
+  KQ_TRY(launch_row_pass(HX, KRONQ_FP32, ldx, HX, ldx, d_in, d_in, mh_in, mh_in, nullptr,
+                         nullptr, rot_in, ri, q28_in, false, s, "rot_row_pass"));
+  if (rot_in) KQ_TRY(col_transform(HX, ldx, HX, ldx, d_in, d_in, ri, q28_in, false, s));
+  // H_G <- U S^-1 H_G S^-1 U^T
+  if (HG) {
+    KQ_TRY(launch_row_pass(HG, KRONQ_FP32, ldg, HG, ldg, d_out, d_out, mh_out, mh_out, nullptr,
+                           nullptr, rot_out, ro, q28_out, false, s, "rot_row_pass"));
+    if (rot_out) KQ_TRY(col_transform(HG, ldg, HG, ldg, d_out, d_out, ro, q28_out, false, s));
+  }
+  return KRONQ_OK;
+}
+
+}  // namespace kq

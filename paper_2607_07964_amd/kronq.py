@@ -1,0 +1,248 @@
+"""Python binding of libkronq (the KronQ per-layer path on MI355X).
+
+Argument marshalling only: every function checks tensor placement and dtype, supplies the
+workspace and the current HIP stream, and calls the C-ABI entry point of the same name
+(declared in include/kronq.h). PyTorch provides device memory and streams; all arithmetic runs
+in the library's HIP kernels. There is no fallback: if libkronq.so is missing or a call fails,
+an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkronq.so")
+
+KRONQ_BF16, KRONQ_FP32 = 1, 2
+RESCALE_IN, RESCALE_OUT, ROT_IN, ROT_OUT, INVERSE = 1, 2, 4, 8, 16
+BIIP = RESCALE_IN | RESCALE_OUT | ROT_IN | ROT_OUT
+OP_COV, OP_ROTATE, OP_CHOL, OP_OBS, OP_LOSS = 1, 2, 3, 4, 5
+ERRORS = {0: "OK", -1: "INVALID_ARG", -2: "SHAPE", -3: "NOT_PD", -4: "HIP", -5: "WORKSPACE",
+          -6: "UNSUPPORTED"}
+
+EXPORTS = (
+    "kronq_workspace_bytes", "kronq_last_error", "kronq_version", "kronq_accumulate_cov",
+    "kronq_traces", "kronq_rotate", "kronq_cholesky_inv", "kronq_obs_quantize_layer",
+    "kronq_layer_loss", "kronq_allocate_bits", "kronq_profile_enable", "kronq_profile_reset",
+    "kronq_profile_read",
+)
+
+
+class KronqError(RuntimeError):
+    def __init__(self, code: int, func: str, msg: str):
+        super().__init__(f"{func}: {ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libkronq.so (once). Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2607_07964_amd.build`")
+    lib = ctypes.CDLL(path)
+    P, I64, I, F, D, SZ = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float,
+                           ctypes.c_double, ctypes.c_size_t)
+    sig = {
+        "kronq_workspace_bytes": (SZ, [I, I64, I64, I64]),
+        "kronq_last_error": (ctypes.c_char_p, []),
+        "kronq_version": (I, []),
+        "kronq_accumulate_cov": (I, [P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
+        "kronq_traces": (I, [P, I64, I64, P, I64, I64, P, P]),
+        "kronq_rotate": (I, [P, I, I64, P, I64, I64, I64, P, I64, P, I64, P, P, P, P, P, P, I, P,
+                             SZ, P]),
+        "kronq_cholesky_inv": (I, [P, I64, I64, F, P, I64, P, P, SZ, P]),
+        "kronq_obs_quantize_layer": (I, [P, I64, I64, I64, P, I64, I, I, I, P, P, P, P, P, P, SZ,
+                                         P]),
+        "kronq_layer_loss": (I, [P, I, I64, P, I64, I64, I64, P, I64, P, I64, P, P, SZ, P]),
+        "kronq_allocate_bits": (I, [P, P, I, P, I, D, P, P]),
+        "kronq_profile_enable": (I, [I]),
+        "kronq_profile_reset": (None, []),
+        "kronq_profile_read": (I, [ctypes.c_char_p, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(rc: int, func: str):
+    if rc != 0:
+        raise KronqError(rc, func, load().kronq_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("libkronq works on device tensors only")
+
+
+def _ld(t: torch.Tensor) -> int:
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("expected a row-major 2-D tensor (unit column stride)")
+    return t.stride(0)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return KRONQ_BF16
+    if t.dtype == torch.float32:
+        return KRONQ_FP32
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+def workspace(op: int, d_out: int, d_in: int, n_rows: int, device) -> torch.Tensor:
+    n = load().kronq_workspace_bytes(op, d_out, d_in, n_rows)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+
+
+def kronq_workspace_bytes(op: int, d_out: int, d_in: int, n_rows: int) -> int:
+    return int(load().kronq_workspace_bytes(op, d_out, d_in, n_rows))
+
+
+def kronq_version() -> int:
+    return int(load().kronq_version())
+
+
+# ------------------------------------------------------------------------------------ steps
+def kronq_accumulate_cov(A: torch.Tensor, H: torch.Tensor, alpha: float = 1.0, beta: float = 0.0,
+                         ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """H <- beta H + alpha A^T A (token-major A [N x d], bf16 or fp32; H fp32 [d x d])."""
+    _dev(A, H)
+    n, d = A.shape
+    if ws is None:
+        ws = workspace(OP_COV, 0, d, n, A.device) if A.dtype == torch.bfloat16 else \
+            torch.empty(256, dtype=torch.uint8, device=A.device)
+    rc = load().kronq_accumulate_cov(_ptr(A), _dtype_code(A), n, d, _ld(A), _ptr(H), _ld(H),
+                                     alpha, beta, _ptr(ws), ws.numel(), _stream(A.device))
+    _check(rc, "kronq_accumulate_cov")
+    return H
+
+
+def kronq_traces(HX: torch.Tensor, HG: torch.Tensor, out: Optional[torch.Tensor] = None):
+    """Device float64 tensor [tr H_X, tr H_G, tr H_X * tr H_G]."""
+    _dev(HX, HG)
+    if out is None:
+        out = torch.empty(3, dtype=torch.float64, device=HX.device)
+    rc = load().kronq_traces(_ptr(HX), HX.shape[0], _ld(HX), _ptr(HG), HG.shape[0], _ld(HG),
+                             _ptr(out), _stream(HX.device))
+    _check(rc, "kronq_traces")
+    return out
+
+
+def kronq_rotate(W_in: torch.Tensor, W: torch.Tensor, HX: Optional[torch.Tensor],
+                 HG: Optional[torch.Tensor], sign_in: Optional[torch.Tensor],
+                 sign_out: Optional[torch.Tensor], q28_in: Optional[torch.Tensor],
+                 q28_out: Optional[torch.Tensor], sx: torch.Tensor, sg: torch.Tensor,
+                 flags: int = BIIP, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """BiIP forward (W <- U S_G W_in S_X V^T, H_X and H_G in place) or, with INVERSE, the revert."""
+    _dev(W_in, W, HX, HG, sign_in, sign_out, q28_in, q28_out, sx, sg)
+    d_out, d_in = W.shape
+    if ws is None:
+        ws = workspace(OP_ROTATE, d_out, d_in, 0, W.device)
+    rc = load().kronq_rotate(
+        _ptr(W_in), _dtype_code(W_in), _ld(W_in), _ptr(W), d_out, d_in, _ld(W), _ptr(HX),
+        _ld(HX) if HX is not None else 0, _ptr(HG), _ld(HG) if HG is not None else 0,
+        _ptr(sign_in), _ptr(sign_out), _ptr(q28_in), _ptr(q28_out), _ptr(sx), _ptr(sg), flags,
+        _ptr(ws), ws.numel(), _stream(W.device))
+    _check(rc, "kronq_rotate")
+    return W
+
+
+def kronq_cholesky_inv(H: torch.Tensor, U: torch.Tensor, damp: float = 0.01,
+                       info: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """Damp H in place and write the upper U with inv(H~) = U^T U. Returns the device info."""
+    _dev(H, U)
+    d = H.shape[0]
+    if info is None:
+        info = torch.empty(1, dtype=torch.int32, device=H.device)
+    if ws is None:
+        ws = workspace(OP_CHOL, 0, d, 0, H.device)
+    rc = load().kronq_cholesky_inv(_ptr(H), d, _ld(H), damp, _ptr(U), _ld(U), _ptr(info),
+                                   _ptr(ws), ws.numel(), _stream(H.device))
+    _check(rc, "kronq_cholesky_inv")
+    return info
+
+
+def kronq_obs_quantize_layer(W: torch.Tensor, U: torch.Tensor, bits: int, codes: torch.Tensor,
+                             scales: torch.Tensor, zeros: torch.Tensor,
+                             err: Optional[torch.Tensor] = None,
+                             W_hat: Optional[torch.Tensor] = None, group: int = 128,
+                             block: int = 128, ws: Optional[torch.Tensor] = None):
+    """Lazy-block OBS sweep with group quantisation; W ends as the dequantised W_hat."""
+    _dev(W, U, codes, scales, zeros, err, W_hat)
+    d_out, d_in = W.shape
+    if ws is None:
+        ws = workspace(OP_OBS, d_out, d_in, 0, W.device)
+    rc = load().kronq_obs_quantize_layer(
+        _ptr(W), d_out, d_in, _ld(W), _ptr(U), _ld(U), bits, group, block, _ptr(codes),
+        _ptr(scales), _ptr(zeros), _ptr(err), _ptr(W_hat), _ptr(ws), ws.numel(),
+        _stream(W.device))
+    _check(rc, "kronq_obs_quantize_layer")
+
+
+def kronq_layer_loss(W: torch.Tensor, W_hat: Optional[torch.Tensor], HX: torch.Tensor,
+                     HG: torch.Tensor, out: Optional[torch.Tensor] = None,
+                     ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Device float64 scalar tr(H_G dW H_X dW^T), dW = W - W_hat."""
+    _dev(W, W_hat, HX, HG)
+    d_out, d_in = W.shape
+    if out is None:
+        out = torch.empty(1, dtype=torch.float64, device=W.device)
+    if ws is None:
+        ws = workspace(OP_LOSS, d_out, d_in, 0, W.device)
+    rc = load().kronq_layer_loss(
+        _ptr(W), _dtype_code(W), _ld(W), _ptr(W_hat), _ld(W_hat) if W_hat is not None else 0,
+        d_out, d_in, _ptr(HX), _ld(HX), _ptr(HG), _ld(HG), _ptr(out), _ptr(ws), ws.numel(),
+        _stream(W.device))
+    _check(rc, "kronq_layer_loss")
+    return out
+
+
+def kronq_allocate_bits(scores, weights, choices=(2, 3, 4), avg_bits: float = 3.0):
+    """Host-side exhaustive bit allocation. Returns (bits tuple, objective)."""
+    n = len(scores)
+    s = (ctypes.c_double * n)(*[float(x) for x in scores])
+    w = (ctypes.c_int64 * n)(*[int(x) for x in weights])
+    c = (ctypes.c_int * len(choices))(*[int(x) for x in choices])
+    out = (ctypes.c_int * n)()
+    obj = ctypes.c_double()
+    rc = load().kronq_allocate_bits(s, w, n, c, len(choices), avg_bits, out, ctypes.byref(obj))
+    _check(rc, "kronq_allocate_bits")
+    return tuple(out[i] for i in range(n)), obj.value
+
+
+# ------------------------------------------------------------------------------------ profiler
+def kronq_profile_enable(on: bool = True):
+    _check(load().kronq_profile_enable(int(on)), "kronq_profile_enable")
+
+
+def kronq_profile_reset():
+    load().kronq_profile_reset()
+
+
+def kronq_profile_read(kernel: str):
+    """(total milliseconds, launches) of the named kernel since the last reset."""
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    _check(load().kronq_profile_read(kernel.encode(), ctypes.byref(ms), ctypes.byref(n)),
+           "kronq_profile_read")
+    return ms.value, n.value

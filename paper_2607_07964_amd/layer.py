@@ -1,0 +1,130 @@
+"""Per-layer and per-block drivers: the KronQ hot path as a sequence of libkronq calls.
+
+One layer (Alg. 1 then Alg. 2 with P = 0):
+  H_X = X^T X, H_G = G^T G  ->  traces (pre)  ->  BiIP (rescale + both rotations)
+  ->  traces (post: the sensitivity score)  ->  damping + inverse-Cholesky factor
+  ->  lazy-block OBS sweep with group quantisation.
+All calls are enqueued on the current stream; nothing here synchronises except ``check()``.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import torch
+
+from . import kronq as K
+
+
+@dataclasses.dataclass
+class RotParams:
+    """Device copies of one side's randomised-Hadamard draw."""
+    sign: torch.Tensor  # int8 [d]
+    q28: Optional[torch.Tensor]  # fp32 [28, 28] or None
+
+    @staticmethod
+    def to_device(sign, q28, device) -> "RotParams":
+        s = torch.as_tensor(sign, dtype=torch.int8).to(device)
+        q = None if q28 is None else torch.as_tensor(q28, dtype=torch.float32).contiguous().to(device)
+        return RotParams(s, q)
+
+
+@dataclasses.dataclass
+class LayerState:
+    """Device buffers of one layer's solve (allocated once, reused across calls)."""
+    d_out: int
+    d_in: int
+    n_tokens: int
+    HX: torch.Tensor
+    HG: torch.Tensor
+    W: torch.Tensor  # fp32 working copy (rotated, then dequantised)
+    U: torch.Tensor
+    codes: torch.Tensor
+    scales: torch.Tensor
+    zeros: torch.Tensor
+    sx: torch.Tensor
+    sg: torch.Tensor
+    tr_pre: torch.Tensor
+    tr_post: torch.Tensor
+    info: torch.Tensor
+    ws_cov_x: torch.Tensor
+    ws_cov_g: torch.Tensor
+    ws_rot: torch.Tensor
+    ws_chol: torch.Tensor
+    ws_obs: torch.Tensor
+    err: Optional[torch.Tensor] = None
+
+    @staticmethod
+    def allocate(d_out: int, d_in: int, n_tokens: int, device, keep_err: bool = False,
+                 x_dtype=torch.bfloat16, g_dtype=torch.bfloat16) -> "LayerState":
+        f32 = dict(dtype=torch.float32, device=device)
+
+        def ws(op, a, b, n, dt=torch.bfloat16):
+            if op == K.OP_COV and dt != torch.bfloat16:
+                return torch.empty(256, dtype=torch.uint8, device=device)
+            return K.workspace(op, a, b, n, device)
+
+        return LayerState(
+            d_out=d_out, d_in=d_in, n_tokens=n_tokens,
+            HX=torch.empty(d_in, d_in, **f32), HG=torch.empty(d_out, d_out, **f32),
+            W=torch.empty(d_out, d_in, **f32), U=torch.empty(d_in, d_in, **f32),
+            codes=torch.empty(d_out, d_in, dtype=torch.uint8, device=device),
+            scales=torch.empty(d_out, d_in // 128, **f32),
+            zeros=torch.empty(d_out, d_in // 128, **f32),
+            sx=torch.empty(d_in, **f32), sg=torch.empty(d_out, **f32),
+            tr_pre=torch.empty(3, dtype=torch.float64, device=device),
+            tr_post=torch.empty(3, dtype=torch.float64, device=device),
+            info=torch.empty(1, dtype=torch.int32, device=device),
+            ws_cov_x=ws(K.OP_COV, 0, d_in, n_tokens, x_dtype),
+            ws_cov_g=ws(K.OP_COV, 0, d_out, n_tokens, g_dtype),
+            ws_rot=ws(K.OP_ROTATE, d_out, d_in, 0), ws_chol=ws(K.OP_CHOL, 0, d_in, 0),
+            ws_obs=ws(K.OP_OBS, d_out, d_in, 0),
+            err=torch.empty(d_out, d_in, **f32) if keep_err else None,
+        )
+
+
+def covariances(st: LayerState, X: torch.Tensor, G: torch.Tensor, skip_x: bool = False):
+    """Steps a1/a2: H_X = X^T X (unless shared and already computed) and H_G = G^T G."""
+    if not skip_x:
+        K.kronq_accumulate_cov(X, st.HX, 1.0, 0.0, st.ws_cov_x)
+    K.kronq_accumulate_cov(G, st.HG, 1.0, 0.0, st.ws_cov_g)
+
+
+def biip(st: LayerState, W0: torch.Tensor, rin: RotParams, rout: RotParams, flags: int = K.BIIP):
+    """Steps a3-a5: pre traces, BiIP, post traces."""
+    K.kronq_traces(st.HX, st.HG, st.tr_pre)
+    K.kronq_rotate(W0, st.W, st.HX, st.HG, rin.sign, rout.sign, rin.q28, rout.q28, st.sx, st.sg,
+                   flags, st.ws_rot)
+    K.kronq_traces(st.HX, st.HG, st.tr_post)
+
+
+def solve(st: LayerState, bits: int, damp: float = 0.01):
+    """Steps a6-a8: damping + inverse-Cholesky factor, then the lazy-block OBS sweep."""
+    K.kronq_cholesky_inv(st.HX, st.U, damp, st.info, st.ws_chol)
+    K.kronq_obs_quantize_layer(st.W, st.U, bits, st.codes, st.scales, st.zeros, st.err, None,
+                               ws=st.ws_obs)
+
+
+def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bits: int,
+                   damp: float = 0.01, flags: int = K.BIIP, skip_x: bool = False):
+    """The whole hot path of one layer (enqueue only)."""
+    covariances(st, X, G, skip_x)
+    biip(st, W0, rin, rout, flags)
+    solve(st, bits, damp)
+
+
+def check(st: LayerState):
+    """Synchronise and raise if the factorisation met a non-positive pivot."""
+    info = int(st.info.item())
+    if info != 0:
+        raise K.KronqError(-3, "kronq_cholesky_inv", f"pivot of column {info} is not positive")
+
+
+def revert(st: LayerState, rin: RotParams, rout: RotParams, out: Optional[torch.Tensor] = None,
+           flags: int = K.BIIP, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Original-space dequantised weights: S_G^-1 U^T W_hat' V S_X^-1 (Alg. 2, last line)."""
+    if out is None:
+        out = torch.empty_like(st.W)
+    K.kronq_rotate(st.W, out, None, None, rin.sign, rout.sign, rin.q28, rout.q28, st.sx, st.sg,
+                   flags | K.INVERSE, ws if ws is not None else st.ws_rot)
+    return out

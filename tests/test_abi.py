@@ -1,0 +1,104 @@
+"""The C-ABI library: loads, exports every declared symbol, host-side logic (CPU only).
+
+No call here launches GPU work: only symbol lookup, workspace queries, argument checks that fail
+before any HIP call, and the host-only bit allocation.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2607_07964_amd import kronq as K
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kronq.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kronq_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = K.load()
+    names = declared_functions()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(K.EXPORTS)
+
+
+def test_version_and_workspace_queries():
+    assert K.kronq_version() >= 100
+    assert K.kronq_workspace_bytes(K.OP_COV, 0, 4096, 262144) > 0
+    assert K.kronq_workspace_bytes(K.OP_CHOL, 0, 4096, 0) >= 2 * 4096 * 4096 * 4
+    assert K.kronq_workspace_bytes(K.OP_OBS, 4096, 4096, 0) > 0
+    assert K.kronq_workspace_bytes(99, 1, 1, 1) == 0
+    assert K.kronq_workspace_bytes(K.OP_COV, 0, -1, 10) == 0
+
+
+def _err(rc):
+    return rc, K.load().kronq_last_error().decode()
+
+
+def test_argument_checks_fail_before_any_launch():
+    lib = K.load()
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: checks fail first
+    # unsupported group / block / bits
+    rc, msg = _err(lib.kronq_obs_quantize_layer(fake, 8, 256, 256, fake, 256, 4, 64, 128, fake,
+                                                fake, fake, nul, nul, nul, 0, nul))
+    assert rc == -6 and "group" in msg
+    rc, _ = _err(lib.kronq_obs_quantize_layer(fake, 8, 256, 256, fake, 256, 9, 128, 128, fake,
+                                              fake, fake, nul, nul, nul, 0, nul))
+    assert rc == -6
+    rc, _ = _err(lib.kronq_obs_quantize_layer(fake, 8, 256, 256, fake, 256, 4, 128, 64, fake,
+                                              fake, fake, nul, nul, nul, 0, nul))
+    assert rc == -6
+    # bad dtype, null H
+    rc, _ = _err(lib.kronq_accumulate_cov(fake, 7, 10, 8, 8, fake, 8, 1.0, 0.0, nul, 0, nul))
+    assert rc == -1
+    rc, _ = _err(lib.kronq_accumulate_cov(fake, 1, 10, 8, 8, nul, 8, 1.0, 0.0, nul, 0, nul))
+    assert rc == -1
+    # too small a workspace
+    rc, msg = _err(lib.kronq_accumulate_cov(fake, 1, 1000, 64, 64, fake, 64, 1.0, 0.0, nul, 16,
+                                            nul))
+    assert rc == -5 and "workspace" in msg
+    # rotation of a dimension that is neither 2^k nor 28 * 2^k
+    ws = ctypes.c_void_p(1 << 30)
+    rc, msg = _err(lib.kronq_rotate(fake, 2, 96, fake, 8, 96, 96, fake, 96, nul, 0, fake, nul,
+                                    nul, nul, fake, fake, K.ROT_IN, ws, 1 << 30, nul))
+    assert rc == -6 and "96" in msg
+    # 28 * 2^k without the 28 x 28 factor
+    rc, msg = _err(lib.kronq_rotate(fake, 2, 112, fake, 8, 112, 112, fake, 112, nul, 0, fake, nul,
+                                    nul, nul, fake, fake, K.ROT_IN, ws, 1 << 30, nul))
+    assert rc == -1 and "28" in msg
+    # d_in not a multiple of the group
+    rc, _ = _err(lib.kronq_obs_quantize_layer(fake, 8, 200, 200, fake, 200, 4, 128, 128, fake,
+                                              fake, fake, nul, nul, nul, 0, nul))
+    assert rc == -2
+    # Cholesky output aliasing its input
+    rc, _ = _err(lib.kronq_cholesky_inv(fake, 8, 8, 0.01, fake, 8, fake, ws, 1 << 30, nul))
+    assert rc == -1
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_allocation_matches_oracle(seed):
+    r = np.random.default_rng(seed)
+    n = int(r.integers(2, 8))
+    scores = np.exp(3 * r.standard_normal(n))
+    weights = r.integers(1, 1000, size=n)
+    avg = float(r.choice([2.5, 3.0, 3.5]))
+    lib_bits, lib_val = K.kronq_allocate_bits(scores, weights, (2, 3, 4), avg)
+    ora_bits, ora_val = O.allocate_bits(scores, weights, (2, 3, 4), avg)
+    assert lib_bits == ora_bits
+    assert lib_val == ora_val  # same float64 operations in the same order
+
+
+def test_allocation_infeasible_budget():
+    with pytest.raises(K.KronqError):
+        K.kronq_allocate_bits([1.0, 2.0], [1, 1], (3, 4), 2.0)

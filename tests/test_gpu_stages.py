@@ -1,0 +1,279 @@
+"""Stage-isolated parity: each HIP step through the C ABI against the float64 oracle.
+
+Each stage gets inputs from the seeded generator or from the oracle (rounded to the fp32 the
+library takes), never from another HIP step. Sizes span several tiles and ragged tails.
+Tolerances: 1e-3 relative Frobenius error for covariances, traces and rotated matrices;
+codes bit-exact in the round-to-nearest case and >= 99.5 % identical otherwise; loss 1e-3.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from gpu_util import DEV, note, oracle_view, rel_frob, rot_device, rot_oracle, to_np
+from paper_2607_07964_amd import kronq as K
+from paper_2607_07964_amd.layer import RotParams
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    K.load()
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+
+
+def f32(a) -> torch.Tensor:
+    """fp32 device copy with rows padded to 16 bytes (the library's layout contract)."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    if a.ndim == 2 and a.shape[1] % 4:
+        buf = torch.zeros(a.shape[0], a.shape[1] + 4 - a.shape[1] % 4, device=DEV)
+        buf[:, :a.shape[1]] = torch.from_numpy(a).to(DEV)
+        return buf[:, :a.shape[1]]
+    return torch.tensor(a, device=DEV)
+
+
+def spd_from_tokens(d, n, seed, kind="normal_t3"):
+    """An oracle covariance of generator tokens, rounded to fp32 (the form the library takes)."""
+    spec = synth.small_spec(d, d, n, seed=seed, xkind=kind).x
+    H = O.covariance(oracle_view(synth.gen_matrix(spec)))
+    return H.astype(np.float32).astype(np.float64)
+
+
+# ------------------------------------------------------------------------------ generator
+def test_generator_gpu_matches_cpu():
+    s = synth.small_spec(448, 256, 3000)
+    for spec in (s.x, s.g, s.w):
+        note(f"generator {spec.tag} {spec.rows}x{spec.cols}")
+        assert torch.equal(synth.gen_matrix(spec, DEV).cpu(), synth.gen_matrix(spec))
+
+
+# ------------------------------------------------------------------------------ covariance
+@pytest.mark.parametrize("n,d", [(1000, 300), (5000, 600), (64, 8), (4099, 1024), (70, 257)])
+def test_cov_bf16(n, d):
+    dp = (d + 7) // 8 * 8  # rows padded to 16 bytes; the first d channels are used
+    spec = synth.small_spec(dp, dp, n, seed=n + d).x
+    X = synth.gen_matrix(spec, DEV)[:, :d]
+    H = torch.full((d, d), float("nan"), device=DEV)
+    note(f"cov bf16 n={n} d={d}")
+    K.kronq_accumulate_cov(X, H)
+    torch.cuda.synchronize()
+    ref = O.covariance(oracle_view(synth.gen_matrix(spec))[:, :d])
+    h = to_np(H)
+    assert rel_frob(h, ref) < TOL
+    assert np.array_equal(h, h.T)
+
+
+def test_cov_chained_scaled_and_strided():
+    n1, n2, d = 1500, 900, 520
+    spec = synth.small_spec(d + 8, d + 8, n1 + n2, seed=5).x
+    Xw = synth.gen_matrix(spec, DEV)  # [n, d + 8]; use the first d columns (lda = d + 8)
+    X1, X2 = Xw[:n1, :d], Xw[n1:, :d]
+    H = torch.empty(d, d, device=DEV)
+    note("cov chained beta=1, alpha=1/N, lda > d")
+    K.kronq_accumulate_cov(X1, H, alpha=1.0 / (n1 + n2), beta=0.0)
+    K.kronq_accumulate_cov(X2, H, alpha=1.0 / (n1 + n2), beta=1.0)
+    torch.cuda.synchronize()
+    ref = O.covariance(oracle_view(synth.gen_matrix(spec))[:, :d]) / (n1 + n2)
+    assert rel_frob(to_np(H), ref) < TOL
+
+
+def test_cov_fp32_and_empty():
+    s = synth.workload(1)
+    X = synth.gen_matrix(s.x, DEV)
+    H = torch.empty(256, 256, device=DEV)
+    note("cov fp32 2048x256")
+    K.kronq_accumulate_cov(X, H)
+    torch.cuda.synchronize()
+    ref = O.covariance(synth.gen_matrix(s.x).numpy())
+    assert rel_frob(to_np(H), ref) < TOL
+    note("cov n_rows=0")
+    H2 = H.clone()
+    K.kronq_accumulate_cov(X[:0], H2, beta=0.5)
+    torch.cuda.synchronize()
+    assert torch.equal(H2, H * 0.5)
+
+
+# ------------------------------------------------------------------------------ traces
+def test_traces():
+    hx, hg = spd_from_tokens(300, 700, 1), spd_from_tokens(448, 900, 2)
+    note("traces")
+    out = K.kronq_traces(f32(hx), f32(hg))
+    torch.cuda.synchronize()
+    ref = np.array(O.traces(hx, hg))
+    np.testing.assert_allclose(to_np(out), ref, rtol=1e-9)
+
+
+# ------------------------------------------------------------------------------ rotation
+ROT_CASES = [
+    (448, 256, K.BIIP), (512, 224, K.BIIP), (256, 256, K.RESCALE_IN | K.RESCALE_OUT),
+    (448, 256, K.ROT_IN | K.ROT_OUT), (448, 256, K.RESCALE_IN | K.ROT_IN),
+    (448, 256, K.RESCALE_OUT | K.ROT_OUT), (2048, 1024, K.BIIP), (28 * 32, 4096, K.BIIP),
+]
+
+
+def _rot_problem(d_out, d_in, seed=3):
+    s = synth.small_spec(d_out, d_in, 4 * max(d_in, d_out), seed=seed)
+    W = synth.gen_matrix(s.w)
+    hx = spd_from_tokens(d_in, 2 * d_in, seed + 1)
+    hg = spd_from_tokens(d_out, 2 * d_out, seed + 2)
+    ri = synth.rotation_params(d_in, seed, "in")
+    ro = synth.rotation_params(d_out, seed, "out")
+    return s, W, hx, hg, ri, ro
+
+
+@pytest.mark.parametrize("d_out,d_in,flags", ROT_CASES)
+def test_rotate_forward(d_out, d_in, flags):
+    s, W, hx, hg, ri, ro = _rot_problem(d_out, d_in)
+    HX, HG = f32(hx), f32(hg)
+    Wd = torch.empty(d_out, d_in, device=DEV)
+    sx = torch.empty(d_in, device=DEV)
+    sg = torch.empty(d_out, device=DEV)
+    rin, rout = rot_device(ri), rot_device(ro)
+    note(f"rotate {d_out}x{d_in} flags={flags}")
+    K.kronq_rotate(W.to(DEV), Wd, HX, HG, rin.sign, rout.sign, rin.q28, rout.q28, sx, sg, flags)
+    torch.cuda.synchronize()
+    ref = O.biip_forward(oracle_view(W), hx, hg, rot_oracle(ri), rot_oracle(ro), flags)
+    assert rel_frob(to_np(Wd), ref["W"]) < TOL
+    assert rel_frob(to_np(HX), ref["HX"]) < TOL
+    assert rel_frob(to_np(HG), ref["HG"]) < TOL
+    np.testing.assert_allclose(to_np(sx), ref["sx"], rtol=1e-5)
+    np.testing.assert_allclose(to_np(sg), ref["sg"], rtol=1e-5)
+
+
+def test_rotate_inverse_and_in_place():
+    d_out, d_in = 448, 256
+    s, W, hx, hg, ri, ro = _rot_problem(d_out, d_in, 9)
+    rin, rout = rot_device(ri), rot_device(ro)
+    Wf = W.float().to(DEV)
+    Wd = Wf.clone()
+    sx = torch.empty(d_in, device=DEV)
+    sg = torch.empty(d_out, device=DEV)
+    note("rotate in place fp32, then inverse")
+    K.kronq_rotate(Wd, Wd, f32(hx), f32(hg), rin.sign, rout.sign, rin.q28, rout.q28, sx, sg,
+                   K.BIIP)
+    back = torch.empty_like(Wd)
+    K.kronq_rotate(Wd, back, None, None, rin.sign, rout.sign, rin.q28, rout.q28, sx, sg,
+                   K.BIIP | K.INVERSE)
+    torch.cuda.synchronize()
+    assert rel_frob(to_np(back), oracle_view(W.float())) < 1e-5
+    # inverse of an arbitrary matrix against the oracle's revert (sx, sg as inputs)
+    rng = np.random.default_rng(4)
+    Wh = rng.standard_normal((d_out, d_in)).astype(np.float32)
+    sxv = np.exp(rng.standard_normal(d_in) * 0.3).astype(np.float32)
+    sgv = np.exp(rng.standard_normal(d_out) * 0.3).astype(np.float32)
+    out = torch.empty(d_out, d_in, device=DEV)
+    note("rotate inverse of a random matrix")
+    K.kronq_rotate(f32(Wh), out, None, None, rin.sign, rout.sign, rin.q28, rout.q28, f32(sxv),
+                   f32(sgv), K.BIIP | K.INVERSE)
+    torch.cuda.synchronize()
+    V = O.rht_matrix(d_in, *rot_oracle(ri))
+    U = O.rht_matrix(d_out, *rot_oracle(ro))
+    ref = O.biip_revert(Wh, sxv.astype(np.float64), sgv.astype(np.float64), V, U)
+    assert rel_frob(to_np(out), ref) < TOL
+
+
+# ------------------------------------------------------------------------------ Cholesky
+@pytest.mark.parametrize("d", [256, 300, 1024, 77])
+def test_cholesky_inverse_factor(d):
+    h = spd_from_tokens(d, 3 * d, d)
+    H = f32(h)
+    U = torch.full((d, d), float("nan"), device=DEV)
+    note(f"cholesky_inv d={d}")
+    info = K.kronq_cholesky_inv(H, U, 0.01)
+    torch.cuda.synchronize()
+    assert int(info.item()) == 0
+    hd = O.damp(h, 0.01)
+    np.testing.assert_allclose(to_np(H), hd, rtol=2e-6, atol=1e-6 * np.abs(hd).max())
+    ref = O.inverse_cholesky_factor(hd)
+    u = to_np(U)
+    assert np.all(np.tril(u, -1) == 0.0)
+    assert rel_frob(u, ref) < TOL
+
+
+def test_cholesky_not_pd_reports_pivot():
+    d = 300
+    h = np.eye(d)
+    h[5, 5] = -1.0
+    H = f32(h)
+    U = torch.empty(d, d, device=DEV)
+    note("cholesky_inv not PD")
+    info = K.kronq_cholesky_inv(H, U, 0.01)
+    torch.cuda.synchronize()
+    assert int(info.item()) == 6  # 1-based column of the failing pivot (original order)
+
+
+# ------------------------------------------------------------------------------ OBS sweep
+def _obs_run(W32: np.ndarray, U32: np.ndarray, bits: int, with_err=True):
+    d_out, d_in = W32.shape
+    W = f32(W32)
+    codes = torch.empty(d_out, d_in, dtype=torch.uint8, device=DEV)
+    scales = torch.empty(d_out, d_in // 128, device=DEV)
+    zeros = torch.empty(d_out, d_in // 128, device=DEV)
+    err = torch.empty(d_out, d_in, device=DEV) if with_err else None
+    W_hat = torch.empty(d_out, d_in, device=DEV)
+    K.kronq_obs_quantize_layer(W, f32(U32), bits, codes, scales, zeros, err, W_hat)
+    torch.cuda.synchronize()
+    return dict(W=to_np(W), codes=to_np(codes), scales=to_np(scales), zeros=to_np(zeros),
+                err=None if err is None else to_np(err), w_hat=to_np(W_hat))
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_obs_rtn_bit_exact(bits):
+    d_out, d_in = 200, 384
+    W = synth.gen_matrix(synth.small_spec(d_out, d_in, 16, seed=bits).w).float().numpy()
+    U = O.inverse_cholesky_factor(O.damp(np.eye(d_in))).astype(np.float32)
+    note(f"obs RTN bits={bits}")
+    g = _obs_run(W, U, bits)
+    ref = O.obs_blocked(W.astype(np.float64), U.astype(np.float64), bits, 128, 128)
+    assert np.array_equal(g["codes"], ref["codes"])
+    assert np.array_equal(g["scales"], ref["scales"].astype(np.float32))
+    assert np.array_equal(g["zeros"], ref["zeros"])
+    np.testing.assert_allclose(g["w_hat"], ref["w_hat"], rtol=1e-6, atol=1e-9)
+    np.testing.assert_array_equal(g["W"], g["w_hat"])
+
+
+@pytest.mark.parametrize("d_out,d_in,bits", [(200, 384, 4), (130, 512, 2), (64, 128, 3)])
+def test_obs_general(d_out, d_in, bits):
+    W = synth.gen_matrix(synth.small_spec(d_out, d_in, 16, seed=d_out).w).float().numpy()
+    h = O.damp(spd_from_tokens(d_in, 2 * d_in, d_in + 1))
+    U = O.inverse_cholesky_factor(h).astype(np.float32)
+    note(f"obs general {d_out}x{d_in} bits={bits}")
+    g = _obs_run(W, U, bits)
+    ref = O.obs_blocked(W.astype(np.float64), U.astype(np.float64), bits, 128, 128)
+    same = g["codes"] == ref["codes"]
+    agree = float(np.mean(same))
+    print(f"code agreement {agree:.6f}")
+    assert agree >= 0.995, agree
+    rows = np.all(same, axis=1)  # rows whose codes all agree follow the same path
+    assert rows.mean() > 0.5
+    assert rel_frob(g["w_hat"][rows], ref["w_hat"][rows]) < TOL
+    assert rel_frob(g["err"][rows], ref["err"][rows]) < TOL
+    assert rel_frob(g["scales"], ref["scales"]) < TOL
+
+
+def test_obs_without_err_output():
+    d_out, d_in = 96, 256
+    W = synth.gen_matrix(synth.small_spec(d_out, d_in, 16, seed=8).w).float().numpy()
+    U = O.inverse_cholesky_factor(O.damp(spd_from_tokens(d_in, 600, 3))).astype(np.float32)
+    note("obs without err")
+    a = _obs_run(W, U, 4, with_err=False)
+    b = _obs_run(W, U, 4, with_err=True)
+    assert np.array_equal(a["codes"], b["codes"]) and np.array_equal(a["W"], b["W"])
+
+
+# ------------------------------------------------------------------------------ loss
+@pytest.mark.parametrize("d_out,d_in", [(448, 256), (130, 203)])
+def test_layer_loss(d_out, d_in):
+    W = synth.gen_matrix(synth.small_spec(d_out, d_in, 16, seed=1).w)
+    rng = np.random.default_rng(0)
+    Wh = (W.float().numpy() + 1e-3 * rng.standard_normal((d_out, d_in))).astype(np.float32)
+    hx, hg = spd_from_tokens(d_in, 700, 4), spd_from_tokens(d_out, 700, 5)
+    note(f"loss {d_out}x{d_in}")
+    out = K.kronq_layer_loss(W.to(DEV), f32(Wh), f32(hx), f32(hg))
+    torch.cuda.synchronize()
+    ref = O.kfac_loss(oracle_view(W.float()) - Wh.astype(np.float64), hx, hg)
+    assert abs(float(out.item()) / ref - 1.0) < TOL
