@@ -1,0 +1,203 @@
+#!/usr/bin/env python3
+"""Seconds per layer of the KronQ hot path on one MI355X.
+
+One step = the whole per-layer path on one batch of synthetic calibration data already
+resident in HBM: H_X = X^T X, H_G = G^T G, traces, BiIP (rescale + both randomised Hadamard
+rotations of W, H_X, H_G), traces, damping + inverse-Cholesky factor, lazy-block OBS sweep with
+group quantisation. Default workload: the LLaMA-3-8B q_proj shape, W 4096 x 4096, 262144 tokens
+(128 x 2048), 4-bit, group 128.
+
+The JSON line carries
+  * roofline: the covariance syrk (the dominant kernel) timed by libkronq's hipEvent profiler on
+    its own stream inside the timed region, algorithmic flops N d (d + 1) per launch, against
+    the 2.5 PFLOP/s dense bf16 MFMA peak; HBM traffic from the committed rocprofv3 counter
+    summary when it was taken on the current kernel source;
+  * cpu_baseline: the float64 oracle on this host's cores on a bounded sample (the covariances
+    on the first --cpu-tokens tokens, scaled linearly to N; every other step at full size).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "seconds per layer quantised (cov+rotate+OBS) at 8B/70B shapes; % MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0
+DOMINANT = "syrk_bf16_mfma"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "syrk_bf16_traffic.json")
+KERNELS = ["syrk_bf16_mfma", "syrk_reduce", "traces", "rot_w_norms", "rot_factors",
+           "rot_row_pass", "fwht_col", "mix28_col", "chol_diag_shift", "chol_add_diag",
+           "chol_reverse_copy", "chol_potrf_diag", "chol_trsm", "chol_syrk", "trtri_row",
+           "trtri_put_diag", "trtri_update", "chol_reverse_out", "obs_sweep",
+           "obs_trailing_update"]
+WORKLOADS = {"q_proj": 2, "down_proj": 3, "up_proj_70b": 4}
+
+
+def cov_source_hash() -> str:
+    with open(os.path.join(ROOT, "paper_2607_07964_amd", "csrc", "cov.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic(launch_bytes_alg: float):
+    """HBM bytes per launch from the rocprofv3 FETCH_SIZE/WRITE_SIZE summary (or None)."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    t = json.load(open(TRAFFIC_FILE))
+    if t.get("cov_source_sha256_16") != cov_source_hash():
+        return None  # counters were taken on another version of the kernel
+    return float(t["bytes_per_launch"])
+
+
+def cpu_baseline(spec, rot_in, rot_out, n_sample: int, X_dev, G_dev, W_dev):
+    import numpy as np
+    import oracle as O
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+
+    def view(t):
+        t = t.cpu()
+        return synth.bf16_bits(t) if str(t.dtype) == "torch.bfloat16" else t.numpy()
+
+    Xs, Gs, W = view(X_dev[:n_sample]), view(G_dev[:n_sample]), view(W_dev)
+    t0 = time.perf_counter()
+    hx = O.covariance(Xs)
+    hg = O.covariance(Gs)
+    t_cov = time.perf_counter() - t0
+    t1 = time.perf_counter()
+    O.traces(hx, hg)
+    b = O.biip_forward(W, hx, hg, (rot_in.sign, rot_in.q28), (rot_out.sign, rot_out.q28))
+    O.traces(b["HX"], b["HG"])
+    U = O.inverse_cholesky_factor(O.damp(b["HX"], spec.damp))
+    O.obs_blocked(b["W"], U, spec.bits, 128, 128)
+    t_rest = time.perf_counter() - t1
+    scale = spec.n_tokens / n_sample
+    return {
+        "value": t_cov * scale + t_rest, "unit": "s/layer", "cores": int(cores), "kind": "oracle",
+        "sample": (f"float64 oracle: covariances on the first {n_sample} of {spec.n_tokens} tokens "
+                   f"({t_cov:.2f} s, scaled x{scale:g}); traces, BiIP with dense rotations, "
+                   f"factor and blocked OBS sweep at full size ({t_rest:.2f} s)"),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="q_proj")
+    ap.add_argument("--cpu-tokens", type=int, default=16384)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true", help="per-kernel times (stderr)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md for how the layer solve would shard).", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import synth
+    from paper_2607_07964_amd import kronq as K
+    from paper_2607_07964_amd import layer as L
+
+    K.load()
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    spec = synth.workload(WORKLOADS[args.workload])
+    print(f"[bench] generating {spec.name}: W {spec.d_out}x{spec.d_in}, N={spec.n_tokens}",
+          file=sys.stderr, flush=True)
+    X = synth.gen_matrix(spec.x, dev)
+    G = synth.gen_matrix(spec.g, dev)
+    W0 = synth.gen_matrix(spec.w, dev)
+    ri = synth.rotation_params(spec.d_in, spec.seed, spec.name + ":in")
+    ro = synth.rotation_params(spec.d_out, spec.seed, spec.name + ":out")
+    rin = L.RotParams.to_device(ri.sign, ri.q28, dev)
+    rout = L.RotParams.to_device(ro.sign, ro.q28, dev)
+    st = L.LayerState.allocate(spec.d_out, spec.d_in, spec.n_tokens, dev, x_dtype=X.dtype,
+                               g_dtype=G.dtype)
+    torch.cuda.synchronize()
+
+    def step():
+        L.quantize_layer(st, X, G, W0, rin, rout, spec.bits, spec.damp)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    L.check(st)
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    K.kronq_profile_only(DOMINANT)
+    K.kronq_profile_reset()
+    K.kronq_profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    K.kronq_profile_enable(False)
+    syrk_ms, syrk_n = K.kronq_profile_read(DOMINANT)
+    L.check(st)
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # dominant kernel roofline: algorithmic flops N d (d + 1) per covariance launch
+    flops = float(spec.n_tokens) * (spec.d_in * (spec.d_in + 1) + spec.d_out * (spec.d_out + 1)) / 2
+    avg_ms = syrk_ms / max(syrk_n, 1)
+    achieved = flops / (avg_ms * 1e-3) / 1e12
+    roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic(flops), "kernel": DOMINANT, "launches": syrk_n,
+            "avg_launch_ms": round(avg_ms, 4)}
+
+    breakdown = None
+    if args.breakdown:
+        K.kronq_profile_only(None)
+        K.kronq_profile_reset()
+        K.kronq_profile_enable(True)
+        step()
+        torch.cuda.synchronize()
+        K.kronq_profile_enable(False)
+        breakdown = {}
+        for k in KERNELS:
+            ms, n = K.kronq_profile_read(k)
+            if n:
+                breakdown[k] = {"ms": round(ms, 4), "launches": n}
+        print("[bench] per-kernel (one profiled step): " + json.dumps(breakdown), file=sys.stderr)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the float64 oracle on the host (bounded sample)", file=sys.stderr,
+              flush=True)
+        cpu = cpu_baseline(spec, ri, ro, min(args.cpu_tokens, spec.n_tokens), X, G, W0)
+
+    out = {
+        "metric": METRIC, "value": round(ms_step / 1e3, 6), "unit": "s/layer", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16 (covariances, MFMA) + fp32 (rotations, factor, OBS)", "data": "synthetic",
+        "config": {"workload": f"{spec.name} W {spec.d_out}x{spec.d_in}, N={spec.n_tokens} tokens, "
+                               f"{spec.bits}-bit, group {spec.group}",
+                   "d_out": spec.d_out, "d_in": spec.d_in, "n_tokens": spec.n_tokens,
+                   "bits": spec.bits, "group": spec.group, "block": 128, "damp": spec.damp,
+                   "parallelism": "single GPU"},
+        "roofline": roof, "cpu_baseline": cpu,
+    }
+    if breakdown is not None:
+        out["kernels_ms"] = breakdown
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -180,6 +180,9 @@ int kronq_allocate_bits(const double* scores, const int64_t* weights, int n_laye
  * synchronises the recorded events and returns the summed milliseconds and the launch count
  * of the named kernel (0 if never launched). Not thread-safe; meant for benchmarks. */
 int kronq_profile_enable(int on);
+/* Restrict the profiler to launches of one kernel name (NULL or "": every kernel), so that
+ * timing one kernel adds no events around the others. */
+int kronq_profile_only(const char* kernel);
 void kronq_profile_reset(void);
 int kronq_profile_read(const char* kernel, double* total_ms, int64_t* launches);
 

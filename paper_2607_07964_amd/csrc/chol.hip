@@ -56,66 +56,104 @@ __global__ void reverse_copy(const float* __restrict__ H, int64_t d, int64_t ldh
   }
 }
 
-// Factor the diagonal block M[kb:kb+bs, kb:kb+bs] (lower) in LDS and invert it.
-// Writes L_kk back to M (lower part) and Linv_kk (bs x bs, zero above the diagonal) to dinv.
+// Factor the diagonal block M[kb:kb+bs, kb:kb+bs] (lower) and invert the factor, in one
+// workgroup, in a single pass over the columns j = 0..bs-1. Thread (ty, tx) of a 16 x 16 grid
+// keeps entries (ty + 16 p, tx + 16 q), p, q < 8, of two matrices in registers:
+//   r: the trailing matrix of the right-looking factorisation (entries above the diagonal ride
+//      along unused), updated by the rank-1 term of column j;
+//   y: R = I - (already eliminated terms), turned into rows of Y = L^-1 by forward
+//      substitution: at step j, Y[j, :] = R[j, :] / L_jj, then R[i, :] -= L_ij Y[j, :] for i > j.
+// Column j of the trailing matrix and row j of Y are exchanged through LDS, two barriers per
+// column. Writes L_kk to M (lower part), Linv_kk (exact zeros above the diagonal) to dinv and X.
 __global__ __launch_bounds__(256) void potrf_diag(float* __restrict__ M, int64_t ldm, int64_t kb,
                                                   int bs, int64_t d, float* __restrict__ dinv,
-                                                  int* __restrict__ info) {
-  __shared__ float a[NB * DLD];
-  __shared__ float x[NB * DLD];  // column c of the inverse lives in x[.][c]
+                                                  float* __restrict__ X, int* __restrict__ info) {
+  __shared__ float l[NB * DLD];   // the factor L
+  __shared__ float col[2][NB];    // column j of the trailing matrix
+  __shared__ float yrow[NB];      // row j of Y
   const int tid = threadIdx.x;
-  for (int idx = tid; idx < bs * bs; idx += 256) {
-    const int i = idx / bs, j = idx % bs;
-    a[i * DLD + j] = M[(kb + i) * ldm + kb + j];
+  const int tx = tid & 15, ty = tid >> 4;
+  float r[8][8], y[8][8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int i = ty + 16 * p, j = tx + 16 * q;
+      r[p][q] = (i < bs && j < bs) ? M[(kb + i) * ldm + kb + j] : 0.f;
+      y[p][q] = (i == j) ? 1.f : 0.f;
+    }
+  if (tx == 0) {
+#pragma unroll
+    for (int p = 0; p < 8; ++p) col[0][ty + 16 * p] = r[p][0];
   }
   __syncthreads();
   for (int j = 0; j < bs; ++j) {
-    const float piv = a[j * DLD + j];
+    const float* cj = col[j & 1];
+    const float piv = cj[j];
     if (!(piv > 0.f) && tid == 0) atomicCAS(info, 0, int(d - (kb + j)));  // also catches NaN
     const float ljj = sqrtf(piv);
-    __syncthreads();
-    if (tid == 0) a[j * DLD + j] = ljj;
-    for (int i = j + 1 + tid; i < bs; i += 256) a[i * DLD + j] /= ljj;
-    __syncthreads();
-    const int n = bs - j - 1;  // trailing order
-    for (int idx = tid; idx < n * n; idx += 256) {
-      const int i = j + 1 + idx / n, c = j + 1 + idx % n;
-      if (c <= i) a[i * DLD + c] -= a[i * DLD + j] * a[c * DLD + j];
+    const float rl = 1.f / ljj;
+    if (tid >= j && tid < bs) l[tid * DLD + j] = (tid == j) ? ljj : cj[tid] * rl;
+    // row j of Y from its owners
+    if (ty == (j & 15)) {
+#pragma unroll
+      for (int p = 0; p < 8; ++p)
+        if (p == (j >> 4)) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            y[p][q] *= rl;
+            yrow[tx + 16 * q] = y[p][q];
+          }
+        }
     }
     __syncthreads();
-  }
-  // inverse: thread c solves L x = e_c; rows in order, all threads read the same L entries
-  if (tid < bs) {
-    const int c = tid;
-    for (int i = 0; i < bs; ++i) {
-      float v;
-      if (i < c) {
-        v = 0.f;
-      } else if (i == c) {
-        v = 1.f / a[i * DLD + i];
-      } else {
-        float s = 0.f;
-        for (int k = c; k < i; ++k) s = fmaf(a[i * DLD + k], x[k * DLD + c], s);
-        v = -s / a[i * DLD + i];
+    float lc[8], cc[8], yj[8];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      lc[p] = cj[ty + 16 * p] * rl;  // L[i][j] for this thread's rows
+      cc[p] = cj[tx + 16 * p];
+      yj[p] = yrow[tx + 16 * p];
+    }
+    // row blocks p < j / 16 hold only finished rows: skip them (a wave-uniform branch); the
+    // block containing row j is masked per row, later blocks are updated unconditionally
+    const int jb = j >> 4;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      if (p < jb) continue;
+      const float f = -lc[p] * rl;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) r[p][q] = fmaf(f, cc[q], r[p][q]);
+      if (p > jb) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) y[p][q] = fmaf(-lc[p], yj[q], y[p][q]);
+      } else if (ty > (j & 15)) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) y[p][q] = fmaf(-lc[p], yj[q], y[p][q]);
       }
-      x[i * DLD + c] = v;
     }
+    const int jn = j + 1;
+    if (jn < bs && tx == (jn & 15)) {
+      float* cn = col[jn & 1];
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (q == (jn >> 4)) {
+#pragma unroll
+          for (int p = 0; p < 8; ++p) cn[ty + 16 * p] = r[p][q];
+        }
+    }
+    __syncthreads();
   }
-  __syncthreads();
-  for (int idx = tid; idx < bs * bs; idx += 256) {
-    const int i = idx / bs, j = idx % bs;
-    if (j <= i) M[(kb + i) * ldm + kb + j] = a[i * DLD + j];
-    dinv[i * NB + j] = x[i * DLD + j];
-  }
-}
-
-// X[kb:kb+bs, kb:kb+bs] = Linv_kk (full block, zeros above the diagonal)
-__global__ void put_diag(float* __restrict__ X, int64_t ldm, int64_t kb, int bs,
-                         const float* __restrict__ dinv) {
-  for (int idx = threadIdx.x; idx < bs * bs; idx += blockDim.x) {
-    const int i = idx / bs, j = idx % bs;
-    X[(kb + i) * ldm + kb + j] = dinv[i * NB + j];
-  }
+#pragma unroll
+  for (int p = 0; p < 8; ++p)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int i = ty + 16 * p, j = tx + 16 * q;
+      if (i < bs && j < bs) {
+        if (j <= i) M[(kb + i) * ldm + kb + j] = l[i * DLD + j];
+        dinv[i * NB + j] = y[p][q];
+        X[(kb + i) * ldm + kb + j] = y[p][q];
+      }
+    }
 }
 
 // U[i][j] = X[d-1-i][d-1-j] for i <= j, else 0
@@ -163,7 +201,7 @@ int chol_launch(float* H, int64_t d, int64_t ldh, float damp_rel, float* U, int6
     const int bs = int(d - kb < NB ? d - kb : NB);
     float* dk = dinv + k * NB * NB;
     KQ_TRY(launch("chol_potrf_diag", potrf_diag, dim3(1), dim3(256), 0, s, M, ld, kb, bs, d, dk,
-                  info));
+                  X, info));
     const int64_t rest = d - kb - bs;
     if (rest > 0) {
       float* P = M + (kb + bs) * ld + kb;
@@ -186,7 +224,6 @@ int chol_launch(float* H, int64_t d, int64_t ldh, float damp_rel, float* U, int6
       KQ_TRY(gemm_f32(GEMM_A_LOWER, bs, kb, bs, 1.f, dk, NB, Xk, ld, 0.f, Xk, ld, s,
                       "trtri_row"));
     }
-    KQ_TRY(launch("trtri_put_diag", put_diag, dim3(1), dim3(256), 0, s, X, ld, kb, bs, dk));
     const int64_t rest = d - kb - bs;
     if (rest > 0) {
       // Y[kb+bs:, :kb+bs] -= L[kb+bs:, kb:kb+bs] X[k, :kb+bs]

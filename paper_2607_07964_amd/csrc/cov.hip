@@ -3,19 +3,19 @@
 // bf16 path: a syrk on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16). bf16 x bf16 products
 // are exact in fp32 and accumulate in fp32.
 //   * Work split: the token dimension is cut into S slices (split-K). Workgroup b takes slice
-//     b % S, so with S = 8 each XCD (workgroups are dealt round-robin over the 8 XCDs) streams
+//     b % S; workgroups are dealt round-robin over the 8 XCDs, so with S = 8 each XCD streams
 //     its own eighth of the tokens and every tile on that XCD reuses it through the XCD's L2.
 //   * Each workgroup owns one 256 x 256 tile (I <= J) of the upper triangle of H for its slice:
 //     4 waves, each a 128 x 128 sub-tile = 4 x 4 MFMA blocks of 32 x 32, 256 fp32
 //     accumulators per lane.
-//   * Per stage, 64 tokens x 256 columns of each operand are loaded as 8 x 8 bf16 blocks
-//     (eight 16-byte loads along the channel axis), transposed in registers with v_perm, and
-//     written token-contiguous to LDS with 16-byte stores. An MFMA operand is then a single
-//     16-byte LDS read. The LDS row stride of 72 bf16 (36 dwords) makes both the stores and
-//     the operand reads conflict-free. LDS is double-buffered: the loads for stage s+1 are in
-//     flight while stage s runs, one barrier per stage. A diagonal tile loads one operand.
-//   * Partial tiles go to the workspace; a reduction kernel sums the S slices, applies
-//     alpha/beta and writes both triangles (the mirror through an LDS transpose).
+//   * Interior tiles (syrk_bf16_dma below) stream 32-token stages straight from HBM into a
+//     ring of LDS buffers and transpose on the LDS read. Tiles of a ragged last channel block
+//     and a ragged token tail (< 32 tokens) go through syrk_bf16_partial, which stages 64
+//     tokens through registers: 8 x 8 bf16 blocks are loaded, transposed with v_perm and
+//     written token-contiguous to LDS so that an MFMA operand is one 16-byte read.
+//   * Partial tiles go to the workspace; a reduction kernel sums the slices, applies
+//     alpha/beta and writes both triangles (the mirror through an LDS transpose), so H is
+//     exactly symmetric.
 // fp32 path (small fp32 inputs): a plain LDS-tiled fp32 FMA kernel over the full matrix.
 #include "kq_common.hpp"
 
@@ -50,12 +50,19 @@ __device__ __forceinline__ u32x4_t load_row8(const uint16_t* __restrict__ A, int
   return v;
 }
 
-// Load the 8 x 8 block (tokens t..t+7, channels col..col+7) into v[8].
+// Load the 8 x 8 block (tokens t..t+7, channels col..col+7) into v[8]. Interior blocks take
+// eight unconditional 16-byte loads; blocks at the token or channel edge are zero-filled.
 __device__ __forceinline__ void load_block(u32x4_t v[8], const uint16_t* __restrict__ A,
                                            int64_t lda, int64_t t, int64_t t_end, int64_t col,
                                            int64_t d) {
+  if (t + 8 <= t_end && col + 8 <= d) {
+    const uint16_t* p = A + t * lda + col;
 #pragma unroll
-  for (int r = 0; r < 8; ++r) v[r] = load_row8(A, lda, t + r, t_end, col, d);
+    for (int r = 0; r < 8; ++r) v[r] = *reinterpret_cast<const u32x4_t*>(p + r * lda);
+  } else {
+#pragma unroll
+    for (int r = 0; r < 8; ++r) v[r] = load_row8(A, lda, t + r, t_end, col, d);
+  }
 }
 
 // Transpose the block in registers and store channel c's 8 tokens to LDS row (rowbase + c).
@@ -76,25 +83,33 @@ __device__ __forceinline__ void store_block_t(uint32_t* __restrict__ lds, const 
 }
 
 __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
-    const uint16_t* __restrict__ A, int64_t n_rows, int64_t d, int64_t lda,
-    float* __restrict__ part, int n_slices, int64_t rows_per_slice, int T) {
+    const uint16_t* __restrict__ A, int64_t tok0, int64_t tok_end, int64_t d, int64_t lda,
+    float* __restrict__ part, int n_slices, int64_t rows_per_slice, int T, int edge_only,
+    int out_slice0) {
   __shared__ uint32_t lds[2 * 2 * OPER];  // [buffer][operand][256 rows][36 dwords]
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
   const int lane = tid & 63;
   const int slice = blockIdx.x % n_slices;
-  const int pos = blockIdx.x / n_slices;
-  int I = 0, rem = pos;
-  while (rem >= T - I) {
-    rem -= T - I;
-    ++I;
+  int I, J;
+  if (edge_only) {  // tiles of the last (ragged) column block: (I, T-1), I = 0..T-1
+    I = blockIdx.x / n_slices;
+    J = T - 1;
+  } else {
+    int rem = blockIdx.x / n_slices;
+    I = 0;
+    while (rem >= T - I) {
+      rem -= T - I;
+      ++I;
+    }
+    J = I + rem;
   }
-  const int J = I + rem;
+  const int64_t pos = int64_t(I) * T - int64_t(I) * (I - 1) / 2 + (J - I);
   const bool diag = (I == J);
   const int64_t i0 = int64_t(I) * TT, j0 = int64_t(J) * TT;
-  const int64_t t_begin = int64_t(slice) * rows_per_slice;
-  const int64_t t_end = min(n_rows, t_begin + rows_per_slice);
+  const int64_t t_begin = tok0 + int64_t(slice) * rows_per_slice;
+  const int64_t t_end = min(tok_end, t_begin + rows_per_slice);
   const int64_t n_st = t_end > t_begin ? cdiv(t_end - t_begin, KC) : 0;
 
   // loader role: token group tg (8 tokens), channel group ig (8 channels)
@@ -119,6 +134,20 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
   }
   __syncthreads();
 
+  // MFMA operand fragments, double-buffered across the 16-token steps of a stage so that the
+  // LDS reads of step ks+1 are in flight while the 16 MFMAs of step ks run
+  bf16x8_t fa[2][4], fb[2][4];
+  auto frags = [&](const uint32_t* sa, const uint32_t* sb, int ks, int slot) {
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi)
+      fa[slot][bi] = *reinterpret_cast<const bf16x8_t*>(
+          sa + (wm * 128 + bi * 32 + l32) * LROW + ks * 8 + lhi * 4);
+#pragma unroll
+    for (int bj = 0; bj < 4; ++bj)
+      fb[slot][bj] = *reinterpret_cast<const bf16x8_t*>(
+          sb + (wn * 128 + bj * 32 + l32) * LROW + ks * 8 + lhi * 4);
+  };
+
   for (int64_t st = 0; st < n_st; ++st) {
     const int buf = int(st & 1);
     const bool more = st + 1 < n_st;
@@ -129,24 +158,20 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
     }
     const uint32_t* sa = lds + buf * 2 * OPER;
     const uint32_t* sb = diag ? sa : sa + OPER;
+    frags(sa, sb, 0, 0);
 #pragma unroll
     for (int ks = 0; ks < KC / 16; ++ks) {
-      bf16x8_t fa[4], fb[4];
-#pragma unroll
-      for (int bi = 0; bi < 4; ++bi) {
-        const int row = wm * 128 + bi * 32 + l32;
-        fa[bi] = *reinterpret_cast<const bf16x8_t*>(sa + row * LROW + ks * 8 + lhi * 4);
-      }
-#pragma unroll
-      for (int bj = 0; bj < 4; ++bj) {
-        const int row = wn * 128 + bj * 32 + l32;
-        fb[bj] = *reinterpret_cast<const bf16x8_t*>(sb + row * LROW + ks * 8 + lhi * 4);
-      }
+      if (ks + 1 < KC / 16) frags(sa, sb, ks + 1, (ks + 1) & 1);
+      // keep the next step's LDS reads ahead of this step's MFMAs (the scheduler would
+      // otherwise sink each read next to its first use and expose its latency)
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
         for (int bj = 0; bj < 4; ++bj)
-          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[bi], fb[bj], acc[bi][bj], 0, 0, 0);
+          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks & 1][bi], fb[ks & 1][bj],
+                                                                acc[bi][bj], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (more) {
       uint32_t* dst = lds + (buf ^ 1) * 2 * OPER;
@@ -158,7 +183,162 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
 
   // partial tile, row-major 256 x 256 (rows: channels i of the tile, cols: channels j)
   const int64_t npos = int64_t(T) * (T + 1) / 2;
+  float* out = part + (int64_t(out_slice0 + slice) * npos + pos) * (TT * TT);
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 4; ++bj)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = wm * 128 + bi * 32 + (r >> 2) * 8 + lhi * 4 + (r & 3);
+        const int col = wn * 128 + bj * 32 + l32;
+        out[row * TT + col] = acc[bi][bj][r];
+      }
+}
+
+
+// ---- interior tiles: direct-to-LDS loads and transposing LDS reads ---------------------------
+// Stage = 32 tokens x 256 channels per operand (16 KB), kept in a ring of 4 LDS buffers filled by
+// global_load_lds_dwordx4 (64 lanes x 16 bytes straight into LDS, no VGPR staging), so loads run
+// three stages ahead. The LDS image is token-major with the 16-byte chunk c8 of token row t
+// stored at position c8 ^ (4 (t & 3)); this spreads the rows a transposing read touches over all
+// banks. An MFMA operand (32 channels x 8 tokens per lane) is two ds_read_b64_tr_b16: within a
+// group of 16 lanes, lane L names token row tb + L/4 at channels cb + 4 (L % 4) .. +3 and gets
+// back its own channel cb + L at tokens tb .. tb+3.
+// Per stage: 16 MFMAs on the first 16 tokens, then one raw s_barrier (after this wave's own
+// loads for the next stage have landed, s_waitcnt vmcnt), which both publishes the next stage
+// and frees the oldest buffer for the next load, then 16 MFMAs on the last 16 tokens while the
+// next stage's first operands are read. A diagonal tile loads its block into both operand rings
+// so that no buffer is chosen at run time (which would force full waits on every load).
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+#define KQ_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+constexpr int DK = 32;        // tokens per stage
+constexpr int SBUF = 4096;    // dwords per operand per stage
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  // s_waitcnt vmcnt(N) with expcnt / lgkmcnt left unconstrained (gfx9 encoding)
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ bf16x8_t tr_frag(const uint32_t* buf, int tb, int cb, int lane) {
+  const int L = lane & 15, g = (lane >> 4) & 1, kh = lane >> 5;
+  const int c8 = (cb + g * 16 + 4 * (L & 3)) >> 3;
+  v4s_t r[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int t = tb + kh * 8 + h * 4 + (L >> 2);
+    const int byte = t * 512 + ((c8 ^ (4 * (t & 3))) << 4) + 8 * (L & 1);
+    r[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4s_t*)((const char*)buf + byte));
+  }
+  bf16x8_t out;
+  __builtin_memcpy(&out, r, 16);
+  return out;
+}
+
+__global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restrict__ A,
+                                                        int64_t n_rows, int64_t lda,
+                                                        float* __restrict__ part, int n_slices,
+                                                        int64_t rows_per_slice, int T, int Tf) {
+  __shared__ __attribute__((aligned(16))) uint32_t a0[SBUF], a1[SBUF], a2[SBUF], a3[SBUF];
+  __shared__ __attribute__((aligned(16))) uint32_t b0[SBUF], b1[SBUF], b2[SBUF], b3[SBUF];
+  uint32_t* const bufa[4] = {a0, a1, a2, a3};
+  uint32_t* const bufb[4] = {b0, b1, b2, b3};
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int slice = blockIdx.x % n_slices;
+  int I = 0, rem = blockIdx.x / n_slices;
+  while (rem >= Tf - I) {
+    rem -= Tf - I;
+    ++I;
+  }
+  const int J = I + rem;
+  const int64_t pos = int64_t(I) * T - int64_t(I) * (I - 1) / 2 + (J - I);
+  const int64_t t_begin = int64_t(slice) * rows_per_slice;
+  const int64_t t_end = min(n_rows, t_begin + rows_per_slice);
+  const int n_st = t_end > t_begin ? int((t_end - t_begin) / DK) : 0;  // full stages
+  int64_t off[4];  // this lane's source offsets (elements) for its 4 chunks per operand
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int q = (wave * 4 + k) * 64 + lane;
+    const int t = q >> 5, c8 = (q & 31) ^ (4 * (t & 3));
+    off[k] = int64_t(t) * lda + 8 * c8;
+  }
+  const uint16_t* Ai = A + t_begin * lda + int64_t(I) * TT;
+  const uint16_t* Aj = A + t_begin * lda + int64_t(J) * TT;
+  auto issue = [&](int st, int b) {
+    const int64_t so = int64_t(st) * DK * lda;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      __builtin_amdgcn_global_load_lds(Ai + so + off[k], KQ_LDS(bufa[b] + (wave * 4 + k) * 256),
+                                       16, 0, 0);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      __builtin_amdgcn_global_load_lds(Aj + so + off[k], KQ_LDS(bufb[b] + (wave * 4 + k) * 256),
+                                       16, 0, 0);
+  };
+  const int wm = wave & 1, wn = wave >> 1;
+  f32x16_t acc[4][4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) acc[x][y] = f32x16_t{};
+  bf16x8_t fa[2][4], fb[2][4];
+  auto frags = [&](int b, int ks, int slot) {
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi) fa[slot][bi] = tr_frag(bufa[b], ks * 16, wm * 128 + bi * 32, lane);
+#pragma unroll
+    for (int bj = 0; bj < 4; ++bj) fb[slot][bj] = tr_frag(bufb[b], ks * 16, wn * 128 + bj * 32, lane);
+  };
+  auto mfmas = [&](int slot) {
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj)
+        acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][bi], fb[slot][bj],
+                                                              acc[bi][bj], 0, 0, 0);
+  };
+  // this wave's loads of a stage are done when at most `later` newer stages are outstanding
+  auto wait_stage = [&](int later) {
+    if (later >= 2)
+      wait_vm<16>();
+    else if (later == 1)
+      wait_vm<8>();
+    else
+      wait_vm<0>();
+  };
+  if (n_st > 0) {
+    issue(0, 0);
+    if (n_st > 1) issue(1, 1);
+    if (n_st > 2) issue(2, 2);
+    wait_stage(n_st > 2 ? 2 : n_st - 1);
+    __builtin_amdgcn_s_barrier();
+    frags(0, 0, 0);
+  }
+  for (int s0 = 0; s0 < n_st; s0 += 4) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int s = s0 + u;  // stage s lives in buffer u
+      if (s < n_st) {
+        frags(u, 1, 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (s + 1 < n_st) {
+          wait_stage(s + 2 < n_st ? 1 : 0);
+          __builtin_amdgcn_s_barrier();
+          if (s + 3 < n_st) issue(s + 3, (u + 3) & 3);
+          frags((u + 1) & 3, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+  const int64_t npos = int64_t(T) * (T + 1) / 2;
   float* out = part + (int64_t(slice) * npos + pos) * (TT * TT);
+  const int l32 = lane & 31, lhi = lane >> 5;
 #pragma unroll
   for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
@@ -296,20 +476,27 @@ __global__ void scale_matrix(float* __restrict__ H, int64_t d, int64_t ldh, floa
 }
 
 struct CovPlan {
-  int T = 0;
-  int S = 0;
+  int T = 0;    // 256-channel blocks (the last may be ragged)
+  int Tf = 0;   // full 256-channel blocks
+  int S = 0;    // token slices (one per XCD when there are enough tokens)
   int64_t rows_per_slice = 0;
   int64_t npos = 0;
+  int64_t tail_begin = 0;  // tokens [tail_begin, n_rows) do not fill a 32-token stage
+  bool tail = false;
 };
 
 CovPlan cov_plan(int64_t n_rows, int64_t d) {
   CovPlan p;
   p.T = int(cdiv(d, TT));
+  p.Tf = int(d / TT);
   p.npos = int64_t(p.T) * (p.T + 1) / 2;
-  // one token slice per XCD when there are enough tokens; fewer slices for short inputs
   int64_t s = n_rows / (4 * KC);
   p.S = int(s < 1 ? 1 : (s > 8 ? 8 : s));
   p.rows_per_slice = cdiv(cdiv(n_rows, p.S), KC) * KC;
+  const int64_t last = int64_t(p.S - 1) * p.rows_per_slice;
+  const int64_t in_last = n_rows > last ? n_rows - last : 0;
+  p.tail_begin = last + (in_last / DK) * DK;
+  p.tail = p.tail_begin < n_rows;
   return p;
 }
 
@@ -318,7 +505,7 @@ CovPlan cov_plan(int64_t n_rows, int64_t d) {
 size_t cov_ws_bytes(int dtype, int64_t n_rows, int64_t d) {
   if (dtype != KRONQ_BF16 || n_rows <= 0 || d <= 0) return 0;
   const CovPlan p = cov_plan(n_rows, d);
-  return align256(size_t(p.S) * size_t(p.npos) * TT * TT * sizeof(float));
+  return align256(size_t(p.S + 1) * size_t(p.npos) * TT * TT * sizeof(float));
 }
 
 int cov_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda, float* H,
@@ -333,12 +520,25 @@ int cov_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
                   static_cast<const float*>(A), n_rows, d, lda, H, ldh, alpha, beta);
   }
   const CovPlan p = cov_plan(n_rows, d);
+  const uint16_t* X = static_cast<const uint16_t*>(A);
   float* part = static_cast<float*>(ws);
-  KQ_TRY(launch("syrk_bf16_mfma", syrk_bf16_partial, dim3(unsigned(p.S * p.npos)), dim3(256), 0, s,
-                static_cast<const uint16_t*>(A), n_rows, d, lda, part, p.S, p.rows_per_slice,
-                p.T));
+  // interior tiles, whole 32-token stages of every slice
+  if (p.Tf > 0)
+    KQ_TRY(launch("syrk_bf16_mfma", syrk_bf16_dma,
+                  dim3(unsigned(int64_t(p.S) * p.Tf * (p.Tf + 1) / 2)), dim3(256), 0, s, X, n_rows,
+                  lda, part, p.S, p.rows_per_slice, p.T, p.Tf));
+  // tiles of a ragged last channel block, same tokens
+  const int64_t body_end = p.tail ? p.tail_begin : n_rows;
+  if (p.T > p.Tf)
+    KQ_TRY(launch("syrk_bf16_edge", syrk_bf16_partial, dim3(unsigned(p.S * p.T)), dim3(256), 0, s,
+                  X, int64_t(0), body_end, d, lda, part, p.S, p.rows_per_slice, p.T, 1, 0));
+  // the last < 32 tokens, every tile, as one extra slice
+  if (p.tail)
+    KQ_TRY(launch("syrk_bf16_tail", syrk_bf16_partial, dim3(unsigned(p.npos)), dim3(256), 0, s,
+                  X, p.tail_begin, n_rows, d, lda, part, 1, n_rows - p.tail_begin, p.T, 0, p.S));
   return launch("syrk_reduce", syrk_reduce, dim3(unsigned(p.npos * 16)), dim3(256), 0, s,
-                static_cast<const float*>(part), p.S, p.T, d, H, ldh, alpha, beta);
+                static_cast<const float*>(part), p.S + (p.tail ? 1 : 0), p.T, d, H, ldh, alpha,
+                beta);
 }
 
 }  // namespace kq

@@ -41,6 +41,7 @@ void clear_error();
 
 // ---- profiler: optional hipEvent pair around every launch ----------------------------------
 bool prof_on();
+bool prof_wants(const char* name);
 void prof_begin(const char* name, hipStream_t s);
 void prof_end(const char* name, hipStream_t s);
 
@@ -57,7 +58,7 @@ int launch(const char* name, Kernel kernel, dim3 grid, dim3 block, size_t shmem,
       return KRONQ_ERR_HIP;
     }
   }
-  const bool p = prof_on();
+  const bool p = prof_on() && prof_wants(name);
   if (p) prof_begin(name, s);
   hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
   hipError_t e = hipGetLastError();

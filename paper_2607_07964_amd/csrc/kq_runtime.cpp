@@ -22,6 +22,7 @@ struct ProfEntry {
   int64_t launches = 0;
 };
 bool g_prof = false;
+std::string g_prof_only;  // empty: every kernel; else only kernels with exactly this name
 std::map<std::string, ProfEntry> g_prof_tab;
 std::vector<hipEvent_t> g_event_pool;
 hipEvent_t g_open = nullptr;
@@ -63,6 +64,8 @@ void clear_error() { g_err[0] = '\0'; }
 
 bool prof_on() { return g_prof; }
 
+bool prof_wants(const char* name) { return g_prof_only.empty() || g_prof_only == name; }
+
 void prof_begin(const char* name, hipStream_t s) {
   (void)name;
   g_open = take_event();
@@ -100,6 +103,11 @@ int kronq_version(void) { return 100; }
 
 int kronq_profile_enable(int on) {
   kq::g_prof = on != 0;
+  return KRONQ_OK;
+}
+
+int kronq_profile_only(const char* kernel) {
+  kq::g_prof_only = kernel ? kernel : "";
   return KRONQ_OK;
 }
 

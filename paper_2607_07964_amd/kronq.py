@@ -27,8 +27,8 @@ ERRORS = {0: "OK", -1: "INVALID_ARG", -2: "SHAPE", -3: "NOT_PD", -4: "HIP", -5: 
 EXPORTS = (
     "kronq_workspace_bytes", "kronq_last_error", "kronq_version", "kronq_accumulate_cov",
     "kronq_traces", "kronq_rotate", "kronq_cholesky_inv", "kronq_obs_quantize_layer",
-    "kronq_layer_loss", "kronq_allocate_bits", "kronq_profile_enable", "kronq_profile_reset",
-    "kronq_profile_read",
+    "kronq_layer_loss", "kronq_allocate_bits", "kronq_profile_enable", "kronq_profile_only",
+    "kronq_profile_reset", "kronq_profile_read",
 )
 
 
@@ -65,6 +65,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_layer_loss": (I, [P, I, I64, P, I64, I64, I64, P, I64, P, I64, P, P, SZ, P]),
         "kronq_allocate_bits": (I, [P, P, I, P, I, D, P, P]),
         "kronq_profile_enable": (I, [I]),
+        "kronq_profile_only": (I, [ctypes.c_char_p]),
         "kronq_profile_reset": (None, []),
         "kronq_profile_read": (I, [ctypes.c_char_p, P, P]),
     }
@@ -233,6 +234,11 @@ def kronq_allocate_bits(scores, weights, choices=(2, 3, 4), avg_bits: float = 3.
 # ------------------------------------------------------------------------------------ profiler
 def kronq_profile_enable(on: bool = True):
     _check(load().kronq_profile_enable(int(on)), "kronq_profile_enable")
+
+
+def kronq_profile_only(kernel: Optional[str]):
+    _check(load().kronq_profile_only(None if kernel is None else kernel.encode()),
+           "kronq_profile_only")
 
 
 def kronq_profile_reset():
