@@ -98,6 +98,8 @@ def main() -> int:
     ap.add_argument("--cpu-tokens", type=int, default=16384)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="per-kernel times (stderr)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run 3 plain 1 GiB device copies (reference for counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -113,6 +115,14 @@ def main() -> int:
     K.load()
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        print("[bench] calibration copies done: 3 x 1 GiB", file=sys.stderr, flush=True)
     spec = synth.workload(WORKLOADS[args.workload])
     print(f"[bench] generating {spec.name}: W {spec.d_out}x{spec.d_in}, N={spec.n_tokens}",
           file=sys.stderr, flush=True)
