@@ -61,6 +61,15 @@ extern "C" {
 #define KRONQ_ROT_OUT 8      /* U: W <- U W, H_G <- U H_G U^T                 (eq. biip)    */
 #define KRONQ_INVERSE 16     /* revert W only: W <- S_G^-1 U^T W V S_X^-1     (Alg. 2, last line) */
 #define KRONQ_BIIP (KRONQ_RESCALE_IN | KRONQ_RESCALE_OUT | KRONQ_ROT_IN | KRONQ_ROT_OUT)
+/* Split forms of the forward transform, so that the H_X side (which the factorisation needs)
+ * can run as soon as H_X exists while H_G is still being accumulated:
+ *   KRONQ_HX_ONLY:  compute sx (from W_in and diag H_X) and transform H_X only; W (may be NULL),
+ *                   H_G and sg are not touched.
+ *   KRONQ_SX_GIVEN: sx is an input (from a KRONQ_HX_ONLY call with the same W_in); compute sg and
+ *                   transform W and H_G; H_X is not touched (may be NULL).
+ * HX_ONLY followed by SX_GIVEN gives exactly the result of one call without either flag. */
+#define KRONQ_HX_ONLY 32
+#define KRONQ_SX_GIVEN 64
 
 /* ---- workspace queries ------------------------------------------------------------------- */
 #define KRONQ_OP_COV 1
@@ -98,6 +107,9 @@ int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, in
  *   HX device fp32 [d_in x ldx]; HG device fp32 [d_out x ldg]; out3 device double[3]. */
 int kronq_traces(const float* HX, int64_t d_in, int64_t ldx, const float* HG, int64_t d_out,
                  int64_t ldg, double* out3, void* stream);
+/* Either matrix may be NULL: its slot of out3 is then taken as already holding that trace
+ * (written by an earlier call on the same out3, ordered before this one), and out3[2] is the
+ * product of the two slots. This lets the two traces be taken on different streams. */
 
 /* ---- 3. bidirectional incoherence processing (Sec. 4.2 eqs. rescale, biip; Alg. 1) -------
  * Forward (no KRONQ_INVERSE):

@@ -90,9 +90,9 @@ int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, in
 int kronq_traces(const float* HX, int64_t d_in, int64_t ldx, const float* HG, int64_t d_out,
                  int64_t ldg, double* out3, void* stream) {
   kq::clear_error();
-  KQ_REQUIRE(HX && HG && out3, KRONQ_ERR_INVALID_ARG, "null pointer");
-  KQ_REQUIRE(d_in >= 1 && d_out >= 1 && ldx >= d_in && ldg >= d_out, KRONQ_ERR_INVALID_ARG,
-             "bad sizes");
+  KQ_REQUIRE((HX || HG) && out3, KRONQ_ERR_INVALID_ARG, "null pointer");
+  KQ_REQUIRE((!HX || (d_in >= 1 && ldx >= d_in)) && (!HG || (d_out >= 1 && ldg >= d_out)),
+             KRONQ_ERR_INVALID_ARG, "bad sizes");
   KQ_REQUIRE(aligned(out3, 8), KRONQ_ERR_INVALID_ARG, "out3 must be 8-byte aligned");
   return kq::traces_launch(HX, d_in, ldx, HG, d_out, ldg, out3, as_stream(stream));
 }
@@ -103,31 +103,35 @@ int kronq_rotate(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_
                  const float* q28_out, float* sx, float* sg, int flags, void* ws,
                  size_t ws_bytes, void* stream) {
   kq::clear_error();
-  const int known = KRONQ_BIIP | KRONQ_INVERSE;
+  const int known = KRONQ_BIIP | KRONQ_INVERSE | KRONQ_HX_ONLY | KRONQ_SX_GIVEN;
   KQ_REQUIRE((flags & ~known) == 0, KRONQ_ERR_INVALID_ARG, "unknown flag bits 0x%x",
              flags & ~known);
   KQ_REQUIRE(W_in && valid_dtype(w_dtype), KRONQ_ERR_INVALID_ARG, "bad W_in");
   KQ_REQUIRE(ldw_in >= d_in, KRONQ_ERR_INVALID_ARG, "ldw_in < d_in");
   KQ_REQUIRE(aligned(W_in, w_dtype == KRONQ_BF16 ? 2 : 4), KRONQ_ERR_INVALID_ARG,
              "W_in misaligned");
-  KQ_TRY(check_f32_mat(W, d_out, d_in, ldw, "W"));
-  KQ_REQUIRE(sx && sg && aligned(sx, 4) && aligned(sg, 4), KRONQ_ERR_INVALID_ARG,
-             "sx and sg are required");
   const bool inv = flags & KRONQ_INVERSE;
+  const bool hx_only = flags & KRONQ_HX_ONLY, sx_given = flags & KRONQ_SX_GIVEN;
+  KQ_REQUIRE(!(hx_only && sx_given) && !(inv && (hx_only || sx_given)), KRONQ_ERR_INVALID_ARG,
+             "KRONQ_HX_ONLY, KRONQ_SX_GIVEN and KRONQ_INVERSE exclude each other");
+  if (!hx_only) KQ_TRY(check_f32_mat(W, d_out, d_in, ldw, "W"));
+  KQ_REQUIRE(sx && aligned(sx, 4) && (hx_only || (sg && aligned(sg, 4))), KRONQ_ERR_INVALID_ARG,
+             "sx and sg are required");
   if (inv) {
     KQ_REQUIRE(w_dtype == KRONQ_FP32, KRONQ_ERR_INVALID_ARG, "KRONQ_INVERSE needs fp32 W_in");
     KQ_REQUIRE(ldw_in % 4 == 0 && aligned(W_in, 16), KRONQ_ERR_INVALID_ARG,
                "W_in must be 16-byte aligned with ldw_in divisible by 4");
   } else {
-    KQ_TRY(check_f32_mat(HX, d_in, d_in, ldx, "HX"));
-    if (HG) KQ_TRY(check_f32_mat(HG, d_out, d_out, ldg, "HG"));
-    KQ_REQUIRE(HG || !(flags & KRONQ_RESCALE_OUT), KRONQ_ERR_INVALID_ARG,
+    if (!sx_given) KQ_TRY(check_f32_mat(HX, d_in, d_in, ldx, "HX"));
+    if (HG && !hx_only) KQ_TRY(check_f32_mat(HG, d_out, d_out, ldg, "HG"));
+    KQ_REQUIRE(HG || hx_only || !(flags & KRONQ_RESCALE_OUT), KRONQ_ERR_INVALID_ARG,
                "KRONQ_RESCALE_OUT needs H_G");
     KQ_REQUIRE(W_in != static_cast<const void*>(W) || w_dtype == KRONQ_FP32,
                KRONQ_ERR_INVALID_ARG, "in-place rotation needs fp32 W");
   }
   if (flags & KRONQ_ROT_IN) KQ_TRY(check_rot_side(d_in, sign_in, q28_in, "input"));
-  if (flags & KRONQ_ROT_OUT) KQ_TRY(check_rot_side(d_out, sign_out, q28_out, "output"));
+  if ((flags & KRONQ_ROT_OUT) && !hx_only)
+    KQ_TRY(check_rot_side(d_out, sign_out, q28_out, "output"));
   KQ_REQUIRE(d_in <= (int64_t(1) << 24) && d_out <= (int64_t(1) << 24), KRONQ_ERR_UNSUPPORTED,
              "dimension too large");
   KQ_TRY(check_ws(ws, ws_bytes, kq::rotate_ws_bytes(d_out, d_in)));

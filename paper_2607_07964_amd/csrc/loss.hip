@@ -16,8 +16,10 @@ __global__ __launch_bounds__(256) void traces_kernel(const float* __restrict__ H
   __shared__ double rx[256], rg[256];
   const int tid = threadIdx.x;
   double sx = 0.0, sg = 0.0;
-  for (int64_t i = tid; i < d_in; i += 256) sx += HX[i * ldx + i];
-  for (int64_t i = tid; i < d_out; i += 256) sg += HG[i * ldg + i];
+  if (HX)
+    for (int64_t i = tid; i < d_in; i += 256) sx += HX[i * ldx + i];
+  if (HG)
+    for (int64_t i = tid; i < d_out; i += 256) sg += HG[i * ldg + i];
   rx[tid] = sx;
   rg[tid] = sg;
   __syncthreads();
@@ -29,9 +31,11 @@ __global__ __launch_bounds__(256) void traces_kernel(const float* __restrict__ H
     __syncthreads();
   }
   if (tid == 0) {
-    out3[0] = rx[0];
-    out3[1] = rg[0];
-    out3[2] = rx[0] * rg[0];
+    const double tx = HX ? rx[0] : out3[0];
+    const double tg = HG ? rg[0] : out3[1];
+    out3[0] = tx;
+    out3[1] = tg;
+    out3[2] = tx * tg;
   }
 }
 

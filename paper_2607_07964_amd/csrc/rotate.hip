@@ -98,6 +98,14 @@ __global__ void side_factors(int64_t n, const float* __restrict__ H, int64_t ldh
   mul_h[j] = sg / s;
 }
 
+// multipliers from a given s: s * sign
+__global__ void given_factors(int64_t n, const float* __restrict__ s, const int8_t* __restrict__ sign,
+                              float* __restrict__ mul) {
+  const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  mul[j] = s[j] * (sign ? float(sign[j]) : 1.f);
+}
+
 // inverse multipliers: sign / s
 __global__ void inv_factors(int64_t n, const float* __restrict__ s, const int8_t* __restrict__ sign,
                             float* __restrict__ mul) {
@@ -432,8 +440,10 @@ int rotate_launch(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64
                            mw_in, rot_in, ri, q28_in, true, s, "rot_row_pass");
   }
 
-  // ---- forward
-  const bool need_norms = flags & (KRONQ_RESCALE_IN | KRONQ_RESCALE_OUT);
+  // ---- forward (optionally split into the H_X half and the W / H_G half)
+  const bool hx_only = flags & KRONQ_HX_ONLY, sx_given = flags & KRONQ_SX_GIVEN;
+  const bool need_norms = ((flags & KRONQ_RESCALE_IN) && !sx_given) ||
+                          ((flags & KRONQ_RESCALE_OUT) && !hx_only);
   if (need_norms) {
     if (w_dtype == KRONQ_BF16)
       KQ_TRY(launch("rot_w_norms", w_norms<uint16_t>, dim3(unsigned(nb)), dim3(256), 0, s,
@@ -442,24 +452,32 @@ int rotate_launch(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64
       KQ_TRY(launch("rot_w_norms", w_norms<float>, dim3(unsigned(nb)), dim3(256), 0, s,
                     static_cast<const float*>(W_in), d_out, d_in, ldw_in, colp, rows));
   }
-  KQ_TRY(launch("rot_factors", side_factors, dim3(unsigned(cdiv(d_in, 256))), dim3(256), 0, s,
-                d_in, static_cast<const float*>(HX), ldx, static_cast<const double*>(colp), nb,
-                static_cast<const double*>(nullptr), rot_in ? sign_in : nullptr,
-                int((flags & KRONQ_RESCALE_IN) != 0), sx, mw_in, mh_in));
-  KQ_TRY(launch("rot_factors", side_factors, dim3(unsigned(cdiv(d_out, 256))), dim3(256), 0, s,
-                d_out, static_cast<const float*>(HG), ldg, static_cast<const double*>(nullptr),
-                int64_t(0), static_cast<const double*>(rows), rot_out ? sign_out : nullptr,
-                int((flags & KRONQ_RESCALE_OUT) != 0), sg, mw_out, mh_out));
-  // W: rescale + signs + V side (row pass), then U side (column pass)
-  KQ_TRY(launch_row_pass(W_in, w_dtype, ldw_in, W, ldw, d_out, d_in, mw_out, mw_in, nullptr,
-                         nullptr, rot_in, ri, q28_in, false, s, "rot_row_pass"));
-  if (rot_out) KQ_TRY(col_transform(W, ldw, W, ldw, d_out, d_in, ro, q28_out, false, s));
+  if (!sx_given)
+    KQ_TRY(launch("rot_factors", side_factors, dim3(unsigned(cdiv(d_in, 256))), dim3(256), 0, s,
+                  d_in, static_cast<const float*>(HX), ldx, static_cast<const double*>(colp), nb,
+                  static_cast<const double*>(nullptr), rot_in ? sign_in : nullptr,
+                  int((flags & KRONQ_RESCALE_IN) != 0), sx, mw_in, mh_in));
+  else
+    KQ_TRY(launch("rot_factors", given_factors, dim3(unsigned(cdiv(d_in, 256))), dim3(256), 0, s,
+                  d_in, static_cast<const float*>(sx), rot_in ? sign_in : nullptr, mw_in));
+  if (!hx_only) {
+    KQ_TRY(launch("rot_factors", side_factors, dim3(unsigned(cdiv(d_out, 256))), dim3(256), 0, s,
+                  d_out, static_cast<const float*>(HG), ldg, static_cast<const double*>(nullptr),
+                  int64_t(0), static_cast<const double*>(rows), rot_out ? sign_out : nullptr,
+                  int((flags & KRONQ_RESCALE_OUT) != 0), sg, mw_out, mh_out));
+    // W: rescale + signs + V side (row pass), then U side (column pass)
+    KQ_TRY(launch_row_pass(W_in, w_dtype, ldw_in, W, ldw, d_out, d_in, mw_out, mw_in, nullptr,
+                           nullptr, rot_in, ri, q28_in, false, s, "rot_row_pass"));
+    if (rot_out) KQ_TRY(col_transform(W, ldw, W, ldw, d_out, d_in, ro, q28_out, false, s));
+  }
   // H_X <- V S^-1 H_X S^-1 V^T
-  KQ_TRY(launch_row_pass(HX, KRONQ_FP32, ldx, HX, ldx, d_in, d_in, mh_in, mh_in, nullptr,
-                         nullptr, rot_in, ri, q28_in, false, s, "rot_row_pass"));
-  if (rot_in) KQ_TRY(col_transform(HX, ldx, HX, ldx, d_in, d_in, ri, q28_in, false, s));
+  if (!sx_given) {
+    KQ_TRY(launch_row_pass(HX, KRONQ_FP32, ldx, HX, ldx, d_in, d_in, mh_in, mh_in, nullptr,
+                           nullptr, rot_in, ri, q28_in, false, s, "rot_row_pass"));
+    if (rot_in) KQ_TRY(col_transform(HX, ldx, HX, ldx, d_in, d_in, ri, q28_in, false, s));
+  }
   // H_G <- U S^-1 H_G S^-1 U^T
-  if (HG) {
+  if (HG && !hx_only) {
     KQ_TRY(launch_row_pass(HG, KRONQ_FP32, ldg, HG, ldg, d_out, d_out, mh_out, mh_out, nullptr,
                            nullptr, rot_out, ro, q28_out, false, s, "rot_row_pass"));
     if (rot_out) KQ_TRY(col_transform(HG, ldg, HG, ldg, d_out, d_out, ro, q28_out, false, s));

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libkronq.so")
 
 KRONQ_BF16, KRONQ_FP32 = 1, 2
 RESCALE_IN, RESCALE_OUT, ROT_IN, ROT_OUT, INVERSE = 1, 2, 4, 8, 16
+HX_ONLY, SX_GIVEN = 32, 64
 BIIP = RESCALE_IN | RESCALE_OUT | ROT_IN | ROT_OUT
 OP_COV, OP_ROTATE, OP_CHOL, OP_OBS, OP_LOSS = 1, 2, 3, 4, 5
 ERRORS = {0: "OK", -1: "INVALID_ARG", -2: "SHAPE", -3: "NOT_PD", -4: "HIP", -5: "WORKSPACE",
@@ -138,32 +139,37 @@ def kronq_accumulate_cov(A: torch.Tensor, H: torch.Tensor, alpha: float = 1.0, b
     return H
 
 
-def kronq_traces(HX: torch.Tensor, HG: torch.Tensor, out: Optional[torch.Tensor] = None):
-    """Device float64 tensor [tr H_X, tr H_G, tr H_X * tr H_G]."""
+def kronq_traces(HX: Optional[torch.Tensor], HG: Optional[torch.Tensor],
+                 out: Optional[torch.Tensor] = None):
+    """Device float64 tensor [tr H_X, tr H_G, tr H_X * tr H_G] (a None side leaves its slot)."""
     _dev(HX, HG)
+    ref = HX if HX is not None else HG
     if out is None:
-        out = torch.empty(3, dtype=torch.float64, device=HX.device)
-    rc = load().kronq_traces(_ptr(HX), HX.shape[0], _ld(HX), _ptr(HG), HG.shape[0], _ld(HG),
-                             _ptr(out), _stream(HX.device))
+        out = torch.empty(3, dtype=torch.float64, device=ref.device)
+    rc = load().kronq_traces(_ptr(HX), HX.shape[0] if HX is not None else 0,
+                             _ld(HX) if HX is not None else 0, _ptr(HG),
+                             HG.shape[0] if HG is not None else 0,
+                             _ld(HG) if HG is not None else 0, _ptr(out), _stream(ref.device))
     _check(rc, "kronq_traces")
     return out
 
 
-def kronq_rotate(W_in: torch.Tensor, W: torch.Tensor, HX: Optional[torch.Tensor],
+def kronq_rotate(W_in: torch.Tensor, W: Optional[torch.Tensor], HX: Optional[torch.Tensor],
                  HG: Optional[torch.Tensor], sign_in: Optional[torch.Tensor],
                  sign_out: Optional[torch.Tensor], q28_in: Optional[torch.Tensor],
                  q28_out: Optional[torch.Tensor], sx: torch.Tensor, sg: torch.Tensor,
                  flags: int = BIIP, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
     """BiIP forward (W <- U S_G W_in S_X V^T, H_X and H_G in place) or, with INVERSE, the revert."""
     _dev(W_in, W, HX, HG, sign_in, sign_out, q28_in, q28_out, sx, sg)
-    d_out, d_in = W.shape
+    d_out, d_in = W_in.shape
     if ws is None:
-        ws = workspace(OP_ROTATE, d_out, d_in, 0, W.device)
+        ws = workspace(OP_ROTATE, d_out, d_in, 0, W_in.device)
     rc = load().kronq_rotate(
-        _ptr(W_in), _dtype_code(W_in), _ld(W_in), _ptr(W), d_out, d_in, _ld(W), _ptr(HX),
+        _ptr(W_in), _dtype_code(W_in), _ld(W_in), _ptr(W), d_out, d_in,
+        _ld(W) if W is not None else 0, _ptr(HX),
         _ld(HX) if HX is not None else 0, _ptr(HG), _ld(HG) if HG is not None else 0,
         _ptr(sign_in), _ptr(sign_out), _ptr(q28_in), _ptr(q28_out), _ptr(sx), _ptr(sg), flags,
-        _ptr(ws), ws.numel(), _stream(W.device))
+        _ptr(ws), ws.numel(), _stream(W_in.device))
     _check(rc, "kronq_rotate")
     return W
 

@@ -53,6 +53,8 @@ class LayerState:
     ws_chol: torch.Tensor
     ws_obs: torch.Tensor
     err: Optional[torch.Tensor] = None
+    side: Optional[torch.cuda.Stream] = None
+    ev: tuple = ()
 
     @staticmethod
     def allocate(d_out: int, d_in: int, n_tokens: int, device, keep_err: bool = False,
@@ -80,6 +82,8 @@ class LayerState:
             ws_rot=ws(K.OP_ROTATE, d_out, d_in, 0), ws_chol=ws(K.OP_CHOL, 0, d_in, 0),
             ws_obs=ws(K.OP_OBS, d_out, d_in, 0),
             err=torch.empty(d_out, d_in, **f32) if keep_err else None,
+            side=torch.cuda.Stream(device=device),  # default priority
+            ev=tuple(torch.cuda.Event() for _ in range(3)),
         )
 
 
@@ -106,11 +110,42 @@ def solve(st: LayerState, bits: int, damp: float = 0.01):
 
 
 def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bits: int,
-                   damp: float = 0.01, flags: int = K.BIIP, skip_x: bool = False):
-    """The whole hot path of one layer (enqueue only)."""
-    covariances(st, X, G, skip_x)
-    biip(st, W0, rin, rout, flags)
-    solve(st, bits, damp)
+                   damp: float = 0.01, flags: int = K.BIIP, skip_x: bool = False,
+                   overlap: bool = True):
+    """The whole hot path of one layer (enqueue only).
+
+    With ``overlap`` the work is split over two streams: the factorisation depends only on H_X
+    and S_X, so it runs on the current stream right after H_X is rotated, while the second
+    stream accumulates H_G (after H_X is done, so the two covariances do not share the GPU)
+    and rotates W and H_G. The sweep starts when both are done."""
+    if not overlap:
+        covariances(st, X, G, skip_x)
+        biip(st, W0, rin, rout, flags)
+        solve(st, bits, damp)
+        return
+    main = torch.cuda.current_stream(st.HX.device)
+    ev_x, ev_sx, ev_w = st.ev
+    if not skip_x:
+        K.kronq_accumulate_cov(X, st.HX, 1.0, 0.0, st.ws_cov_x)
+    K.kronq_traces(st.HX, None, st.tr_pre)
+    ev_x.record(main)
+    K.kronq_rotate(W0, None, st.HX, None, rin.sign, None, rin.q28, None, st.sx, st.sg,
+                   flags | K.HX_ONLY, st.ws_rot)
+    K.kronq_traces(st.HX, None, st.tr_post)
+    ev_sx.record(main)
+    K.kronq_cholesky_inv(st.HX, st.U, damp, st.info, st.ws_chol)
+    with torch.cuda.stream(st.side):
+        st.side.wait_event(ev_x)
+        K.kronq_accumulate_cov(G, st.HG, 1.0, 0.0, st.ws_cov_g)
+        K.kronq_traces(None, st.HG, st.tr_pre)
+        st.side.wait_event(ev_sx)
+        K.kronq_rotate(W0, st.W, None, st.HG, rin.sign, rout.sign, rin.q28, rout.q28, st.sx,
+                       st.sg, flags | K.SX_GIVEN, st.ws_rot)
+        K.kronq_traces(None, st.HG, st.tr_post)
+        ev_w.record(st.side)
+    main.wait_event(ev_w)
+    K.kronq_obs_quantize_layer(st.W, st.U, bits, st.codes, st.scales, st.zeros, st.err, None,
+                               ws=st.ws_obs)
 
 
 def check(st: LayerState):

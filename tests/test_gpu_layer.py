@@ -101,3 +101,25 @@ def test_rotated_space_identities_any_size():
     dW = to_np(Wr).astype(np.float64) - to_np(st.W).astype(np.float64)
     EU = to_np(st.err).astype(np.float64) @ to_np(st.U).astype(np.float64)
     assert rel_frob(EU, dW) < 1e-3
+
+
+def test_overlapped_schedule_matches_single_stream():
+    """The two-stream schedule computes exactly what the single-stream sequence computes."""
+    spec = synth.small_spec(448, 512, 3000, bits=2, seed=31)
+    X = synth.gen_matrix(spec.x, DEV)
+    G = synth.gen_matrix(spec.g, DEV)
+    W0 = synth.gen_matrix(spec.w, DEV)
+    ri = synth.rotation_params(spec.d_in, spec.seed, spec.name + ":in")
+    ro = synth.rotation_params(spec.d_out, spec.seed, spec.name + ":out")
+    rin, rout = rot_device(ri), rot_device(ro)
+    res = []
+    for overlap in (False, True):
+        st = L.LayerState.allocate(spec.d_out, spec.d_in, spec.n_tokens, DEV)
+        note(f"layer overlap={overlap}")
+        for _ in range(2):  # twice: the second step reuses every buffer and event
+            L.quantize_layer(st, X, G, W0, rin, rout, spec.bits, spec.damp, overlap=overlap)
+        L.check(st)
+        torch.cuda.synchronize()
+        res.append([to_np(t) for t in (st.codes, st.W, st.U, st.tr_pre, st.tr_post, st.sx, st.sg)])
+    for a, b in zip(*res):
+        np.testing.assert_array_equal(a, b)

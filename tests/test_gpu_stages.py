@@ -277,3 +277,39 @@ def test_layer_loss(d_out, d_in):
     torch.cuda.synchronize()
     ref = O.kfac_loss(oracle_view(W.float()) - Wh.astype(np.float64), hx, hg)
     assert abs(float(out.item()) / ref - 1.0) < TOL
+
+
+def test_rotate_split_equals_one_call():
+    """H_X half then the W / H_G half (the two-stream schedule) gives the one-call result."""
+    d_out, d_in = 448, 512
+    s, W, hx, hg, ri, ro = _rot_problem(d_out, d_in, 12)
+    rin, rout = rot_device(ri), rot_device(ro)
+    Wb = W.to(DEV)
+    outs = []
+    for split in (False, True):
+        HX, HG = f32(hx), f32(hg)
+        Wd = torch.empty(d_out, d_in, device=DEV)
+        sx = torch.empty(d_in, device=DEV)
+        sg = torch.empty(d_out, device=DEV)
+        note(f"rotate split={split}")
+        if split:
+            K.kronq_rotate(Wb, None, HX, None, rin.sign, None, rin.q28, None, sx, sg,
+                           K.BIIP | K.HX_ONLY)
+            K.kronq_rotate(Wb, Wd, None, HG, rin.sign, rout.sign, rin.q28, rout.q28, sx, sg,
+                           K.BIIP | K.SX_GIVEN)
+        else:
+            K.kronq_rotate(Wb, Wd, HX, HG, rin.sign, rout.sign, rin.q28, rout.q28, sx, sg, K.BIIP)
+        torch.cuda.synchronize()
+        outs.append([to_np(t) for t in (Wd, HX, HG, sx, sg)])
+    for a, b in zip(*outs):
+        np.testing.assert_array_equal(a, b)
+
+
+def test_traces_split_across_calls():
+    hx, hg = spd_from_tokens(300, 700, 1), spd_from_tokens(448, 900, 2)
+    out = torch.zeros(3, dtype=torch.float64, device=DEV)
+    note("traces split")
+    K.kronq_traces(f32(hx), None, out)
+    K.kronq_traces(None, f32(hg), out)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(to_np(out), np.array(O.traces(hx, hg)), rtol=1e-9)
