@@ -97,7 +97,10 @@ def main() -> int:
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="q_proj")
     ap.add_argument("--cpu-tokens", type=int, default=16384)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--breakdown", action="store_true", help="per-kernel times (stderr)")
+    ap.add_argument("--breakdown", action="store_true",
+                    help="per-kernel times of one extra step run on a single stream (stderr)")
+    ap.add_argument("--serial", action="store_true",
+                    help="time the single-stream schedule instead of the two-stream one")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run 3 plain 1 GiB device copies (reference for counter scaling)")
     args = ap.parse_args()
@@ -137,8 +140,8 @@ def main() -> int:
                                g_dtype=G.dtype)
     torch.cuda.synchronize()
 
-    def step():
-        L.quantize_layer(st, X, G, W0, rin, rout, spec.bits, spec.damp)
+    def step(overlap=not args.serial):
+        L.quantize_layer(st, X, G, W0, rin, rout, spec.bits, spec.damp, overlap=overlap)
 
     for _ in range(args.warmup):
         step()
@@ -175,7 +178,7 @@ def main() -> int:
         K.kronq_profile_only(None)
         K.kronq_profile_reset()
         K.kronq_profile_enable(True)
-        step()
+        step(overlap=False)
         torch.cuda.synchronize()
         K.kronq_profile_enable(False)
         breakdown = {}
@@ -200,7 +203,8 @@ def main() -> int:
                                f"{spec.bits}-bit, group {spec.group}",
                    "d_out": spec.d_out, "d_in": spec.d_in, "n_tokens": spec.n_tokens,
                    "bits": spec.bits, "group": spec.group, "block": 128, "damp": spec.damp,
-                   "parallelism": "single GPU"},
+                   "parallelism": "single GPU",
+                   "schedule": "one stream" if args.serial else "two streams"},
         "roofline": roof, "cpu_baseline": cpu,
     }
     if breakdown is not None:

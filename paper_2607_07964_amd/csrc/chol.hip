@@ -3,12 +3,15 @@
 // inv(H~) = U^T U with U upper. With J the index reversal, J H~ J = L L^T (ordinary lower
 // Cholesky) gives H~ = (J L J)(J L J)^T, so U = (J L J)^-1 = J L^-1 J. Steps:
 //   1. damping: H~ = H + damp * mean(diag H) * I (in place), M = J H~ J (workspace copy);
-//   2. blocked right-looking Cholesky of M with 128-wide panels: the diagonal block is factored
-//      and inverted in LDS by one workgroup; the panel solve is P <- P Linv_kk^T and the trailing
-//      update M22 -= P P^T (lower tiles only), both on the fp32 MFMA GEMM;
-//   3. X = L^-1 by right-looking blocked forward substitution on the identity:
-//      X[k, :k] = Linv_kk Y[k, :k], X[k, k] = Linv_kk, Y[k+1:, :k+1] -= L[k+1:, k] X[k, :k+1];
-//   4. U[i][j] = X[d-1-i][d-1-j] for i <= j, 0 below the diagonal.
+//   2. L and X = L^-1 together, recursively on [[M11, .], [M21, M22]] split at a multiple of 128:
+//        factor and invert M11 (X11 = L11^-1);
+//        L21 = M21 X11^T                  (written to the X21 slot, which is still free);
+//        M22 -= L21 L21^T                 (lower tiles only);
+//        factor and invert M22 (X22);
+//        X21 = -X22 (L21 X11)             (through a scratch product, then over L21).
+//      Leaves of at most 128 columns are factored and inverted in LDS by one workgroup; every
+//      other step is a fp32 MFMA GEMM, so the large updates have a long K;
+//   3. U[i][j] = X[d-1-i][d-1-j] for i <= j, 0 below the diagonal.
 // A non-positive pivot sets *info to its 1-based column in the original order (first failure).
 #include <cmath>
 
@@ -45,115 +48,211 @@ __global__ void add_diag(float* __restrict__ H, int64_t d, int64_t ldh,
   if (i < d) H[i * ldh + i] += *shift;
 }
 
-// M[i][j] = H[d-1-i][d-1-j]; X = 0
+// M[i][j] = H[d-1-i][d-1-j]
 __global__ void reverse_copy(const float* __restrict__ H, int64_t d, int64_t ldh,
-                             float* __restrict__ M, float* __restrict__ X, int64_t ldm) {
+                             float* __restrict__ M, int64_t ldm) {
   const int64_t i = blockIdx.y;
   for (int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; j < d;
-       j += int64_t(gridDim.x) * blockDim.x) {
+       j += int64_t(gridDim.x) * blockDim.x)
     M[i * ldm + j] = H[(d - 1 - i) * ldh + (d - 1 - j)];
-    X[i * ldm + j] = 0.f;
+}
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// One 32 x 32 block C = alpha * A op(B) + beta * C on LDS arrays, by one wave on the fp32
+// matrix cores (v_mfma_f32_32x32x2f32, two k per instruction). A is 32 x k (row stride lda);
+// op(B) is k x 32: B[k][n] at B[k * ldb + n], or with bt, B^T with (k, n) at B[n * ldb + k].
+// k is even. The caller orders the LDS traffic (a wave's LDS accesses complete in order).
+__device__ __forceinline__ void mfma_block(float* C, int ldc, const float* A, int lda,
+                                           const float* B, int ldb, bool bt, int k, float alpha,
+                                           float beta, int lane) {
+  const int l32 = lane & 31, lhi = lane >> 5;
+  f32x16_t acc = {};
+  for (int k0 = 0; k0 < k; k0 += 2) {
+    const float av = A[l32 * lda + k0 + lhi];
+    const float bv = bt ? B[l32 * ldb + k0 + lhi] : B[(k0 + lhi) * ldb + l32];
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    float* c = C + (8 * (r >> 2) + 4 * lhi + (r & 3)) * ldc + l32;
+    *c = beta == 0.f ? alpha * acc[r] : alpha * acc[r] + beta * *c;
   }
 }
 
-// Factor the diagonal block M[kb:kb+bs, kb:kb+bs] (lower) and invert the factor, in one
-// workgroup, in a single pass over the columns j = 0..bs-1. Thread (ty, tx) of a 16 x 16 grid
-// keeps entries (ty + 16 p, tx + 16 q), p, q < 8, of two matrices in registers:
-//   r: the trailing matrix of the right-looking factorisation (entries above the diagonal ride
-//      along unused), updated by the rank-1 term of column j;
-//   y: R = I - (already eliminated terms), turned into rows of Y = L^-1 by forward
-//      substitution: at step j, Y[j, :] = R[j, :] / L_jj, then R[i, :] -= L_ij Y[j, :] for i > j.
-// Column j of the trailing matrix and row j of Y are exchanged through LDS, two barriers per
-// column. Writes L_kk to M (lower part), Linv_kk (exact zeros above the diagonal) to dinv and X.
-__global__ __launch_bounds__(256) void potrf_diag(float* __restrict__ M, int64_t ldm, int64_t kb,
-                                                  int bs, int64_t d, float* __restrict__ dinv,
-                                                  float* __restrict__ X, int* __restrict__ info) {
-  __shared__ float l[NB * DLD];   // the factor L
-  __shared__ float col[2][NB];    // column j of the trailing matrix
-  __shared__ float yrow[NB];      // row j of Y
-  const int tid = threadIdx.x;
-  const int tx = tid & 15, ty = tid >> 4;
-  float r[8][8], y[8][8];
+// One 32-column panel of the diagonal-block factorisation (see potrf_diag), then the rank-32
+// update of the lower blocks of the rest of the block.
+template <int c0>
+__device__ __forceinline__ void panel_step(float* a, float* colbuf, float* dummy, int64_t kb,
+                                           int64_t d, int* info, int wave, int lane) {
+  if (wave == 0) {
+    const int r0 = c0 + lane, r1 = c0 + 64 + lane;
+    const bool ok0 = r0 < NB, ok1 = r1 < NB;  // r1 < NB only for c0 < 64
+    float v0[32], v1[32];
+    int first_bad = 32;  // first column of the panel with a non-positive pivot
+    // lanes past the last row work on a copy of row NB - 1 (never stored): no divergent loads
+    const int q0 = ok0 ? r0 : NB - 1, q1 = ok1 ? r1 : NB - 1;
 #pragma unroll
-  for (int p = 0; p < 8; ++p)
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int i = ty + 16 * p, j = tx + 16 * q;
-      r[p][q] = (i < bs && j < bs) ? M[(kb + i) * ldm + kb + j] : 0.f;
-      y[p][q] = (i == j) ? 1.f : 0.f;
+    for (int k = 0; k < 32; ++k) {
+      v0[k] = a[q0 * DLD + c0 + k];
+      v1[k] = c0 < 64 ? a[q1 * DLD + c0 + k] : 0.f;
     }
-  if (tx == 0) {
 #pragma unroll
-    for (int p = 0; p < 8; ++p) col[0][ty + 16 * p] = r[p][0];
+    for (int j = 0; j < 32; ++j) {
+      colbuf[lane] = v0[j];  // every lane stores (no branch); entries 0..31 are read
+      float raw[32];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float4 t = reinterpret_cast<const float4*>(colbuf)[q];
+        raw[4 * q] = t.x, raw[4 * q + 1] = t.y, raw[4 * q + 2] = t.z, raw[4 * q + 3] = t.w;
+      }
+      const float piv = raw[j];
+      if (!(piv > 0.f) && first_bad == 32) first_bad = j;  // also catches NaN; a select
+      const float rl = rsqrtf(piv);
+      const float ljj = piv * rl;
+      const float l0 = v0[j] * rl, l1 = v1[j] * rl;
+      // A[i][k] -= L[i][j] L[k][j] = (l_i rl) raw_k
+      const float g0 = l0 * rl, g1 = l1 * rl;
+#pragma unroll
+      for (int k = j + 1; k < 32; ++k) {
+        v0[k] = fmaf(-g0, raw[k], v0[k]);
+        if (c0 < 64) v1[k] = fmaf(-g1, raw[k], v1[k]);
+      }
+      v0[j] = lane > j ? l0 : (lane == j ? ljj : 0.f);
+      v1[j] = l1;
+    }
+    // unconditional stores (a divergent branch here would make the compiler sink the row
+    // updates into it): rows past the end go to a dummy area of the idle product scratch
+    const int dummy_off = int(dummy - a) + lane * 33;  // same LDS array: an index select
+    float* d0 = a + (ok0 ? r0 * DLD + c0 : dummy_off);
+    float* d1 = a + (ok1 ? r1 * DLD + c0 : dummy_off);
+#pragma unroll
+    for (int k = 0; k < 32; ++k) {
+      d0[k] = v0[k];
+      if (c0 < 64) d1[k] = v1[k];
+    }
+    if (lane == 0 && first_bad < 32 && kb + c0 + first_bad < d)
+      atomicCAS(info, 0, int(d - (kb + c0 + first_bad)));
   }
   __syncthreads();
-  for (int j = 0; j < bs; ++j) {
-    const float* cj = col[j & 1];
-    const float piv = cj[j];
-    if (!(piv > 0.f) && tid == 0) atomicCAS(info, 0, int(d - (kb + j)));  // also catches NaN
-    const float ljj = sqrtf(piv);
-    const float rl = 1.f / ljj;
-    if (tid >= j && tid < bs) l[tid * DLD + j] = (tid == j) ? ljj : cj[tid] * rl;
-    // row j of Y from its owners
-    if (ty == (j & 15)) {
-#pragma unroll
-      for (int p = 0; p < 8; ++p)
-        if (p == (j >> 4)) {
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            y[p][q] *= rl;
-            yrow[tx + 16 * q] = y[p][q];
-          }
-        }
-    }
-    __syncthreads();
-    float lc[8], cc[8], yj[8];
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      lc[p] = cj[ty + 16 * p] * rl;  // L[i][j] for this thread's rows
-      cc[p] = cj[tx + 16 * p];
-      yj[p] = yrow[tx + 16 * p];
-    }
-    // row blocks p < j / 16 hold only finished rows: skip them (a wave-uniform branch); the
-    // block containing row j is masked per row, later blocks are updated unconditionally
-    const int jb = j >> 4;
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      if (p < jb) continue;
-      const float f = -lc[p] * rl;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) r[p][q] = fmaf(f, cc[q], r[p][q]);
-      if (p > jb) {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) y[p][q] = fmaf(-lc[p], yj[q], y[p][q]);
-      } else if (ty > (j & 15)) {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) y[p][q] = fmaf(-lc[p], yj[q], y[p][q]);
-      }
-    }
-    const int jn = j + 1;
-    if (jn < bs && tx == (jn & 15)) {
-      float* cn = col[jn & 1];
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        if (q == (jn >> 4)) {
-#pragma unroll
-          for (int p = 0; p < 8; ++p) cn[ty + 16 * p] = r[p][q];
-        }
+  const int c1 = c0 + 32, nb = (NB - c1) / 32;
+  if (nb > 0) {
+    // lower 32-blocks (bi >= bj) of A22 -= P P^T, P = L[c1:, c0:c0+32]
+    for (int t = wave; t < nb * (nb + 1) / 2; t += 4) {
+      int bi = 0, rem = t;
+      while (rem > bi) rem -= ++bi;
+      const int bj = rem;
+      mfma_block(a + (c1 + 32 * bi) * DLD + c1 + 32 * bj, DLD, a + (c1 + 32 * bi) * DLD + c0,
+                 DLD, a + (c1 + 32 * bj) * DLD + c0, DLD, true, 32, -1.f, 1.f, lane);
     }
     __syncthreads();
   }
+}
+
+// Factor the diagonal block M[kb:kb+bs, kb:kb+bs] (lower) and invert the factor, one workgroup.
+// The block is padded to 128 x 128 with the identity, so a partial block needs no special case.
+// Factorisation, in four 32-column panels:
+//   * panel: wave 0 factors the panel for every row at or below it; lane l keeps rows c0 + l
+//     and c0 + 64 + l (32 panel entries each) in registers. Column j of the panel's diagonal
+//     rows is published once through a 64-float LDS buffer and read back as broadcasts, and the
+//     1 / L_jj scaling is folded into the per-row coefficient, so each column costs one LDS
+//     round trip and one FMA per remaining entry;
+//   * rank-32 update of the lower blocks of the rest of the block by all four waves (MFMA).
+// Inverse Y = L^-1 by recursive doubling, inv([[A, 0], [B, C]]) = [[A^-1, 0], [-C^-1 B A^-1, C^-1]]:
+//   32 x 32 diagonal blocks (one wave each, columns by forward substitution), then 64, then 128.
+// Writes Linv_kk, with exact zeros above the diagonal, to X (M itself is left as read).
+__global__ __launch_bounds__(256) void potrf_diag(const float* __restrict__ M, int64_t ldm,
+                                                  int64_t kb, int bs, int64_t d,
+                                                  float* __restrict__ X, int* __restrict__ info) {
+  __shared__ __attribute__((aligned(16))) float lds[2 * NB * DLD + 64 * 68];
+  float* const a = lds;                 // the block, becomes L (lower part meaningful)
+  float* const y = lds + NB * DLD;      // Y = L^-1
+  float* const tb = lds + 2 * NB * DLD; // product scratch (a dummy store target in the panels)
+  __shared__ __attribute__((aligned(16))) float colbuf[64];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const bool full = bs == NB;
+  if (full) {
+    float4 q[NB * NB / 1024];
 #pragma unroll
-  for (int p = 0; p < 8; ++p)
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int i = ty + 16 * p, j = tx + 16 * q;
-      if (i < bs && j < bs) {
-        if (j <= i) M[(kb + i) * ldm + kb + j] = l[i * DLD + j];
-        dinv[i * NB + j] = y[p][q];
-        X[(kb + i) * ldm + kb + j] = y[p][q];
-      }
+    for (int it = 0; it < NB * NB / 1024; ++it) {
+      const int e = tid + 256 * it, i = e >> 5, j = (e & 31) * 4;
+      q[it] = *reinterpret_cast<const float4*>(M + (kb + i) * ldm + kb + j);
     }
+#pragma unroll
+    for (int it = 0; it < NB * NB / 1024; ++it) {
+      const int e = tid + 256 * it, i = e >> 5, j = (e & 31) * 4;
+      a[i * DLD + j] = q[it].x, a[i * DLD + j + 1] = q[it].y;
+      a[i * DLD + j + 2] = q[it].z, a[i * DLD + j + 3] = q[it].w;
+    }
+  } else {
+    for (int e = tid; e < NB * NB; e += 256) {
+      const int i = e >> 7, j = e & 127;
+      a[i * DLD + j] = (i < bs && j < bs) ? M[(kb + i) * ldm + kb + j] : (i == j ? 1.f : 0.f);
+    }
+  }
+  // upper 32-blocks of Y that the doubling reads as operands: (0, 1) and (2, 3)
+  for (int e = tid; e < 2 * 32 * 32; e += 256) {
+    const int o = (e >> 10) * 64, i = (e >> 5) & 31, j = e & 31;
+    y[(o + i) * DLD + o + 32 + j] = 0.f;
+  }
+  __syncthreads();
+  panel_step<0>(a, colbuf, tb, kb, d, info, wave, lane);
+  panel_step<32>(a, colbuf, tb, kb, d, info, wave, lane);
+  panel_step<64>(a, colbuf, tb, kb, d, info, wave, lane);
+  panel_step<96>(a, colbuf, tb, kb, d, info, wave, lane);
+  // inverse: 32 x 32 diagonal blocks, wave w takes block w; lane c solves column c
+  {
+    const int b0 = wave * 32;
+    if (lane < 32) {
+      float x[32];
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        float s = (i == lane) ? 1.f : 0.f;
+#pragma unroll
+        for (int k = 0; k < i; ++k) s = fmaf(-a[(b0 + i) * DLD + b0 + k], x[k], s);
+        x[i] = s / a[(b0 + i) * DLD + b0 + i];
+        __builtin_amdgcn_sched_barrier(0);  // read one row of L at a time
+      }
+#pragma unroll
+      for (int i = 0; i < 32; ++i) y[(b0 + i) * DLD + b0 + lane] = x[i];
+    }
+  }
+  __syncthreads();
+  // 64: Y10 = -Y11 (L10 Y00) for the block pairs at 0 and 64, one wave each
+  if (wave < 2) {
+    const int o = wave * 64;
+    float* T = tb + wave * 32 * 33;
+    mfma_block(T, 33, a + (o + 32) * DLD + o, DLD, y + o * DLD + o, DLD, false, 32, 1.f, 0.f,
+               lane);
+    mfma_block(y + (o + 32) * DLD + o, DLD, y + (o + 32) * DLD + o + 32, DLD, T, 33, false, 32,
+               -1.f, 0.f, lane);
+  }
+  __syncthreads();
+  // 128: Y[64:, :64] = -Y[64:, 64:] (L[64:, :64] Y[:64, :64]), one 32-block per wave
+  {
+    const int bi = wave >> 1, bj = wave & 1;
+    mfma_block(tb + 32 * bi * 68 + 32 * bj, 68, a + (64 + 32 * bi) * DLD, DLD, y + 32 * bj, DLD,
+               false, 64, 1.f, 0.f, lane);
+    __syncthreads();
+    mfma_block(y + (64 + 32 * bi) * DLD + 32 * bj, DLD, y + (64 + 32 * bi) * DLD + 64, DLD,
+               tb + 32 * bj, 68, false, 64, -1.f, 0.f, lane);
+  }
+  __syncthreads();
+  if (full) {
+#pragma unroll 4
+    for (int it = 0; it < NB * NB / 1024; ++it) {
+      const int e = tid + 256 * it, i = e >> 5, j = (e & 31) * 4;
+      float v[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) v[c] = (j + c <= i) ? y[i * DLD + j + c] : 0.f;
+      *reinterpret_cast<float4*>(X + (kb + i) * ldm + kb + j) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+  } else {
+    for (int e = tid; e < bs * NB; e += 256) {
+      const int i = e >> 7, j = e & 127;
+      if (j < bs) X[(kb + i) * ldm + kb + j] = (j <= i) ? y[i * DLD + j] : 0.f;
+    }
+  }
 }
 
 // U[i][j] = X[d-1-i][d-1-j] for i <= j, else 0
@@ -167,24 +266,55 @@ __global__ void reverse_out(const float* __restrict__ X, int64_t ldm, int64_t d,
 
 int64_t ld_for(int64_t d) { return ((d + 63) / 64) * 64; }
 
+// split of an n-column block: the first h columns, a multiple of NB, about half
+int64_t split_at(int64_t n) { return (cdiv(n, NB) / 2) * NB; }
+
+// L and L^-1 of the block [n0, n0 + n) of M; the lower part of the same block of X receives
+// L^-1 (zeros on the upper part of the diagonal leaves), T is scratch of split rows x cols.
+int chol_rec(float* M, float* X, float* T, int64_t tcap, int64_t ld, int64_t n0, int64_t n,
+             int64_t d, int* info, hipStream_t s) {
+  if (n <= NB)
+    return launch("chol_potrf_diag", potrf_diag, dim3(1), dim3(256), 0, s,
+                  static_cast<const float*>(M), ld, n0, int(n), d, X, info);
+  const int64_t h = split_at(n), r = n - h;
+  KQ_REQUIRE(r * h <= tcap, KRONQ_ERR_WORKSPACE, "chol_rec: scratch too small");
+  KQ_TRY(chol_rec(M, X, T, tcap, ld, n0, h, d, info, s));
+  const float* M21 = M + (n0 + h) * ld + n0;
+  const float* X11 = X + n0 * ld + n0;
+  float* X21 = X + (n0 + h) * ld + n0;
+  float* X22 = X + (n0 + h) * ld + n0 + h;
+  float* M22 = M + (n0 + h) * ld + n0 + h;
+  // L21 = M21 X11^T (op(B) = X11^T is upper triangular)
+  KQ_TRY(gemm_f32(GEMM_TB | GEMM_OPB_UPPER, r, h, h, 1.f, M21, ld, X11, ld, 0.f, X21, ld, s,
+                  "chol_trsm"));
+  // M22 -= L21 L21^T
+  KQ_TRY(gemm_f32(GEMM_TB | GEMM_LOWER_C, r, r, h, -1.f, X21, ld, X21, ld, 1.f, M22, ld, s,
+                  "chol_syrk"));
+  KQ_TRY(chol_rec(M, X, T, tcap, ld, n0 + h, r, d, info, s));
+  // T = L21 X11, then X21 = -X22 T
+  KQ_TRY(gemm_f32(GEMM_B_LOWER, r, h, h, 1.f, X21, ld, X11, ld, 0.f, T, h, s, "trtri_row"));
+  return gemm_f32(GEMM_A_LOWER, r, h, r, -1.f, X22, ld, T, h, 0.f, X21, ld, s, "trtri_update");
+}
+
 }  // namespace
 
 size_t chol_ws_bytes(int64_t d) {
   if (d <= 0) return 0;
   const int64_t ld = ld_for(d);
-  const int64_t nblk = cdiv(d, NB);
+  const int64_t h = split_at(d);
   return 2 * align256(size_t(d) * ld * sizeof(float)) +
-         align256(size_t(nblk) * NB * NB * sizeof(float)) + 256;
+         align256(size_t(d - h) * size_t(h > 0 ? h : 1) * sizeof(float)) + 256;
 }
 
 int chol_launch(float* H, int64_t d, int64_t ldh, float damp_rel, float* U, int64_t ldu,
                 int* info, void* ws, hipStream_t s) {
   const int64_t ld = ld_for(d);
-  const int64_t nblk = cdiv(d, NB);
+  const int64_t h = split_at(d);
   Carver cv(ws);
   float* M = cv.take<float>(size_t(d) * ld);
   float* X = cv.take<float>(size_t(d) * ld);
-  float* dinv = cv.take<float>(size_t(nblk) * NB * NB);
+  const int64_t tcap = (d - h) * (h > 0 ? h : 1);
+  float* T = cv.take<float>(size_t(tcap));
   float* shift = cv.take<float>(1);
 
   KQ_TRY(launch("chol_diag_shift", diag_shift, dim3(1), dim3(256), 0, s,
@@ -193,44 +323,8 @@ int chol_launch(float* H, int64_t d, int64_t ldh, float damp_rel, float* U, int6
                 ldh, static_cast<const float*>(shift)));
   const unsigned gx = unsigned(cdiv(d, 256) < 64 ? cdiv(d, 256) : 64);
   KQ_TRY(launch("chol_reverse_copy", reverse_copy, dim3(gx, unsigned(d)), dim3(256), 0, s,
-                static_cast<const float*>(H), d, ldh, M, X, ld));
-
-  // Cholesky of M (lower)
-  for (int64_t k = 0; k < nblk; ++k) {
-    const int64_t kb = k * NB;
-    const int bs = int(d - kb < NB ? d - kb : NB);
-    float* dk = dinv + k * NB * NB;
-    KQ_TRY(launch("chol_potrf_diag", potrf_diag, dim3(1), dim3(256), 0, s, M, ld, kb, bs, d, dk,
-                  X, info));
-    const int64_t rest = d - kb - bs;
-    if (rest > 0) {
-      float* P = M + (kb + bs) * ld + kb;
-      // P <- P Linv_kk^T  (in place: each workgroup owns whole rows of P, N = bs <= 128)
-      KQ_TRY(gemm_f32(GEMM_TB, rest, bs, bs, 1.f, P, ld, dk, NB, 0.f, P, ld, s, "chol_trsm"));
-      // M22 -= P P^T (lower tiles)
-      float* M22 = M + (kb + bs) * ld + kb + bs;
-      KQ_TRY(gemm_f32(GEMM_TB | GEMM_LOWER_C, rest, rest, bs, -1.f, P, ld, P, ld, 1.f, M22, ld, s,
-                      "chol_syrk"));
-    }
-  }
-  // X = L^-1
-  for (int64_t k = 0; k < nblk; ++k) {
-    const int64_t kb = k * NB;
-    const int bs = int(d - kb < NB ? d - kb : NB);
-    const float* dk = dinv + k * NB * NB;
-    if (kb > 0) {
-      // X[k, :kb] = Linv_kk Y[k, :kb]   (in place: M = bs <= 128 rows, one row tile)
-      float* Xk = X + kb * ld;
-      KQ_TRY(gemm_f32(GEMM_A_LOWER, bs, kb, bs, 1.f, dk, NB, Xk, ld, 0.f, Xk, ld, s,
-                      "trtri_row"));
-    }
-    const int64_t rest = d - kb - bs;
-    if (rest > 0) {
-      // Y[kb+bs:, :kb+bs] -= L[kb+bs:, kb:kb+bs] X[k, :kb+bs]
-      KQ_TRY(gemm_f32(0, rest, kb + bs, bs, -1.f, M + (kb + bs) * ld + kb, ld, X + kb * ld, ld,
-                      1.f, X + (kb + bs) * ld, ld, s, "trtri_update"));
-    }
-  }
+                static_cast<const float*>(H), d, ldh, M, ld));
+  KQ_TRY(chol_rec(M, X, T, tcap, ld, 0, d, d, info, s));
   return launch("chol_reverse_out", reverse_out, dim3(gx, unsigned(d)), dim3(256), 0, s,
                 static_cast<const float*>(X), ld, d, U, ldu);
 }

@@ -100,6 +100,7 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_mfma(int flags, int64_t M, in
   int64_t kbeg = 0, kend = K;
   if (flags & GEMM_B_LOWER) kbeg = (n0 / GK) * GK;  // B[k][n] = 0 for k < n
   if ((flags & GEMM_A_LOWER) && m0 + GT < kend) kend = m0 + GT;  // A[m][k] = 0 for k > m
+  if ((flags & GEMM_OPB_UPPER) && n0 + GT < kend) kend = n0 + GT;  // op(B)[k][n] = 0, k > n
 
   const bool a_kc = !(flags & GEMM_TA);  // A[m][k] row-major: k contiguous
   const bool b_kc = (flags & GEMM_TB);   // B^T stored [n][k]: k contiguous

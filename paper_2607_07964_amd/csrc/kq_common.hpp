@@ -119,6 +119,7 @@ enum GemmFlags : int {
   GEMM_LOWER_C = 4,     // only output tiles that touch the lower triangle (i >= j)
   GEMM_B_LOWER = 8,     // B is lower triangular: skip k < column-tile start
   GEMM_A_LOWER = 16,    // A is lower triangular: skip k > row-tile end
+  GEMM_OPB_UPPER = 32,  // op(B) is upper triangular: skip k > column-tile end
 };
 int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,

@@ -177,7 +177,9 @@ def test_rotate_inverse_and_in_place():
 
 
 # ------------------------------------------------------------------------------ Cholesky
-@pytest.mark.parametrize("d", [256, 300, 1024, 77])
+# sizes cover one leaf, a ragged last leaf, odd leaf counts (uneven recursive splits) and
+# several levels of the recursion
+@pytest.mark.parametrize("d", [77, 128, 256, 300, 384, 640, 1000, 1024, 2112])
 def test_cholesky_inverse_factor(d):
     h = spd_from_tokens(d, 3 * d, d)
     H = f32(h)
@@ -194,16 +196,18 @@ def test_cholesky_inverse_factor(d):
     assert rel_frob(u, ref) < TOL
 
 
-def test_cholesky_not_pd_reports_pivot():
-    d = 300
+@pytest.mark.parametrize("d,bad", [(300, 5), (512, 200)])
+def test_cholesky_not_pd_reports_pivot(d, bad):
+    """A negative diagonal entry in a ragged last leaf (300) and inside a later panel of a full
+    leaf (512): *info is the 1-based column of the failing pivot in the original order."""
     h = np.eye(d)
-    h[5, 5] = -1.0
+    h[bad, bad] = -1.0
     H = f32(h)
     U = torch.empty(d, d, device=DEV)
-    note("cholesky_inv not PD")
+    note(f"cholesky_inv not PD d={d}")
     info = K.kronq_cholesky_inv(H, U, 0.01)
     torch.cuda.synchronize()
-    assert int(info.item()) == 6  # 1-based column of the failing pivot (original order)
+    assert int(info.item()) == bad + 1
 
 
 # ------------------------------------------------------------------------------ OBS sweep
