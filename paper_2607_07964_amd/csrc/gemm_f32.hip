@@ -10,6 +10,13 @@
 //     the two k rows a wave reads at once in disjoint bank halves.
 //   * The next K chunk is fetched into registers while the current one is multiplied.
 //   * Triangular flags skip tiles or K ranges that are known to be zero or unused.
+// Problems too small to give the 128 x 128 kernel enough workgroups (the short products of the
+// recursive Cholesky) use gemm_f32_small: a 32 x 32 or 64 x 64 tile per workgroup, K staged 64
+// at a time through LDS, and for 32 x 32 tiles each stage's K split over the four waves (the
+// partial blocks are summed through LDS at the end). The dispatcher takes the largest tile that
+// still gives at least 128 workgroups.
+#include <algorithm>
+
 #include "kq_common.hpp"
 
 namespace kq {
@@ -160,14 +167,159 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_mfma(int flags, int64_t M, in
       }
 }
 
+
+// Small-tile variant (see the file comment). A, B and C must not overlap.
+template <int TM>
+__global__ __launch_bounds__(256) void gemm_f32_small(int flags, int64_t M, int64_t N, int64_t K,
+                                                      float alpha, const float* __restrict__ A,
+                                                      int64_t lda, const float* __restrict__ B,
+                                                      int64_t ldb, float beta,
+                                                      float* __restrict__ C, int64_t ldc) {
+  constexpr int KC = 64;                      // K per stage
+  constexpr int NB32 = TM / 32;               // 32 x 32 blocks per tile edge
+  constexpr int SK = 4 / (NB32 * NB32);       // waves per block (split of each stage's K)
+  constexpr int KW = KC / SK;                 // K per wave per stage
+  constexpr int AS = KC + 1;                  // LDS row stride of the A tile, [m][k]
+  constexpr int BS = TM == 32 ? 32 : 96;      // LDS row stride of the B tile, [k][n]
+  constexpr int NV = TM * KC / 1024;          // float4 per thread per operand per stage
+  __shared__ float sA[TM * AS];
+  __shared__ float sB[KC * BS];
+  __shared__ float red[(SK - 1) * 1024 + 1];
+  const int tid = threadIdx.x;
+  const int64_t m0 = int64_t(blockIdx.y) * TM, n0 = int64_t(blockIdx.x) * TM;
+  if ((flags & GEMM_LOWER_C) && m0 + TM <= n0) return;
+  int64_t kbeg = 0, kend = K;
+  if (flags & GEMM_B_LOWER) kbeg = n0;
+  if ((flags & GEMM_A_LOWER) && m0 + TM < kend) kend = m0 + TM;
+  if ((flags & GEMM_OPB_UPPER) && n0 + TM < kend) kend = n0 + TM;
+  const bool a_kc = !(flags & GEMM_TA), b_kc = (flags & GEMM_TB);
+  const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, lhi = lane >> 5;
+  const int blk = wave % (NB32 * NB32), part = wave / (NB32 * NB32);
+  const int bm = (blk / NB32) * 32, bn = (blk % NB32) * 32;
+
+  float4 ra[NV], rb[NV];
+  // load 4 consecutive elements X[r][c..c+3] (row stride ldx) with bounds rows < R, cols < Cn
+  auto ld4 = [](const float* X, int64_t ldx, int64_t r, int64_t c, int64_t R, int64_t Cn) {
+    if (r < R && c + 4 <= Cn) return *reinterpret_cast<const float4*>(X + r * ldx + c);
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < R) {
+      if (c < Cn) v.x = X[r * ldx + c];
+      if (c + 1 < Cn) v.y = X[r * ldx + c + 1];
+      if (c + 2 < Cn) v.z = X[r * ldx + c + 2];
+      if (c + 3 < Cn) v.w = X[r * ldx + c + 3];
+    }
+    return v;
+  };
+  auto fetch = [&](int64_t k0) {
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int e = tid + 256 * v;
+      if (a_kc) {  // A[m][k]
+        const int m = e / (KC / 4), k4 = (e % (KC / 4)) * 4;
+        ra[v] = ld4(A, lda, m0 + m, k0 + k4, M, kend);
+      } else {     // A stored [k][m]
+        const int k = e / (TM / 4), m4 = (e % (TM / 4)) * 4;
+        ra[v] = (k0 + k < kend) ? ld4(A, lda, k0 + k, m0 + m4, K, M) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      if (b_kc) {  // B stored [n][k]
+        const int n = e / (KC / 4), k4 = (e % (KC / 4)) * 4;
+        rb[v] = ld4(B, ldb, n0 + n, k0 + k4, N, kend);
+      } else {     // B[k][n]
+        const int k = e / (TM / 4), n4 = (e % (TM / 4)) * 4;
+        rb[v] = (k0 + k < kend) ? ld4(B, ldb, k0 + k, n0 + n4, K, N) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  };
+  auto stash = [&]() {
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int e = tid + 256 * v;
+      const float x[4] = {ra[v].x, ra[v].y, ra[v].z, ra[v].w};
+      const float z[4] = {rb[v].x, rb[v].y, rb[v].z, rb[v].w};
+      if (a_kc) {
+        const int m = e / (KC / 4), k4 = (e % (KC / 4)) * 4;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sA[m * AS + k4 + c] = x[c];
+      } else {
+        const int k = e / (TM / 4), m4 = (e % (TM / 4)) * 4;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sA[(m4 + c) * AS + k] = x[c];
+      }
+      if (b_kc) {
+        const int n = e / (KC / 4), k4 = (e % (KC / 4)) * 4;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sB[(k4 + c) * BS + n] = z[c];
+      } else {
+        const int k = e / (TM / 4), n4 = (e % (TM / 4)) * 4;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sB[k * BS + n4 + c] = z[c];
+      }
+    }
+  };
+
+  f32x16_t acc = f32x16_t{};
+  if (kbeg < kend) fetch(kbeg);
+  for (int64_t k0 = kbeg; k0 < kend; k0 += KC) {
+    __syncthreads();
+    stash();
+    __syncthreads();
+    if (k0 + KC < kend) fetch(k0 + KC);
+#pragma unroll
+    for (int s2 = 0; s2 < KW / 2; ++s2) {
+      const int kk = part * KW + 2 * s2 + lhi;
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sA[(bm + l32) * AS + kk], sB[kk * BS + bn + l32],
+                                                 acc, 0, 0, 0);
+    }
+  }
+  if (SK > 1) {
+    if (part > 0) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) red[(part - 1) * 1024 + r * 64 + lane] = acc[r];
+    }
+    __syncthreads();
+    if (part > 0) return;
+#pragma unroll
+    for (int p = 0; p < SK - 1; ++p)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] += red[p * 1024 + r * 64 + lane];
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int64_t gm = m0 + bm + 8 * (r >> 2) + 4 * lhi + (r & 3), gn = n0 + bn + l32;
+    if (gm < M && gn < N) {
+      float* c = C + gm * ldc + gn;
+      const float x = alpha * acc[r];
+      *c = beta == 0.f ? x : x + beta * *c;
+    }
+  }
+}
+
 }  // namespace
 
 int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
              hipStream_t s, const char* name) {
   if (M <= 0 || N <= 0) return KRONQ_OK;
-  const dim3 grid(unsigned(cdiv(N, GT)), unsigned(cdiv(M, GT)));
-  return launch(name, gemm_f32_mfma, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B,
+  // workgroups that do work for a tile edge t (LOWER_C drops the tiles above the diagonal)
+  auto work = [&](int64_t t) {
+    const int64_t tm = cdiv(M, t), tn = cdiv(N, t);
+    if (!(flags & GEMM_LOWER_C)) return tm * tn;
+    int64_t c = 0;
+    for (int64_t i = 0; i < tm; ++i) c += std::min(tn, i + 1);
+    return c;
+  };
+  if (work(GT) >= 128) {
+    const dim3 grid(unsigned(cdiv(N, GT)), unsigned(cdiv(M, GT)));
+    return launch(name, gemm_f32_mfma, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B,
+                  ldb, beta, C, ldc);
+  }
+  if (work(64) >= 128) {
+    const dim3 grid(unsigned(cdiv(N, 64)), unsigned(cdiv(M, 64)));
+    return launch(name, gemm_f32_small<64>, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda,
+                  B, ldb, beta, C, ldc);
+  }
+  const dim3 grid(unsigned(cdiv(N, 32)), unsigned(cdiv(M, 32)));
+  return launch(name, gemm_f32_small<32>, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B,
                 ldb, beta, C, ldc);
 }
 
