@@ -2,156 +2,216 @@
 // correction P = 0; Alg. 2).
 //
 // Per block of 128 columns (= one quantisation group):
-//   * sweep kernel, one wave per 64 rows, one row per lane (rows are independent given U):
-//     the W block is staged column-major in LDS (lane r touches column c at a conflict-free
-//     address), the 128 x 128 block of U in LDS (every U read is a broadcast). Group
-//     parameters come from the row's current 128 values. Columns are processed in sub-blocks
-//     of 8 held in registers: quantise, scaled error e_j = (w_j - w_hat_j) / U_jj, update the
-//     remaining sub-block columns in registers, then apply the 8 errors to the rest of the
-//     block (8 FMAs per LDS read/write). The error replaces the column in LDS; codes stay in
-//     LDS and everything is written back coalesced at the end, the dequantised values being
-//     recomputed from code, scale and zero with the same operations.
-//   * trailing update W[:, blk_end:] -= E U[blk, blk_end:] on the fp32 MFMA GEMM (K = 128).
+//   * sweep kernel: rows are independent given U, so each row is one 16-lane group of a wave
+//     (4 rows per wave, 16 rows per workgroup) and each lane keeps 8 consecutive columns of the
+//     block in registers. Column j: the owning lane quantises it and forms the scaled error
+//     e_j = (w_j - w_hat_j) / U_jj, one DPP row broadcast hands e_j to the other 15 lanes, and
+//     every lane applies it to its 8 columns with U[j, its columns] read from the workgroup's
+//     LDS copy of the 128 x 128 block of U (upper triangular, so columns already done are left
+//     alone). Group parameters come from the row's 128 values at the start of the block.
+//     Codes, errors and dequantised values are written from registers at the end.
+//   * trailing updates, lazily in two levels: after each block, W[:, rest of its group of 4
+//     blocks] -= E_b U[b, rest of group] (K = 128); after the last block of a group,
+//     W[:, beyond the group] -= E_group U[group, beyond] (K = 512). Every column still receives
+//     the update of every earlier block before it is swept, as in the one-level scheme, with a
+//     quarter of the passes over W. Both products run on the fp32 MFMA GEMM.
 // The quantiser (reading of the paper's "quant"): xmin = min(0, min w), xmax = max(0, max w),
 // (-1, 1) when both are 0; scale = float32((xmax - xmin) / (2^b - 1)) in float64;
 // zero = rint(-xmin / scale); q = clamp(rint(w / scale) + zero, 0, 2^b - 1);
-// w_hat = float32(scale * (q - zero)). Divisions are IEEE float64 (no reciprocal), rint rounds
-// half to even, so a code depends only on (w, scale).
+// w_hat = float32(scale * (q - zero)). The code must be the one of the exact quotient w / scale
+// rounded half to even: the kernel forms t = w * (1 / scale) in fp32 (relative error below
+// 2.4e-7) and takes rint(t) unless t lies within 1e-6 (|t| + 1) of a half-integer, where it
+// falls back to the IEEE float64 division. w_hat in fp32 equals the float64 form exactly
+// (scale and q - zero are exact fp32 operands of one correctly rounded product).
+#include <utility>
+
 #include "kq_common.hpp"
 
 namespace kq {
 namespace {
 
-constexpr int OB = 128;       // block = group
-constexpr int OR = 64;        // rows per workgroup (one wave)
-constexpr int WLD = OR + 1;   // LDS stride of a W-block column
-constexpr int SB = 8;         // columns per register sub-block
+constexpr int OB = 128;          // block = group
+constexpr int LPR = 16;          // lanes per row
+constexpr int CPL = OB / LPR;    // columns per lane
+constexpr int RPW = 64 / LPR;    // rows per wave
+constexpr int RPG = 4 * RPW;     // rows per workgroup (4 waves)
+constexpr int GRP = 4;           // blocks per group of the two-level lazy update
 
-__device__ __forceinline__ float dequant(float scale, double zero, double q) {
-  return float(double(scale) * (q - zero));
+// v broadcast from lane `src` of each 16-lane row to the whole row (DPP row_newbcast)
+template <int src>
+__device__ __forceinline__ float row_bcast(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x150 + src, 0xF, 0xF,
+                                                    false));
 }
 
-__global__ __launch_bounds__(OR) void obs_sweep(float* __restrict__ W, int64_t d_out, int64_t ldw,
-                                                const float* __restrict__ U, int64_t ldu,
-                                                int64_t c0, int bits, uint8_t* __restrict__ codes,
-                                                int64_t ldq, float* __restrict__ scales,
-                                                float* __restrict__ zeros, int64_t ldsz,
-                                                int64_t blk, float* __restrict__ E, int64_t lde,
-                                                float* __restrict__ W_hat, int64_t ldwh) {
-  __shared__ float wb[OB * WLD];   // wb[c * WLD + r]
-  __shared__ float ub[OB * OB];    // ub[j * OB + k] = U[c0 + j][c0 + k]
-  __shared__ uint32_t qb[OR * OB / 4];
-  __shared__ float sc[OR];
-  __shared__ double zr[OR];
-  const int lane = threadIdx.x;
-  const int64_t r0 = int64_t(blockIdx.x) * OR;
-  const double maxq = double((1 << bits) - 1);
+// one column of the sweep: j = 8 * OWN + S (compile-time)
+template <int OWN, int S>
+__device__ __forceinline__ void sweep_col(float (&w)[CPL], float (&ev)[CPL], uint32_t (&qc)[CPL],
+                                          const float* ub, const float* rinv, int sub, int cb,
+                                          float scale, float inv_s, double dscale, float fzero,
+                                          float fmaxq) {
+  constexpr int j = OWN * CPL + S;
+  const float x = w[S];
+  const float t = x * inv_s;
+  float qf = __builtin_rintf(t);
+  const bool tie = fabsf(t - floorf(t) - 0.5f) <= 1e-6f * (fabsf(t) + 1.f);
+  if (tie && sub == OWN) qf = float(__builtin_rint(double(x) / dscale));
+  const float q = fminf(fmaxf(qf + fzero, 0.f), fmaxq);
+  const float wh = scale * (q - fzero);
+  const float e = (x - wh) * rinv[j];
+  if (sub == OWN) {
+    ev[S] = e;
+    qc[S] = uint32_t(q);
+  }
+  const float eb = row_bcast<OWN>(e);
+  const float4 u0 = *reinterpret_cast<const float4*>(ub + j * OB + cb);
+  const float4 u1 = *reinterpret_cast<const float4*>(ub + j * OB + cb + 4);
+  w[0] = fmaf(-eb, u0.x, w[0]);
+  w[1] = fmaf(-eb, u0.y, w[1]);
+  w[2] = fmaf(-eb, u0.z, w[2]);
+  w[3] = fmaf(-eb, u0.w, w[3]);
+  w[4] = fmaf(-eb, u1.x, w[4]);
+  w[5] = fmaf(-eb, u1.y, w[5]);
+  w[6] = fmaf(-eb, u1.z, w[6]);
+  w[7] = fmaf(-eb, u1.w, w[7]);
+}
 
-  for (int idx = lane; idx < OB * OB / 4; idx += OR) {
+template <int OWN>
+__device__ __forceinline__ void sweep_lane_cols(float (&w)[CPL], float (&ev)[CPL],
+                                                uint32_t (&qc)[CPL], const float* ub,
+                                                const float* rinv, int sub, int cb, float scale,
+                                                float inv_s, double dscale, float fzero,
+                                                float fmaxq) {
+  sweep_col<OWN, 0>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
+  sweep_col<OWN, 1>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
+  sweep_col<OWN, 2>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
+  sweep_col<OWN, 3>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
+  sweep_col<OWN, 4>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
+  sweep_col<OWN, 5>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
+  sweep_col<OWN, 6>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
+  sweep_col<OWN, 7>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
+}
+
+template <int... OWN>
+__device__ __forceinline__ void sweep_all(std::integer_sequence<int, OWN...>, float (&w)[CPL],
+                                          float (&ev)[CPL], uint32_t (&qc)[CPL], const float* ub,
+                                          const float* rinv, int sub, int cb, float scale,
+                                          float inv_s, double dscale, float fzero, float fmaxq) {
+  (sweep_lane_cols<OWN>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq), ...);
+}
+
+__global__ __launch_bounds__(256) void obs_sweep(float* __restrict__ W, int64_t d_out,
+                                                 int64_t ldw, const float* __restrict__ U,
+                                                 int64_t ldu, int64_t c0, int bits,
+                                                 uint8_t* __restrict__ codes, int64_t ldq,
+                                                 float* __restrict__ scales,
+                                                 float* __restrict__ zeros, int64_t ldsz,
+                                                 int64_t blk, float* __restrict__ E, int64_t lde,
+                                                 float* __restrict__ W_hat, int64_t ldwh) {
+  __shared__ __attribute__((aligned(16))) float ub[OB * OB];  // U[c0 + j][c0 + k]
+  __shared__ float rinv[OB];                                   // 1 / U_jj
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sub = lane & (LPR - 1), cb = sub * CPL;
+  const int64_t row = int64_t(blockIdx.x) * RPG + wave * RPW + (lane >> 4);
+  const bool live = row < d_out;
+  const int64_t rr = live ? row : d_out - 1;  // rows past the end recompute the last row
+
+  for (int idx = tid; idx < OB * OB / 4; idx += 256) {
     const int j = idx / (OB / 4), k4 = (idx % (OB / 4)) * 4;
     *reinterpret_cast<float4*>(ub + j * OB + k4) =
         *reinterpret_cast<const float4*>(U + (c0 + j) * ldu + c0 + k4);
   }
-  for (int idx = lane; idx < OR * OB / 4; idx += OR) {
-    const int r = idx / (OB / 4), c4 = (idx % (OB / 4)) * 4;
-    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r0 + r < d_out) x = *reinterpret_cast<const float4*>(W + (r0 + r) * ldw + c0 + c4);
-    wb[(c4 + 0) * WLD + r] = x.x;
-    wb[(c4 + 1) * WLD + r] = x.y;
-    wb[(c4 + 2) * WLD + r] = x.z;
-    wb[(c4 + 3) * WLD + r] = x.w;
+  if (tid < OB) rinv[tid] = 1.f / U[(c0 + tid) * ldu + c0 + tid];
+  float w[CPL];
+  {
+    const float4 a = *reinterpret_cast<const float4*>(W + rr * ldw + c0 + cb);
+    const float4 b = *reinterpret_cast<const float4*>(W + rr * ldw + c0 + cb + 4);
+    w[0] = a.x, w[1] = a.y, w[2] = a.z, w[3] = a.w, w[4] = b.x, w[5] = b.y, w[6] = b.z, w[7] = b.w;
   }
-  __syncthreads();
-
-  // group parameters from the current W (group start = block start)
+  // group parameters from the row's current 128 values (group start = block start)
   float xmin = 0.f, xmax = 0.f;
-  for (int c = 0; c < OB; ++c) {
-    const float v = wb[c * WLD + lane];
-    xmin = fminf(xmin, v);
-    xmax = fmaxf(xmax, v);
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    xmin = fminf(xmin, w[c]);
+    xmax = fmaxf(xmax, w[c]);
+  }
+#pragma unroll
+  for (int o = 1; o < LPR; o <<= 1) {
+    xmin = fminf(xmin, __shfl_xor(xmin, o, LPR));
+    xmax = fmaxf(xmax, __shfl_xor(xmax, o, LPR));
   }
   if (xmax == xmin) {
     xmin = -1.f;
     xmax = 1.f;
   }
+  const double maxq = double((1 << bits) - 1);
   const float scale = float((double(xmax) - double(xmin)) / maxq);
   const double zero = __builtin_rint(-double(xmin) / double(scale));
-  sc[lane] = scale;
-  zr[lane] = zero;
-  if (r0 + lane < d_out) {
-    scales[(r0 + lane) * ldsz + blk] = scale;
-    zeros[(r0 + lane) * ldsz + blk] = float(zero);
-  }
-  uint8_t* qrow = reinterpret_cast<uint8_t*>(qb) + lane * OB;
-
-  for (int j0 = 0; j0 < OB; j0 += SB) {
-    float w[SB], e[SB];
-#pragma unroll
-    for (int jj = 0; jj < SB; ++jj) w[jj] = wb[(j0 + jj) * WLD + lane];
-#pragma unroll
-    for (int jj = 0; jj < SB; ++jj) {
-      double q = __builtin_rint(double(w[jj]) / double(scale)) + zero;
-      q = q < 0.0 ? 0.0 : (q > maxq ? maxq : q);
-      const float wh = dequant(scale, zero, q);
-      const float ej = (w[jj] - wh) / ub[(j0 + jj) * OB + j0 + jj];
-      e[jj] = ej;
-      qrow[j0 + jj] = uint8_t(q);
-#pragma unroll
-      for (int kk = jj + 1; kk < SB; ++kk) w[kk] = fmaf(-ej, ub[(j0 + jj) * OB + j0 + kk], w[kk]);
-    }
-#pragma unroll
-    for (int jj = 0; jj < SB; ++jj) wb[(j0 + jj) * WLD + lane] = e[jj];
-    for (int k = j0 + SB; k < OB; ++k) {
-      float acc = wb[k * WLD + lane];
-#pragma unroll
-      for (int jj = 0; jj < SB; ++jj) acc = fmaf(-e[jj], ub[(j0 + jj) * OB + k], acc);
-      wb[k * WLD + lane] = acc;
-    }
-  }
+  const float fzero = float(zero), inv_s = 1.f / scale;
   __syncthreads();
 
-  // write back: errors, dequantised values (W and W_hat), codes
-  for (int idx = lane; idx < OR * OB / 4; idx += OR) {
-    const int r = idx / (OB / 4), c4 = (idx % (OB / 4)) * 4;
-    const int64_t gr = r0 + r;
-    if (gr >= d_out) continue;
-    const float4 ev = make_float4(wb[(c4 + 0) * WLD + r], wb[(c4 + 1) * WLD + r],
-                                  wb[(c4 + 2) * WLD + r], wb[(c4 + 3) * WLD + r]);
-    *reinterpret_cast<float4*>(E + gr * lde + c4) = ev;
-    const uint32_t qw = qb[r * (OB / 4) + c4 / 4];
-    const float s = sc[r];
-    const double z = zr[r];
-    const float4 hv = make_float4(dequant(s, z, double(qw & 0xFF)), dequant(s, z, double((qw >> 8) & 0xFF)),
-                                  dequant(s, z, double((qw >> 16) & 0xFF)), dequant(s, z, double(qw >> 24)));
-    *reinterpret_cast<float4*>(W + gr * ldw + c0 + c4) = hv;
-    if (W_hat) *reinterpret_cast<float4*>(W_hat + gr * ldwh + c0 + c4) = hv;
-    *reinterpret_cast<uint32_t*>(codes + gr * ldq + c0 + c4) = qw;
+  float ev[CPL];
+  uint32_t qc[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) ev[c] = 0.f, qc[c] = 0u;
+  sweep_all(std::make_integer_sequence<int, LPR>{}, w, ev, qc, ub, rinv, sub, cb, scale, inv_s,
+            double(scale), fzero, float(maxq));
+
+  if (!live) return;
+  if (sub == 0) {
+    scales[row * ldsz + blk] = scale;
+    zeros[row * ldsz + blk] = fzero;
   }
+  float wh[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) wh[c] = scale * (float(qc[c]) - fzero);
+  const float4 h0 = make_float4(wh[0], wh[1], wh[2], wh[3]);
+  const float4 h1 = make_float4(wh[4], wh[5], wh[6], wh[7]);
+  *reinterpret_cast<float4*>(W + row * ldw + c0 + cb) = h0;
+  *reinterpret_cast<float4*>(W + row * ldw + c0 + cb + 4) = h1;
+  if (W_hat) {
+    *reinterpret_cast<float4*>(W_hat + row * ldwh + c0 + cb) = h0;
+    *reinterpret_cast<float4*>(W_hat + row * ldwh + c0 + cb + 4) = h1;
+  }
+  *reinterpret_cast<float4*>(E + row * lde + cb) = make_float4(ev[0], ev[1], ev[2], ev[3]);
+  *reinterpret_cast<float4*>(E + row * lde + cb + 4) = make_float4(ev[4], ev[5], ev[6], ev[7]);
+  uint2 pk;
+  pk.x = qc[0] | (qc[1] << 8) | (qc[2] << 16) | (qc[3] << 24);
+  pk.y = qc[4] | (qc[5] << 8) | (qc[6] << 16) | (qc[7] << 24);
+  *reinterpret_cast<uint2*>(codes + row * ldq + c0 + cb) = pk;
 }
 
 }  // namespace
 
 size_t obs_ws_bytes(int64_t d_out, int64_t d_in) {
   if (d_out <= 0 || d_in <= 0) return 0;
-  return align256(size_t(d_out) * OB * sizeof(float)) + 256;
+  return align256(size_t(d_out) * GRP * OB * sizeof(float)) + 256;
 }
 
 int obs_launch(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* U, int64_t ldu,
                int bits, uint8_t* codes, float* scales, float* zeros, float* err, float* W_hat,
                void* ws, hipStream_t s) {
   const int64_t nblk = d_in / OB;
-  const unsigned grid = unsigned(cdiv(d_out, OR));
-  for (int64_t b = 0; b < nblk; ++b) {
-    const int64_t c0 = b * OB;
-    float* E = err ? err + c0 : static_cast<float*>(ws);
-    const int64_t lde = err ? d_in : OB;
-    KQ_TRY(launch("obs_sweep", obs_sweep, dim3(grid), dim3(OR), 0, s, W, d_out, ldw, U, ldu, c0,
-                  bits, codes, d_in, scales, zeros, nblk, b, E, lde, W_hat ? W_hat : nullptr,
-                  d_in));
-    const int64_t rem = d_in - c0 - OB;
+  const unsigned grid = unsigned(cdiv(d_out, RPG));
+  for (int64_t g0 = 0; g0 < nblk; g0 += GRP) {
+    const int64_t gend = g0 + GRP < nblk ? g0 + GRP : nblk;
+    // errors of this group's blocks: the caller's err (ld d_in) or the workspace (ld GRP * OB)
+    float* Eg = err ? err + g0 * OB : static_cast<float*>(ws);
+    const int64_t lde = err ? d_in : GRP * OB;
+    for (int64_t b = g0; b < gend; ++b) {
+      const int64_t c0 = b * OB;
+      float* Eb = Eg + (b - g0) * OB;
+      KQ_TRY(launch("obs_sweep", obs_sweep, dim3(grid), dim3(256), 0, s, W, d_out, ldw, U, ldu,
+                    c0, bits, codes, d_in, scales, zeros, nblk, b, Eb, lde, W_hat, d_in));
+      const int64_t near = (gend - b - 1) * OB;  // rest of the group
+      if (near > 0)
+        KQ_TRY(gemm_f32(0, d_out, near, OB, -1.f, Eb, lde, U + c0 * ldu + c0 + OB, ldu, 1.f,
+                        W + c0 + OB, ldw, s, "obs_trailing_update"));
+    }
+    const int64_t rem = d_in - gend * OB;  // beyond the group
     if (rem > 0)
-      KQ_TRY(gemm_f32(0, d_out, rem, OB, -1.f, E, lde, U + c0 * ldu + c0 + OB, ldu, 1.f,
-                      W + c0 + OB, ldw, s, "obs_trailing_update"));
+      KQ_TRY(gemm_f32(0, d_out, rem, (gend - g0) * OB, -1.f, Eg, lde, U + g0 * OB * ldu + gend * OB,
+                      ldu, 1.f, W + gend * OB, ldw, s, "obs_trailing_update"));
   }
   return KRONQ_OK;
 }
