@@ -17,6 +17,9 @@
 //     alpha/beta and writes both triangles (the mirror through an LDS transpose), so H is
 //     exactly symmetric.
 // fp32 path (small fp32 inputs): a plain LDS-tiled fp32 FMA kernel over the full matrix.
+#include <type_traits>
+#include <utility>
+
 #include "kq_common.hpp"
 
 namespace kq {
@@ -205,14 +208,19 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
 // banks. An MFMA operand (32 channels x 8 tokens per lane) is two ds_read_b64_tr_b16: within a
 // group of 16 lanes, lane L names token row tb + L/4 at channels cb + 4 (L % 4) .. +3 and gets
 // back its own channel cb + L at tokens tb .. tb+3.
-// Per stage: 16 MFMAs on the first 16 tokens, then one raw s_barrier (after this wave's own
-// loads for the next stage have landed, s_waitcnt vmcnt), which both publishes the next stage
-// and frees the oldest buffer for the next load, then 16 MFMAs on the last 16 tokens while the
-// next stage's first operands are read. A diagonal tile loads its block into both operand rings
-// so that no buffer is chosen at run time (which would force full waits on every load).
+// Schedule. A stage is two half-stages of 16 tokens; each half-stage is 16 MFMAs on operands read
+// during the previous half-stage, with the next half-stage's 16 reads issued two per MFMA over
+// its first eight MFMAs. Between the two halves of stage s, one raw s_barrier (after this wave's
+// own loads of stage s + 1 have landed, s_waitcnt vmcnt) both publishes stage s + 1 and frees
+// the buffer of stage s - 1, into which stage s + 3 is then issued. The steady state is unrolled
+// over the four buffers with every index a constant and no branch, so the compiler places only
+// the waits the data needs; the last few stages run a checked copy of the same schedule.
+// A diagonal tile loads its block into both operand rings so that no buffer is chosen at run
+// time (which would force full waits on every load).
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 #define KQ_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 constexpr int DK = 32;        // tokens per stage
+constexpr int RING = 4;       // stage buffers per operand
 constexpr int SBUF = 4096;    // dwords per operand per stage
 
 template <int N>
@@ -243,8 +251,8 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
                                                         int64_t rows_per_slice, int T, int Tf) {
   __shared__ __attribute__((aligned(16))) uint32_t a0[SBUF], a1[SBUF], a2[SBUF], a3[SBUF];
   __shared__ __attribute__((aligned(16))) uint32_t b0[SBUF], b1[SBUF], b2[SBUF], b3[SBUF];
-  uint32_t* const bufa[4] = {a0, a1, a2, a3};
-  uint32_t* const bufb[4] = {b0, b1, b2, b3};
+  uint32_t* const bufa[RING] = {a0, a1, a2, a3};
+  uint32_t* const bufb[RING] = {b0, b1, b2, b3};
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int slice = blockIdx.x % n_slices;
   int I = 0, rem = blockIdx.x / n_slices;
@@ -307,17 +315,61 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
     else
       wait_vm<0>();
   };
+  // interleave pattern for one half-stage: 16 (MFMA, DS read) pairs
+  // the next half-stage's 16 operand reads go out two per MFMA over the first 8 MFMAs: a use of
+  // a transposing read's result waits for every outstanding LDS read, so they must all have
+  // landed by the start of the next half-stage
+  auto interleave = [&]() {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // two LDS reads
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+  };
+  // this wave's loads of stage s + 1 are done when at most `newer` later stages are pending
+  auto wait_newer = [&](int newer) {
+    if (newer >= 3) wait_vm<24>();
+    else if (newer == 2) wait_vm<16>();
+    else if (newer == 1) wait_vm<8>();
+    else wait_vm<0>();
+  };
   if (n_st > 0) {
-    issue(0, 0);
-    if (n_st > 1) issue(1, 1);
-    if (n_st > 2) issue(2, 2);
-    wait_stage(n_st > 2 ? 2 : n_st - 1);
+#pragma unroll
+    for (int p = 0; p < RING - 1; ++p)
+      if (p < n_st) issue(p, p);
+    wait_newer(min(RING - 2, n_st - 1));
     __builtin_amdgcn_s_barrier();
     frags(0, 0, 0);
   }
-  for (int s0 = 0; s0 < n_st; s0 += 4) {
+  // steady state: stage s issues stage s + RING - 1 unconditionally, no branches inside
+  const int s_main = n_st >= 2 * RING - 1 ? ((n_st - RING + 1) / RING) * RING : 0;
+  auto body = [&](auto ucst, int s) {
+    constexpr int u = decltype(ucst)::value;
+    __builtin_amdgcn_sched_barrier(0);
+    frags(u, 1, 1);
+    mfmas(0);
+    interleave();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm<(RING - 3) * 8>();
+    __builtin_amdgcn_s_barrier();
+    issue(s + RING - 1, (u + RING - 1) % RING);
+    __builtin_amdgcn_sched_barrier(0);
+    frags((u + 1) % RING, 0, 0);
+    mfmas(1);
+    interleave();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  for (int s0 = 0; s0 < s_main; s0 += RING) {
+    body(std::integral_constant<int, 0>{}, s0);
+    body(std::integral_constant<int, 1>{}, s0 + 1);
+    body(std::integral_constant<int, 2>{}, s0 + 2);
+    body(std::integral_constant<int, 3>{}, s0 + 3);
+  }
+  // tail (the last few stages), with the bounds checks
+  for (int s0 = s_main; s0 < n_st; s0 += RING) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < RING; ++u) {
       const int s = s0 + u;  // stage s lives in buffer u
       if (s < n_st) {
         frags(u, 1, 1);
@@ -325,10 +377,11 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
         mfmas(0);
         __builtin_amdgcn_sched_barrier(0);
         if (s + 1 < n_st) {
-          wait_stage(s + 2 < n_st ? 1 : 0);
+          const int last = min(n_st - 1, s + RING - 2);  // newest stage already issued
+          wait_newer(last - (s + 1));
           __builtin_amdgcn_s_barrier();
-          if (s + 3 < n_st) issue(s + 3, (u + 3) & 3);
-          frags((u + 1) & 3, 0, 0);
+          if (s + RING - 1 < n_st) issue(s + RING - 1, (u + RING - 1) % RING);
+          frags((u + 1) % RING, 0, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
         mfmas(1);
