@@ -43,7 +43,8 @@ import itertools
 import numpy as np
 
 __all__ = [
-    "widen_bf16", "as_f64", "covariance", "traces", "rescale_factors", "hadamard", "rht_matrix",
+    "widen_bf16", "as_f64", "covariance", "covariance_diag", "traces", "rescale_factors",
+    "hadamard", "rht_matrix",
     "biip_forward", "biip_revert", "damp", "inverse_cholesky_factor", "group_params",
     "quantize", "obs_unblocked", "obs_blocked", "kfac_loss", "allocate_bits", "count_avg_bits",
     "RESCALE_IN", "RESCALE_OUT", "ROT_IN", "ROT_OUT", "BIIP",
@@ -90,6 +91,17 @@ def covariance(A, chunk: int = 8192) -> np.ndarray:
 # ----------------------------------------------------------------------------------------------
 # O2: traces and the sensitivity score  (Sec. 4.3 eq. sensitivity)
 # ----------------------------------------------------------------------------------------------
+def covariance_diag(A, chunk: int = 8192) -> np.ndarray:
+    """diag(A^T A) in float64: each channel's sum of squares over the tokens (the diagonal of
+    O1, without the off-diagonal products)."""
+    n, d = A.shape
+    out = np.zeros(d, dtype=np.float64)
+    for t0 in range(0, n, chunk):
+        blk = as_f64(A[t0:t0 + chunk])
+        out += np.einsum("ij,ij->j", blk, blk)
+    return out
+
+
 def traces(HX: np.ndarray, HG: np.ndarray) -> tuple[float, float, float]:
     """(tr H_X, tr H_G, s = tr H_G * tr H_X)."""
     tx = float(np.sum(np.diag(HX)))
@@ -107,17 +119,23 @@ def _quarter_ratio(h: np.ndarray, a: np.ndarray) -> np.ndarray:
     return s  # reading R10: 1 where a norm or a diagonal entry is zero
 
 
+def _diag(H) -> np.ndarray:
+    H = np.asarray(H)
+    return (H if H.ndim == 1 else np.diag(H)).astype(np.float64)
+
+
 def rescale_factors(W: np.ndarray, HX: np.ndarray, HG: np.ndarray | None, flags: int = BIIP):
     """s^X_j = (H_X,jj / ||W_:,j||^2)^(1/4) and s^G_i = (H_G,ii / ||W_i,:||^2)^(1/4), both from
-    the original W (1 for a side whose rescale is off)."""
+    the original W (1 for a side whose rescale is off). Only the diagonals of H_X and H_G enter,
+    so either the matrices or their diagonals (1-D) may be passed."""
     W = as_f64(W)
     a = np.sum(W * W, axis=0)  # squared column norms (input side)
     b = np.sum(W * W, axis=1)  # squared row norms (output side)
-    sx = _quarter_ratio(np.diag(HX).astype(np.float64), a) if flags & RESCALE_IN else np.ones(W.shape[1])
+    sx = _quarter_ratio(_diag(HX), a) if flags & RESCALE_IN else np.ones(W.shape[1])
     if flags & RESCALE_OUT:
         if HG is None:
             raise ValueError("output-side rescaling needs H_G")
-        sg = _quarter_ratio(np.diag(HG).astype(np.float64), b)
+        sg = _quarter_ratio(_diag(HG), b)
     else:
         sg = np.ones(W.shape[0])
     return sx, sg

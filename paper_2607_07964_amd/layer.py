@@ -58,11 +58,13 @@ class LayerState:
 
     @staticmethod
     def allocate(d_out: int, d_in: int, n_tokens: int, device, keep_err: bool = False,
-                 x_dtype=torch.bfloat16, g_dtype=torch.bfloat16) -> "LayerState":
+                 x_dtype=torch.bfloat16, g_dtype=torch.bfloat16,
+                 cov_ws: bool = True) -> "LayerState":
+        """``cov_ws=False`` leaves the covariance workspaces out (a caller that shares one)."""
         f32 = dict(dtype=torch.float32, device=device)
 
         def ws(op, a, b, n, dt=torch.bfloat16):
-            if op == K.OP_COV and dt != torch.bfloat16:
+            if op == K.OP_COV and (dt != torch.bfloat16 or not cov_ws):
                 return torch.empty(256, dtype=torch.uint8, device=device)
             return K.workspace(op, a, b, n, device)
 
@@ -163,3 +165,51 @@ def revert(st: LayerState, rin: RotParams, rout: RotParams, out: Optional[torch.
     K.kronq_rotate(st.W, out, None, None, rin.sign, rout.sign, rin.q28, rout.q28, st.sx, st.sg,
                    flags | K.INVERSE, ws if ws is not None else st.ws_rot)
     return out
+
+
+@dataclasses.dataclass
+class BlockResult:
+    """Outcome of ``quantize_block``: per-layer states (codes, scales, ...) and the allocation."""
+    names: list
+    states: list
+    scores: list      # post-BiIP tr(H_X) tr(H_G) per layer (Sec. 4.3 sensitivity)
+    bits: tuple
+    objective: float
+
+
+def quantize_block(specs, X_by_key: dict, Gs: list, W0s: list, rots: list,
+                   avg_bits: float = 3.0, choices=(2, 3, 4), flags: int = K.BIIP,
+                   keep_err: bool = False) -> BlockResult:
+    """The layers of one decoder block with sensitivity-driven bit allocation (Sec. 4.3).
+
+    1. One raw covariance per distinct input (q/k/v share one X, gate/up another); each layer
+       takes a copy, since BiIP rescales H_X with that layer's own S_X. Then per layer: H_G,
+       BiIP and the post-BiIP traces.
+    2. Bits from the exhaustive allocation over the layers' scores s = tr(H_X) tr(H_G) under the
+       parameter-weighted average budget (host side; needs the traces, so it synchronises).
+    3. Per layer: damping + inverse-Cholesky factor and the OBS sweep at the allocated width.
+    ``X_by_key`` maps each spec's ``x_key`` to its X; ``rots`` holds (RotParams in, out) pairs."""
+    dev = Gs[0].device
+    n = specs[0].n_tokens
+    d_max = max(max(sp.d_in, sp.d_out) for sp in specs)
+    ws_cov = K.workspace(K.OP_COV, 0, d_max, n, dev)  # shared: the calls are stream-ordered
+    raw = {}
+    for sp in specs:
+        if sp.x_key not in raw:
+            H = torch.empty(sp.d_in, sp.d_in, dtype=torch.float32, device=dev)
+            K.kronq_accumulate_cov(X_by_key[sp.x_key], H, 1.0, 0.0, ws_cov)
+            raw[sp.x_key] = H
+    states = []
+    for sp, G, W0, (rin, rout) in zip(specs, Gs, W0s, rots):
+        st = LayerState.allocate(sp.d_out, sp.d_in, n, dev, keep_err=keep_err, cov_ws=False)
+        st.HX.copy_(raw[sp.x_key])
+        K.kronq_accumulate_cov(G, st.HG, 1.0, 0.0, ws_cov)
+        biip(st, W0, rin, rout, flags)
+        states.append(st)
+    del raw
+    scores = [float(v) for v in torch.stack([st.tr_post[2] for st in states]).cpu()]
+    weights = [sp.d_out * sp.d_in for sp in specs]
+    bits, obj = K.kronq_allocate_bits(scores, weights, choices, avg_bits)
+    for sp, st, b in zip(specs, states, bits):
+        solve(st, int(b), sp.damp)
+    return BlockResult([sp.name for sp in specs], states, scores, tuple(bits), obj)

@@ -265,12 +265,15 @@ BLOCK_SHAPES = (  # LLaMA-3-8B decoder block: (name, d_out, d_in, shared-X key)
 )
 
 
-def block_layers(n_tokens: Optional[int] = None, seed: int = 4) -> list[LayerSpec]:
+def block_layers(n_tokens: Optional[int] = None, seed: int = 4, shrink: int = 1) -> list[LayerSpec]:
     """Workload 5: the 7 linears of one LLaMA-3-8B block. q/k/v share one X, gate/up share one
-    X; bits are assigned later by the sensitivity-driven allocation."""
+    X; bits are assigned later by the sensitivity-driven allocation. ``shrink`` divides every
+    dimension (16 keeps d_in a multiple of 128 and 14336 / 16 = 896 = 28 * 32 of the 28 * 2^k
+    form), for block runs the float64 oracle can repeat in seconds."""
     n = n_tokens or N_CAL
     out = []
     for li, (name, d_out, d_in, xkey) in enumerate(BLOCK_SHAPES):
+        d_out, d_in = d_out // shrink, d_in // shrink
         lseed = int(np.random.SeedSequence([seed, li]).generate_state(1)[0])
         xkind = "laplace" if xkey == "mlp_act" else "normal_t3"
         out.append(_layer(name, d_out, d_in, n, 3, lseed, xkind, 1.5, 0.02, torch.bfloat16,

@@ -1,0 +1,124 @@
+"""Workload 5: the seven linears of one LLaMA-3-8B decoder block with the sensitivity-driven bit
+allocation of Sec. 4.3 (q/k/v share one input covariance, gate/up another).
+
+* At 1/16 of every dimension the float64 oracle repeats the whole block: covariances, BiIP,
+  post-BiIP scores, the exhaustive allocation, the factor and the blocked sweep per layer.
+* At full size (N = 262144) the oracle checks what it can compute exactly at that size: the
+  post-BiIP score of every layer from the covariance diagonals and W's norms (rotations keep the
+  trace, so tr(S^-1 H S^-1) = sum_j h_jj / s_j^2), and the allocation those scores give.
+"""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from gpu_util import DEV, note, oracle_view, rel_frob, rot_device, rot_oracle, to_np
+from paper_2607_07964_amd import kronq as K
+from paper_2607_07964_amd import layer as L
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-3
+CHOICES, AVG = (2, 3, 4), 3.0
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    K.load()
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+
+
+def _inputs(specs):
+    Xs, Gs, Ws, rots, rots_np = {}, [], [], [], []
+    for sp in specs:
+        if sp.x_key not in Xs:
+            Xs[sp.x_key] = synth.gen_matrix(sp.x, DEV)
+        Gs.append(synth.gen_matrix(sp.g, DEV))
+        Ws.append(synth.gen_matrix(sp.w, DEV))
+        ri = synth.rotation_params(sp.d_in, sp.seed, sp.name + ":in")
+        ro = synth.rotation_params(sp.d_out, sp.seed, sp.name + ":out")
+        rots.append((rot_device(ri), rot_device(ro)))
+        rots_np.append((rot_oracle(ri), rot_oracle(ro)))
+    return Xs, Gs, Ws, rots, rots_np
+
+
+def _allocation_matches(gpu_bits, scores, weights, avg):
+    """The oracle's allocation on the oracle's scores. A different vector is accepted only when
+    the oracle's own two best feasible assignments are within the score tolerance of each other
+    (a near tie that the 1e-3 score agreement cannot decide) and the GPU's vector is one of them."""
+    ref_bits, ref_obj = O.allocate_bits(scores, weights, CHOICES, avg)
+    if tuple(gpu_bits) == tuple(ref_bits):
+        return True
+    budget = avg * sum(weights)
+    objs = {}
+    for b in itertools.product(CHOICES, repeat=len(scores)):
+        if sum(w * x for w, x in zip(weights, b)) <= budget:
+            objs[b] = sum(s / (2 ** x - 1) ** 2 for s, x in zip(scores, b))
+    return tuple(gpu_bits) in objs and objs[tuple(gpu_bits)] <= ref_obj * (1 + 4 * TOL)
+
+
+@pytest.mark.parametrize("avg", [3.0, 2.5])
+def test_block_small_end_to_end(avg):
+    """avg 3.0 is the workload's budget; at 2.5 the allocation is not uniform."""
+    specs = synth.block_layers(n_tokens=4096, shrink=16)
+    Xs, Gs, Ws, rots, rots_np = _inputs(specs)
+    note(f"block 1/16 dims, N=4096, avg {avg}")
+    res = L.quantize_block(specs, Xs, Gs, Ws, rots, avg, CHOICES)
+    for st in res.states:
+        L.check(st)
+    torch.cuda.synchronize()
+    # oracle: the same three phases
+    hx_raw = {k: O.covariance(oracle_view(X.cpu())) for k, X in Xs.items()}
+    refs, scores = [], []
+    for sp, G, W, (ri, ro) in zip(specs, Gs, Ws, rots_np):
+        hg = O.covariance(oracle_view(G.cpu()))
+        b = O.biip_forward(oracle_view(W.cpu()), hx_raw[sp.x_key], hg, ri, ro)
+        scores.append(O.traces(b["HX"], b["HG"])[2])
+        refs.append(b)
+    weights = [sp.d_out * sp.d_in for sp in specs]
+    np.testing.assert_allclose(res.scores, scores, rtol=TOL)
+    assert _allocation_matches(res.bits, scores, weights, avg)
+    print(f"block bits {res.bits} (avg {np.dot(weights, res.bits) / sum(weights):.3f})")
+    for sp, st, b, nbits in zip(specs, res.states, refs, res.bits):
+        U = O.inverse_cholesky_factor(O.damp(b["HX"], sp.damp))
+        assert rel_frob(to_np(st.U), U) < TOL, sp.name
+        q = O.obs_blocked(b["W"], U, nbits, 128, 128)
+        agree = float(np.mean(to_np(st.codes) == q["codes"]))
+        print(f"{sp.name} {sp.d_out}x{sp.d_in} {nbits}-bit: code agreement {agree:.6f}")
+        assert agree >= 0.995, sp.name
+
+
+@pytest.mark.slow
+def test_block_full_size_scores_and_allocation():
+    specs = synth.block_layers()
+    Xs, Gs, Ws, rots, rots_np = _inputs(specs)
+    note("block full size, N=262144")
+    res = L.quantize_block(specs, Xs, Gs, Ws, rots, AVG, CHOICES)
+    for st in res.states:
+        L.check(st)
+    torch.cuda.synchronize()
+
+    def diag(A):  # float64 sums of squares over CPU copies of the generator's tensor
+        acc = np.zeros(A.shape[1])
+        for t0 in range(0, A.shape[0], 8192):
+            acc += O.covariance_diag(oracle_view(A[t0:t0 + 8192].cpu()))
+        return acc
+
+    hx_diag = {k: diag(X) for k, X in Xs.items()}
+    scores = []
+    for sp, G, W in zip(specs, Gs, Ws):
+        w = oracle_view(W.cpu())
+        hg_diag = diag(G)
+        sx, sg = O.rescale_factors(w, hx_diag[sp.x_key], hg_diag)
+        scores.append(float(np.sum(hx_diag[sp.x_key] / sx ** 2) * np.sum(hg_diag / sg ** 2)))
+    weights = [sp.d_out * sp.d_in for sp in specs]
+    print("scores gpu", res.scores, "oracle", scores, "bits", res.bits)
+    np.testing.assert_allclose(res.scores, scores, rtol=TOL)
+    assert _allocation_matches(res.bits, scores, weights, AVG)
+    for sp, st, nbits in zip(specs, res.states, res.bits):
+        codes = to_np(st.codes)
+        assert codes.max() <= 2 ** nbits - 1, sp.name
+        u = to_np(st.U)
+        assert np.all(np.diag(u) > 0) and np.all(np.tril(u, -1) == 0), sp.name

@@ -64,6 +64,18 @@ def test_covariance_bf16_exact():
     np.testing.assert_array_equal(h1, xf.T @ xf)
 
 
+def test_covariance_diag_is_brute_force_diagonal():
+    # per-channel sums of squares by a plain loop, on bf16 bits (exact) and on floats
+    X = synth.gen_matrix(synth.small_spec(8, 16, 300).x)
+    bits = synth.bf16_bits(X)
+    xf = X.double().numpy()
+    ref = np.array([sum(xf[t, j] ** 2 for t in range(300)) for j in range(16)])
+    np.testing.assert_array_equal(O.covariance_diag(bits, chunk=7), ref)
+    A = rng(2).standard_normal((41, 6))
+    ref = np.array([sum(A[t, j] * A[t, j] for t in range(41)) for j in range(6)])
+    np.testing.assert_allclose(O.covariance_diag(A, chunk=5), ref, rtol=1e-14)
+
+
 # ------------------------------------------------------------------------------------ O2/O3
 def test_traces_closed_form():
     hx, hg = np.diag([1.0, 2.0, 3.0]), np.diag([4.0, 5.0])
@@ -94,6 +106,14 @@ def test_rescale_output_side_closed_form():
     np.testing.assert_allclose(np.sum(out["W"] ** 2, 1), np.diag(out["HG"]), rtol=1e-12)
     np.testing.assert_allclose(np.diag(out["HG"]), np.sqrt(h * b), rtol=1e-12)
     assert np.all(out["sx"] == 1.0)
+
+
+def test_rescale_from_diagonals_only():
+    # only diag(H_X), diag(H_G) enter eq. rescale: the 1-D form gives identical factors
+    W, HX, HG = _problem()
+    sx, sg = O.rescale_factors(W, HX, HG)
+    sx1, sg1 = O.rescale_factors(W, np.diag(HX).copy(), np.diag(HG).copy())
+    assert np.array_equal(sx, sx1) and np.array_equal(sg, sg1)
 
 
 def test_rescale_zero_norm_gives_one():
