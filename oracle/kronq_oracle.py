@@ -44,7 +44,7 @@ import numpy as np
 
 __all__ = [
     "widen_bf16", "as_f64", "covariance", "covariance_diag", "traces", "rescale_factors",
-    "hadamard", "rht_matrix",
+    "hadamard", "rht_matrix", "rht_rows",
     "biip_forward", "biip_revert", "damp", "inverse_cholesky_factor", "group_params",
     "quantize", "obs_unblocked", "obs_blocked", "kfac_loss", "allocate_bits", "count_avg_bits",
     "RESCALE_IN", "RESCALE_OUT", "ROT_IN", "ROT_OUT", "BIIP",
@@ -169,6 +169,31 @@ def rht_matrix(d: int, sign, q28=None) -> np.ndarray:
             raise ValueError("d must be 28 * 2^k when a 28-point factor is given")
         core = np.kron(np.asarray(q28, dtype=np.float64), hadamard(m) / np.sqrt(m))
     return core * sign[None, :]
+
+
+def rht_rows(d: int, sign, q28, rows) -> np.ndarray:
+    """Selected rows of the V of ``rht_matrix``, entry by entry from the same definition:
+    V[i, j] = (-1)^popcount(i & j) sigma_j / sqrt(d), or, when d = 28 m with i = a m + b and
+    j = a' m + b', V[i, j] = Q28[a, a'] (-1)^popcount(b & b') sigma_j / sqrt(m). For sizes whose
+    dense matrix is too large to form (d = 28672 is 6.6 GB)."""
+    sign = np.asarray(sign, dtype=np.float64)
+    rows = np.asarray(rows, dtype=np.int64)
+    j = np.arange(d, dtype=np.int64)
+    if q28 is None:
+        m, lo_i, lo_j, scale = d, rows, j, np.ones((len(rows), d))
+    else:
+        m = d // 28
+        if 28 * m != d:
+            raise ValueError("d must be 28 * 2^k when a 28-point factor is given")
+        q = np.asarray(q28, dtype=np.float64)
+        lo_i, lo_j = rows % m, j % m
+        scale = q[(rows // m)[:, None], (j // m)[None, :]]
+    x = lo_i[:, None] & lo_j[None, :]
+    par = np.zeros_like(x)
+    while np.any(x):
+        par ^= x & 1
+        x = x >> 1
+    return scale * np.where(par == 1, -1.0, 1.0) / np.sqrt(m) * sign[None, :]
 
 
 def biip_forward(W, HX, HG, rot_in=None, rot_out=None, flags: int = BIIP):

@@ -140,6 +140,30 @@ def test_loss_invariant_under_rescale():
 
 
 # ------------------------------------------------------------------------------------ O4
+@pytest.mark.parametrize("d", [64, 28 * 8])
+def test_rht_rows_entrywise(d):
+    """Rows formed entry by entry: equal to the dense builder's rows, and, for the 28-factor
+    form, to rows of the explicit Kronecker product built here with a 2 x 2 block loop."""
+    r = rng(d)
+    sign = np.where(r.standard_normal(d) < 0, -1.0, 1.0)
+    q28 = None
+    if d % 28 == 0:
+        q28, _ = np.linalg.qr(r.standard_normal((28, 28)))
+    rows = [0, 1, d // 2 + 3, d - 1]
+    V = O.rht_matrix(d, sign, q28)
+    np.testing.assert_allclose(O.rht_rows(d, sign, q28, rows), V[rows], rtol=0, atol=1e-15)
+    R = O.rht_rows(d, sign, q28, np.arange(d))
+    np.testing.assert_allclose(R @ R.T, np.eye(d), atol=1e-12)
+    if q28 is not None:
+        m = d // 28
+        for i in rows:
+            a, b = divmod(i, m)
+            for j in range(0, d, 37):
+                a2, b2 = divmod(j, m)
+                h = (-1.0) ** bin(b & b2).count("1")
+                assert abs(R[i, j] - q28[a, a2] * h / np.sqrt(m) * sign[j]) < 1e-15
+
+
 @pytest.mark.parametrize("m", [1, 2, 8, 64])
 def test_hadamard_matches_scipy(m):
     assert np.array_equal(O.hadamard(m), scipy.linalg.hadamard(m).astype(float))
