@@ -123,7 +123,8 @@ int kronq_traces(const float* HX, int64_t d_in, int64_t ldx, const float* HG, in
  * on the slow index), and U likewise from sign_out / q28_out. H is the Sylvester Hadamard.
  * Inverse (KRONQ_INVERSE, W only, sx and sg are inputs):
  *   W <- diag(1/sg) U^T W_in V diag(1/sx).
- *   W_in   device, w_dtype KRONQ_BF16 or KRONQ_FP32, [d_out x ldw_in]; may alias W when fp32.
+ *   W_in   device, w_dtype KRONQ_BF16 or KRONQ_FP32, [d_out x ldw_in], 16-byte aligned rows
+ *          (ldw_in divisible by 8 for bf16, by 4 for fp32); may alias W when fp32.
  *   W      device fp32 [d_out x ldw].
  *   HX     device fp32 [d_in x ldx] (forward; may be NULL for INVERSE).
  *   HG     device fp32 [d_out x ldg] or NULL; required by KRONQ_RESCALE_OUT.

@@ -2,9 +2,10 @@
 //
 // bf16 path: a syrk on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16). bf16 x bf16 products
 // are exact in fp32 and accumulate in fp32.
-//   * Work split: the token dimension is cut into S slices (split-K). Workgroup b takes slice
-//     b % S; workgroups are dealt round-robin over the 8 XCDs, so with S = 8 each XCD streams
-//     its own eighth of the tokens and every tile on that XCD reuses it through the XCD's L2.
+//   * Work split: the token dimension is cut into S slices (split-K); workgroup b takes slice
+//     b % S. S is chosen so that the tiles x slices workgroups fill whole rounds of the CUs
+//     (see cov_plan); with S = 8 each XCD would stream its own eighth of the tokens, which
+//     measured no faster than other mappings.
 //   * Each workgroup owns one 256 x 256 tile (I <= J) of the upper triangle of H for its slice:
 //     4 waves, each a 128 x 128 sub-tile = 4 x 4 MFMA blocks of 32 x 32, 256 fp32
 //     accumulators per lane.
@@ -17,6 +18,8 @@
 //     alpha/beta and writes both triangles (the mirror through an LDS transpose), so H is
 //     exactly symmetric.
 // fp32 path (small fp32 inputs): a plain LDS-tiled fp32 FMA kernel over the full matrix.
+#include <algorithm>
+#include <cmath>
 #include <type_traits>
 #include <utility>
 
@@ -254,8 +257,21 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
   uint32_t* const bufa[RING] = {a0, a1, a2, a3};
   uint32_t* const bufb[RING] = {b0, b1, b2, b3};
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int slice = blockIdx.x % n_slices;
-  int I = 0, rem = blockIdx.x / n_slices;
+  // work item: with S a multiple of 8, XCD x = b % 8 (workgroups are dealt round-robin over the
+  // 8 XCDs) runs the tiles of its slices x, x + 8, ... one slice after another, so the
+  // workgroups that run together on an XCD read the same tokens through its L2; otherwise
+  // slice = b % S
+  const int ntile = Tf * (Tf + 1) / 2;
+  int slice, rem;
+  if ((n_slices & 7) == 0) {
+    const int kk = int(blockIdx.x >> 3);
+    slice = (kk / ntile) * 8 + int(blockIdx.x & 7);
+    rem = kk % ntile;
+  } else {
+    slice = int(blockIdx.x) % n_slices;
+    rem = int(blockIdx.x) / n_slices;
+  }
+  int I = 0;
   while (rem >= Tf - I) {
     rem -= Tf - I;
     ++I;
@@ -538,14 +554,53 @@ struct CovPlan {
   bool tail = false;
 };
 
+// compute units of the current device (cached per device; workgroup rounds are counted in them)
+int device_cus() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cache[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        v <= 0)
+      v = 256;
+    cache[dev] = v;
+  }
+  return cache[dev];
+}
+
+// Token slices S (split-K). Each interior tile x slice is one workgroup holding a whole CU, so
+// the launch runs in ceil(W / CUs) rounds of equal length for W = tiles * S workgroups; the
+// last round is partly idle unless W fills it. Each slice also costs one partial tile per tile
+// to write and to reduce, worth about 500 tokens of that tile's MFMA time (256 KB at HBM speed
+// against 256 x 256 x 2 flops per token at MFMA speed). S minimises
+//   ceil(W / CUs) * CUs / W + 500 S / N
+// over S in 1..7 and the multiples of 8 up to 32 (which keep each XCD on its own slices; other
+// counts mix token ranges on an XCD and measured slower), with at least 4 * KC tokens per
+// slice. At d = 4096, N = 262144 this gives S = 32: 4352 workgroups in exactly 17 rounds,
+// instead of S = 8 in 4.25 rounds.
 CovPlan cov_plan(int64_t n_rows, int64_t d) {
   CovPlan p;
   p.T = int(cdiv(d, TT));
   p.Tf = int(d / TT);
   p.npos = int64_t(p.T) * (p.T + 1) / 2;
-  int64_t s = n_rows / (4 * KC);
-  p.S = int(s < 1 ? 1 : (s > 8 ? 8 : s));
+  const int64_t tiles = int64_t(p.Tf) * (p.Tf + 1) / 2 > 0 ? int64_t(p.Tf) * (p.Tf + 1) / 2
+                                                          : p.npos;
+  const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(32, n_rows / (4 * KC)));
+  const double cus = double(device_cus());
+  double best = 1e300;
+  for (int64_t S = 1; S <= smax; S += (S < 8 ? 1 : 8)) {
+    const double W = double(tiles * S);
+    const double cost = std::ceil(W / cus) * cus / W + 500.0 * double(S) / double(n_rows);
+    if (cost < best - 1e-12) {
+      best = cost;
+      p.S = int(S);
+    }
+  }
   p.rows_per_slice = cdiv(cdiv(n_rows, p.S), KC) * KC;
+  // rounding the slice up to whole stages can leave trailing slices empty: keep only the
+  // non-empty ones, so that every slice but the last is full and the last starts before n_rows
+  p.S = int(cdiv(n_rows, p.rows_per_slice));
   const int64_t last = int64_t(p.S - 1) * p.rows_per_slice;
   const int64_t in_last = n_rows > last ? n_rows - last : 0;
   p.tail_begin = last + (in_last / DK) * DK;

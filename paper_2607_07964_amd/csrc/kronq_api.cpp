@@ -108,8 +108,10 @@ int kronq_rotate(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_
              flags & ~known);
   KQ_REQUIRE(W_in && valid_dtype(w_dtype), KRONQ_ERR_INVALID_ARG, "bad W_in");
   KQ_REQUIRE(ldw_in >= d_in, KRONQ_ERR_INVALID_ARG, "ldw_in < d_in");
-  KQ_REQUIRE(aligned(W_in, w_dtype == KRONQ_BF16 ? 2 : 4), KRONQ_ERR_INVALID_ARG,
-             "W_in misaligned");
+  // W_in is read with 16-byte vector loads (8 bf16 or 4 fp32 values)
+  KQ_REQUIRE(aligned(W_in, 16) && ldw_in % (w_dtype == KRONQ_BF16 ? 8 : 4) == 0,
+             KRONQ_ERR_INVALID_ARG,
+             "W_in must be 16-byte aligned with ldw_in divisible by 8 (bf16) or 4 (fp32)");
   const bool inv = flags & KRONQ_INVERSE;
   const bool hx_only = flags & KRONQ_HX_ONLY, sx_given = flags & KRONQ_SX_GIVEN;
   KQ_REQUIRE(!(hx_only && sx_given) && !(inv && (hx_only || sx_given)), KRONQ_ERR_INVALID_ARG,

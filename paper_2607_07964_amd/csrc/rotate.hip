@@ -25,7 +25,7 @@ namespace {
 constexpr int RP_THREADS = 512;
 constexpr int CP_THREADS = 256;
 constexpr int CP_MAXL = 512;
-constexpr int NORM_ROWS = 32;
+constexpr int NORM_ROWS = 16;
 
 // ----------------------------------------------------------------------------- norms
 template <typename T>
@@ -37,38 +37,80 @@ __device__ __forceinline__ float ld_as_f32<uint16_t>(const uint16_t* p, int64_t 
   return __uint_as_float(uint32_t(p[i]) << 16);
 }
 
+__device__ __forceinline__ void load8_f32(const uint16_t* p, int64_t n, float (&x)[8]) {
+  if (n >= 8) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(w[e] << 16);
+      x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = e < n ? __uint_as_float(uint32_t(p[e]) << 16) : 0.f;
+  }
+}
+__device__ __forceinline__ void load8_f32(const float* p, int64_t n, float (&x)[8]) {
+  if (n >= 8) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    x[0] = a.x, x[1] = a.y, x[2] = a.z, x[3] = a.w, x[4] = b.x, x[5] = b.y, x[6] = b.z, x[7] = b.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = e < n ? p[e] : 0.f;
+  }
+}
+
+// Squared column norms (as per-block partials over NORM_ROWS rows) and squared row norms of W.
+// Each thread loads 8 consecutive columns per row with one vector load and keeps the block's
+// row sums and its 8 column sums in registers; row sums are reduced with wave shuffles.
+// Squares of bf16 / fp32 values summed over at most NORM_ROWS rows (columns) or one row's
+// share of a thread (rows) in fp32; the partials are stored and combined in fp64.
 template <typename T>
 __global__ __launch_bounds__(256) void w_norms(const T* __restrict__ W, int64_t d_out,
                                                int64_t d_in, int64_t ldw,
                                                double* __restrict__ col_part,
                                                double* __restrict__ rowsq) {
-  __shared__ double red[256];
-  const int tid = threadIdx.x;
+  __shared__ float red[4][NORM_ROWS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t r0 = int64_t(blockIdx.x) * NORM_ROWS;
-  const int64_t r1 = min(d_out, r0 + NORM_ROWS);
-  for (int64_t c = tid; c < d_in; c += 256) {
-    double s = 0.0;
-    for (int64_t r = r0; r < r1; ++r) {
-      const double x = ld_as_f32(W, r * ldw + c);
-      s += x * x;
+  const int nr = int(min(int64_t(NORM_ROWS), d_out - r0));
+  float rs[NORM_ROWS];
+#pragma unroll
+  for (int r = 0; r < NORM_ROWS; ++r) rs[r] = 0.f;
+  for (int64_t c0 = int64_t(tid) * 8; c0 < d_in; c0 += 256 * 8) {
+    float cs[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < NORM_ROWS; ++r) {
+      if (r < nr) {
+        float x[8];
+        load8_f32(W + (r0 + r) * ldw + c0, d_in - c0, x);
+        float t = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          cs[e] = fmaf(x[e], x[e], cs[e]);
+          t = fmaf(x[e], x[e], t);
+        }
+        rs[r] += t;
+      }
     }
-    col_part[int64_t(blockIdx.x) * d_in + c] = s;
+    double* cp = col_part + int64_t(blockIdx.x) * d_in + c0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (c0 + e < d_in) cp[e] = cs[e];
   }
-  for (int64_t r = r0; r < r1; ++r) {
-    double s = 0.0;
-    for (int64_t c = tid; c < d_in; c += 256) {
-      const double x = ld_as_f32(W, r * ldw + c);
-      s += x * x;
-    }
-    red[tid] = s;
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-      if (tid < w) red[tid] += red[tid + w];
-      __syncthreads();
-    }
-    if (tid == 0) rowsq[r] = red[0];
-    __syncthreads();
+#pragma unroll
+  for (int r = 0; r < NORM_ROWS; ++r) {
+    float v = rs[r];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    if (lane == 0) red[wave][r] = v;
   }
+  __syncthreads();
+  if (tid < nr)
+    rowsq[r0 + tid] = double(red[0][tid]) + double(red[1][tid]) + double(red[2][tid]) +
+                      double(red[3][tid]);
 }
 
 // s = (h / a)^(1/4), 1 when either is zero (or the side is off). Also the multipliers used by

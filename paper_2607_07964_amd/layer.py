@@ -135,7 +135,9 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
                    flags | K.HX_ONLY, st.ws_rot)
     K.kronq_traces(st.HX, None, st.tr_post)
     ev_sx.record(main)
-    K.kronq_cholesky_inv(st.HX, st.U, damp, st.info, st.ws_chol)
+    # the side stream's work is enqueued before the factorisation's ~160 launches, so that the
+    # H_G covariance is dispatched as soon as H_X is done rather than after the host has
+    # issued the whole factorisation
     with torch.cuda.stream(st.side):
         st.side.wait_event(ev_x)
         K.kronq_accumulate_cov(G, st.HG, 1.0, 0.0, st.ws_cov_g)
@@ -145,6 +147,7 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
                        st.sg, flags | K.SX_GIVEN, st.ws_rot)
         K.kronq_traces(None, st.HG, st.tr_post)
         ev_w.record(st.side)
+    K.kronq_cholesky_inv(st.HX, st.U, damp, st.info, st.ws_chol)
     main.wait_event(ev_w)
     K.kronq_obs_quantize_layer(st.W, st.U, bits, st.codes, st.scales, st.zeros, st.err, None,
                                ws=st.ws_obs)

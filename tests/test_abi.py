@@ -77,6 +77,14 @@ def test_argument_checks_fail_before_any_launch():
     rc, msg = _err(lib.kronq_rotate(fake, 2, 112, fake, 8, 112, 112, fake, 112, nul, 0, fake, nul,
                                     nul, nul, fake, fake, K.ROT_IN, ws, 1 << 30, nul))
     assert rc == -1 and "28" in msg
+    # W_in rows not 16-byte aligned (bf16 with ldw_in % 8 != 0; a misaligned base pointer)
+    rc, msg = _err(lib.kronq_rotate(fake, 1, 132, fake, 8, 128, 128, fake, 128, nul, 0, fake,
+                                    nul, nul, nul, fake, fake, K.ROT_IN, ws, 1 << 30, nul))
+    assert rc == -1 and "W_in" in msg
+    odd = ctypes.c_void_p((1 << 20) + 8)
+    rc, msg = _err(lib.kronq_rotate(odd, 2, 128, fake, 8, 128, 128, fake, 128, nul, 0, fake,
+                                    nul, nul, nul, fake, fake, K.ROT_IN, ws, 1 << 30, nul))
+    assert rc == -1 and "W_in" in msg
     # d_in not a multiple of the group
     rc, _ = _err(lib.kronq_obs_quantize_layer(fake, 8, 200, 200, fake, 200, 4, 128, 128, fake,
                                               fake, fake, nul, nul, nul, 0, nul))
