@@ -369,11 +369,23 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
     __builtin_amdgcn_sched_barrier(0);
     wait_vm<(RING - 3) * 8>();
     __builtin_amdgcn_s_barrier();
-    issue(s + RING - 1, (u + RING - 1) % RING);
     __builtin_amdgcn_sched_barrier(0);
+    // second half-stage: the operand reads over the first 8 MFMAs, then this wave's 8 loads of
+    // stage s + 3 one per MFMA over the last 8 (a burst of loads right after the barrier, on
+    // top of the reads, measured 5-10% slower)
+    issue(s + RING - 1, (u + RING - 1) % RING);
     frags((u + 1) % RING, 0, 0);
     mfmas(1);
-    interleave();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // two LDS reads
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global-to-LDS load
+    }
     __builtin_amdgcn_sched_barrier(0);
   };
   for (int s0 = 0; s0 < s_main; s0 += RING) {
