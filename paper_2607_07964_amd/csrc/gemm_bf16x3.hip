@@ -1,0 +1,185 @@
+// C -= A B with fp32 operands on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16), fp32-accurate
+// through a three-term split: x = x_hi + x_lo with x_hi = bf16(x), x_lo = bf16(x - x_hi), and
+// A B ~ A_hi B_hi + A_hi B_lo + A_lo B_hi (the dropped A_lo B_lo term and the parts of x below
+// x_lo are ~2^-16 of each product). Used for the OBS trailing updates W[:, rest] -= E U[blk, rest],
+// where A = E (fp32, k contiguous) is split as it is staged and B = U rows comes pre-split and
+// transposed (Ut_hi / Ut_lo, [n][k] bf16) by split_transpose, once per layer.
+//   * TM x TM output tile per workgroup (TM = 128 or 64), 4 waves in a 2 x 2 grid, each wave
+//     (TM/2) x (TM/2) = up to 2 x 2 MFMA blocks of 32 x 32 with fp32 accumulators.
+//   * K advances 32 at a time through one LDS stage: A_hi, A_lo [m][k] and B_hi, B_lo [n][k],
+//     rows padded to 80 bytes so that the 16-byte operand reads of 8 consecutive lanes hit
+//     distinct banks; the next stage is fetched into registers during the MFMAs.
+#include "kq_common.hpp"
+
+namespace kq {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int BK = 32;      // K per stage
+constexpr int RS = 40;      // LDS row stride in bf16 (32 + 8 pad = 80 bytes)
+
+// round-to-nearest-even fp32 -> bf16 bits (finite inputs)
+__device__ __forceinline__ uint32_t bf16_rne(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+template <int TM>
+__global__ __launch_bounds__(256) void gemm_bf16x3_sub(int64_t M, int64_t N, int64_t K,
+                                                       const float* __restrict__ A, int64_t lda,
+                                                       const uint16_t* __restrict__ Bh,
+                                                       const uint16_t* __restrict__ Bl,
+                                                       int64_t ldb, float* __restrict__ C,
+                                                       int64_t ldc) {
+  constexpr int NB = TM / 64;                  // 32 x 32 blocks per wave edge (1 or 2)
+  constexpr int AV = TM * BK / 4 / 256;        // float4 of A per thread per stage
+  constexpr int BV = TM * BK / 8 / 256;        // 16-byte chunks of each B half per thread
+  __shared__ __attribute__((aligned(16))) uint16_t sAh[TM * RS], sAl[TM * RS];
+  __shared__ __attribute__((aligned(16))) uint16_t sBh[TM * RS], sBl[TM * RS];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave & 1, wn = wave >> 1, l32 = lane & 31, lhi = lane >> 5;
+  const int64_t m0 = int64_t(blockIdx.y) * TM, n0 = int64_t(blockIdx.x) * TM;
+
+  float4 ra[AV];
+  uint4 rbh[BV], rbl[BV];
+  auto fetch = [&](int64_t k0) {
+#pragma unroll
+    for (int v = 0; v < AV; ++v) {
+      const int e = tid + 256 * v, m = e / (BK / 4), kq = (e % (BK / 4)) * 4;
+      ra[v] = (m0 + m < M) ? *reinterpret_cast<const float4*>(A + (m0 + m) * lda + k0 + kq)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int v = 0; v < BV; ++v) {
+      const int e = tid + 256 * v, n = e / (BK / 8), kc = (e % (BK / 8)) * 8;
+      const bool ok = n0 + n < N;
+      rbh[v] = ok ? *reinterpret_cast<const uint4*>(Bh + (n0 + n) * ldb + k0 + kc)
+                  : make_uint4(0u, 0u, 0u, 0u);
+      rbl[v] = ok ? *reinterpret_cast<const uint4*>(Bl + (n0 + n) * ldb + k0 + kc)
+                  : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto stash = [&]() {
+#pragma unroll
+    for (int v = 0; v < AV; ++v) {
+      const int e = tid + 256 * v, m = e / (BK / 4), kq = (e % (BK / 4)) * 4;
+      const float x[4] = {ra[v].x, ra[v].y, ra[v].z, ra[v].w};
+      uint32_t h[4], l[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        h[c] = bf16_rne(x[c]);
+        l[c] = bf16_rne(x[c] - bf16_to_f32(h[c]));
+      }
+      *reinterpret_cast<uint2*>(sAh + m * RS + kq) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+      *reinterpret_cast<uint2*>(sAl + m * RS + kq) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
+    }
+#pragma unroll
+    for (int v = 0; v < BV; ++v) {
+      const int e = tid + 256 * v, n = e / (BK / 8), kc = (e % (BK / 8)) * 8;
+      *reinterpret_cast<uint4*>(sBh + n * RS + kc) = rbh[v];
+      *reinterpret_cast<uint4*>(sBl + n * RS + kc) = rbl[v];
+    }
+  };
+
+  f32x16_t acc[NB][NB];
+#pragma unroll
+  for (int a = 0; a < NB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[a][b] = f32x16_t{};
+  if (K > 0) fetch(0);
+  for (int64_t k0 = 0; k0 < K; k0 += BK) {
+    __syncthreads();
+    stash();
+    __syncthreads();
+    if (k0 + BK < K) fetch(k0 + BK);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int kc = ks * 16 + 8 * lhi;  // this lane's 8 k of the 16
+      bf16x8_t ah[NB], al[NB], bh[NB], bl[NB];
+#pragma unroll
+      for (int bi = 0; bi < NB; ++bi) {
+        const int m = wm * (TM / 2) + bi * 32 + l32;
+        ah[bi] = *reinterpret_cast<const bf16x8_t*>(sAh + m * RS + kc);
+        al[bi] = *reinterpret_cast<const bf16x8_t*>(sAl + m * RS + kc);
+      }
+#pragma unroll
+      for (int bj = 0; bj < NB; ++bj) {
+        const int n = wn * (TM / 2) + bj * 32 + l32;
+        bh[bj] = *reinterpret_cast<const bf16x8_t*>(sBh + n * RS + kc);
+        bl[bj] = *reinterpret_cast<const bf16x8_t*>(sBl + n * RS + kc);
+      }
+#pragma unroll
+      for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < NB; ++bj) {
+          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[bi], bh[bj], acc[bi][bj], 0, 0, 0);
+          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[bi], bl[bj], acc[bi][bj], 0, 0, 0);
+          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[bi], bh[bj], acc[bi][bj], 0, 0, 0);
+        }
+    }
+  }
+#pragma unroll
+  for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < NB; ++bj)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t gm = m0 + wm * (TM / 2) + bi * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
+        const int64_t gn = n0 + wn * (TM / 2) + bj * 32 + l32;
+        if (gm < M && gn < N) C[gm * ldc + gn] -= acc[bi][bj][r];
+      }
+}
+
+// Ut_hi[n][k] + Ut_lo[n][k] = U[k][n] (the three-term split of U^T), 32 x 32 tiles through LDS
+__global__ __launch_bounds__(256) void split_transpose(const float* __restrict__ U, int64_t ldu,
+                                                       int64_t d, uint16_t* __restrict__ Th,
+                                                       uint16_t* __restrict__ Tl, int64_t ldt) {
+  __shared__ float t[32][33];
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+  const int64_t k0 = int64_t(blockIdx.y) * 32, n0 = int64_t(blockIdx.x) * 32;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t k = k0 + ty + 8 * i, n = n0 + tx;
+    t[ty + 8 * i][tx] = (k < d && n < d) ? U[k * ldu + n] : 0.f;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t n = n0 + ty + 8 * i, k = k0 + tx;
+    if (n < d && k < d) {
+      const float x = t[tx][ty + 8 * i];
+      const uint32_t h = bf16_rne(x);
+      Th[n * ldt + k] = uint16_t(h);
+      Tl[n * ldt + k] = uint16_t(bf16_rne(x - bf16_to_f32(h)));
+    }
+  }
+}
+
+}  // namespace
+
+int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th, uint16_t* Tl,
+                           int64_t ldt, hipStream_t s) {
+  const dim3 grid(unsigned(cdiv(d, 32)), unsigned(cdiv(d, 32)));
+  return launch("obs_split_u", split_transpose, grid, dim3(256), 0, s, U, ldu, d, Th, Tl, ldt);
+}
+
+int gemm_bf16x3_sub(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                    const uint16_t* Bh, const uint16_t* Bl, int64_t ldb, float* C, int64_t ldc,
+                    hipStream_t s, const char* name) {
+  if (M <= 0 || N <= 0 || K <= 0) return KRONQ_OK;
+  KQ_REQUIRE(K % BK == 0 && lda % 4 == 0 && ldb % 8 == 0, KRONQ_ERR_INVALID_ARG,
+             "gemm_bf16x3_sub: K %% 32, lda %% 4 and ldb %% 8 must be 0");
+  if (cdiv(M, 128) * cdiv(N, 128) >= 192) {
+    const dim3 grid(unsigned(cdiv(N, 128)), unsigned(cdiv(M, 128)));
+    return launch(name, gemm_bf16x3_sub<128>, grid, dim3(256), 0, s, M, N, K, A, lda, Bh, Bl, ldb,
+                  C, ldc);
+  }
+  const dim3 grid(unsigned(cdiv(N, 64)), unsigned(cdiv(M, 64)));
+  return launch(name, gemm_bf16x3_sub<64>, grid, dim3(256), 0, s, M, N, K, A, lda, Bh, Bl, ldb, C,
+                ldc);
+}
+
+}  // namespace kq

@@ -121,6 +121,14 @@ enum GemmFlags : int {
   GEMM_A_LOWER = 16,    // A is lower triangular: skip k > row-tile end
   GEMM_OPB_UPPER = 32,  // op(B) is upper triangular: skip k > column-tile end
 };
+// C -= A B, A fp32 [M x K] (k contiguous), B given as the bf16 three-term split of B^T
+// (Bh + Bl, [N x K], k contiguous); K % 32 == 0
+int gemm_bf16x3_sub(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                    const uint16_t* Bh, const uint16_t* Bl, int64_t ldb, float* C, int64_t ldc,
+                    hipStream_t s, const char* name);
+// Th + Tl = U^T split into bf16 high and low parts, [d x d] with row stride ldt
+int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th, uint16_t* Tl,
+                           int64_t ldt, hipStream_t s);
 int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
              hipStream_t s, const char* name = "gemm_f32_mfma");

@@ -14,7 +14,8 @@
 //     blocks] -= E_b U[b, rest of group] (K = 128); after the last block of a group,
 //     W[:, beyond the group] -= E_group U[group, beyond] (K = 512). Every column still receives
 //     the update of every earlier block before it is swept, as in the one-level scheme, with a
-//     quarter of the passes over W. Both products run on the fp32 MFMA GEMM.
+//     quarter of the passes over W. Both products run on the bf16 matrix cores with the
+//     fp32-accurate three-term split (gemm_bf16x3.hip); U^T is split once per layer.
 // The quantiser (reading of the paper's "quant"): xmin = min(0, min w), xmax = max(0, max w),
 // (-1, 1) when both are 0; scale = float32((xmax - xmin) / (2^b - 1)) in float64;
 // zero = rint(-xmin / scale); q = clamp(rint(w / scale) + zero, 0, 2^b - 1);
@@ -185,7 +186,8 @@ __global__ __launch_bounds__(256) void obs_sweep(float* __restrict__ W, int64_t 
 
 size_t obs_ws_bytes(int64_t d_out, int64_t d_in) {
   if (d_out <= 0 || d_in <= 0) return 0;
-  return align256(size_t(d_out) * GRP * OB * sizeof(float)) + 256;
+  return align256(size_t(d_out) * GRP * OB * sizeof(float)) +
+         2 * align256(size_t(d_in) * size_t(d_in) * sizeof(uint16_t)) + 256;
 }
 
 int obs_launch(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* U, int64_t ldu,
@@ -193,10 +195,16 @@ int obs_launch(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* 
                void* ws, hipStream_t s) {
   const int64_t nblk = d_in / OB;
   const unsigned grid = unsigned(cdiv(d_out, RPG));
+  Carver cv(ws);
+  float* Ews = cv.take<float>(size_t(d_out) * GRP * OB);
+  uint16_t* Uth = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
+  uint16_t* Utl = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
+  // U^T split once into bf16 high and low parts: the B operand of the trailing updates
+  KQ_TRY(split_transpose_launch(U, ldu, d_in, Uth, Utl, d_in, s));
   for (int64_t g0 = 0; g0 < nblk; g0 += GRP) {
     const int64_t gend = g0 + GRP < nblk ? g0 + GRP : nblk;
     // errors of this group's blocks: the caller's err (ld d_in) or the workspace (ld GRP * OB)
-    float* Eg = err ? err + g0 * OB : static_cast<float*>(ws);
+    float* Eg = err ? err + g0 * OB : Ews;
     const int64_t lde = err ? d_in : GRP * OB;
     for (int64_t b = g0; b < gend; ++b) {
       const int64_t c0 = b * OB;
@@ -204,14 +212,16 @@ int obs_launch(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* 
       KQ_TRY(launch("obs_sweep", obs_sweep, dim3(grid), dim3(256), 0, s, W, d_out, ldw, U, ldu,
                     c0, bits, codes, d_in, scales, zeros, nblk, b, Eb, lde, W_hat, d_in));
       const int64_t near = (gend - b - 1) * OB;  // rest of the group
-      if (near > 0)
-        KQ_TRY(gemm_f32(0, d_out, near, OB, -1.f, Eb, lde, U + c0 * ldu + c0 + OB, ldu, 1.f,
-                        W + c0 + OB, ldw, s, "obs_trailing_update"));
+      if (near > 0)  // W[:, c0+OB : gend*OB] -= E_b U[c0 : c0+OB, c0+OB : gend*OB]
+        KQ_TRY(gemm_bf16x3_sub(d_out, near, OB, Eb, lde, Uth + (c0 + OB) * d_in + c0,
+                               Utl + (c0 + OB) * d_in + c0, d_in, W + c0 + OB, ldw, s,
+                               "obs_trailing_update"));
     }
     const int64_t rem = d_in - gend * OB;  // beyond the group
-    if (rem > 0)
-      KQ_TRY(gemm_f32(0, d_out, rem, (gend - g0) * OB, -1.f, Eg, lde, U + g0 * OB * ldu + gend * OB,
-                      ldu, 1.f, W + gend * OB, ldw, s, "obs_trailing_update"));
+    if (rem > 0)  // W[:, gend*OB :] -= E_group U[g0*OB : gend*OB, gend*OB :]
+      KQ_TRY(gemm_bf16x3_sub(d_out, rem, (gend - g0) * OB, Eg, lde,
+                             Uth + gend * OB * d_in + g0 * OB, Utl + gend * OB * d_in + g0 * OB,
+                             d_in, W + gend * OB, ldw, s, "obs_trailing_update"));
   }
   return KRONQ_OK;
 }
