@@ -24,7 +24,7 @@ namespace {
 
 constexpr int RP_THREADS = 512;
 constexpr int CP_THREADS = 256;
-constexpr int CP_MAXL = 512;
+constexpr int CP_MAXL = 256;
 constexpr int NORM_ROWS = 16;
 
 // ----------------------------------------------------------------------------- norms
@@ -239,24 +239,55 @@ __global__ __launch_bounds__(RP_THREADS) void row_pass(
       continue;
     }
     __syncthreads();  // previous row finished with buf
-    for (int64_t c = tid; c < n; c += RP_THREADS) {
-      float x = ld_as_f32(s, c) * pr;
-      if (pre_col) x *= pre_col[c];
-      buf[c] = x;
+    if ((n & 7) == 0) {  // 16-byte rows (checked by the API): 8 values per vector load
+      for (int64_t c0 = int64_t(tid) * 8; c0 < n; c0 += int64_t(RP_THREADS) * 8) {
+        float x[8];
+        load8_f32(s + c0, 8, x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] *= pre_col ? pr * pre_col[c0 + e] : pr;
+        *reinterpret_cast<float4*>(buf + c0) = make_float4(x[0], x[1], x[2], x[3]);
+        *reinterpret_cast<float4*>(buf + c0 + 4) = make_float4(x[4], x[5], x[6], x[7]);
+      }
+    } else {
+      for (int64_t c = tid; c < n; c += RP_THREADS) {
+        float x = ld_as_f32(s, c) * pr;
+        if (pre_col) x *= pre_col[c];
+        buf[c] = x;
+      }
     }
     __syncthreads();
     fwht_lds(buf, n, m, tid, RP_THREADS);
     if (q28) {
-      const int64_t items = n;  // (a, b): output a * m + b
-      for (int64_t it = tid; it < items; it += RP_THREADS) {
-        const int64_t a = it / m, b = it % m;
-        float acc = 0.f;
-#pragma unroll 4
-        for (int k = 0; k < 28; ++k) acc = fmaf(qs[a * 28 + k], buf[k * m + b], acc);
-        const int64_t c = a * m + b;
-        float y = acc * po;
-        if (post_col) y *= post_col[c];
-        o[c] = y;
+      // output a * m + b = sum_k Q[a][k] buf[k * m + b]: one b per thread, its 28 inputs held in
+      // registers, the rows of Q read as 16-byte broadcasts
+      for (int64_t b = tid; b < m; b += RP_THREADS) {
+        float x[28];
+#pragma unroll
+        for (int k = 0; k < 28; ++k) x[k] = buf[k * m + b];
+        for (int a = 0; a < 28; ++a) {
+          const float4* qa = reinterpret_cast<const float4*>(qs + a * 28);
+          float acc = 0.f;
+#pragma unroll
+          for (int k4 = 0; k4 < 7; ++k4) {
+            const float4 q = qa[k4];
+            acc = fmaf(q.x, x[4 * k4], acc);
+            acc = fmaf(q.y, x[4 * k4 + 1], acc);
+            acc = fmaf(q.z, x[4 * k4 + 2], acc);
+            acc = fmaf(q.w, x[4 * k4 + 3], acc);
+          }
+          const int64_t c = a * m + b;
+          float y = acc * po;
+          if (post_col) y *= post_col[c];
+          o[c] = y;
+        }
+      }
+    } else if ((n & 3) == 0) {
+      for (int64_t c = int64_t(tid) * 4; c < n; c += int64_t(RP_THREADS) * 4) {
+        float4 y = *reinterpret_cast<const float4*>(buf + c);
+        const float4 pc = post_col ? *reinterpret_cast<const float4*>(post_col + c)
+                                   : make_float4(1.f, 1.f, 1.f, 1.f);
+        y.x *= po * pc.x, y.y *= po * pc.y, y.z *= po * pc.z, y.w *= po * pc.w;
+        *reinterpret_cast<float4*>(o + c) = y;
       }
     } else {
       for (int64_t c = tid; c < n; c += RP_THREADS) {
@@ -296,22 +327,37 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
     }
   }
   const int cw4 = CW / 4;
-  for (int64_t it = tid; it < L * cw4; it += CP_THREADS) {
-    const int64_t a = it / cw4;
-    const int c = int(it % cw4) * 4;
-    const int64_t gr = row0 + a * n_lo;
-    const int64_t gc = c0 + c;
-    float4 x;
-    if (gc + 4 <= cols) {
-      x = *reinterpret_cast<const float4*>(src + gr * lds_ + gc);
-    } else {
-      const float* p = src + gr * lds_;
-      x.x = gc + 0 < cols ? p[gc + 0] : 0.f;
-      x.y = gc + 1 < cols ? p[gc + 1] : 0.f;
-      x.z = gc + 2 < cols ? p[gc + 2] : 0.f;
-      x.w = gc + 3 < cols ? p[gc + 3] : 0.f;
+  // load the L x CW tile: 8 independent float4 loads in flight per thread before they are
+  // stored (one workgroup per CU at L = 1024, so latency must be hidden within the thread)
+  const int64_t n_items = L * cw4;
+  for (int64_t it0 = tid; it0 < n_items; it0 += 8 * CP_THREADS) {
+    float4 x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t it = it0 + int64_t(u) * CP_THREADS;
+      x[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (it < n_items) {
+        const int64_t a = it / cw4;
+        const int c = int(it % cw4) * 4;
+        const int64_t gr = row0 + a * n_lo;
+        const int64_t gc = c0 + c;
+        const float* p = src + gr * lds_;
+        if (gc + 4 <= cols) {
+          x[u] = *reinterpret_cast<const float4*>(p + gc);
+        } else {
+          x[u].x = gc + 0 < cols ? p[gc + 0] : 0.f;
+          x[u].y = gc + 1 < cols ? p[gc + 1] : 0.f;
+          x[u].z = gc + 2 < cols ? p[gc + 2] : 0.f;
+          x[u].w = gc + 3 < cols ? p[gc + 3] : 0.f;
+        }
+      }
     }
-    *reinterpret_cast<float4*>(tile + a * CWP + c) = x;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t it = it0 + int64_t(u) * CP_THREADS;
+      if (it < n_items)
+        *reinterpret_cast<float4*>(tile + (it / cw4) * CWP + int(it % cw4) * 4) = x[u];
+    }
   }
   __syncthreads();
   if (kind == 0) {
@@ -368,15 +414,26 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
       }
     }
   } else {
-    // 28-point mix: out[a][c] = sum_k Q[a][k] tile[k][c]
-    for (int64_t it = tid; it < 28 * CW; it += CP_THREADS) {
-      const int a = int(it / CW);
-      const int c = int(it % CW);
+    // 28-point mix: out[a][c] = sum_k Q[a][k] tile[k][c]; one column per thread, its 28 inputs
+    // in registers, the rows of Q read as 16-byte broadcasts
+    for (int c = tid; c < CW; c += CP_THREADS) {
       const int64_t gc = c0 + c;
-      float acc = 0.f;
-#pragma unroll 4
-      for (int k = 0; k < 28; ++k) acc = fmaf(qs[a * 28 + k], tile[k * CWP + c], acc);
-      if (gc < cols) dst[(row0 + a * n_lo) * ldd + gc] = acc * norm;
+      float x[28];
+#pragma unroll
+      for (int k = 0; k < 28; ++k) x[k] = tile[k * CWP + c];
+      for (int a = 0; a < 28; ++a) {
+        const float4* qa = reinterpret_cast<const float4*>(qs + a * 28);
+        float acc = 0.f;
+#pragma unroll
+        for (int k4 = 0; k4 < 7; ++k4) {
+          const float4 q = qa[k4];
+          acc = fmaf(q.x, x[4 * k4], acc);
+          acc = fmaf(q.y, x[4 * k4 + 1], acc);
+          acc = fmaf(q.z, x[4 * k4 + 2], acc);
+          acc = fmaf(q.w, x[4 * k4 + 3], acc);
+        }
+        if (gc < cols) dst[(row0 + a * n_lo) * ldd + gc] = acc * norm;
+      }
     }
   }
 }
@@ -403,7 +460,9 @@ int launch_row_pass(const void* src, int dtype, int64_t lds_, float* dst, int64_
 int launch_col_step(const float* src, int64_t lds_, float* dst, int64_t ldd, int64_t rows,
                     int64_t cols, int64_t L, int64_t n_lo, int kind, const float* q28,
                     bool q_trans, hipStream_t s) {
-  const int CW = L <= 128 ? 64 : (L <= 256 ? 64 : 32);
+  // strips of CW columns: 28-point mix 256 (one column per thread), FWHT 64 up to L = 256
+  // and 32 beyond (L = 1024: 1024 x 36 floats + the 28 x 28 factor = 150 KB of LDS)
+  const int CW = kind == 1 ? 256 : (L <= 256 ? 64 : 32);
   const int64_t n_groups = rows / L;
   const int64_t strips = cdiv(cols, CW);
   const size_t shmem = (size_t(L) * (CW + 4) + 28 * 28) * sizeof(float);
@@ -416,13 +475,22 @@ int launch_col_step(const float* src, int64_t lds_, float* dst, int64_t ldd, int
 // Full transform of every column (rows axis, length d): T = (Q (x) H_m) / sqrt(m).
 int col_transform(const float* src, int64_t lds_, float* dst, int64_t ldd, int64_t d,
                   int64_t cols, const RotDim& rd, const float* q28, bool q_trans, hipStream_t s) {
-  // Hadamard factors, fast index first: m = m1 * m2 * ..., each <= CP_MAXL
+  // Hadamard factors, fast index first: m = m1 * m2 * ..., each <= CP_MAXL, in as few passes
+  // as possible and as even as possible (1024: one pass; 4096: 64 x 64; 8192: 128 x 64)
   int64_t n_lo = 1;
   int64_t left = rd.m;
   const float* cur = src;
   int64_t ldc = lds_;
+  int lg = 0;
+  while ((int64_t(1) << lg) < left) ++lg;
+  int lgmax = 0;
+  while ((int64_t(1) << (lgmax + 1)) <= CP_MAXL) ++lgmax;
+  int passes = (lg + lgmax - 1) / (lgmax > 0 ? lgmax : 1);
   while (left > 1) {
-    const int64_t L = left > CP_MAXL ? CP_MAXL : left;
+    const int lgl = (lg + passes - 1) / passes;  // ceil: earlier passes take the larger share
+    const int64_t L = int64_t(1) << lgl;
+    lg -= lgl;
+    --passes;
     KQ_TRY(launch_col_step(cur, ldc, dst, ldd, d, cols, L, n_lo, 0, nullptr, false, s));
     cur = dst;
     ldc = ldd;
