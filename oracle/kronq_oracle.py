@@ -19,7 +19,8 @@ Readings taken where the paper is silent or garbled (each also listed in DESIGN.
 R1  covariances are plain sums, H_X = X^T X, H_G = G^T G (token-major X, G).
 R3  the inverse-Cholesky factor is the UPPER U with inv(H~) = U^T U; the sweep uses rows of U
     (Algorithm 2 prints rows of a lower L, which would be zero blocks).
-R5  no drift statistics: the P correction of Algorithm 2 is zero ("KronQ+GPTQ").
+R5  the drift correction P of Algorithm 2 is optional: zero ("KronQ+GPTQ") unless the drift
+    statistic D = dX^T X is given (the paper's default "KronQ+GPTAQ").
 R6  damping lambda = 0.01 of the mean diagonal, on the post-BiIP H_X.
 R7  asymmetric min-max grid per row and group (GPTQ convention): xmin = min(0, min w),
     xmax = max(0, max w), (-1, 1) if both are 0; scale = float32((xmax - xmin) / (2^b - 1));
@@ -35,6 +36,17 @@ R13 traces are reported before and after BiIP; the sensitivity score uses post-B
 R14 bit allocation: exhaustive search minimising sum_l s_l (2^b_l - 1)^-2 under a
     parameter-weighted average-bit budget, ties to the lexicographically smallest vector.
 R15 the reported loss is taken in the original space with undamped H_X, H_G.
+R16 drift correction (Prop. 1, Algorithm 2): the paper's L with inv(H~) = L L^T is the
+    transpose of the upper U of R3, so P = alpha ((D U^T) . M_U) U, where M_U is the STRICTLY
+    upper mask (Prop. 1 says strictly, Algorithm 2's comment drops the word). Row p of P is then
+    alpha D[p, p+1:] inv(H~[p+1:, p+1:]), which is the least-squares absorption of column p's
+    drift by the columns after it. D is the token-major dX^T X (dX = X~ - X).
+R17 the W in the drift term of the sweep is the column as it stands when it is quantised; in
+    the trailing update the block's columns enter with those same values, so that the lazy batch
+    equals the per-column update of eq. kronq_update. (Read literally, Algorithm 2's trailing
+    update would use the block after its sweep, which holds the quantised values.)
+R18 alpha is an input; 1 is the value for which the update is the exact least-squares
+    absorption. The paper leaves alpha's value to GPTAQ.
 """
 from __future__ import annotations
 
@@ -43,10 +55,11 @@ import itertools
 import numpy as np
 
 __all__ = [
-    "widen_bf16", "as_f64", "covariance", "covariance_diag", "traces", "rescale_factors",
-    "hadamard", "rht_matrix", "rht_rows",
-    "biip_forward", "biip_revert", "damp", "inverse_cholesky_factor", "group_params",
-    "quantize", "obs_unblocked", "obs_blocked", "kfac_loss", "allocate_bits", "count_avg_bits",
+    "widen_bf16", "as_f64", "covariance", "covariance_diag", "cross_covariance", "traces",
+    "rescale_factors", "hadamard", "rht_matrix", "rht_rows",
+    "biip_forward", "biip_revert", "damp", "inverse_cholesky_factor", "gptaq_correction",
+    "group_params", "quantize", "obs_unblocked", "obs_blocked", "kfac_loss", "kronq_objective",
+    "allocate_bits", "count_avg_bits",
     "RESCALE_IN", "RESCALE_OUT", "ROT_IN", "ROT_OUT", "BIIP",
 ]
 
@@ -86,6 +99,20 @@ def covariance(A, chunk: int = 8192) -> np.ndarray:
         C = as_f64(A[t0:t0 + chunk])
         H += C.T @ C
     return H
+
+
+def cross_covariance(A, B, chunk: int = 8192) -> np.ndarray:
+    """D = A^T B for token-major A, B [N x d], summed over token chunks in float64. With A the
+    input drift dX = X~ - X and B the input X this is the drift statistic of Algorithm 1's first
+    line (the paper's dX X^T for column-stacked samples; eq. gptaq_obj)."""
+    A, B = np.asarray(A), np.asarray(B)
+    if A.shape != B.shape:
+        raise ValueError("A and B must have the same shape")
+    n, d = A.shape
+    D = np.zeros((d, d), dtype=np.float64)
+    for t0 in range(0, n, chunk):
+        D += as_f64(A[t0:t0 + chunk]).T @ as_f64(B[t0:t0 + chunk])
+    return D
 
 
 # ----------------------------------------------------------------------------------------------
@@ -196,13 +223,14 @@ def rht_rows(d: int, sign, q28, rows) -> np.ndarray:
     return scale * np.where(par == 1, -1.0, 1.0) / np.sqrt(m) * sign[None, :]
 
 
-def biip_forward(W, HX, HG, rot_in=None, rot_out=None, flags: int = BIIP):
-    """Algorithm 1 without the drift statistic (reading R5):
-    W' = S_G W S_X; H_X' = S_X^-1 H_X S_X^-1; H_G' = S_G^-1 H_G S_G^-1; then
-    W'' = U W' V^T, H_X'' = V H_X' V^T, H_G'' = U H_G' U^T.
+def biip_forward(W, HX, HG, rot_in=None, rot_out=None, flags: int = BIIP, D=None):
+    """Algorithm 1:
+    W' = S_G W S_X; H_X' = S_X^-1 H_X S_X^-1; H_G' = S_G^-1 H_G S_G^-1; D' = S_X^-1 D S_X^-1;
+    then W'' = U W' V^T, H_X'' = V H_X' V^T, H_G'' = U H_G' U^T, D'' = V D' V^T.
 
-    ``rot_in`` / ``rot_out`` are (sign, q28-or-None). Returns a dict with W, HX, HG, sx, sg,
-    V, U (V, U are identities for a side whose rotation is off)."""
+    ``rot_in`` / ``rot_out`` are (sign, q28-or-None); ``D`` is the optional drift statistic
+    (reading R5). Returns a dict with W, HX, HG, D, sx, sg, V, U (V, U are identities for a
+    side whose rotation is off; D is None when not given)."""
     W = as_f64(W)
     HX = np.asarray(HX, dtype=np.float64)
     HG = None if HG is None else np.asarray(HG, dtype=np.float64)
@@ -213,10 +241,12 @@ def biip_forward(W, HX, HG, rot_in=None, rot_out=None, flags: int = BIIP):
     HG1 = None if HG is None else HG / np.outer(sg, sg)
     V = rht_matrix(d_in, *rot_in) if flags & ROT_IN else np.eye(d_in)
     U = rht_matrix(d_out, *rot_out) if flags & ROT_OUT else np.eye(d_out)
+    D1 = None if D is None else np.asarray(D, dtype=np.float64) / np.outer(sx, sx)
     return {
         "W": U @ W1 @ V.T,
         "HX": V @ HX1 @ V.T,
         "HG": None if HG1 is None else U @ HG1 @ U.T,
+        "D": None if D1 is None else V @ D1 @ V.T,
         "sx": sx, "sg": sg, "V": V, "U": U,
     }
 
@@ -242,6 +272,14 @@ def inverse_cholesky_factor(Hd) -> np.ndarray:
     Hinv = np.linalg.inv(np.asarray(Hd, dtype=np.float64))
     Hinv = 0.5 * (Hinv + Hinv.T)
     return np.linalg.cholesky(Hinv).T
+
+
+def gptaq_correction(D, U, alpha: float = 1.0) -> np.ndarray:
+    """The drift correction of Prop. 1 and Algorithm 2's third line,
+    P = alpha ((D L) . M_U) L^T with L = U^T (readings R16, R18): strictly upper triangular."""
+    D = np.asarray(D, dtype=np.float64)
+    U = np.asarray(U, dtype=np.float64)
+    return alpha * (np.triu(D @ U.T, 1) @ U)
 
 
 # ----------------------------------------------------------------------------------------------
@@ -277,14 +315,17 @@ def _outputs(d_out, d_in, group):
             np.zeros((d_out, d_in)), np.zeros((d_out, d_in)))
 
 
-def obs_unblocked(W, U, bits: int, group: int = 128):
+def obs_unblocked(W, U, bits: int, group: int = 128, P=None):
     """Sequential OBS: for each column p, quantise it (group parameters taken at the group's
     first column from the current W), form the scaled error e_p = (w_p - w_hat_p) / U_pp and
-    subtract e_p U_{p, p:} from the columns p onward. Column p then holds w_hat_p.
+    subtract e_p U_{p, p:} from the columns p onward; with the drift correction P also add
+    w_p P_{p, p:}, w_p being column p before it is quantised (eq. kronq_update; R17). Column p
+    then holds w_hat_p.
 
     Returns dict(codes, scales, zeros, err, w_hat, W) with W the final compensated matrix."""
     W = as_f64(W).copy()
     U = np.asarray(U, dtype=np.float64)
+    P = None if P is None else np.asarray(P, dtype=np.float64)
     d_out, d_in = W.shape
     if d_in % group:
         raise ValueError("d_in must be a multiple of the group size")
@@ -294,17 +335,23 @@ def obs_unblocked(W, U, bits: int, group: int = 128):
             s, z = group_params(W[:, p:p + group], bits)
             scales[:, p // group], zeros[:, p // group] = s, z
         q, wh = quantize(W[:, p], s, z, bits)
-        e = (W[:, p] - wh) / U[p, p]
+        x = W[:, p].copy()
+        e = (x - wh) / U[p, p]
         W[:, p:] -= np.outer(e, U[p, p:])
+        if P is not None:
+            W[:, p:] += np.outer(x, P[p, p:])
         codes[:, p], err[:, p], w_hat[:, p] = q, e, wh
     return {"codes": codes, "scales": scales, "zeros": zeros, "err": err, "w_hat": w_hat, "W": W}
 
 
-def obs_blocked(W, U, bits: int, group: int = 128, block: int = 128):
-    """Algorithm 2 with P = 0: in-block sequential updates restricted to the block, then one
-    trailing update W[:, i+B:] -= E U[i:i+B, i+B:] per block (lazy batch)."""
+def obs_blocked(W, U, bits: int, group: int = 128, block: int = 128, P=None):
+    """Algorithm 2: in-block sequential updates restricted to the block, then one trailing
+    update W[:, i+B:] -= E U[i:i+B, i+B:] - W_blk P[i:i+B, i+B:] per block (lazy batch), where
+    W_blk holds the block's columns as they stood when each was quantised (R17). P = None is
+    the P = 0 case."""
     W = as_f64(W).copy()
     U = np.asarray(U, dtype=np.float64)
+    P = None if P is None else np.asarray(P, dtype=np.float64)
     d_out, d_in = W.shape
     if d_in % group:
         raise ValueError("d_in must be a multiple of the group size")
@@ -312,17 +359,23 @@ def obs_blocked(W, U, bits: int, group: int = 128, block: int = 128):
     for i in range(0, d_in, block):
         j_end = min(i + block, d_in)
         E = np.zeros((d_out, j_end - i))
+        Wq = np.zeros((d_out, j_end - i))
         for j in range(i, j_end):
             if j % group == 0:
                 s, z = group_params(W[:, j:j + group], bits)
                 scales[:, j // group], zeros[:, j // group] = s, z
             q, wh = quantize(W[:, j], s, z, bits)
-            e = (W[:, j] - wh) / U[j, j]
+            x = W[:, j].copy()
+            e = (x - wh) / U[j, j]
             W[:, j:j_end] -= np.outer(e, U[j, j:j_end])
-            E[:, j - i] = e
+            if P is not None:
+                W[:, j:j_end] += np.outer(x, P[j, j:j_end])
+            E[:, j - i], Wq[:, j - i] = e, x
             codes[:, j], err[:, j], w_hat[:, j] = q, e, wh
         if j_end < d_in:
             W[:, j_end:] -= E @ U[i:j_end, j_end:]
+            if P is not None:
+                W[:, j_end:] += Wq @ P[i:j_end, j_end:]
     return {"codes": codes, "scales": scales, "zeros": zeros, "err": err, "w_hat": w_hat, "W": W}
 
 
@@ -333,6 +386,18 @@ def kfac_loss(dW, HX, HG) -> float:
     """tr(H_G dW H_X dW^T) = sum_ij (H_G dW)_ij (dW H_X)_ij."""
     dW = np.asarray(dW, dtype=np.float64)
     return float(np.sum((np.asarray(HG, np.float64) @ dW) * (dW @ np.asarray(HX, np.float64))))
+
+
+def kronq_objective(W, W_hat, HX, HG, D=None) -> float:
+    """The full layer objective of eq. kronq_full without its constant term:
+    tr(H_G (dW H_X dW^T + 2 W D dW^T)) with dW = W - W_hat (D = None drops the drift term)."""
+    W = np.asarray(W, dtype=np.float64)
+    dW = W - np.asarray(W_hat, dtype=np.float64)
+    HG = np.asarray(HG, dtype=np.float64)
+    val = kfac_loss(dW, HX, HG)
+    if D is not None:
+        val += 2.0 * float(np.sum((HG @ W @ np.asarray(D, dtype=np.float64)) * dW))
+    return val
 
 
 # ----------------------------------------------------------------------------------------------
