@@ -9,6 +9,10 @@
  *      Hadamard rotations on both sides                                   (Sec. 4.2, eqs. rescale, biip; Alg. 1);
  *   4. damping and the inverse-Cholesky factor of H_X                      (Alg. 2, first lines);
  *   5. the column-wise OBS sweep with group quantisation, in lazy blocks   (eq. obs_update, Prop. 1; Alg. 2).
+ * With the drift correction of GPTAQ (the paper's default, KronQ+GPTAQ; eqs. gptaq_obj,
+ * kronq_full, kronq_update) the path also accumulates D = dX^T X (dX = X~ - X, the input drift),
+ * transforms it with H_X's input-side BiIP, forms P = alpha ((D U^T) . M_U) U and sweeps with
+ * W_j P[j, :] added to every compensation.
  *
  * Conventions (all entry points):
  *   - Matrices are row-major with an explicit leading dimension (elements). Pointers marked
@@ -25,8 +29,10 @@
  *
  * Readings of the paper that fix the semantics (the paper is silent or garbled there):
  *   covariances are plain sums; the inverse-Cholesky factor is the upper U with
- *   inv(H~) = U^T U and the sweep uses its rows; the drift correction P of Algorithm 2 is
- *   zero; the quantiser is the asymmetric min-max grid per row and group of 128 columns,
+ *   inv(H~) = U^T U and the sweep uses its rows; the paper's lower L (inv(H~) = L L^T) of the
+ *   drift correction is U^T and its mask M_U is strictly upper; the drift term uses each column
+ *   as it stood when it was quantised; the quantiser is the asymmetric min-max grid per row and
+ *   group of columns (128, or wider up to the whole row: the per-channel grid),
  *   with scale = float32((xmax - xmin) / (2^b - 1)), zero = rint(-xmin / scale),
  *   q = clamp(rint(w / scale) + zero, 0, 2^b - 1), divisions in IEEE float64, rint half to even.
  */
@@ -47,8 +53,8 @@ extern "C" {
 #define KRONQ_ERR_NOT_PD (-3)      /* reported by the host binding after reading *info */
 #define KRONQ_ERR_HIP (-4)         /* a HIP launch or runtime call failed */
 #define KRONQ_ERR_WORKSPACE (-5)   /* ws_bytes smaller than kronq_workspace_bytes() */
-#define KRONQ_ERR_UNSUPPORTED (-6) /* valid but not implemented: group != 128, bits not in 2..4,
-                                      rotated dimension not 2^k or 28 * 2^k */
+#define KRONQ_ERR_UNSUPPORTED (-6) /* valid but not implemented: group not a multiple of 128,
+                                      block != 128, rotated dimension not 2^k or 28 * 2^k */
 
 /* ---- element types --------------------------------------------------------------------- */
 #define KRONQ_BF16 1
@@ -77,6 +83,10 @@ extern "C" {
 #define KRONQ_OP_CHOL 3
 #define KRONQ_OP_OBS 4
 #define KRONQ_OP_LOSS 5
+#define KRONQ_OP_CROSS 6         /* kronq_accumulate_cross: d as d_in, tokens as n_rows */
+#define KRONQ_OP_ROTATE_DRIFT 7  /* kronq_rotate_drift: d_in */
+#define KRONQ_OP_GPTAQ 8         /* kronq_gptaq_correction: d as d_in */
+#define KRONQ_OP_OBS_DRIFT 9     /* kronq_obs_quantize_layer_drift: d_out, d_in */
 
 /* Bytes of scratch the operation needs for these sizes. For KRONQ_OP_COV pass the covariance
  * dimension d as d_in and the token count as n_rows (d_out ignored); for KRONQ_OP_CHOL pass
@@ -100,6 +110,18 @@ int kronq_version(void);
 int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
                          float* H, int64_t ldh, float alpha, float beta, void* ws,
                          size_t ws_bytes, void* stream);
+
+/* ---- 1b. drift statistic (Alg. 1 first line; eq. gptaq_obj) ------------------------------
+ * C <- beta * C + alpha * A^T B for token-major A, B [n_rows x d] with the same leading
+ * dimension ld; every entry of the d x d matrix C is written (it is not symmetric). With
+ * A = dX (the full-precision model's input minus the quantised model's, bf16) and B = X this
+ * is the paper's dX X^T. Chainable over token chunks with beta = 1, like kronq_accumulate_cov.
+ *   A, B  device, dtype KRONQ_BF16 (exact products, fp32 accumulation on MFMA) or KRONQ_FP32;
+ *         16-byte aligned, ld * elem_size a multiple of 16 for bf16.
+ *   C     device fp32 [d x ldc], ldc >= d. Workspace: KRONQ_OP_CROSS. */
+int kronq_accumulate_cross(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d,
+                           int64_t ld, float* C, int64_t ldc, float alpha, float beta, void* ws,
+                           size_t ws_bytes, void* stream);
 
 /* ---- 2. traces and sensitivity (Sec. 4.3 eq. sensitivity) --------------------------------
  * out3[0] = tr H_X, out3[1] = tr H_G, out3[2] = tr H_X * tr H_G, accumulated in fp64.
@@ -139,6 +161,18 @@ int kronq_rotate(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_
                  const float* q28_out, float* sx, float* sg, int flags, void* ws,
                  size_t ws_bytes, void* stream);
 
+/* ---- 3b. BiIP of the drift statistic (Alg. 1; Sec. 4.2) -------------------------------------
+ * D <- V diag(1/sx) D diag(1/sx) V^T, the input-side transform that kronq_rotate applies to H_X,
+ * for the drift statistic (the objective eq. kronq_full is then unchanged).
+ *   D       device fp32 [d_in x ldd], in place (16-byte aligned, ldd % 4 == 0).
+ *   sx      device fp32 [d_in] from the forward kronq_rotate; read with KRONQ_RESCALE_IN.
+ *   sign_in, q28_in  the input-side rotation draw (as for kronq_rotate); read with KRONQ_ROT_IN.
+ *   flags   a subset of KRONQ_RESCALE_IN | KRONQ_ROT_IN (the input-side flags of that call).
+ * Workspace: KRONQ_OP_ROTATE_DRIFT. */
+int kronq_rotate_drift(float* D, int64_t d_in, int64_t ldd, const float* sx,
+                       const int8_t* sign_in, const float* q28_in, int flags, void* ws,
+                       size_t ws_bytes, void* stream);
+
 /* ---- 4. damping + inverse-Cholesky factor (Alg. 2 first two lines; Prop. 1) --------------
  * H <- H + damp_rel * mean(diag H) * I (in place), then Uout = upper-triangular U with
  * inv(H) = U^T U (zeros below the diagonal are written). U = R^-1 where H = R R^T, R upper
@@ -150,6 +184,17 @@ int kronq_rotate(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_
 int kronq_cholesky_inv(float* H, int64_t d, int64_t ldh, float damp_rel, float* Uout,
                        int64_t ldu, int* info, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- 4b. drift correction (Prop. 1 eq. kronq_update; Alg. 2 third line) ------------------
+ * P = alpha ((D U^T) . M_U) U with U from kronq_cholesky_inv (the paper's L is U^T) and M_U the
+ * strictly upper mask; P is strictly upper triangular (zeros on and below the diagonal are
+ * written). Row p of P is alpha D[p, p+1:] inv(H~[p+1:, p+1:]). fp32 products, 2 d^3 / 3 flops.
+ *   D  device fp32 [d x ldd]: the transformed drift statistic (kronq_rotate_drift).
+ *   U  device fp32 [d x ldu], upper.   P  device fp32 [d x ldp]; must not alias D or U.
+ *   All 16-byte aligned with leading dimensions divisible by 4. Workspace: KRONQ_OP_GPTAQ. */
+int kronq_gptaq_correction(const float* D, int64_t d, int64_t ldd, const float* U, int64_t ldu,
+                           float alpha, float* P, int64_t ldp, void* ws, size_t ws_bytes,
+                           void* stream);
+
 /* ---- 5. lazy-block column-wise OBS with group quantisation (Alg. 2 with P = 0) -----------
  * For each block of `block` columns and each column p in it: group parameters per row are
  * taken from the current W when p is a group start; q = quant(W[:, p]);
@@ -157,7 +202,8 @@ int kronq_cholesky_inv(float* H, int64_t d, int64_t ldh, float damp_rel, float* 
  * block W[:, blk_end:] -= E_blk U[blk, blk_end:]. Column p is left holding w_hat_p.
  *   W      device fp32 [d_out x ldw], consumed (ends as the dequantised W_hat).
  *   U      device fp32 upper [d_in x ldu] from kronq_cholesky_inv.
- *   bits   2, 3 or 4; group must be 128; block must be 128.
+ *   bits   2 to 8; block must be 128; group a multiple of 128 dividing d_in (group = d_in is
+ *          the per-channel grid: one scale and zero per row, from the row before the sweep).
  *   codes  device uint8 [d_out x d_in] (ld = d_in), one code per byte.
  *   scales, zeros  device fp32 [d_out x d_in/group] (zeros are integer-valued).
  *   err    device fp32 [d_out x d_in] or NULL: the scaled errors e (ld = d_in).
@@ -166,6 +212,18 @@ int kronq_obs_quantize_layer(float* W, int64_t d_out, int64_t d_in, int64_t ldw,
                              const float* U, int64_t ldu, int bits, int group, int block,
                              uint8_t* codes, float* scales, float* zeros, float* err,
                              float* W_hat, void* ws, size_t ws_bytes, void* stream);
+
+/* ---- 5b. the sweep with the drift correction (Alg. 2; Prop. 1 eq. kronq_update) ------------
+ * As kronq_obs_quantize_layer, with every compensation of the sweep and of the trailing updates
+ * also adding w_p P[p, cols] (w_p: column p as it stood when it was quantised):
+ * W[:, p:blk_end] += w_p P[p, p:blk_end]; after the block W[:, blk_end:] += W_blk P[blk, blk_end:].
+ *   P  device fp32 [d_in x ldp] from kronq_gptaq_correction (strictly upper), not NULL.
+ * Workspace: KRONQ_OP_OBS_DRIFT. */
+int kronq_obs_quantize_layer_drift(float* W, int64_t d_out, int64_t d_in, int64_t ldw,
+                                   const float* U, int64_t ldu, const float* P, int64_t ldp,
+                                   int bits, int group, int block, uint8_t* codes, float* scales,
+                                   float* zeros, float* err, float* W_hat, void* ws,
+                                   size_t ws_bytes, void* stream);
 
 /* ---- 6. K-FAC loss (Sec. 4.1 eq. kron_obj) -----------------------------------------------
  * loss = tr(H_G dW H_X dW^T) = sum_ij (H_G dW)_ij (dW H_X)_ij with dW = W - W_hat (W_hat NULL:

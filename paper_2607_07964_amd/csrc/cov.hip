@@ -1,12 +1,13 @@
-// Covariance accumulation H <- beta H + alpha A^T A (Sec. 4.1 eq. kfac; Alg. 1 first line).
+// Covariance accumulation H <- beta H + alpha A^T A (Sec. 4.1 eq. kfac; Alg. 1 first line), and
+// the drift statistic C <- beta C + alpha A^T B (Alg. 1 first line, dX X^T in token-major form)
+// with the same kernels over all tiles instead of the upper triangle ("cross" below).
 //
 // bf16 path: a syrk on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16). bf16 x bf16 products
 // are exact in fp32 and accumulate in fp32.
-//   * Work split: the token dimension is cut into S slices (split-K); workgroup b takes slice
-//     b % S. S is chosen so that the tiles x slices workgroups fill whole rounds of the CUs
-//     (see cov_plan); with S = 8 each XCD would stream its own eighth of the tokens, which
-//     measured no faster than other mappings.
-//   * Each workgroup owns one 256 x 256 tile (I <= J) of the upper triangle of H for its slice:
+//   * Work split: the token dimension is cut into S slices (split-K). S is chosen so that the
+//     tiles x slices workgroups fill whole rounds of the CUs, in multiples of 8 that keep each
+//     XCD on its own slices (see cov_plan).
+//   * Each workgroup owns one 256 x 256 tile (I <= J; any I, J for cross) of H for its slice:
 //     4 waves, each a 128 x 128 sub-tile = 4 x 4 MFMA blocks of 32 x 32, 256 fp32
 //     accumulators per lane.
 //   * Interior tiles (syrk_bf16_dma below) stream 32-token stages straight from HBM into a
@@ -16,7 +17,7 @@
 //     written token-contiguous to LDS so that an MFMA operand is one 16-byte read.
 //   * Partial tiles go to the workspace; a reduction kernel sums the slices, applies
 //     alpha/beta and writes both triangles (the mirror through an LDS transpose), so H is
-//     exactly symmetric.
+//     exactly symmetric; for cross every tile is written as it is.
 // fp32 path (small fp32 inputs): a plain LDS-tiled fp32 FMA kernel over the full matrix.
 #include <algorithm>
 #include <cmath>
@@ -88,10 +89,11 @@ __device__ __forceinline__ void store_block_t(uint32_t* __restrict__ lds, const 
   }
 }
 
+template <bool CROSS>
 __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
-    const uint16_t* __restrict__ A, int64_t tok0, int64_t tok_end, int64_t d, int64_t lda,
-    float* __restrict__ part, int n_slices, int64_t rows_per_slice, int T, int edge_only,
-    int out_slice0) {
+    const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, int64_t tok0,
+    int64_t tok_end, int64_t d, int64_t lda, float* __restrict__ part, int n_slices,
+    int64_t rows_per_slice, int T, int edge_only, int out_slice0) {
   __shared__ uint32_t lds[2 * 2 * OPER];  // [buffer][operand][256 rows][36 dwords]
 
   const int tid = threadIdx.x;
@@ -99,9 +101,20 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
   const int lane = tid & 63;
   const int slice = blockIdx.x % n_slices;
   int I, J;
-  if (edge_only) {  // tiles of the last (ragged) column block: (I, T-1), I = 0..T-1
-    I = blockIdx.x / n_slices;
-    J = T - 1;
+  if (edge_only) {  // tiles of the last (ragged) block: (I, T-1), I = 0..T-1 (and for cross
+                    // also (T-1, J), J = 0..T-2)
+    const int e = blockIdx.x / n_slices;
+    if (CROSS && e >= T) {
+      I = T - 1;
+      J = e - T;
+    } else {
+      I = e;
+      J = T - 1;
+    }
+  } else if (CROSS) {
+    const int rem = blockIdx.x / n_slices;
+    I = rem / T;
+    J = rem % T;
   } else {
     int rem = blockIdx.x / n_slices;
     I = 0;
@@ -111,8 +124,10 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
     }
     J = I + rem;
   }
-  const int64_t pos = int64_t(I) * T - int64_t(I) * (I - 1) / 2 + (J - I);
-  const bool diag = (I == J);
+  const int64_t pos =
+      CROSS ? int64_t(I) * T + J : int64_t(I) * T - int64_t(I) * (I - 1) / 2 + (J - I);
+  const bool diag = !CROSS && (I == J);
+  const uint16_t* const Bm = CROSS ? B : A;
   const int64_t i0 = int64_t(I) * TT, j0 = int64_t(J) * TT;
   const int64_t t_begin = tok0 + int64_t(slice) * rows_per_slice;
   const int64_t t_end = min(tok_end, t_begin + rows_per_slice);
@@ -134,7 +149,7 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
   u32x4_t va[8], vb[8];
   if (n_st > 0) {
     load_block(va, A, lda, t_begin + tg * 8, t_end, i0 + ig * 8, d);
-    if (!diag) load_block(vb, A, lda, t_begin + tg * 8, t_end, j0 + ig * 8, d);
+    if (!diag) load_block(vb, Bm, lda, t_begin + tg * 8, t_end, j0 + ig * 8, d);
     store_block_t(lds, va, ig * 8, tg * 4);
     if (!diag) store_block_t(lds + OPER, vb, ig * 8, tg * 4);
   }
@@ -160,7 +175,7 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
     if (more) {
       const int64_t t = t_begin + (st + 1) * KC + tg * 8;
       load_block(va, A, lda, t, t_end, i0 + ig * 8, d);
-      if (!diag) load_block(vb, A, lda, t, t_end, j0 + ig * 8, d);
+      if (!diag) load_block(vb, Bm, lda, t, t_end, j0 + ig * 8, d);
     }
     const uint32_t* sa = lds + buf * 2 * OPER;
     const uint32_t* sb = diag ? sa : sa + OPER;
@@ -188,7 +203,7 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
   }
 
   // partial tile, row-major 256 x 256 (rows: channels i of the tile, cols: channels j)
-  const int64_t npos = int64_t(T) * (T + 1) / 2;
+  const int64_t npos = CROSS ? int64_t(T) * T : int64_t(T) * (T + 1) / 2;
   float* out = part + (int64_t(out_slice0 + slice) * npos + pos) * (TT * TT);
 #pragma unroll
   for (int bi = 0; bi < 4; ++bi)
@@ -249,7 +264,9 @@ __device__ __forceinline__ bf16x8_t tr_frag(const uint32_t* buf, int tb, int cb,
   return out;
 }
 
+template <bool CROSS>
 __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restrict__ A,
+                                                        const uint16_t* __restrict__ B,
                                                         int64_t n_rows, int64_t lda,
                                                         float* __restrict__ part, int n_slices,
                                                         int64_t rows_per_slice, int T, int Tf) {
@@ -262,7 +279,7 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
   // 8 XCDs) runs the tiles of its slices x, x + 8, ... one slice after another, so the
   // workgroups that run together on an XCD read the same tokens through its L2; otherwise
   // slice = b % S
-  const int ntile = Tf * (Tf + 1) / 2;
+  const int ntile = CROSS ? Tf * Tf : Tf * (Tf + 1) / 2;
   int slice, rem;
   if ((n_slices & 7) == 0) {
     const int kk = int(blockIdx.x >> 3);
@@ -272,11 +289,17 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
     slice = int(blockIdx.x) % n_slices;
     rem = int(blockIdx.x) / n_slices;
   }
-  // tile (I <= J) of sequence number rem: panels of PJ tile columns, within a panel by rows, so
-  // that the 32 workgroups running together on an XCD form an 8 x 4 block of tiles that reads
-  // 12 channel blocks rather than up to 64 (at d = 28672 this cut the time by 9-11%)
+  // tile (I <= J; any I, J for cross) of sequence number rem: panels of PJ tile columns, within
+  // a panel by rows, so that the 32 workgroups running together on an XCD form an 8 x 4 block of
+  // tiles that reads 12 channel blocks rather than up to 64 (at d = 28672 this cut the time by
+  // 9-11%)
   int I, J;
-  {
+  if (CROSS) {
+    const int pp = rem / (Tf * PJ), r = rem % (Tf * PJ);
+    const int j0 = pp * PJ, w = min(Tf, j0 + PJ) - j0;
+    I = r / w;
+    J = j0 + r % w;
+  } else {
     int pp = 0, r = rem;
     while (true) {
       const int j0 = pp * PJ, w = min(Tf, j0 + PJ) - j0;
@@ -300,7 +323,8 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
       J = I + r;
     }
   }
-  const int64_t pos = int64_t(I) * T - int64_t(I) * (I - 1) / 2 + (J - I);
+  const int64_t pos =
+      CROSS ? int64_t(I) * T + J : int64_t(I) * T - int64_t(I) * (I - 1) / 2 + (J - I);
   const int64_t t_begin = int64_t(slice) * rows_per_slice;
   const int64_t t_end = min(n_rows, t_begin + rows_per_slice);
   const int n_st = t_end > t_begin ? int((t_end - t_begin) / DK) : 0;  // full stages
@@ -312,7 +336,7 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
     off[k] = int64_t(t) * lda + 8 * c8;
   }
   const uint16_t* Ai = A + t_begin * lda + int64_t(I) * TT;
-  const uint16_t* Aj = A + t_begin * lda + int64_t(J) * TT;
+  const uint16_t* Aj = (CROSS ? B : A) + t_begin * lda + int64_t(J) * TT;
   auto issue = [&](int st, int b) {
     const int64_t so = int64_t(st) * DK * lda;
 #pragma unroll
@@ -344,15 +368,6 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
       for (int bj = 0; bj < 4; ++bj)
         acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][bi], fb[slot][bj],
                                                               acc[bi][bj], 0, 0, 0);
-  };
-  // this wave's loads of a stage are done when at most `later` newer stages are outstanding
-  auto wait_stage = [&](int later) {
-    if (later >= 2)
-      wait_vm<16>();
-    else if (later == 1)
-      wait_vm<8>();
-    else
-      wait_vm<0>();
   };
   // interleave pattern for one half-stage: 16 (MFMA, DS read) pairs
   // the next half-stage's 16 operand reads go out two per MFMA over the first 8 MFMAs: a use of
@@ -440,7 +455,7 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
       }
     }
   }
-  const int64_t npos = int64_t(T) * (T + 1) / 2;
+  const int64_t npos = CROSS ? int64_t(T) * T : int64_t(T) * (T + 1) / 2;
   float* out = part + (int64_t(slice) * npos + pos) * (TT * TT);
   const int l32 = lane & 31, lhi = lane >> 5;
 #pragma unroll
@@ -455,22 +470,30 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
       }
 }
 
-// Sum the S partial tiles of one 64 x 64 sub-block and write H (and its mirror).
+// Sum the S partial tiles of one 64 x 64 sub-block and write H (and its mirror; cross: the
+// sub-block as it is).
+template <bool CROSS>
 __global__ __launch_bounds__(256) void syrk_reduce(const float* __restrict__ part, int n_slices,
                                                    int T, int64_t d, float* __restrict__ H,
                                                    int64_t ldh, float alpha, float beta) {
   __shared__ float tr[64][65];
   const int pos = blockIdx.x >> 4;
   const int sub = blockIdx.x & 15;
-  int I = 0, rem = pos;
-  while (rem >= T - I) {
-    rem -= T - I;
-    ++I;
+  int I = 0, J = 0;
+  if (CROSS) {
+    I = pos / T;
+    J = pos % T;
+  } else {
+    int rem = pos;
+    while (rem >= T - I) {
+      rem -= T - I;
+      ++I;
+    }
+    J = I + rem;
   }
-  const int J = I + rem;
   const int sr = (sub >> 2) * 64, sc = (sub & 3) * 64;  // sub-block origin inside the tile
   const int64_t gi0 = int64_t(I) * TT + sr, gj0 = int64_t(J) * TT + sc;
-  const int64_t npos = int64_t(T) * (T + 1) / 2;
+  const int64_t npos = CROSS ? int64_t(T) * T : int64_t(T) * (T + 1) / 2;
   const int tid = threadIdx.x;
   const int c4 = (tid & 15) * 4;
   const int rb = tid >> 4;
@@ -491,6 +514,21 @@ __global__ __launch_bounds__(256) void syrk_reduce(const float* __restrict__ par
     v[k][1] = s1;
     v[k][2] = s2;
     v[k][3] = s3;
+  }
+  if (CROSS) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int64_t gi = gi0 + rb + 16 * k;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t gj = gj0 + c4 + e;
+        if (gi < d && gj < d) {
+          float* h = H + gi * ldh + gj;
+          *h = beta == 0.f ? alpha * v[k][e] : alpha * v[k][e] + beta * *h;
+        }
+      }
+    }
+    return;
   }
   // upper triangle (i <= j) from the sums; the strict lower triangle is its mirror, so H is
   // exactly symmetric (diagonal tiles included)
@@ -522,8 +560,10 @@ __global__ __launch_bounds__(256) void syrk_reduce(const float* __restrict__ par
   }
 }
 
-// Plain fp32 syrk for fp32 inputs: 64 x 64 tiles, 4 x 4 outputs per thread.
-__global__ __launch_bounds__(256) void syrk_f32(const float* __restrict__ A, int64_t n_rows,
+// Plain fp32 A^T B for fp32 inputs (B = A for the covariance): 64 x 64 tiles, 4 x 4 outputs per
+// thread.
+__global__ __launch_bounds__(256) void syrk_f32(const float* __restrict__ A,
+                                                const float* __restrict__ B, int64_t n_rows,
                                                 int64_t d, int64_t lda, float* __restrict__ H,
                                                 int64_t ldh, float alpha, float beta) {
   __shared__ float sa[16][64];
@@ -539,7 +579,7 @@ __global__ __launch_bounds__(256) void syrk_f32(const float* __restrict__ A, int
       const int r = idx >> 6, c = idx & 63;
       const int64_t t = t0 + r;
       sa[r][c] = (t < n_rows && i0 + c < d) ? A[t * lda + i0 + c] : 0.f;
-      sb[r][c] = (t < n_rows && j0 + c < d) ? A[t * lda + j0 + c] : 0.f;
+      sb[r][c] = (t < n_rows && j0 + c < d) ? B[t * lda + j0 + c] : 0.f;
     }
     __syncthreads();
 #pragma unroll
@@ -614,13 +654,13 @@ int device_cus() {
 // token ranges on an XCD and measured slower), or 1..7 when there are too few tokens for 8
 // slices of 4 * KC. At d = 4096, N = 262144 this gives S = 32: 4352 workgroups in exactly 17
 // rounds, instead of S = 8 in 4.25 rounds.
-CovPlan cov_plan(int64_t n_rows, int64_t d) {
+CovPlan cov_plan(int64_t n_rows, int64_t d, bool cross) {
   CovPlan p;
   p.T = int(cdiv(d, TT));
   p.Tf = int(d / TT);
-  p.npos = int64_t(p.T) * (p.T + 1) / 2;
-  const int64_t tiles = int64_t(p.Tf) * (p.Tf + 1) / 2 > 0 ? int64_t(p.Tf) * (p.Tf + 1) / 2
-                                                          : p.npos;
+  p.npos = cross ? int64_t(p.T) * p.T : int64_t(p.T) * (p.T + 1) / 2;
+  const int64_t full = cross ? int64_t(p.Tf) * p.Tf : int64_t(p.Tf) * (p.Tf + 1) / 2;
+  const int64_t tiles = full > 0 ? full : p.npos;
   const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(32, n_rows / (4 * KC)));
   const double cus = double(device_cus());
   double best = 1e300;
@@ -645,45 +685,74 @@ CovPlan cov_plan(int64_t n_rows, int64_t d) {
   return p;
 }
 
+// the bf16 pipeline shared by the covariance (B == nullptr) and the cross product
+int gram_bf16(const uint16_t* A, const uint16_t* B, int64_t n_rows, int64_t d, int64_t lda,
+              float* H, int64_t ldh, float alpha, float beta, void* ws, hipStream_t s) {
+  const bool cross = B != nullptr;
+  const CovPlan p = cov_plan(n_rows, d, cross);
+  float* part = static_cast<float*>(ws);
+  const int64_t full = cross ? int64_t(p.Tf) * p.Tf : int64_t(p.Tf) * (p.Tf + 1) / 2;
+  // interior tiles, whole 32-token stages of every slice
+  if (p.Tf > 0) {
+    const dim3 grid(unsigned(int64_t(p.S) * full));
+    if (cross)
+      KQ_TRY(launch("cross_bf16_mfma", syrk_bf16_dma<true>, grid, dim3(256), 0, s, A, B, n_rows,
+                    lda, part, p.S, p.rows_per_slice, p.T, p.Tf));
+    else
+      KQ_TRY(launch("syrk_bf16_mfma", syrk_bf16_dma<false>, grid, dim3(256), 0, s, A, A, n_rows,
+                    lda, part, p.S, p.rows_per_slice, p.T, p.Tf));
+  }
+  // tiles of a ragged last channel block, same tokens
+  const int64_t body_end = p.tail ? p.tail_begin : n_rows;
+  if (p.T > p.Tf) {
+    const dim3 grid(unsigned(p.S * (cross ? 2 * p.T - 1 : p.T)));
+    if (cross)
+      KQ_TRY(launch("cross_bf16_edge", syrk_bf16_partial<true>, grid, dim3(256), 0, s, A, B,
+                    int64_t(0), body_end, d, lda, part, p.S, p.rows_per_slice, p.T, 1, 0));
+    else
+      KQ_TRY(launch("syrk_bf16_edge", syrk_bf16_partial<false>, grid, dim3(256), 0, s, A, A,
+                    int64_t(0), body_end, d, lda, part, p.S, p.rows_per_slice, p.T, 1, 0));
+  }
+  // the last < 32 tokens, every tile, as one extra slice
+  if (p.tail) {
+    const dim3 grid(unsigned(p.npos));
+    if (cross)
+      KQ_TRY(launch("cross_bf16_tail", syrk_bf16_partial<true>, grid, dim3(256), 0, s, A, B,
+                    p.tail_begin, n_rows, d, lda, part, 1, n_rows - p.tail_begin, p.T, 0, p.S));
+    else
+      KQ_TRY(launch("syrk_bf16_tail", syrk_bf16_partial<false>, grid, dim3(256), 0, s, A, A,
+                    p.tail_begin, n_rows, d, lda, part, 1, n_rows - p.tail_begin, p.T, 0, p.S));
+  }
+  const int ns = p.S + (p.tail ? 1 : 0);
+  if (cross)
+    return launch("cross_reduce", syrk_reduce<true>, dim3(unsigned(p.npos * 16)), dim3(256), 0, s,
+                  static_cast<const float*>(part), ns, p.T, d, H, ldh, alpha, beta);
+  return launch("syrk_reduce", syrk_reduce<false>, dim3(unsigned(p.npos * 16)), dim3(256), 0, s,
+                static_cast<const float*>(part), ns, p.T, d, H, ldh, alpha, beta);
+}
+
 }  // namespace
 
-size_t cov_ws_bytes(int dtype, int64_t n_rows, int64_t d) {
+size_t cov_ws_bytes(int dtype, int64_t n_rows, int64_t d, bool cross) {
   if (dtype != KRONQ_BF16 || n_rows <= 0 || d <= 0) return 0;
-  const CovPlan p = cov_plan(n_rows, d);
+  const CovPlan p = cov_plan(n_rows, d, cross);
   return align256(size_t(p.S + 1) * size_t(p.npos) * TT * TT * sizeof(float));
 }
 
-int cov_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda, float* H,
-               int64_t ldh, float alpha, float beta, void* ws, hipStream_t s) {
+int cov_launch(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d, int64_t lda,
+               float* H, int64_t ldh, float alpha, float beta, void* ws, hipStream_t s) {
   if (n_rows == 0) {
     return launch("cov_scale", scale_matrix, dim3(unsigned(cdiv(d, 256)), unsigned(d)), dim3(256),
                   0, s, H, d, ldh, beta);
   }
   if (dtype == KRONQ_FP32) {
     const unsigned g = unsigned(cdiv(d, 64));
-    return launch("syrk_f32", syrk_f32, dim3(g, g), dim3(256), 0, s,
-                  static_cast<const float*>(A), n_rows, d, lda, H, ldh, alpha, beta);
+    const float* a = static_cast<const float*>(A);
+    return launch(B ? "cross_f32" : "syrk_f32", syrk_f32, dim3(g, g), dim3(256), 0, s, a,
+                  B ? static_cast<const float*>(B) : a, n_rows, d, lda, H, ldh, alpha, beta);
   }
-  const CovPlan p = cov_plan(n_rows, d);
-  const uint16_t* X = static_cast<const uint16_t*>(A);
-  float* part = static_cast<float*>(ws);
-  // interior tiles, whole 32-token stages of every slice
-  if (p.Tf > 0)
-    KQ_TRY(launch("syrk_bf16_mfma", syrk_bf16_dma,
-                  dim3(unsigned(int64_t(p.S) * p.Tf * (p.Tf + 1) / 2)), dim3(256), 0, s, X, n_rows,
-                  lda, part, p.S, p.rows_per_slice, p.T, p.Tf));
-  // tiles of a ragged last channel block, same tokens
-  const int64_t body_end = p.tail ? p.tail_begin : n_rows;
-  if (p.T > p.Tf)
-    KQ_TRY(launch("syrk_bf16_edge", syrk_bf16_partial, dim3(unsigned(p.S * p.T)), dim3(256), 0, s,
-                  X, int64_t(0), body_end, d, lda, part, p.S, p.rows_per_slice, p.T, 1, 0));
-  // the last < 32 tokens, every tile, as one extra slice
-  if (p.tail)
-    KQ_TRY(launch("syrk_bf16_tail", syrk_bf16_partial, dim3(unsigned(p.npos)), dim3(256), 0, s,
-                  X, p.tail_begin, n_rows, d, lda, part, 1, n_rows - p.tail_begin, p.T, 0, p.S));
-  return launch("syrk_reduce", syrk_reduce, dim3(unsigned(p.npos * 16)), dim3(256), 0, s,
-                static_cast<const float*>(part), p.S + (p.tail ? 1 : 0), p.T, d, H, ldh, alpha,
-                beta);
+  return gram_bf16(static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), n_rows, d,
+                   lda, H, ldh, alpha, beta, ws, s);
 }
 
 }  // namespace kq

@@ -1,12 +1,14 @@
 // C -= A B with fp32 operands on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16), fp32-accurate
 // through a three-term split: x = x_hi + x_lo with x_hi = bf16(x), x_lo = bf16(x - x_hi), and
 // A B ~ A_hi B_hi + A_hi B_lo + A_lo B_hi (the dropped A_lo B_lo term and the parts of x below
-// x_lo are ~2^-16 of each product). Used for the OBS trailing updates W[:, rest] -= E U[blk, rest],
+// x_lo are ~2^-16 of each product). Used for the OBS trailing updates W[:, rest] -= E U[blk, rest]
+// (and, with the drift correction, the second product -W_blk P[blk, rest] in the same pass),
 // where A = E (fp32, k contiguous) is split as it is staged and B = U rows comes pre-split and
 // transposed (Ut_hi / Ut_lo, [n][k] bf16) by split_transpose, once per layer.
 //   * TM x TM output tile per workgroup (TM = 128 or 64), 4 waves in a 2 x 2 grid, each wave
 //     (TM/2) x (TM/2) = up to 2 x 2 MFMA blocks of 32 x 32 with fp32 accumulators.
 //   * K advances 32 at a time through one LDS stage: A_hi, A_lo [m][k] and B_hi, B_lo [n][k],
+//     first over the K of the first pair, then over the K2 of the second;
 //     rows padded to 80 bytes so that the 16-byte operand reads of 8 consecutive lanes hit
 //     distinct banks; the next stage is fetched into registers during the MFMAs.
 #include "kq_common.hpp"
@@ -28,12 +30,11 @@ __device__ __forceinline__ uint32_t bf16_rne(float x) {
 __device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
 
 template <int TM>
-__global__ __launch_bounds__(256) void gemm_bf16x3_sub(int64_t M, int64_t N, int64_t K,
-                                                       const float* __restrict__ A, int64_t lda,
-                                                       const uint16_t* __restrict__ Bh,
-                                                       const uint16_t* __restrict__ Bl,
-                                                       int64_t ldb, float* __restrict__ C,
-                                                       int64_t ldc) {
+__global__ __launch_bounds__(256) void gemm_bf16x3_sub(
+    int64_t M, int64_t N, int64_t K, const float* __restrict__ A, int64_t lda,
+    const uint16_t* __restrict__ Bh, const uint16_t* __restrict__ Bl, int64_t ldb, int64_t K2,
+    const float* __restrict__ A2, int64_t lda2, const uint16_t* __restrict__ B2h,
+    const uint16_t* __restrict__ B2l, int64_t ldb2, float* __restrict__ C, int64_t ldc) {
   constexpr int NB = TM / 64;                  // 32 x 32 blocks per wave edge (1 or 2)
   constexpr int AV = TM * BK / 4 / 256;        // float4 of A per thread per stage
   constexpr int BV = TM * BK / 8 / 256;        // 16-byte chunks of each B half per thread
@@ -45,20 +46,26 @@ __global__ __launch_bounds__(256) void gemm_bf16x3_sub(int64_t M, int64_t N, int
 
   float4 ra[AV];
   uint4 rbh[BV], rbl[BV];
-  auto fetch = [&](int64_t k0) {
+  auto fetch = [&](int64_t kk) {
+    // stage kk of the concatenated K: the first pair for kk < K, else the second
+    const bool first = kk < K;
+    const float* a = first ? A : A2;
+    const uint16_t* bh = first ? Bh : B2h;
+    const uint16_t* bl = first ? Bl : B2l;
+    const int64_t la = first ? lda : lda2, lb = first ? ldb : ldb2, k0 = first ? kk : kk - K;
 #pragma unroll
     for (int v = 0; v < AV; ++v) {
       const int e = tid + 256 * v, m = e / (BK / 4), kq = (e % (BK / 4)) * 4;
-      ra[v] = (m0 + m < M) ? *reinterpret_cast<const float4*>(A + (m0 + m) * lda + k0 + kq)
+      ra[v] = (m0 + m < M) ? *reinterpret_cast<const float4*>(a + (m0 + m) * la + k0 + kq)
                            : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
     for (int v = 0; v < BV; ++v) {
       const int e = tid + 256 * v, n = e / (BK / 8), kc = (e % (BK / 8)) * 8;
       const bool ok = n0 + n < N;
-      rbh[v] = ok ? *reinterpret_cast<const uint4*>(Bh + (n0 + n) * ldb + k0 + kc)
+      rbh[v] = ok ? *reinterpret_cast<const uint4*>(bh + (n0 + n) * lb + k0 + kc)
                   : make_uint4(0u, 0u, 0u, 0u);
-      rbl[v] = ok ? *reinterpret_cast<const uint4*>(Bl + (n0 + n) * ldb + k0 + kc)
+      rbl[v] = ok ? *reinterpret_cast<const uint4*>(bl + (n0 + n) * lb + k0 + kc)
                   : make_uint4(0u, 0u, 0u, 0u);
     }
   };
@@ -89,12 +96,13 @@ __global__ __launch_bounds__(256) void gemm_bf16x3_sub(int64_t M, int64_t N, int
   for (int a = 0; a < NB; ++a)
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[a][b] = f32x16_t{};
-  if (K > 0) fetch(0);
-  for (int64_t k0 = 0; k0 < K; k0 += BK) {
+  const int64_t KT = K + K2;
+  if (KT > 0) fetch(0);
+  for (int64_t k0 = 0; k0 < KT; k0 += BK) {
     __syncthreads();
     stash();
     __syncthreads();
-    if (k0 + BK < K) fetch(k0 + BK);
+    if (k0 + BK < KT) fetch(k0 + BK);
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int kc = ks * 16 + 8 * lhi;  // this lane's 8 k of the 16
@@ -133,17 +141,19 @@ __global__ __launch_bounds__(256) void gemm_bf16x3_sub(int64_t M, int64_t N, int
       }
 }
 
-// Ut_hi[n][k] + Ut_lo[n][k] = U[k][n] (the three-term split of U^T), 32 x 32 tiles through LDS
+// Ut_hi[n][k] + Ut_lo[n][k] = sgn U[k][n] (the three-term split of +-U^T), 32 x 32 tiles
+// through LDS
 __global__ __launch_bounds__(256) void split_transpose(const float* __restrict__ U, int64_t ldu,
                                                        int64_t d, uint16_t* __restrict__ Th,
-                                                       uint16_t* __restrict__ Tl, int64_t ldt) {
+                                                       uint16_t* __restrict__ Tl, int64_t ldt,
+                                                       float sgn) {
   __shared__ float t[32][33];
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
   const int64_t k0 = int64_t(blockIdx.y) * 32, n0 = int64_t(blockIdx.x) * 32;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int64_t k = k0 + ty + 8 * i, n = n0 + tx;
-    t[ty + 8 * i][tx] = (k < d && n < d) ? U[k * ldu + n] : 0.f;
+    t[ty + 8 * i][tx] = (k < d && n < d) ? sgn * U[k * ldu + n] : 0.f;
   }
   __syncthreads();
 #pragma unroll
@@ -161,25 +171,26 @@ __global__ __launch_bounds__(256) void split_transpose(const float* __restrict__
 }  // namespace
 
 int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th, uint16_t* Tl,
-                           int64_t ldt, hipStream_t s) {
+                           int64_t ldt, hipStream_t s, bool neg) {
   const dim3 grid(unsigned(cdiv(d, 32)), unsigned(cdiv(d, 32)));
-  return launch("obs_split_u", split_transpose, grid, dim3(256), 0, s, U, ldu, d, Th, Tl, ldt);
+  return launch(neg ? "obs_split_p" : "obs_split_u", split_transpose, grid, dim3(256), 0, s, U,
+                ldu, d, Th, Tl, ldt, neg ? -1.f : 1.f);
 }
 
-int gemm_bf16x3_sub(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
-                    const uint16_t* Bh, const uint16_t* Bl, int64_t ldb, float* C, int64_t ldc,
-                    hipStream_t s, const char* name) {
-  if (M <= 0 || N <= 0 || K <= 0) return KRONQ_OK;
-  KQ_REQUIRE(K % BK == 0 && lda % 4 == 0 && ldb % 8 == 0, KRONQ_ERR_INVALID_ARG,
-             "gemm_bf16x3_sub: K %% 32, lda %% 4 and ldb %% 8 must be 0");
+int gemm_bf16x3_sub(int64_t M, int64_t N, const Bf16x3Pair& p1, const Bf16x3Pair& p2, float* C,
+                    int64_t ldc, hipStream_t s, const char* name) {
+  if (M <= 0 || N <= 0 || p1.K + p2.K <= 0) return KRONQ_OK;
+  KQ_REQUIRE(p1.K % BK == 0 && p1.lda % 4 == 0 && p1.ldb % 8 == 0 && p2.K % BK == 0 &&
+                 (p2.K == 0 || (p2.lda % 4 == 0 && p2.ldb % 8 == 0)),
+             KRONQ_ERR_INVALID_ARG, "gemm_bf16x3_sub: K %% 32, lda %% 4 and ldb %% 8 must be 0");
   if (cdiv(M, 128) * cdiv(N, 128) >= 192) {
     const dim3 grid(unsigned(cdiv(N, 128)), unsigned(cdiv(M, 128)));
-    return launch(name, gemm_bf16x3_sub<128>, grid, dim3(256), 0, s, M, N, K, A, lda, Bh, Bl, ldb,
-                  C, ldc);
+    return launch(name, gemm_bf16x3_sub<128>, grid, dim3(256), 0, s, M, N, p1.K, p1.A, p1.lda,
+                  p1.Bh, p1.Bl, p1.ldb, p2.K, p2.A, p2.lda, p2.Bh, p2.Bl, p2.ldb, C, ldc);
   }
   const dim3 grid(unsigned(cdiv(N, 64)), unsigned(cdiv(M, 64)));
-  return launch(name, gemm_bf16x3_sub<64>, grid, dim3(256), 0, s, M, N, K, A, lda, Bh, Bl, ldb, C,
-                ldc);
+  return launch(name, gemm_bf16x3_sub<64>, grid, dim3(256), 0, s, M, N, p1.K, p1.A, p1.lda, p1.Bh,
+                p1.Bl, p1.ldb, p2.K, p2.A, p2.lda, p2.Bh, p2.Bl, p2.ldb, C, ldc);
 }
 
 }  // namespace kq

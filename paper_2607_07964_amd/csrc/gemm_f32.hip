@@ -103,9 +103,11 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_mfma(int flags, int64_t M, in
   const int tid = threadIdx.x;
   const int64_t m0 = int64_t(blockIdx.y) * GT, n0 = int64_t(blockIdx.x) * GT;
   if ((flags & GEMM_LOWER_C) && m0 + GT <= n0) return;  // tile strictly above the diagonal
+  if ((flags & GEMM_UPPER_C) && n0 + GT <= m0) return;  // tile strictly below the diagonal
 
   int64_t kbeg = 0, kend = K;
   if (flags & GEMM_B_LOWER) kbeg = (n0 / GK) * GK;  // B[k][n] = 0 for k < n
+  if ((flags & GEMM_A_UPPER) && m0 > kbeg) kbeg = (m0 / GK) * GK;  // A[m][k] = 0 for k < m
   if ((flags & GEMM_A_LOWER) && m0 + GT < kend) kend = m0 + GT;  // A[m][k] = 0 for k > m
   if ((flags & GEMM_OPB_UPPER) && n0 + GT < kend) kend = n0 + GT;  // op(B)[k][n] = 0, k > n
 
@@ -188,8 +190,10 @@ __global__ __launch_bounds__(256) void gemm_f32_small(int flags, int64_t M, int6
   const int tid = threadIdx.x;
   const int64_t m0 = int64_t(blockIdx.y) * TM, n0 = int64_t(blockIdx.x) * TM;
   if ((flags & GEMM_LOWER_C) && m0 + TM <= n0) return;
+  if ((flags & GEMM_UPPER_C) && n0 + TM <= m0) return;
   int64_t kbeg = 0, kend = K;
   if (flags & GEMM_B_LOWER) kbeg = n0;
+  if ((flags & GEMM_A_UPPER) && m0 > kbeg) kbeg = m0;
   if ((flags & GEMM_A_LOWER) && m0 + TM < kend) kend = m0 + TM;
   if ((flags & GEMM_OPB_UPPER) && n0 + TM < kend) kend = n0 + TM;
   const bool a_kc = !(flags & GEMM_TA), b_kc = (flags & GEMM_TB);
@@ -300,12 +304,14 @@ int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const floa
              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
              hipStream_t s, const char* name) {
   if (M <= 0 || N <= 0) return KRONQ_OK;
-  // workgroups that do work for a tile edge t (LOWER_C drops the tiles above the diagonal)
+  // workgroups that do work for a tile edge t (LOWER_C drops the tiles above the diagonal,
+  // UPPER_C those below it)
   auto work = [&](int64_t t) {
     const int64_t tm = cdiv(M, t), tn = cdiv(N, t);
-    if (!(flags & GEMM_LOWER_C)) return tm * tn;
+    if (!(flags & (GEMM_LOWER_C | GEMM_UPPER_C))) return tm * tn;
     int64_t c = 0;
-    for (int64_t i = 0; i < tm; ++i) c += std::min(tn, i + 1);
+    for (int64_t i = 0; i < tm; ++i)
+      c += (flags & GEMM_LOWER_C) ? std::min(tn, i + 1) : std::max<int64_t>(0, tn - i);
     return c;
   };
   if (work(GT) >= 128) {

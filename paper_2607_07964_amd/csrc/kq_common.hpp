@@ -99,9 +99,10 @@ RotDim rot_dim(int64_t d);
 
 // ---- kernel-side entry points (defined in the per-step sources) ------------------------------
 // covariance
-size_t cov_ws_bytes(int dtype, int64_t n_rows, int64_t d);
-int cov_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda, float* H,
-               int64_t ldh, float alpha, float beta, void* ws, hipStream_t s);
+// covariance (B == nullptr: H = A^T A, symmetric) or cross product (H = A^T B, all tiles)
+size_t cov_ws_bytes(int dtype, int64_t n_rows, int64_t d, bool cross = false);
+int cov_launch(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d, int64_t lda,
+               float* H, int64_t ldh, float alpha, float beta, void* ws, hipStream_t s);
 // traces
 int traces_launch(const float* HX, int64_t d_in, int64_t ldx, const float* HG, int64_t d_out,
                   int64_t ldg, double* out3, hipStream_t s);
@@ -112,6 +113,10 @@ int rotate_launch(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64
                   const int8_t* sign_in, const int8_t* sign_out, const float* q28_in,
                   const float* q28_out, float* sx, float* sg, int flags, void* ws,
                   hipStream_t s);
+// drift statistic: D <- V S_X^-1 D S_X^-1 V^T with the given sx
+size_t rotate_drift_ws_bytes(int64_t d);
+int rotate_drift_launch(float* D, int64_t d, int64_t ldd, const float* sx, const int8_t* sign,
+                        const float* q28, int flags, void* ws, hipStream_t s);
 // fp32 GEMM on MFMA: C = alpha * op(A) op(B) + beta * C
 enum GemmFlags : int {
   GEMM_TA = 1,          // op(A) = A^T (A stored [K x M])
@@ -120,15 +125,25 @@ enum GemmFlags : int {
   GEMM_B_LOWER = 8,     // B is lower triangular: skip k < column-tile start
   GEMM_A_LOWER = 16,    // A is lower triangular: skip k > row-tile end
   GEMM_OPB_UPPER = 32,  // op(B) is upper triangular: skip k > column-tile end
+  GEMM_UPPER_C = 64,    // only output tiles that touch the upper triangle (i <= j)
+  GEMM_A_UPPER = 128,   // A is upper triangular: skip k < row-tile start
 };
-// C -= A B, A fp32 [M x K] (k contiguous), B given as the bf16 three-term split of B^T
-// (Bh + Bl, [N x K], k contiguous); K % 32 == 0
-int gemm_bf16x3_sub(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
-                    const uint16_t* Bh, const uint16_t* Bl, int64_t ldb, float* C, int64_t ldc,
-                    hipStream_t s, const char* name);
-// Th + Tl = U^T split into bf16 high and low parts, [d x d] with row stride ldt
+// C -= A B (+ A2 B2), A fp32 [M x K] (k contiguous), B given as the bf16 three-term split of
+// B^T (Bh + Bl, [N x K], k contiguous); likewise A2 [M x K2], B2; K % 32 == 0, K2 % 32 == 0
+struct Bf16x3Pair {
+  const float* A = nullptr;
+  int64_t lda = 0;
+  const uint16_t* Bh = nullptr;
+  const uint16_t* Bl = nullptr;
+  int64_t ldb = 0;
+  int64_t K = 0;
+};
+int gemm_bf16x3_sub(int64_t M, int64_t N, const Bf16x3Pair& p1, const Bf16x3Pair& p2, float* C,
+                    int64_t ldc, hipStream_t s, const char* name);
+// Th + Tl = sign * U^T split into bf16 high and low parts, [d x d] with row stride ldt
+// (sign = -1 when neg)
 int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th, uint16_t* Tl,
-                           int64_t ldt, hipStream_t s);
+                           int64_t ldt, hipStream_t s, bool neg = false);
 int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
              hipStream_t s, const char* name = "gemm_f32_mfma");
@@ -136,11 +151,16 @@ int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const floa
 size_t chol_ws_bytes(int64_t d);
 int chol_launch(float* H, int64_t d, int64_t ldh, float damp_rel, float* U, int64_t ldu,
                 int* info, void* ws, hipStream_t s);
-// OBS sweep
-size_t obs_ws_bytes(int64_t d_out, int64_t d_in);
+// drift correction P = alpha ((D U^T) . M_U) U
+size_t gptaq_ws_bytes(int64_t d);
+int gptaq_launch(const float* D, int64_t d, int64_t ldd, const float* U, int64_t ldu, float alpha,
+                 float* P, int64_t ldp, void* ws, hipStream_t s);
+// OBS sweep (P == nullptr: no drift correction)
+size_t obs_ws_bytes(int64_t d_out, int64_t d_in, bool drift);
+int obs_group_ok(int64_t d_in, int group);
 int obs_launch(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* U, int64_t ldu,
-               int bits, uint8_t* codes, float* scales, float* zeros, float* err, float* W_hat,
-               void* ws, hipStream_t s);
+               int bits, int group, const float* P, int64_t ldp, uint8_t* codes, float* scales,
+               float* zeros, float* err, float* W_hat, void* ws, hipStream_t s);
 // loss
 size_t loss_ws_bytes(int64_t d_out, int64_t d_in);
 int loss_launch(const void* W, int w_dtype, int64_t ldw, const float* W_hat, int64_t ldwh,

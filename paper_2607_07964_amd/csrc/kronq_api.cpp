@@ -46,18 +46,56 @@ int check_rot_side(int64_t d, const int8_t* sign, const float* q28, const char* 
 
 }  // namespace
 
+namespace {
+
+int obs_common(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* U, int64_t ldu,
+               const float* P, int64_t ldp, int bits, int group, int block, uint8_t* codes,
+               float* scales, float* zeros, float* err, float* W_hat, void* ws, size_t ws_bytes,
+               void* stream) {
+  KQ_REQUIRE(bits >= 2 && bits <= 8, KRONQ_ERR_UNSUPPORTED, "bits must be in 2..8");
+  KQ_REQUIRE(block == 128, KRONQ_ERR_UNSUPPORTED, "only block size 128 is implemented");
+  KQ_TRY(check_f32_mat(W, d_out, d_in, ldw, "W"));
+  KQ_REQUIRE(group >= 1 && d_in % group == 0, KRONQ_ERR_SHAPE,
+             "d_in (%lld) must be a multiple of the group (%d)", (long long)d_in, group);
+  KQ_REQUIRE(kq::obs_group_ok(d_in, group) > 0, KRONQ_ERR_UNSUPPORTED,
+             "group %d is not supported: it must be a multiple of 128 that divides d_in", group);
+  KQ_TRY(check_f32_mat(U, d_in, d_in, ldu, "U"));
+  if (P) KQ_TRY(check_f32_mat(P, d_in, d_in, ldp, "P"));
+  KQ_REQUIRE(codes && aligned(codes, 4), KRONQ_ERR_INVALID_ARG, "codes must be 4-byte aligned");
+  KQ_REQUIRE(scales && zeros && aligned(scales, 4) && aligned(zeros, 4), KRONQ_ERR_INVALID_ARG,
+             "scales and zeros are required");
+  KQ_REQUIRE(!err || aligned(err, 16), KRONQ_ERR_INVALID_ARG, "err must be 16-byte aligned");
+  KQ_REQUIRE(!W_hat || aligned(W_hat, 16), KRONQ_ERR_INVALID_ARG,
+             "W_hat must be 16-byte aligned");
+  KQ_REQUIRE(static_cast<const float*>(W) != U && static_cast<const float*>(W) != P,
+             KRONQ_ERR_INVALID_ARG, "W must not alias U or P");
+  KQ_TRY(check_ws(ws, ws_bytes, kq::obs_ws_bytes(d_out, d_in, P != nullptr)));
+  return kq::obs_launch(W, d_out, d_in, ldw, U, ldu, bits, group, P, ldp, codes, scales, zeros,
+                        err, W_hat, ws, as_stream(stream));
+}
+
+}  // namespace
+
 extern "C" {
 
 size_t kronq_workspace_bytes(int op, int64_t d_out, int64_t d_in, int64_t n_rows) {
   switch (op) {
     case KRONQ_OP_COV:
       return kq::cov_ws_bytes(KRONQ_BF16, n_rows, d_in);
+    case KRONQ_OP_CROSS:
+      return kq::cov_ws_bytes(KRONQ_BF16, n_rows, d_in, true);
+    case KRONQ_OP_ROTATE_DRIFT:
+      return kq::rotate_drift_ws_bytes(d_in);
+    case KRONQ_OP_GPTAQ:
+      return kq::gptaq_ws_bytes(d_in);
+    case KRONQ_OP_OBS_DRIFT:
+      return kq::obs_ws_bytes(d_out, d_in, true);
     case KRONQ_OP_ROTATE:
       return kq::rotate_ws_bytes(d_out, d_in);
     case KRONQ_OP_CHOL:
       return kq::chol_ws_bytes(d_in);
     case KRONQ_OP_OBS:
-      return kq::obs_ws_bytes(d_out, d_in);
+      return kq::obs_ws_bytes(d_out, d_in, false);
     case KRONQ_OP_LOSS:
       return kq::loss_ws_bytes(d_out, d_in);
     default:
@@ -84,7 +122,31 @@ int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, in
       KQ_REQUIRE(aligned(A, 4), KRONQ_ERR_INVALID_ARG, "fp32 A must be 4-byte aligned");
     KQ_TRY(check_ws(ws, ws_bytes, kq::cov_ws_bytes(dtype, n_rows, d)));
   }
-  return kq::cov_launch(A, dtype, n_rows, d, lda, H, ldh, alpha, beta, ws, as_stream(stream));
+  return kq::cov_launch(A, nullptr, dtype, n_rows, d, lda, H, ldh, alpha, beta, ws,
+                        as_stream(stream));
+}
+
+int kronq_accumulate_cross(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d,
+                           int64_t ld, float* C, int64_t ldc, float alpha, float beta, void* ws,
+                           size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(valid_dtype(dtype), KRONQ_ERR_INVALID_ARG, "dtype must be KRONQ_BF16 or KRONQ_FP32");
+  KQ_REQUIRE(C, KRONQ_ERR_INVALID_ARG, "C is NULL");
+  KQ_REQUIRE(n_rows >= 0 && d >= 1 && d <= 65535, KRONQ_ERR_INVALID_ARG,
+             "need n_rows >= 0 and 1 <= d <= 65535");
+  KQ_REQUIRE(ldc >= d && aligned(C, 4), KRONQ_ERR_INVALID_ARG, "bad C leading dimension");
+  if (n_rows > 0) {
+    KQ_REQUIRE(A && B, KRONQ_ERR_INVALID_ARG, "A or B is NULL");
+    KQ_REQUIRE(ld >= d, KRONQ_ERR_INVALID_ARG, "ld < d");
+    if (dtype == KRONQ_BF16)
+      KQ_REQUIRE(aligned(A, 16) && aligned(B, 16) && ld % 8 == 0, KRONQ_ERR_INVALID_ARG,
+                 "bf16 A and B must be 16-byte aligned with ld divisible by 8");
+    else
+      KQ_REQUIRE(aligned(A, 4) && aligned(B, 4), KRONQ_ERR_INVALID_ARG,
+                 "fp32 A and B must be 4-byte aligned");
+    KQ_TRY(check_ws(ws, ws_bytes, kq::cov_ws_bytes(dtype, n_rows, d, true)));
+  }
+  return kq::cov_launch(A, B, dtype, n_rows, d, ld, C, ldc, alpha, beta, ws, as_stream(stream));
 }
 
 int kronq_traces(const float* HX, int64_t d_in, int64_t ldx, const float* HG, int64_t d_out,
@@ -141,6 +203,36 @@ int kronq_rotate(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_
                            sign_out, q28_in, q28_out, sx, sg, flags, ws, as_stream(stream));
 }
 
+int kronq_rotate_drift(float* D, int64_t d_in, int64_t ldd, const float* sx,
+                       const int8_t* sign_in, const float* q28_in, int flags, void* ws,
+                       size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  const int known = KRONQ_RESCALE_IN | KRONQ_ROT_IN;
+  KQ_REQUIRE((flags & ~known) == 0, KRONQ_ERR_INVALID_ARG,
+             "kronq_rotate_drift takes only KRONQ_RESCALE_IN and KRONQ_ROT_IN (0x%x given)",
+             flags);
+  KQ_TRY(check_f32_mat(D, d_in, d_in, ldd, "D"));
+  KQ_REQUIRE(!(flags & KRONQ_RESCALE_IN) || (sx && aligned(sx, 4)), KRONQ_ERR_INVALID_ARG,
+             "KRONQ_RESCALE_IN needs sx");
+  if (flags & KRONQ_ROT_IN) KQ_TRY(check_rot_side(d_in, sign_in, q28_in, "input"));
+  KQ_TRY(check_ws(ws, ws_bytes, kq::rotate_drift_ws_bytes(d_in)));
+  return kq::rotate_drift_launch(D, d_in, ldd, sx, sign_in, q28_in, flags, ws, as_stream(stream));
+}
+
+int kronq_gptaq_correction(const float* D, int64_t d, int64_t ldd, const float* U, int64_t ldu,
+                           float alpha, float* P, int64_t ldp, void* ws, size_t ws_bytes,
+                           void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(d <= 65535, KRONQ_ERR_INVALID_ARG, "need d <= 65535");
+  KQ_TRY(check_f32_mat(D, d, d, ldd, "D"));
+  KQ_TRY(check_f32_mat(U, d, d, ldu, "U"));
+  KQ_TRY(check_f32_mat(P, d, d, ldp, "P"));
+  KQ_REQUIRE(static_cast<const float*>(P) != D && static_cast<const float*>(P) != U,
+             KRONQ_ERR_INVALID_ARG, "P must not alias D or U");
+  KQ_TRY(check_ws(ws, ws_bytes, kq::gptaq_ws_bytes(d)));
+  return kq::gptaq_launch(D, d, ldd, U, ldu, alpha, P, ldp, ws, as_stream(stream));
+}
+
 int kronq_cholesky_inv(float* H, int64_t d, int64_t ldh, float damp_rel, float* Uout,
                        int64_t ldu, int* info, void* ws, size_t ws_bytes, void* stream) {
   kq::clear_error();
@@ -160,23 +252,19 @@ int kronq_obs_quantize_layer(float* W, int64_t d_out, int64_t d_in, int64_t ldw,
                              uint8_t* codes, float* scales, float* zeros, float* err,
                              float* W_hat, void* ws, size_t ws_bytes, void* stream) {
   kq::clear_error();
-  KQ_REQUIRE(bits >= 2 && bits <= 8, KRONQ_ERR_UNSUPPORTED, "bits must be in 2..8");
-  KQ_REQUIRE(group == 128, KRONQ_ERR_UNSUPPORTED, "only group size 128 is implemented");
-  KQ_REQUIRE(block == 128, KRONQ_ERR_UNSUPPORTED, "only block size 128 is implemented");
-  KQ_TRY(check_f32_mat(W, d_out, d_in, ldw, "W"));
-  KQ_REQUIRE(d_in % group == 0, KRONQ_ERR_SHAPE, "d_in (%lld) must be a multiple of the group",
-             (long long)d_in);
-  KQ_TRY(check_f32_mat(U, d_in, d_in, ldu, "U"));
-  KQ_REQUIRE(codes && aligned(codes, 4), KRONQ_ERR_INVALID_ARG, "codes must be 4-byte aligned");
-  KQ_REQUIRE(scales && zeros && aligned(scales, 4) && aligned(zeros, 4), KRONQ_ERR_INVALID_ARG,
-             "scales and zeros are required");
-  KQ_REQUIRE(!err || aligned(err, 16), KRONQ_ERR_INVALID_ARG, "err must be 16-byte aligned");
-  KQ_REQUIRE(!W_hat || aligned(W_hat, 16), KRONQ_ERR_INVALID_ARG,
-             "W_hat must be 16-byte aligned");
-  KQ_REQUIRE(static_cast<const float*>(W) != U, KRONQ_ERR_INVALID_ARG, "W must not alias U");
-  if (!err) KQ_TRY(check_ws(ws, ws_bytes, kq::obs_ws_bytes(d_out, d_in)));
-  return kq::obs_launch(W, d_out, d_in, ldw, U, ldu, bits, codes, scales, zeros, err, W_hat, ws,
-                        as_stream(stream));
+  return obs_common(W, d_out, d_in, ldw, U, ldu, nullptr, 0, bits, group, block, codes, scales,
+                    zeros, err, W_hat, ws, ws_bytes, stream);
+}
+
+int kronq_obs_quantize_layer_drift(float* W, int64_t d_out, int64_t d_in, int64_t ldw,
+                                   const float* U, int64_t ldu, const float* P, int64_t ldp,
+                                   int bits, int group, int block, uint8_t* codes, float* scales,
+                                   float* zeros, float* err, float* W_hat, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(P, KRONQ_ERR_INVALID_ARG, "P is NULL");
+  return obs_common(W, d_out, d_in, ldw, U, ldu, P, ldp, bits, group, block, codes, scales, zeros,
+                    err, W_hat, ws, ws_bytes, stream);
 }
 
 int kronq_layer_loss(const void* W, int w_dtype, int64_t ldw, const float* W_hat,

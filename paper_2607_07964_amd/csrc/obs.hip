@@ -1,21 +1,31 @@
-// Lazy-block column-wise OBS with group quantisation (eq. obs_update, Prop. 1 with the drift
-// correction P = 0; Alg. 2).
+// Lazy-block column-wise OBS with group quantisation (eq. obs_update; Prop. 1 eq. kronq_update
+// with or without the drift correction P; Alg. 2).
 //
-// Per block of 128 columns (= one quantisation group):
+// Per block of 128 columns:
 //   * sweep kernel: rows are independent given U, so each row is one 16-lane group of a wave
 //     (4 rows per wave, 16 rows per workgroup) and each lane keeps 8 consecutive columns of the
 //     block in registers. Column j: the owning lane quantises it and forms the scaled error
 //     e_j = (w_j - w_hat_j) / U_jj, one DPP row broadcast hands e_j to the other 15 lanes, and
 //     every lane applies it to its 8 columns with U[j, its columns] read from the workgroup's
 //     LDS copy of the 128 x 128 block of U (upper triangular, so columns already done are left
-//     alone). Group parameters come from the row's 128 values at the start of the block.
-//     Codes, errors and dequantised values are written from registers at the end.
-//   * trailing updates, lazily in two levels: after each block, W[:, rest of its group of 4
-//     blocks] -= E_b U[b, rest of group] (K = 128); after the last block of a group,
-//     W[:, beyond the group] -= E_group U[group, beyond] (K = 512). Every column still receives
-//     the update of every earlier block before it is swept, as in the one-level scheme, with a
-//     quarter of the passes over W. Both products run on the bf16 matrix cores with the
-//     fp32-accurate three-term split (gemm_bf16x3.hip); U^T is split once per layer.
+//     alone). With the drift correction a second broadcast hands out w_j as it stood before
+//     quantisation and every lane adds w_j P[j, its columns] from an LDS copy of the block of P
+//     (strictly upper). Codes, errors, the pre-quantisation values (drift) and dequantised
+//     values are written from registers at the end.
+//   * group parameters: a group of 128 columns takes them from the row's 128 values at the
+//     start of its block, inside the sweep kernel; a wider group (256, ..., d_in: the paper's
+//     per-channel grid is group = d_in) takes them from the row's current values over the whole
+//     group, in a reduction kernel launched when the sweep reaches the group's first block.
+//   * trailing updates, lazily in two levels: after each block, W[:, rest of its lazy group of
+//     (up to) 4 blocks] -= E_b U[b, rest of group] (K = 128); after the last block of a lazy
+//     group, W[:, beyond] -= E_group U[group, beyond] (K = 512). With the drift correction the
+//     same passes also add W_b P[b, ...], as a second K range of the same product. Every column
+//     receives the update of every earlier block before it is swept, as in the one-level scheme,
+//     with a quarter of the passes over W. The lazy group is shortened when needed so that a
+//     wide quantisation group lies inside one lazy group or starts one (its columns are then
+//     current when its parameters are taken). The products run on the bf16 matrix cores with
+//     the fp32-accurate three-term split (gemm_bf16x3.hip); U^T and -P^T are split once per
+//     layer.
 // The quantiser (reading of the paper's "quant"): xmin = min(0, min w), xmax = max(0, max w),
 // (-1, 1) when both are 0; scale = float32((xmax - xmin) / (2^b - 1)) in float64;
 // zero = rint(-xmin / scale); q = clamp(rint(w / scale) + zero, 0, 2^b - 1);
@@ -31,12 +41,12 @@
 namespace kq {
 namespace {
 
-constexpr int OB = 128;          // block = group
+constexpr int OB = 128;          // block (and the smallest group)
 constexpr int LPR = 16;          // lanes per row
 constexpr int CPL = OB / LPR;    // columns per lane
 constexpr int RPW = 64 / LPR;    // rows per wave
 constexpr int RPG = 4 * RPW;     // rows per workgroup (4 waves)
-constexpr int GRP = 4;           // blocks per group of the two-level lazy update
+constexpr int GRP = 4;           // blocks per group of the two-level lazy update (at most)
 
 // v broadcast from lane `src` of each 16-lane row to the whole row (DPP row_newbcast)
 template <int src>
@@ -45,28 +55,36 @@ __device__ __forceinline__ float row_bcast(float v) {
                                                     false));
 }
 
+struct SweepArgs {
+  const float* ub;    // U block in LDS, [OB][OB]
+  const float* pb;    // P block in LDS (drift only)
+  const float* rinv;  // 1 / U_jj
+  int sub, cb;
+  float scale, inv_s, fzero, fmaxq;
+  double dscale;
+};
+
 // one column of the sweep: j = 8 * OWN + S (compile-time)
-template <int OWN, int S>
-__device__ __forceinline__ void sweep_col(float (&w)[CPL], float (&ev)[CPL], uint32_t (&qc)[CPL],
-                                          const float* ub, const float* rinv, int sub, int cb,
-                                          float scale, float inv_s, double dscale, float fzero,
-                                          float fmaxq) {
+template <bool DRIFT, int OWN, int S>
+__device__ __forceinline__ void sweep_col(float (&w)[CPL], float (&ev)[CPL], float (&xv)[CPL],
+                                          uint32_t (&qc)[CPL], const SweepArgs& a) {
   constexpr int j = OWN * CPL + S;
   const float x = w[S];
-  const float t = x * inv_s;
+  const float t = x * a.inv_s;
   float qf = __builtin_rintf(t);
   const bool tie = fabsf(t - floorf(t) - 0.5f) <= 1e-6f * (fabsf(t) + 1.f);
-  if (tie && sub == OWN) qf = float(__builtin_rint(double(x) / dscale));
-  const float q = fminf(fmaxf(qf + fzero, 0.f), fmaxq);
-  const float wh = scale * (q - fzero);
-  const float e = (x - wh) * rinv[j];
-  if (sub == OWN) {
+  if (tie && a.sub == OWN) qf = float(__builtin_rint(double(x) / a.dscale));
+  const float q = fminf(fmaxf(qf + a.fzero, 0.f), a.fmaxq);
+  const float wh = a.scale * (q - a.fzero);
+  const float e = (x - wh) * a.rinv[j];
+  if (a.sub == OWN) {
     ev[S] = e;
     qc[S] = uint32_t(q);
+    if (DRIFT) xv[S] = x;
   }
   const float eb = row_bcast<OWN>(e);
-  const float4 u0 = *reinterpret_cast<const float4*>(ub + j * OB + cb);
-  const float4 u1 = *reinterpret_cast<const float4*>(ub + j * OB + cb + 4);
+  const float4 u0 = *reinterpret_cast<const float4*>(a.ub + j * OB + a.cb);
+  const float4 u1 = *reinterpret_cast<const float4*>(a.ub + j * OB + a.cb + 4);
   w[0] = fmaf(-eb, u0.x, w[0]);
   w[1] = fmaf(-eb, u0.y, w[1]);
   w[2] = fmaf(-eb, u0.z, w[2]);
@@ -75,41 +93,94 @@ __device__ __forceinline__ void sweep_col(float (&w)[CPL], float (&ev)[CPL], uin
   w[5] = fmaf(-eb, u1.y, w[5]);
   w[6] = fmaf(-eb, u1.z, w[6]);
   w[7] = fmaf(-eb, u1.w, w[7]);
+  if (DRIFT) {  // + w_j P[j, its columns], w_j as it stood before quantisation
+    const float xb = row_bcast<OWN>(x);
+    const float4 p0 = *reinterpret_cast<const float4*>(a.pb + j * OB + a.cb);
+    const float4 p1 = *reinterpret_cast<const float4*>(a.pb + j * OB + a.cb + 4);
+    w[0] = fmaf(xb, p0.x, w[0]);
+    w[1] = fmaf(xb, p0.y, w[1]);
+    w[2] = fmaf(xb, p0.z, w[2]);
+    w[3] = fmaf(xb, p0.w, w[3]);
+    w[4] = fmaf(xb, p1.x, w[4]);
+    w[5] = fmaf(xb, p1.y, w[5]);
+    w[6] = fmaf(xb, p1.z, w[6]);
+    w[7] = fmaf(xb, p1.w, w[7]);
+  }
 }
 
-template <int OWN>
+template <bool DRIFT, int OWN>
 __device__ __forceinline__ void sweep_lane_cols(float (&w)[CPL], float (&ev)[CPL],
-                                                uint32_t (&qc)[CPL], const float* ub,
-                                                const float* rinv, int sub, int cb, float scale,
-                                                float inv_s, double dscale, float fzero,
-                                                float fmaxq) {
-  sweep_col<OWN, 0>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
-  sweep_col<OWN, 1>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
-  sweep_col<OWN, 2>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
-  sweep_col<OWN, 3>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
-  sweep_col<OWN, 4>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
-  sweep_col<OWN, 5>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
-  sweep_col<OWN, 6>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
-  sweep_col<OWN, 7>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq);
+                                                float (&xv)[CPL], uint32_t (&qc)[CPL],
+                                                const SweepArgs& a) {
+  sweep_col<DRIFT, OWN, 0>(w, ev, xv, qc, a);
+  sweep_col<DRIFT, OWN, 1>(w, ev, xv, qc, a);
+  sweep_col<DRIFT, OWN, 2>(w, ev, xv, qc, a);
+  sweep_col<DRIFT, OWN, 3>(w, ev, xv, qc, a);
+  sweep_col<DRIFT, OWN, 4>(w, ev, xv, qc, a);
+  sweep_col<DRIFT, OWN, 5>(w, ev, xv, qc, a);
+  sweep_col<DRIFT, OWN, 6>(w, ev, xv, qc, a);
+  sweep_col<DRIFT, OWN, 7>(w, ev, xv, qc, a);
 }
 
-template <int... OWN>
+template <bool DRIFT, int... OWN>
 __device__ __forceinline__ void sweep_all(std::integer_sequence<int, OWN...>, float (&w)[CPL],
-                                          float (&ev)[CPL], uint32_t (&qc)[CPL], const float* ub,
-                                          const float* rinv, int sub, int cb, float scale,
-                                          float inv_s, double dscale, float fzero, float fmaxq) {
-  (sweep_lane_cols<OWN>(w, ev, qc, ub, rinv, sub, cb, scale, inv_s, dscale, fzero, fmaxq), ...);
+                                          float (&ev)[CPL], float (&xv)[CPL], uint32_t (&qc)[CPL],
+                                          const SweepArgs& a) {
+  (sweep_lane_cols<DRIFT, OWN>(w, ev, xv, qc, a), ...);
 }
 
-__global__ __launch_bounds__(256) void obs_sweep(float* __restrict__ W, int64_t d_out,
-                                                 int64_t ldw, const float* __restrict__ U,
-                                                 int64_t ldu, int64_t c0, int bits,
-                                                 uint8_t* __restrict__ codes, int64_t ldq,
-                                                 float* __restrict__ scales,
-                                                 float* __restrict__ zeros, int64_t ldsz,
-                                                 int64_t blk, float* __restrict__ E, int64_t lde,
-                                                 float* __restrict__ W_hat, int64_t ldwh) {
+// (scale, zero) of a group from its range, the same float64 steps as the oracle's reading
+__device__ __forceinline__ void grid_params(float xmin, float xmax, int bits, float& scale,
+                                            float& fzero) {
+  if (xmax == xmin) {
+    xmin = -1.f;
+    xmax = 1.f;
+  }
+  const double maxq = double((1 << bits) - 1);
+  scale = float((double(xmax) - double(xmin)) / maxq);
+  fzero = float(__builtin_rint(-double(xmin) / double(scale)));
+}
+
+// Group parameters of groups wider than one block: one wave per row reduces the row's current
+// values over the group's columns [c0, c0 + g) (taken when the sweep reaches the group).
+__global__ __launch_bounds__(256) void obs_group_params(const float* __restrict__ W,
+                                                        int64_t d_out, int64_t ldw, int64_t c0,
+                                                        int64_t g, int bits,
+                                                        float* __restrict__ scales,
+                                                        float* __restrict__ zeros, int64_t ldsz,
+                                                        int64_t gi) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (row >= d_out) return;  // uniform per wave
+  const float* wr = W + row * ldw + c0;
+  float xmin = 0.f, xmax = 0.f;
+  for (int64_t c = int64_t(lane) * 4; c < g; c += 256) {
+    const float4 v = *reinterpret_cast<const float4*>(wr + c);
+    xmin = fminf(xmin, fminf(fminf(v.x, v.y), fminf(v.z, v.w)));
+    xmax = fmaxf(xmax, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+  }
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    xmin = fminf(xmin, __shfl_xor(xmin, o));
+    xmax = fmaxf(xmax, __shfl_xor(xmax, o));
+  }
+  if (lane == 0) {
+    float scale, fzero;
+    grid_params(xmin, xmax, bits, scale, fzero);
+    scales[row * ldsz + gi] = scale;
+    zeros[row * ldsz + gi] = fzero;
+  }
+}
+
+template <bool DRIFT>
+__global__ __launch_bounds__(256) void obs_sweep(
+    float* __restrict__ W, int64_t d_out, int64_t ldw, const float* __restrict__ U, int64_t ldu,
+    const float* __restrict__ P, int64_t ldp, int64_t c0, int bits, uint8_t* __restrict__ codes,
+    int64_t ldq, float* __restrict__ scales, float* __restrict__ zeros, int64_t ldsz, int64_t gi,
+    int given, float* __restrict__ E, int64_t lde, float* __restrict__ Xq, int64_t ldxq,
+    float* __restrict__ W_hat, int64_t ldwh) {
   __shared__ __attribute__((aligned(16))) float ub[OB * OB];  // U[c0 + j][c0 + k]
+  __shared__ __attribute__((aligned(16))) float pb[DRIFT ? OB * OB : 4];  // P[c0 + j][c0 + k]
   __shared__ float rinv[OB];                                   // 1 / U_jj
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane & (LPR - 1), cb = sub * CPL;
@@ -121,6 +192,9 @@ __global__ __launch_bounds__(256) void obs_sweep(float* __restrict__ W, int64_t 
     const int j = idx / (OB / 4), k4 = (idx % (OB / 4)) * 4;
     *reinterpret_cast<float4*>(ub + j * OB + k4) =
         *reinterpret_cast<const float4*>(U + (c0 + j) * ldu + c0 + k4);
+    if (DRIFT)
+      *reinterpret_cast<float4*>(pb + j * OB + k4) =
+          *reinterpret_cast<const float4*>(P + (c0 + j) * ldp + c0 + k4);
   }
   if (tid < OB) rinv[tid] = 1.f / U[(c0 + tid) * ldu + c0 + tid];
   float w[CPL];
@@ -129,39 +203,38 @@ __global__ __launch_bounds__(256) void obs_sweep(float* __restrict__ W, int64_t 
     const float4 b = *reinterpret_cast<const float4*>(W + rr * ldw + c0 + cb + 4);
     w[0] = a.x, w[1] = a.y, w[2] = a.z, w[3] = a.w, w[4] = b.x, w[5] = b.y, w[6] = b.z, w[7] = b.w;
   }
-  // group parameters from the row's current 128 values (group start = block start)
-  float xmin = 0.f, xmax = 0.f;
+  float scale, fzero;
+  if (given) {  // a wider group: parameters taken at its first block by obs_group_params
+    scale = scales[rr * ldsz + gi];
+    fzero = zeros[rr * ldsz + gi];
+  } else {  // group = block: parameters from the row's current 128 values
+    float xmin = 0.f, xmax = 0.f;
 #pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    xmin = fminf(xmin, w[c]);
-    xmax = fmaxf(xmax, w[c]);
-  }
+    for (int c = 0; c < CPL; ++c) {
+      xmin = fminf(xmin, w[c]);
+      xmax = fmaxf(xmax, w[c]);
+    }
 #pragma unroll
-  for (int o = 1; o < LPR; o <<= 1) {
-    xmin = fminf(xmin, __shfl_xor(xmin, o, LPR));
-    xmax = fmaxf(xmax, __shfl_xor(xmax, o, LPR));
+    for (int o = 1; o < LPR; o <<= 1) {
+      xmin = fminf(xmin, __shfl_xor(xmin, o, LPR));
+      xmax = fmaxf(xmax, __shfl_xor(xmax, o, LPR));
+    }
+    grid_params(xmin, xmax, bits, scale, fzero);
   }
-  if (xmax == xmin) {
-    xmin = -1.f;
-    xmax = 1.f;
-  }
-  const double maxq = double((1 << bits) - 1);
-  const float scale = float((double(xmax) - double(xmin)) / maxq);
-  const double zero = __builtin_rint(-double(xmin) / double(scale));
-  const float fzero = float(zero), inv_s = 1.f / scale;
   __syncthreads();
 
-  float ev[CPL];
+  float ev[CPL], xv[CPL];
   uint32_t qc[CPL];
 #pragma unroll
-  for (int c = 0; c < CPL; ++c) ev[c] = 0.f, qc[c] = 0u;
-  sweep_all(std::make_integer_sequence<int, LPR>{}, w, ev, qc, ub, rinv, sub, cb, scale, inv_s,
-            double(scale), fzero, float(maxq));
+  for (int c = 0; c < CPL; ++c) ev[c] = 0.f, xv[c] = 0.f, qc[c] = 0u;
+  const SweepArgs args{ub,          pb,    rinv, sub, cb, scale, 1.f / scale, fzero,
+                       float((1 << bits) - 1), double(scale)};
+  sweep_all<DRIFT>(std::make_integer_sequence<int, LPR>{}, w, ev, xv, qc, args);
 
   if (!live) return;
-  if (sub == 0) {
-    scales[row * ldsz + blk] = scale;
-    zeros[row * ldsz + blk] = fzero;
+  if (sub == 0 && !given) {
+    scales[row * ldsz + gi] = scale;
+    zeros[row * ldsz + gi] = fzero;
   }
   float wh[CPL];
 #pragma unroll
@@ -176,52 +249,105 @@ __global__ __launch_bounds__(256) void obs_sweep(float* __restrict__ W, int64_t 
   }
   *reinterpret_cast<float4*>(E + row * lde + cb) = make_float4(ev[0], ev[1], ev[2], ev[3]);
   *reinterpret_cast<float4*>(E + row * lde + cb + 4) = make_float4(ev[4], ev[5], ev[6], ev[7]);
+  if (DRIFT) {
+    *reinterpret_cast<float4*>(Xq + row * ldxq + cb) = make_float4(xv[0], xv[1], xv[2], xv[3]);
+    *reinterpret_cast<float4*>(Xq + row * ldxq + cb + 4) = make_float4(xv[4], xv[5], xv[6], xv[7]);
+  }
   uint2 pk;
   pk.x = qc[0] | (qc[1] << 8) | (qc[2] << 16) | (qc[3] << 24);
   pk.y = qc[4] | (qc[5] << 8) | (qc[6] << 16) | (qc[7] << 24);
   *reinterpret_cast<uint2*>(codes + row * ldq + c0 + cb) = pk;
 }
 
+// Blocks per lazy group for a quantisation group of `group` columns: a group's parameters need
+// its columns current when the sweep reaches it, which holds when it lies inside one lazy group
+// or starts one. 0 when the group is not supported.
+int lazy_blocks(int64_t d_in, int group) {
+  if (group < OB || group % OB != 0 || d_in % group != 0) return 0;
+  const int m = group / OB;
+  if (GRP % m == 0 || m % GRP == 0 || group == d_in) return GRP;
+  for (int k = GRP - 1; k > 1; --k)
+    if (m % k == 0) return k;
+  return 1;
+}
+
 }  // namespace
 
-size_t obs_ws_bytes(int64_t d_out, int64_t d_in) {
+int obs_group_ok(int64_t d_in, int group) { return lazy_blocks(d_in, group); }
+
+size_t obs_ws_bytes(int64_t d_out, int64_t d_in, bool drift) {
   if (d_out <= 0 || d_in <= 0) return 0;
-  return align256(size_t(d_out) * GRP * OB * sizeof(float)) +
-         2 * align256(size_t(d_in) * size_t(d_in) * sizeof(uint16_t)) + 256;
+  const size_t per = align256(size_t(d_out) * GRP * OB * sizeof(float)) +
+                     2 * align256(size_t(d_in) * size_t(d_in) * sizeof(uint16_t));
+  return (drift ? 2 : 1) * per + 256;
 }
 
 int obs_launch(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* U, int64_t ldu,
-               int bits, uint8_t* codes, float* scales, float* zeros, float* err, float* W_hat,
-               void* ws, hipStream_t s) {
-  const int64_t nblk = d_in / OB;
+               int bits, int group, const float* P, int64_t ldp, uint8_t* codes, float* scales,
+               float* zeros, float* err, float* W_hat, void* ws, hipStream_t s) {
+  const bool drift = P != nullptr;
+  const int64_t nblk = d_in / OB, ldsz = d_in / group;
+  const int lz = lazy_blocks(d_in, group);
+  KQ_REQUIRE(lz > 0, KRONQ_ERR_UNSUPPORTED, "group %d not supported for d_in %lld", group,
+             (long long)d_in);
   const unsigned grid = unsigned(cdiv(d_out, RPG));
   Carver cv(ws);
   float* Ews = cv.take<float>(size_t(d_out) * GRP * OB);
   uint16_t* Uth = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
   uint16_t* Utl = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
-  // U^T split once into bf16 high and low parts: the B operand of the trailing updates
+  float* Xws = drift ? cv.take<float>(size_t(d_out) * GRP * OB) : nullptr;
+  uint16_t* Pth = drift ? cv.take<uint16_t>(size_t(d_in) * size_t(d_in)) : nullptr;
+  uint16_t* Ptl = drift ? cv.take<uint16_t>(size_t(d_in) * size_t(d_in)) : nullptr;
+  // U^T (and -P^T) split once into bf16 high and low parts: the B operands of the trailing
+  // updates
   KQ_TRY(split_transpose_launch(U, ldu, d_in, Uth, Utl, d_in, s));
-  for (int64_t g0 = 0; g0 < nblk; g0 += GRP) {
-    const int64_t gend = g0 + GRP < nblk ? g0 + GRP : nblk;
-    // errors of this group's blocks: the caller's err (ld d_in) or the workspace (ld GRP * OB)
+  if (drift) KQ_TRY(split_transpose_launch(P, ldp, d_in, Pth, Ptl, d_in, s, true));
+  const int64_t ldx = GRP * OB;
+  for (int64_t g0 = 0; g0 < nblk; g0 += lz) {
+    const int64_t gend = g0 + lz < nblk ? g0 + lz : nblk;
+    // errors of this lazy group's blocks: the caller's err (ld d_in) or the workspace
+    // (ld GRP * OB); pre-quantisation values (drift) always in the workspace
     float* Eg = err ? err + g0 * OB : Ews;
     const int64_t lde = err ? d_in : GRP * OB;
     for (int64_t b = g0; b < gend; ++b) {
       const int64_t c0 = b * OB;
       float* Eb = Eg + (b - g0) * OB;
-      KQ_TRY(launch("obs_sweep", obs_sweep, dim3(grid), dim3(256), 0, s, W, d_out, ldw, U, ldu,
-                    c0, bits, codes, d_in, scales, zeros, nblk, b, Eb, lde, W_hat, d_in));
-      const int64_t near = (gend - b - 1) * OB;  // rest of the group
-      if (near > 0)  // W[:, c0+OB : gend*OB] -= E_b U[c0 : c0+OB, c0+OB : gend*OB]
-        KQ_TRY(gemm_bf16x3_sub(d_out, near, OB, Eb, lde, Uth + (c0 + OB) * d_in + c0,
-                               Utl + (c0 + OB) * d_in + c0, d_in, W + c0 + OB, ldw, s,
-                               "obs_trailing_update"));
+      float* Xb = drift ? Xws + (b - g0) * OB : nullptr;
+      const int64_t gi = c0 / group;
+      const int given = group > OB;
+      if (given && c0 % group == 0)
+        KQ_TRY(launch("obs_group_params", obs_group_params, dim3(unsigned(cdiv(d_out, 4))),
+                      dim3(256), 0, s, static_cast<const float*>(W), d_out, ldw, c0,
+                      int64_t(group), bits, scales, zeros, ldsz, gi));
+      if (drift)
+        KQ_TRY(launch("obs_sweep", obs_sweep<true>, dim3(grid), dim3(256), 0, s, W, d_out, ldw, U,
+                      ldu, P, ldp, c0, bits, codes, d_in, scales, zeros, ldsz, gi, given, Eb, lde,
+                      Xb, ldx, W_hat, d_in));
+      else
+        KQ_TRY(launch("obs_sweep", obs_sweep<false>, dim3(grid), dim3(256), 0, s, W, d_out, ldw,
+                      U, ldu, P, ldp, c0, bits, codes, d_in, scales, zeros, ldsz, gi, given, Eb,
+                      lde, Xb, ldx, W_hat, d_in));
+      const int64_t near = (gend - b - 1) * OB;  // rest of the lazy group
+      if (near > 0) {
+        // W[:, c0+OB : gend*OB] -= E_b U[c0 : c0+OB, c0+OB : gend*OB] (- X_b P[...])
+        Bf16x3Pair pu{Eb, lde, Uth + (c0 + OB) * d_in + c0, Utl + (c0 + OB) * d_in + c0, d_in,
+                      OB};
+        Bf16x3Pair pp;
+        if (drift)
+          pp = Bf16x3Pair{Xb, ldx, Pth + (c0 + OB) * d_in + c0, Ptl + (c0 + OB) * d_in + c0,
+                          d_in, OB};
+        KQ_TRY(gemm_bf16x3_sub(d_out, near, pu, pp, W + c0 + OB, ldw, s, "obs_trailing_update"));
+      }
     }
-    const int64_t rem = d_in - gend * OB;  // beyond the group
-    if (rem > 0)  // W[:, gend*OB :] -= E_group U[g0*OB : gend*OB, gend*OB :]
-      KQ_TRY(gemm_bf16x3_sub(d_out, rem, (gend - g0) * OB, Eg, lde,
-                             Uth + gend * OB * d_in + g0 * OB, Utl + gend * OB * d_in + g0 * OB,
-                             d_in, W + gend * OB, ldw, s, "obs_trailing_update"));
+    const int64_t rem = d_in - gend * OB;  // beyond the lazy group
+    if (rem > 0) {
+      // W[:, gend*OB :] -= E_group U[g0*OB : gend*OB, gend*OB :] (- X_group P[...])
+      const int64_t K = (gend - g0) * OB, off = gend * OB * d_in + g0 * OB;
+      Bf16x3Pair pu{Eg, lde, Uth + off, Utl + off, d_in, K};
+      Bf16x3Pair pp;
+      if (drift) pp = Bf16x3Pair{Xws, ldx, Pth + off, Ptl + off, d_in, K};
+      KQ_TRY(gemm_bf16x3_sub(d_out, rem, pu, pp, W + gend * OB, ldw, s, "obs_trailing_update"));
+    }
   }
   return KRONQ_OK;
 }

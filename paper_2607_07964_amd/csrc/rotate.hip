@@ -148,12 +148,12 @@ __global__ void given_factors(int64_t n, const float* __restrict__ s, const int8
   mul[j] = s[j] * (sign ? float(sign[j]) : 1.f);
 }
 
-// inverse multipliers: sign / s
+// inverse multipliers: sign / s (s == nullptr: 1)
 __global__ void inv_factors(int64_t n, const float* __restrict__ s, const int8_t* __restrict__ sign,
                             float* __restrict__ mul) {
   const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (j >= n) return;
-  mul[j] = (sign ? float(sign[j]) : 1.f) / s[j];
+  mul[j] = (sign ? float(sign[j]) : 1.f) / (s ? s[j] : 1.f);
 }
 
 // ----------------------------------------------------------------------------- butterflies
@@ -504,6 +504,28 @@ int col_transform(const float* src, int64_t lds_, float* dst, int64_t ldd, int64
 }
 
 }  // namespace
+
+size_t rotate_drift_ws_bytes(int64_t d) {
+  if (d <= 0) return 0;
+  return align256(size_t(d) * sizeof(float)) + 256;
+}
+
+// D <- V diag(1/sx) D diag(1/sx) V^T: the input-side transform of H_X applied to the (not
+// symmetric) drift statistic, a row pass and a column pass like H_X's
+int rotate_drift_launch(float* D, int64_t d, int64_t ldd, const float* sx, const int8_t* sign,
+                        const float* q28, int flags, void* ws, hipStream_t s) {
+  const bool rot = flags & KRONQ_ROT_IN;
+  const RotDim r = rot_dim(d);
+  Carver cv(ws);
+  float* mh = cv.take<float>(d);
+  KQ_TRY(launch("rot_inv_factors", inv_factors, dim3(unsigned(cdiv(d, 256))), dim3(256), 0, s, d,
+                (flags & KRONQ_RESCALE_IN) ? sx : static_cast<const float*>(nullptr),
+                rot ? sign : static_cast<const int8_t*>(nullptr), mh));
+  KQ_TRY(launch_row_pass(D, KRONQ_FP32, ldd, D, ldd, d, d, mh, mh, nullptr, nullptr, rot, r, q28,
+                         false, s, "rot_row_pass"));
+  if (rot) KQ_TRY(col_transform(D, ldd, D, ldd, d, d, r, q28, false, s));
+  return KRONQ_OK;
+}
 
 size_t rotate_ws_bytes(int64_t d_out, int64_t d_in) {
   if (d_out <= 0 || d_in <= 0) return 0;

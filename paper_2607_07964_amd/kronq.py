@@ -22,6 +22,7 @@ RESCALE_IN, RESCALE_OUT, ROT_IN, ROT_OUT, INVERSE = 1, 2, 4, 8, 16
 HX_ONLY, SX_GIVEN = 32, 64
 BIIP = RESCALE_IN | RESCALE_OUT | ROT_IN | ROT_OUT
 OP_COV, OP_ROTATE, OP_CHOL, OP_OBS, OP_LOSS = 1, 2, 3, 4, 5
+OP_CROSS, OP_ROTATE_DRIFT, OP_GPTAQ, OP_OBS_DRIFT = 6, 7, 8, 9
 ERRORS = {0: "OK", -1: "INVALID_ARG", -2: "SHAPE", -3: "NOT_PD", -4: "HIP", -5: "WORKSPACE",
           -6: "UNSUPPORTED"}
 
@@ -29,7 +30,8 @@ EXPORTS = (
     "kronq_workspace_bytes", "kronq_last_error", "kronq_version", "kronq_accumulate_cov",
     "kronq_traces", "kronq_rotate", "kronq_cholesky_inv", "kronq_obs_quantize_layer",
     "kronq_layer_loss", "kronq_allocate_bits", "kronq_profile_enable", "kronq_profile_only",
-    "kronq_profile_reset", "kronq_profile_read",
+    "kronq_profile_reset", "kronq_profile_read", "kronq_accumulate_cross", "kronq_rotate_drift",
+    "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift",
 )
 
 
@@ -57,6 +59,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_last_error": (ctypes.c_char_p, []),
         "kronq_version": (I, []),
         "kronq_accumulate_cov": (I, [P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
+        "kronq_accumulate_cross": (I, [P, P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
+        "kronq_rotate_drift": (I, [P, I64, I64, P, P, P, I, P, SZ, P]),
+        "kronq_gptaq_correction": (I, [P, I64, I64, P, I64, F, P, I64, P, SZ, P]),
+        "kronq_obs_quantize_layer_drift": (I, [P, I64, I64, I64, P, I64, P, I64, I, I, I, P, P, P,
+                                               P, P, P, SZ, P]),
         "kronq_traces": (I, [P, I64, I64, P, I64, I64, P, P]),
         "kronq_rotate": (I, [P, I, I64, P, I64, I64, I64, P, I64, P, I64, P, P, P, P, P, P, I, P,
                              SZ, P]),
@@ -204,6 +211,66 @@ def kronq_obs_quantize_layer(W: torch.Tensor, U: torch.Tensor, bits: int, codes:
         _ptr(scales), _ptr(zeros), _ptr(err), _ptr(W_hat), _ptr(ws), ws.numel(),
         _stream(W.device))
     _check(rc, "kronq_obs_quantize_layer")
+
+
+def kronq_accumulate_cross(A: torch.Tensor, B: torch.Tensor, C: torch.Tensor, alpha: float = 1.0,
+                           beta: float = 0.0, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """C <- beta C + alpha A^T B (token-major A, B [N x d] of one dtype and row stride)."""
+    _dev(A, B, C)
+    n, d = A.shape
+    if B.shape != A.shape or B.dtype != A.dtype or _ld(B) != _ld(A):
+        raise ValueError("A and B must have the same shape, dtype and row stride")
+    if ws is None:
+        ws = workspace(OP_CROSS, 0, d, n, C.device)
+    rc = load().kronq_accumulate_cross(_ptr(A), _ptr(B), _dtype_code(A), n, d, _ld(A), _ptr(C),
+                                       _ld(C), alpha, beta, _ptr(ws), ws.numel(),
+                                       _stream(C.device))
+    _check(rc, "kronq_accumulate_cross")
+    return C
+
+
+def kronq_rotate_drift(D: torch.Tensor, sx: Optional[torch.Tensor], sign_in: Optional[torch.Tensor],
+                       q28_in: Optional[torch.Tensor], flags: int = RESCALE_IN | ROT_IN,
+                       ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """D <- V diag(1/sx) D diag(1/sx) V^T in place (the input-side BiIP of H_X)."""
+    _dev(D, sx, sign_in, q28_in)
+    d = D.shape[0]
+    if ws is None:
+        ws = workspace(OP_ROTATE_DRIFT, 0, d, 0, D.device)
+    rc = load().kronq_rotate_drift(_ptr(D), d, _ld(D), _ptr(sx), _ptr(sign_in), _ptr(q28_in),
+                                   flags, _ptr(ws), ws.numel(), _stream(D.device))
+    _check(rc, "kronq_rotate_drift")
+    return D
+
+
+def kronq_gptaq_correction(D: torch.Tensor, U: torch.Tensor, P: torch.Tensor, alpha: float = 1.0,
+                           ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """P = alpha ((D U^T) . M_U) U, strictly upper triangular."""
+    _dev(D, U, P)
+    d = D.shape[0]
+    if ws is None:
+        ws = workspace(OP_GPTAQ, 0, d, 0, D.device)
+    rc = load().kronq_gptaq_correction(_ptr(D), d, _ld(D), _ptr(U), _ld(U), alpha, _ptr(P), _ld(P),
+                                       _ptr(ws), ws.numel(), _stream(D.device))
+    _check(rc, "kronq_gptaq_correction")
+    return P
+
+
+def kronq_obs_quantize_layer_drift(W: torch.Tensor, U: torch.Tensor, P: torch.Tensor, bits: int,
+                                   codes: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor,
+                                   err: Optional[torch.Tensor] = None,
+                                   W_hat: Optional[torch.Tensor] = None, group: int = 128,
+                                   block: int = 128, ws: Optional[torch.Tensor] = None):
+    """The lazy-block OBS sweep with the drift correction P; W ends as the dequantised W_hat."""
+    _dev(W, U, P, codes, scales, zeros, err, W_hat)
+    d_out, d_in = W.shape
+    if ws is None:
+        ws = workspace(OP_OBS_DRIFT, d_out, d_in, 0, W.device)
+    rc = load().kronq_obs_quantize_layer_drift(
+        _ptr(W), d_out, d_in, _ld(W), _ptr(U), _ld(U), _ptr(P), _ld(P), bits, group, block,
+        _ptr(codes), _ptr(scales), _ptr(zeros), _ptr(err), _ptr(W_hat), _ptr(ws), ws.numel(),
+        _stream(W.device))
+    _check(rc, "kronq_obs_quantize_layer_drift")
 
 
 def kronq_layer_loss(W: torch.Tensor, W_hat: Optional[torch.Tensor], HX: torch.Tensor,

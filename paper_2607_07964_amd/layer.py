@@ -1,9 +1,11 @@
 """Per-layer and per-block drivers: the KronQ hot path as a sequence of libkronq calls.
 
-One layer (Alg. 1 then Alg. 2 with P = 0):
+One layer (Alg. 1 then Alg. 2):
   H_X = X^T X, H_G = G^T G  ->  traces (pre)  ->  BiIP (rescale + both rotations)
   ->  traces (post: the sensitivity score)  ->  damping + inverse-Cholesky factor
   ->  lazy-block OBS sweep with group quantisation.
+With the input drift dX (the paper's default KronQ+GPTAQ) also D = dX^T X, its input-side BiIP,
+the correction P = alpha ((D U^T) . M_U) U after the factor, and the drift-corrected sweep.
 All calls are enqueued on the current stream; nothing here synchronises except ``check()``.
 """
 from __future__ import annotations
@@ -53,18 +55,26 @@ class LayerState:
     ws_chol: torch.Tensor
     ws_obs: torch.Tensor
     err: Optional[torch.Tensor] = None
+    group: int = 128
+    D: Optional[torch.Tensor] = None       # drift statistic dX^T X (then transformed)
+    P: Optional[torch.Tensor] = None       # drift correction
+    ws_cross: Optional[torch.Tensor] = None
+    ws_rdrift: Optional[torch.Tensor] = None
+    ws_gptaq: Optional[torch.Tensor] = None
     side: Optional[torch.cuda.Stream] = None
     ev: tuple = ()
 
     @staticmethod
     def allocate(d_out: int, d_in: int, n_tokens: int, device, keep_err: bool = False,
                  x_dtype=torch.bfloat16, g_dtype=torch.bfloat16,
-                 cov_ws: bool = True) -> "LayerState":
-        """``cov_ws=False`` leaves the covariance workspaces out (a caller that shares one)."""
+                 cov_ws: bool = True, group: int = 128, drift: bool = False) -> "LayerState":
+        """``cov_ws=False`` leaves the covariance workspaces out (a caller that shares one);
+        ``group`` is the quantisation group (d_in: per-channel); ``drift`` adds the buffers of
+        the drift correction."""
         f32 = dict(dtype=torch.float32, device=device)
 
         def ws(op, a, b, n, dt=torch.bfloat16):
-            if op == K.OP_COV and (dt != torch.bfloat16 or not cov_ws):
+            if op in (K.OP_COV, K.OP_CROSS) and (dt != torch.bfloat16 or not cov_ws):
                 return torch.empty(256, dtype=torch.uint8, device=device)
             return K.workspace(op, a, b, n, device)
 
@@ -73,8 +83,8 @@ class LayerState:
             HX=torch.empty(d_in, d_in, **f32), HG=torch.empty(d_out, d_out, **f32),
             W=torch.empty(d_out, d_in, **f32), U=torch.empty(d_in, d_in, **f32),
             codes=torch.empty(d_out, d_in, dtype=torch.uint8, device=device),
-            scales=torch.empty(d_out, d_in // 128, **f32),
-            zeros=torch.empty(d_out, d_in // 128, **f32),
+            scales=torch.empty(d_out, d_in // group, **f32),
+            zeros=torch.empty(d_out, d_in // group, **f32),
             sx=torch.empty(d_in, **f32), sg=torch.empty(d_out, **f32),
             tr_pre=torch.empty(3, dtype=torch.float64, device=device),
             tr_post=torch.empty(3, dtype=torch.float64, device=device),
@@ -82,8 +92,14 @@ class LayerState:
             ws_cov_x=ws(K.OP_COV, 0, d_in, n_tokens, x_dtype),
             ws_cov_g=ws(K.OP_COV, 0, d_out, n_tokens, g_dtype),
             ws_rot=ws(K.OP_ROTATE, d_out, d_in, 0), ws_chol=ws(K.OP_CHOL, 0, d_in, 0),
-            ws_obs=ws(K.OP_OBS, d_out, d_in, 0),
+            ws_obs=ws(K.OP_OBS_DRIFT if drift else K.OP_OBS, d_out, d_in, 0),
             err=torch.empty(d_out, d_in, **f32) if keep_err else None,
+            group=group,
+            D=torch.empty(d_in, d_in, **f32) if drift else None,
+            P=torch.empty(d_in, d_in, **f32) if drift else None,
+            ws_cross=ws(K.OP_CROSS, 0, d_in, n_tokens, x_dtype) if drift else None,
+            ws_rdrift=ws(K.OP_ROTATE_DRIFT, 0, d_in, 0) if drift else None,
+            ws_gptaq=ws(K.OP_GPTAQ, 0, d_in, 0) if drift else None,
             side=torch.cuda.Stream(device=device),  # default priority
             ev=tuple(torch.cuda.Event() for _ in range(3)),
         )
@@ -104,26 +120,55 @@ def biip(st: LayerState, W0: torch.Tensor, rin: RotParams, rout: RotParams, flag
     K.kronq_traces(st.HX, st.HG, st.tr_post)
 
 
-def solve(st: LayerState, bits: int, damp: float = 0.01):
+def drift_statistic(st: LayerState, dX: torch.Tensor, X: torch.Tensor):
+    """Alg. 1 first line, second half: D = dX^T X."""
+    K.kronq_accumulate_cross(dX, X, st.D, 1.0, 0.0, st.ws_cross)
+
+
+def drift_biip(st: LayerState, rin: RotParams, flags: int = K.BIIP):
+    """Alg. 1: D <- V S_X^-1 D S_X^-1 V^T (needs S_X from the forward BiIP)."""
+    K.kronq_rotate_drift(st.D, st.sx, rin.sign, rin.q28, flags & (K.RESCALE_IN | K.ROT_IN),
+                         st.ws_rdrift)
+
+
+def sweep(st: LayerState, bits: int, alpha: Optional[float] = None):
+    """Step a7/a8: the lazy-block OBS sweep; with ``alpha`` (drift) first P from D and U."""
+    if alpha is None:
+        K.kronq_obs_quantize_layer(st.W, st.U, bits, st.codes, st.scales, st.zeros, st.err, None,
+                                   group=st.group, ws=st.ws_obs)
+        return
+    K.kronq_gptaq_correction(st.D, st.U, st.P, alpha, st.ws_gptaq)
+    K.kronq_obs_quantize_layer_drift(st.W, st.U, st.P, bits, st.codes, st.scales, st.zeros,
+                                     st.err, None, group=st.group, ws=st.ws_obs)
+
+
+def solve(st: LayerState, bits: int, damp: float = 0.01, alpha: Optional[float] = None):
     """Steps a6-a8: damping + inverse-Cholesky factor, then the lazy-block OBS sweep."""
     K.kronq_cholesky_inv(st.HX, st.U, damp, st.info, st.ws_chol)
-    K.kronq_obs_quantize_layer(st.W, st.U, bits, st.codes, st.scales, st.zeros, st.err, None,
-                               ws=st.ws_obs)
+    sweep(st, bits, alpha)
 
 
 def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bits: int,
                    damp: float = 0.01, flags: int = K.BIIP, skip_x: bool = False,
-                   overlap: bool = True):
-    """The whole hot path of one layer (enqueue only).
+                   overlap: bool = True, dX: Optional[torch.Tensor] = None, alpha: float = 1.0):
+    """The whole hot path of one layer (enqueue only). ``dX`` (with buffers from
+    ``allocate(drift=True)``) adds the drift correction with scaling ``alpha``.
 
     With ``overlap`` the work is split over two streams: the factorisation depends only on H_X
     and S_X, so it runs on the current stream right after H_X is rotated, while the second
     stream accumulates H_G (after H_X is done, so the two covariances do not share the GPU)
     and rotates W and H_G. The sweep starts when both are done."""
+    drift = dX is not None
+    if drift and st.D is None:
+        raise ValueError("the drift correction needs LayerState.allocate(..., drift=True)")
     if not overlap:
         covariances(st, X, G, skip_x)
+        if drift:
+            drift_statistic(st, dX, X)
         biip(st, W0, rin, rout, flags)
-        solve(st, bits, damp)
+        if drift:
+            drift_biip(st, rin, flags)
+        solve(st, bits, damp, alpha if drift else None)
         return
     main = torch.cuda.current_stream(st.HX.device)
     ev_x, ev_sx, ev_w = st.ev
@@ -131,6 +176,8 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
         K.kronq_accumulate_cov(X, st.HX, 1.0, 0.0, st.ws_cov_x)
     K.kronq_traces(st.HX, None, st.tr_pre)
     ev_x.record(main)
+    if drift:
+        drift_statistic(st, dX, X)
     K.kronq_rotate(W0, None, st.HX, None, rin.sign, None, rin.q28, None, st.sx, st.sg,
                    flags | K.HX_ONLY, st.ws_rot)
     K.kronq_traces(st.HX, None, st.tr_post)
@@ -148,9 +195,16 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
         K.kronq_traces(None, st.HG, st.tr_post)
         ev_w.record(st.side)
     K.kronq_cholesky_inv(st.HX, st.U, damp, st.info, st.ws_chol)
+    if drift:
+        drift_biip(st, rin, flags)
+        K.kronq_gptaq_correction(st.D, st.U, st.P, alpha, st.ws_gptaq)
     main.wait_event(ev_w)
-    K.kronq_obs_quantize_layer(st.W, st.U, bits, st.codes, st.scales, st.zeros, st.err, None,
-                               ws=st.ws_obs)
+    if drift:
+        K.kronq_obs_quantize_layer_drift(st.W, st.U, st.P, bits, st.codes, st.scales, st.zeros,
+                                         st.err, None, group=st.group, ws=st.ws_obs)
+    else:
+        K.kronq_obs_quantize_layer(st.W, st.U, bits, st.codes, st.scales, st.zeros, st.err, None,
+                                   group=st.group, ws=st.ws_obs)
 
 
 def check(st: LayerState):

@@ -39,7 +39,8 @@ import torch
 
 __all__ = [
     "LayerSpec", "WORKLOADS", "workload", "block_layers", "quantile_table", "gen_matrix",
-    "gen_columns", "layer_inputs", "rotation_params", "bf16_bits", "Rot",
+    "gen_columns", "layer_inputs", "rotation_params", "bf16_bits", "Rot", "drift_noise_spec",
+    "gen_drift", "gen_drift_columns",
 ]
 
 NQ = 65536  # quantile levels (16 bits of the hash)
@@ -279,6 +280,43 @@ def block_layers(n_tokens: Optional[int] = None, seed: int = 4, shrink: int = 1)
         out.append(_layer(name, d_out, d_in, n, 3, lseed, xkind, 1.5, 0.02, torch.bfloat16,
                           x_key=f"blk:{xkey}", x_seed=seed))
     return out
+
+
+# --------------------------------------------------------------------------------------------
+# input drift (the drift-corrected objective: dX = X~ - X, full-precision minus quantised input)
+# --------------------------------------------------------------------------------------------
+DRIFT_SIGMA = 1.0 / 16   # noise part, relative to each input channel's scale
+DRIFT_SHRINK = 0.0625    # signal part: the quantised model's input is the full one shrunk by 1/16
+
+
+def drift_noise_spec(spec: LayerSpec) -> MatSpec:
+    """The noise part Z of the synthetic drift: normal, X's per-channel scales times 1/16, fp32."""
+    xs = spec.x
+    return MatSpec(xs.seed, xs.tag + ":drift", xs.rows, xs.cols, ("normal",), None,
+                   (xs.col_scale * np.float32(DRIFT_SIGMA)).astype(np.float32), torch.float32)
+
+
+def _drift(Z: torch.Tensor, X: torch.Tensor, dtype) -> torch.Tensor:
+    # one exact scaling by a power of two, one IEEE subtraction, one rounding: identical bytes on
+    # CPU and GPU
+    return (Z - X.float() * DRIFT_SHRINK).to(dtype)
+
+
+def gen_drift(spec: LayerSpec, device="cpu", X: Optional[torch.Tensor] = None,
+              rows: Optional[tuple] = None) -> torch.Tensor:
+    """dX = Z - X / 16 in X's dtype: a stand-in for the gap between the full-precision and the
+    quantised model's inputs, part noise and part a shrink of the signal (so that dX^T X has a
+    systematic component). ``X`` may pass the already generated rows of the layer's input."""
+    Z = gen_matrix(drift_noise_spec(spec), device, rows)
+    if X is None:
+        X = gen_matrix(spec.x, device, rows)
+    return _drift(Z, X, spec.x.dtype)
+
+
+def gen_drift_columns(spec: LayerSpec, cols, rows: Optional[tuple] = None) -> torch.Tensor:
+    """Columns ``cols`` of gen_drift(spec) for rows [r0, r1), on the CPU."""
+    return _drift(gen_columns(drift_noise_spec(spec), cols, rows), gen_columns(spec.x, cols, rows),
+                  spec.x.dtype)
 
 
 # --------------------------------------------------------------------------------------------

@@ -37,6 +37,11 @@ def test_version_and_workspace_queries():
     assert K.kronq_workspace_bytes(K.OP_COV, 0, 4096, 262144) > 0
     assert K.kronq_workspace_bytes(K.OP_CHOL, 0, 4096, 0) >= 2 * 4096 * 4096 * 4
     assert K.kronq_workspace_bytes(K.OP_OBS, 4096, 4096, 0) > 0
+    assert K.kronq_workspace_bytes(K.OP_CROSS, 0, 4096, 262144) >= 256 * 256 * 256 * 4
+    assert K.kronq_workspace_bytes(K.OP_ROTATE_DRIFT, 0, 4096, 0) >= 4096 * 4
+    assert K.kronq_workspace_bytes(K.OP_GPTAQ, 0, 4096, 0) >= 4096 * 4096 * 4
+    assert K.kronq_workspace_bytes(K.OP_OBS_DRIFT, 4096, 4096, 0) > K.kronq_workspace_bytes(
+        K.OP_OBS, 4096, 4096, 0)
     assert K.kronq_workspace_bytes(99, 1, 1, 1) == 0
     assert K.kronq_workspace_bytes(K.OP_COV, 0, -1, 10) == 0
 
@@ -92,6 +97,54 @@ def test_argument_checks_fail_before_any_launch():
     # Cholesky output aliasing its input
     rc, _ = _err(lib.kronq_cholesky_inv(fake, 8, 8, 0.01, fake, 8, fake, ws, 1 << 30, nul))
     assert rc == -1
+    # the sweep's workspace is checked also when the caller keeps the errors
+    rc, msg = _err(lib.kronq_obs_quantize_layer(fake, 8, 256, 256, ctypes.c_void_p(1 << 21), 256,
+                                                4, 128, 128, fake, fake, fake, fake, nul, nul, 16,
+                                                nul))
+    assert rc == -5 and "workspace" in msg
+
+
+def test_drift_and_group_argument_checks():
+    lib = K.load()
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)
+    other = ctypes.c_void_p(1 << 21)
+    ws = ctypes.c_void_p(1 << 30)
+    # groups: multiples of 128 that divide d_in (any of them); others are unsupported
+    rc, msg = _err(lib.kronq_obs_quantize_layer(fake, 8, 768, 768, other, 768, 3, 192, 128, fake,
+                                                fake, fake, nul, nul, nul, 0, nul))
+    assert rc == -6 and "group" in msg
+    rc, msg = _err(lib.kronq_obs_quantize_layer(fake, 8, 768, 768, other, 768, 3, 512, 128, fake,
+                                                fake, fake, nul, nul, nul, 0, nul))
+    assert rc == -2
+    # (a supported wide group gets past the group checks and stops at the workspace)
+    rc, msg = _err(lib.kronq_obs_quantize_layer(fake, 8, 768, 768, other, 768, 3, 384, 128, fake,
+                                                fake, fake, nul, nul, nul, 0, nul))
+    assert rc == -5
+    # the drift sweep needs P, and P must not alias W
+    rc, msg = _err(lib.kronq_obs_quantize_layer_drift(fake, 8, 256, 256, other, 256, nul, 256, 3,
+                                                      128, 128, fake, fake, fake, nul, nul, ws,
+                                                      1 << 30, nul))
+    assert rc == -1 and "P" in msg
+    rc, msg = _err(lib.kronq_obs_quantize_layer_drift(fake, 8, 256, 256, other, 256, fake, 256, 3,
+                                                      128, 128, fake, fake, fake, nul, nul, ws,
+                                                      1 << 30, nul))
+    assert rc == -1 and "alias" in msg
+    # drift statistic: B missing, rows not 16-byte aligned
+    rc, _ = _err(lib.kronq_accumulate_cross(fake, nul, 1, 100, 64, 64, fake, 64, 1.0, 0.0, ws,
+                                            1 << 30, nul))
+    assert rc == -1
+    rc, _ = _err(lib.kronq_accumulate_cross(fake, other, 1, 100, 64, 68, fake, 64, 1.0, 0.0, ws,
+                                            1 << 30, nul))
+    assert rc == -1
+    # its BiIP takes only the input-side flags
+    rc, msg = _err(lib.kronq_rotate_drift(fake, 64, 64, fake, fake, nul, K.ROT_OUT, ws, 1 << 30,
+                                          nul))
+    assert rc == -1 and "RESCALE_IN" in msg
+    # P must not alias D
+    rc, msg = _err(lib.kronq_gptaq_correction(fake, 64, 64, other, 64, 1.0, fake, 64, ws, 1 << 30,
+                                              nul))
+    assert rc == -1 and "alias" in msg
 
 
 @pytest.mark.parametrize("seed", range(6))
