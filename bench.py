@@ -5,13 +5,15 @@ One step = the whole per-layer path on one batch of synthetic calibration data a
 resident in HBM: H_X = X^T X, H_G = G^T G, traces, BiIP (rescale + both randomised Hadamard
 rotations of W, H_X, H_G), traces, damping + inverse-Cholesky factor, lazy-block OBS sweep with
 group quantisation. Default workload: the LLaMA-3-8B q_proj shape, W 4096 x 4096, 262144 tokens
-(128 x 2048), 4-bit, group 128.
+(128 x 2048), 4-bit, group 128. --drift adds the drift correction (KronQ+GPTAQ: D = dX^T X, its
+BiIP, P and the drift-corrected sweep); --group sets the quantisation group (0: per-channel).
 
 The JSON line carries
-  * roofline: the covariance syrk (the dominant kernel) timed by libkronq's hipEvent profiler on
-    its own stream inside the timed region, algorithmic flops N d (d + 1) per launch, against
-    the 2.5 PFLOP/s dense bf16 MFMA peak; HBM traffic from the committed rocprofv3 counter
-    summary when it was taken on the current kernel source;
+  * roofline: the covariance syrk (the dominant kernel; with --drift the drift statistic's
+    kernel, 2 N d_in^2 flops per launch) timed by libkronq's hipEvent profiler on its own stream
+    inside the timed region, algorithmic flops N d (d + 1) per launch, against the 2.5 PFLOP/s
+    dense bf16 MFMA peak; HBM traffic from the committed rocprofv3 counter summary when it was
+    taken on the current kernel source;
   * cpu_baseline: the float64 oracle on this host's cores on a bounded sample (the covariances
     on the first --cpu-tokens tokens, scaled linearly to N; every other step at full size).
 """
@@ -29,13 +31,14 @@ sys.path.insert(0, ROOT)
 
 METRIC = "seconds per layer quantised (cov+rotate+OBS) at 8B/70B shapes; % MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0
-DOMINANT = "syrk_bf16_mfma"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "syrk_bf16_traffic.json")
-KERNELS = ["syrk_bf16_mfma", "syrk_reduce", "traces", "rot_w_norms", "rot_factors",
-           "rot_row_pass", "fwht_col", "mix28_col", "chol_diag_shift", "chol_add_diag",
-           "chol_reverse_copy", "chol_potrf_diag", "chol_trsm", "chol_syrk", "trtri_row",
-           "trtri_put_diag", "trtri_update", "chol_reverse_out", "obs_sweep",
-           "obs_trailing_update"]
+TRAFFIC_FILES = {k: os.path.join(ROOT, "profiles", f"{k.replace('_mfma', '')}_traffic.json")
+                 for k in ("syrk_bf16_mfma", "cross_bf16_mfma")}
+KERNELS = ["syrk_bf16_mfma", "syrk_reduce", "cross_bf16_mfma", "cross_reduce", "traces",
+           "rot_w_norms", "rot_factors", "rot_inv_factors", "rot_row_pass", "fwht_col",
+           "mix28_col", "chol_diag_shift", "chol_add_diag", "chol_reverse_copy",
+           "chol_potrf_diag", "chol_trsm", "chol_syrk", "trtri_row", "trtri_put_diag",
+           "trtri_update", "chol_reverse_out", "gptaq_d_ut", "gptaq_t_u", "gptaq_mask",
+           "obs_split_u", "obs_split_p", "obs_group_params", "obs_sweep", "obs_trailing_update"]
 WORKLOADS = {"q_proj": 2, "down_proj": 3, "up_proj_70b": 4}
 
 
@@ -44,17 +47,19 @@ def cov_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def traffic(launch_bytes_alg: float):
+def traffic(kernel: str):
     """HBM bytes per launch from the rocprofv3 FETCH_SIZE/WRITE_SIZE summary (or None)."""
-    if not os.path.exists(TRAFFIC_FILE):
+    path = TRAFFIC_FILES.get(kernel)
+    if path is None or not os.path.exists(path):
         return None
-    t = json.load(open(TRAFFIC_FILE))
+    t = json.load(open(path))
     if t.get("cov_source_sha256_16") != cov_source_hash():
         return None  # counters were taken on another version of the kernel
     return float(t["bytes_per_launch"])
 
 
-def cpu_baseline(spec, rot_in, rot_out, n_sample: int, X_dev, G_dev, W_dev):
+def cpu_baseline(spec, rot_in, rot_out, n_sample: int, X_dev, G_dev, W_dev, dX_dev=None,
+                 alpha: float = 1.0, group: int = 128):
     import numpy as np
     import oracle as O
     import synth
@@ -72,20 +77,24 @@ def cpu_baseline(spec, rot_in, rot_out, n_sample: int, X_dev, G_dev, W_dev):
     t0 = time.perf_counter()
     hx = O.covariance(Xs)
     hg = O.covariance(Gs)
+    D = None if dX_dev is None else O.cross_covariance(view(dX_dev[:n_sample]), Xs)
     t_cov = time.perf_counter() - t0
     t1 = time.perf_counter()
     O.traces(hx, hg)
-    b = O.biip_forward(W, hx, hg, (rot_in.sign, rot_in.q28), (rot_out.sign, rot_out.q28))
+    b = O.biip_forward(W, hx, hg, (rot_in.sign, rot_in.q28), (rot_out.sign, rot_out.q28), D=D)
     O.traces(b["HX"], b["HG"])
     U = O.inverse_cholesky_factor(O.damp(b["HX"], spec.damp))
-    O.obs_blocked(b["W"], U, spec.bits, 128, 128)
+    P = None if D is None else O.gptaq_correction(b["D"], U, alpha)
+    O.obs_blocked(b["W"], U, spec.bits, group, 128, P=P)
     t_rest = time.perf_counter() - t1
     scale = spec.n_tokens / n_sample
     return {
         "value": t_cov * scale + t_rest, "unit": "s/layer", "cores": int(cores), "kind": "oracle",
-        "sample": (f"float64 oracle: covariances on the first {n_sample} of {spec.n_tokens} tokens "
+        "sample": (f"float64 oracle: covariances{' and drift statistic' if D is not None else ''} "
+                   f"on the first {n_sample} of {spec.n_tokens} tokens "
                    f"({t_cov:.2f} s, scaled x{scale:g}); traces, BiIP with dense rotations, "
-                   f"factor and blocked OBS sweep at full size ({t_rest:.2f} s)"),
+                   f"factor{', P' if D is not None else ''} and blocked OBS sweep at full size "
+                   f"({t_rest:.2f} s)"),
     }
 
 
@@ -101,6 +110,11 @@ def main() -> int:
                     help="per-kernel times of one extra step run on a single stream (stderr)")
     ap.add_argument("--serial", action="store_true",
                     help="time the single-stream schedule instead of the two-stream one")
+    ap.add_argument("--drift", action="store_true",
+                    help="the drift-corrected path (KronQ+GPTAQ) with synthetic input drift")
+    ap.add_argument("--alpha", type=float, default=1.0, help="drift correction scaling")
+    ap.add_argument("--group", type=int, default=128,
+                    help="quantisation group (a multiple of 128 dividing d_in; 0: per-channel)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run 3 plain 1 GiB device copies (reference for counter scaling)")
     args = ap.parse_args()
@@ -132,16 +146,20 @@ def main() -> int:
     X = synth.gen_matrix(spec.x, dev)
     G = synth.gen_matrix(spec.g, dev)
     W0 = synth.gen_matrix(spec.w, dev)
+    dX = synth.gen_drift(spec, dev, X=X) if args.drift else None
     ri = synth.rotation_params(spec.d_in, spec.seed, spec.name + ":in")
     ro = synth.rotation_params(spec.d_out, spec.seed, spec.name + ":out")
     rin = L.RotParams.to_device(ri.sign, ri.q28, dev)
     rout = L.RotParams.to_device(ro.sign, ro.q28, dev)
+    group = args.group if args.group > 0 else spec.d_in
     st = L.LayerState.allocate(spec.d_out, spec.d_in, spec.n_tokens, dev, x_dtype=X.dtype,
-                               g_dtype=G.dtype)
+                               g_dtype=G.dtype, group=group, drift=args.drift)
+    dominant = "cross_bf16_mfma" if args.drift else "syrk_bf16_mfma"
     torch.cuda.synchronize()
 
     def step(overlap=not args.serial):
-        L.quantize_layer(st, X, G, W0, rin, rout, spec.bits, spec.damp, overlap=overlap)
+        L.quantize_layer(st, X, G, W0, rin, rout, spec.bits, spec.damp, overlap=overlap, dX=dX,
+                         alpha=args.alpha)
 
     for _ in range(args.warmup):
         step()
@@ -149,7 +167,7 @@ def main() -> int:
     L.check(st)
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
-    K.kronq_profile_only(DOMINANT)
+    K.kronq_profile_only(dominant)
     K.kronq_profile_reset()
     K.kronq_profile_enable(True)
     torch.cuda.synchronize()
@@ -159,18 +177,23 @@ def main() -> int:
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     K.kronq_profile_enable(False)
-    syrk_ms, syrk_n = K.kronq_profile_read(DOMINANT)
+    dom_ms, dom_n = K.kronq_profile_read(dominant)
     L.check(st)
     ms_step = (t1 - t0) * 1e3 / args.steps
     print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
 
-    # dominant kernel roofline: algorithmic flops N d (d + 1) per covariance launch
-    flops = float(spec.n_tokens) * (spec.d_in * (spec.d_in + 1) + spec.d_out * (spec.d_out + 1)) / 2
-    avg_ms = syrk_ms / max(syrk_n, 1)
+    # dominant kernel roofline: algorithmic flops N d (d + 1) per covariance launch (averaged
+    # over the two covariances), 2 N d_in^2 for the drift statistic
+    if args.drift:
+        flops = 2.0 * spec.n_tokens * spec.d_in * spec.d_in
+    else:
+        flops = float(spec.n_tokens) * (spec.d_in * (spec.d_in + 1) +
+                                        spec.d_out * (spec.d_out + 1)) / 2
+    avg_ms = dom_ms / max(dom_n, 1)
     achieved = flops / (avg_ms * 1e-3) / 1e12
     roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": traffic(flops), "kernel": DOMINANT, "launches": syrk_n,
+            "traffic": traffic(dominant), "kernel": dominant, "launches": dom_n,
             "avg_launch_ms": round(avg_ms, 4)}
 
     breakdown = None
@@ -192,7 +215,8 @@ def main() -> int:
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on the host (bounded sample)", file=sys.stderr,
               flush=True)
-        cpu = cpu_baseline(spec, ri, ro, min(args.cpu_tokens, spec.n_tokens), X, G, W0)
+        cpu = cpu_baseline(spec, ri, ro, min(args.cpu_tokens, spec.n_tokens), X, G, W0, dX,
+                           args.alpha, group)
 
     out = {
         "metric": METRIC, "value": round(ms_step / 1e3, 6), "unit": "s/layer", "n_gpus": 1,
@@ -200,9 +224,11 @@ def main() -> int:
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16 (covariances, MFMA) + fp32 (rotations, factor, OBS)", "data": "synthetic",
         "config": {"workload": f"{spec.name} W {spec.d_out}x{spec.d_in}, N={spec.n_tokens} tokens, "
-                               f"{spec.bits}-bit, group {spec.group}",
+                               f"{spec.bits}-bit, group {group}"
+                               + (f", drift correction (alpha {args.alpha:g})" if args.drift else ""),
                    "d_out": spec.d_out, "d_in": spec.d_in, "n_tokens": spec.n_tokens,
-                   "bits": spec.bits, "group": spec.group, "block": 128, "damp": spec.damp,
+                   "bits": spec.bits, "group": group, "block": 128, "damp": spec.damp,
+                   "drift": bool(args.drift),
                    "parallelism": "single GPU",
                    "schedule": "one stream" if args.serial else "two streams"},
         "roofline": roof, "cpu_baseline": cpu,

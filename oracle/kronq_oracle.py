@@ -274,12 +274,18 @@ def inverse_cholesky_factor(Hd) -> np.ndarray:
     return np.linalg.cholesky(Hinv).T
 
 
-def gptaq_correction(D, U, alpha: float = 1.0) -> np.ndarray:
+def gptaq_correction(D, U, alpha: float = 1.0, rows=None) -> np.ndarray:
     """The drift correction of Prop. 1 and Algorithm 2's third line,
-    P = alpha ((D L) . M_U) L^T with L = U^T (readings R16, R18): strictly upper triangular."""
+    P = alpha ((D L) . M_U) L^T with L = U^T (readings R16, R18): strictly upper triangular.
+    ``rows`` (optional) returns only those rows of P, each from the same row of D."""
     D = np.asarray(D, dtype=np.float64)
     U = np.asarray(U, dtype=np.float64)
-    return alpha * (np.triu(D @ U.T, 1) @ U)
+    if rows is None:
+        return alpha * (np.triu(D @ U.T, 1) @ U)
+    rows = np.asarray(rows)
+    T = D[rows] @ U.T
+    T[np.arange(U.shape[0])[None, :] <= rows[:, None]] = 0.0  # keep columns after each row
+    return alpha * (T @ U)
 
 
 # ----------------------------------------------------------------------------------------------

@@ -90,7 +90,7 @@ __device__ __forceinline__ void store_block_t(uint32_t* __restrict__ lds, const 
 }
 
 template <bool CROSS>
-__global__ __launch_bounds__(256, 1) void syrk_bf16_partial(
+__device__ __forceinline__ void gram_partial(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, int64_t tok0,
     int64_t tok_end, int64_t d, int64_t lda, float* __restrict__ part, int n_slices,
     int64_t rows_per_slice, int T, int edge_only, int out_slice0) {
@@ -265,9 +265,9 @@ __device__ __forceinline__ bf16x8_t tr_frag(const uint32_t* buf, int tb, int cb,
 }
 
 template <bool CROSS>
-__global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restrict__ A,
-                                                        const uint16_t* __restrict__ B,
-                                                        int64_t n_rows, int64_t lda,
+__device__ __forceinline__ void gram_dma(const uint16_t* __restrict__ A,
+                                         const uint16_t* __restrict__ B,
+                                         int64_t n_rows, int64_t lda,
                                                         float* __restrict__ part, int n_slices,
                                                         int64_t rows_per_slice, int T, int Tf) {
   __shared__ __attribute__((aligned(16))) uint32_t a0[SBUF], a1[SBUF], a2[SBUF], a3[SBUF];
@@ -473,9 +473,9 @@ __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(const uint16_t* __restri
 // Sum the S partial tiles of one 64 x 64 sub-block and write H (and its mirror; cross: the
 // sub-block as it is).
 template <bool CROSS>
-__global__ __launch_bounds__(256) void syrk_reduce(const float* __restrict__ part, int n_slices,
-                                                   int T, int64_t d, float* __restrict__ H,
-                                                   int64_t ldh, float alpha, float beta) {
+__device__ __forceinline__ void gram_reduce(const float* __restrict__ part, int n_slices, int T,
+                                            int64_t d, float* __restrict__ H, int64_t ldh,
+                                            float alpha, float beta) {
   __shared__ float tr[64][65];
   const int pos = blockIdx.x >> 4;
   const int sub = blockIdx.x & 15;
@@ -559,6 +559,41 @@ __global__ __launch_bounds__(256) void syrk_reduce(const float* __restrict__ par
     }
   }
 }
+
+// One kernel name per product, so that traces and profiles tell the two apart.
+#define KQ_GRAM_PARTIAL_ARGS                                                                    \
+  const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, int64_t tok0, int64_t tok_end, \
+      int64_t d, int64_t lda, float *__restrict__ part, int n_slices, int64_t rows_per_slice,    \
+      int T, int edge_only, int out_slice0
+__global__ __launch_bounds__(256, 1) void syrk_bf16_partial(KQ_GRAM_PARTIAL_ARGS) {
+  gram_partial<false>(A, B, tok0, tok_end, d, lda, part, n_slices, rows_per_slice, T, edge_only,
+                      out_slice0);
+}
+__global__ __launch_bounds__(256, 1) void cross_bf16_partial(KQ_GRAM_PARTIAL_ARGS) {
+  gram_partial<true>(A, B, tok0, tok_end, d, lda, part, n_slices, rows_per_slice, T, edge_only,
+                     out_slice0);
+}
+#define KQ_GRAM_DMA_ARGS                                                                  \
+  const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, int64_t n_rows, int64_t lda, \
+      float *__restrict__ part, int n_slices, int64_t rows_per_slice, int T, int Tf
+__global__ __launch_bounds__(256, 1) void syrk_bf16_dma(KQ_GRAM_DMA_ARGS) {
+  gram_dma<false>(A, B, n_rows, lda, part, n_slices, rows_per_slice, T, Tf);
+}
+__global__ __launch_bounds__(256, 1) void cross_bf16_dma(KQ_GRAM_DMA_ARGS) {
+  gram_dma<true>(A, B, n_rows, lda, part, n_slices, rows_per_slice, T, Tf);
+}
+#define KQ_GRAM_REDUCE_ARGS                                                                \
+  const float *__restrict__ part, int n_slices, int T, int64_t d, float *__restrict__ H,   \
+      int64_t ldh, float alpha, float beta
+__global__ __launch_bounds__(256) void syrk_reduce(KQ_GRAM_REDUCE_ARGS) {
+  gram_reduce<false>(part, n_slices, T, d, H, ldh, alpha, beta);
+}
+__global__ __launch_bounds__(256) void cross_reduce(KQ_GRAM_REDUCE_ARGS) {
+  gram_reduce<true>(part, n_slices, T, d, H, ldh, alpha, beta);
+}
+#undef KQ_GRAM_PARTIAL_ARGS
+#undef KQ_GRAM_DMA_ARGS
+#undef KQ_GRAM_REDUCE_ARGS
 
 // Plain fp32 A^T B for fp32 inputs (B = A for the covariance): 64 x 64 tiles, 4 x 4 outputs per
 // thread.
@@ -696,10 +731,10 @@ int gram_bf16(const uint16_t* A, const uint16_t* B, int64_t n_rows, int64_t d, i
   if (p.Tf > 0) {
     const dim3 grid(unsigned(int64_t(p.S) * full));
     if (cross)
-      KQ_TRY(launch("cross_bf16_mfma", syrk_bf16_dma<true>, grid, dim3(256), 0, s, A, B, n_rows,
+      KQ_TRY(launch("cross_bf16_mfma", cross_bf16_dma, grid, dim3(256), 0, s, A, B, n_rows,
                     lda, part, p.S, p.rows_per_slice, p.T, p.Tf));
     else
-      KQ_TRY(launch("syrk_bf16_mfma", syrk_bf16_dma<false>, grid, dim3(256), 0, s, A, A, n_rows,
+      KQ_TRY(launch("syrk_bf16_mfma", syrk_bf16_dma, grid, dim3(256), 0, s, A, A, n_rows,
                     lda, part, p.S, p.rows_per_slice, p.T, p.Tf));
   }
   // tiles of a ragged last channel block, same tokens
@@ -707,27 +742,27 @@ int gram_bf16(const uint16_t* A, const uint16_t* B, int64_t n_rows, int64_t d, i
   if (p.T > p.Tf) {
     const dim3 grid(unsigned(p.S * (cross ? 2 * p.T - 1 : p.T)));
     if (cross)
-      KQ_TRY(launch("cross_bf16_edge", syrk_bf16_partial<true>, grid, dim3(256), 0, s, A, B,
+      KQ_TRY(launch("cross_bf16_edge", cross_bf16_partial, grid, dim3(256), 0, s, A, B,
                     int64_t(0), body_end, d, lda, part, p.S, p.rows_per_slice, p.T, 1, 0));
     else
-      KQ_TRY(launch("syrk_bf16_edge", syrk_bf16_partial<false>, grid, dim3(256), 0, s, A, A,
+      KQ_TRY(launch("syrk_bf16_edge", syrk_bf16_partial, grid, dim3(256), 0, s, A, A,
                     int64_t(0), body_end, d, lda, part, p.S, p.rows_per_slice, p.T, 1, 0));
   }
   // the last < 32 tokens, every tile, as one extra slice
   if (p.tail) {
     const dim3 grid(unsigned(p.npos));
     if (cross)
-      KQ_TRY(launch("cross_bf16_tail", syrk_bf16_partial<true>, grid, dim3(256), 0, s, A, B,
+      KQ_TRY(launch("cross_bf16_tail", cross_bf16_partial, grid, dim3(256), 0, s, A, B,
                     p.tail_begin, n_rows, d, lda, part, 1, n_rows - p.tail_begin, p.T, 0, p.S));
     else
-      KQ_TRY(launch("syrk_bf16_tail", syrk_bf16_partial<false>, grid, dim3(256), 0, s, A, A,
+      KQ_TRY(launch("syrk_bf16_tail", syrk_bf16_partial, grid, dim3(256), 0, s, A, A,
                     p.tail_begin, n_rows, d, lda, part, 1, n_rows - p.tail_begin, p.T, 0, p.S));
   }
   const int ns = p.S + (p.tail ? 1 : 0);
   if (cross)
-    return launch("cross_reduce", syrk_reduce<true>, dim3(unsigned(p.npos * 16)), dim3(256), 0, s,
+    return launch("cross_reduce", cross_reduce, dim3(unsigned(p.npos * 16)), dim3(256), 0, s,
                   static_cast<const float*>(part), ns, p.T, d, H, ldh, alpha, beta);
-  return launch("syrk_reduce", syrk_reduce<false>, dim3(unsigned(p.npos * 16)), dim3(256), 0, s,
+  return launch("syrk_reduce", syrk_reduce, dim3(unsigned(p.npos * 16)), dim3(256), 0, s,
                 static_cast<const float*>(part), ns, p.T, d, H, ldh, alpha, beta);
 }
 

@@ -101,7 +101,7 @@ class LayerState:
             ws_rdrift=ws(K.OP_ROTATE_DRIFT, 0, d_in, 0) if drift else None,
             ws_gptaq=ws(K.OP_GPTAQ, 0, d_in, 0) if drift else None,
             side=torch.cuda.Stream(device=device),  # default priority
-            ev=tuple(torch.cuda.Event() for _ in range(3)),
+            ev=tuple(torch.cuda.Event() for _ in range(4)),
         )
 
 
@@ -156,8 +156,9 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
 
     With ``overlap`` the work is split over two streams: the factorisation depends only on H_X
     and S_X, so it runs on the current stream right after H_X is rotated, while the second
-    stream accumulates H_G (after H_X is done, so the two covariances do not share the GPU)
-    and rotates W and H_G. The sweep starts when both are done."""
+    stream accumulates H_G (after H_X is done, so the two covariances do not share the GPU),
+    then the drift statistic, and rotates W and H_G. P waits for the drift statistic, the sweep
+    for both streams."""
     drift = dX is not None
     if drift and st.D is None:
         raise ValueError("the drift correction needs LayerState.allocate(..., drift=True)")
@@ -171,13 +172,11 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
         solve(st, bits, damp, alpha if drift else None)
         return
     main = torch.cuda.current_stream(st.HX.device)
-    ev_x, ev_sx, ev_w = st.ev
+    ev_x, ev_sx, ev_w, ev_d = st.ev
     if not skip_x:
         K.kronq_accumulate_cov(X, st.HX, 1.0, 0.0, st.ws_cov_x)
     K.kronq_traces(st.HX, None, st.tr_pre)
     ev_x.record(main)
-    if drift:
-        drift_statistic(st, dX, X)
     K.kronq_rotate(W0, None, st.HX, None, rin.sign, None, rin.q28, None, st.sx, st.sg,
                    flags | K.HX_ONLY, st.ws_rot)
     K.kronq_traces(st.HX, None, st.tr_post)
@@ -189,6 +188,9 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
         st.side.wait_event(ev_x)
         K.kronq_accumulate_cov(G, st.HG, 1.0, 0.0, st.ws_cov_g)
         K.kronq_traces(None, st.HG, st.tr_pre)
+        if drift:  # the third token contraction, also beside the factorisation
+            drift_statistic(st, dX, X)
+            ev_d.record(st.side)
         st.side.wait_event(ev_sx)
         K.kronq_rotate(W0, st.W, None, st.HG, rin.sign, rout.sign, rin.q28, rout.q28, st.sx,
                        st.sg, flags | K.SX_GIVEN, st.ws_rot)
@@ -196,6 +198,7 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
         ev_w.record(st.side)
     K.kronq_cholesky_inv(st.HX, st.U, damp, st.info, st.ws_chol)
     if drift:
+        main.wait_event(ev_d)
         drift_biip(st, rin, flags)
         K.kronq_gptaq_correction(st.D, st.U, st.P, alpha, st.ws_gptaq)
     main.wait_event(ev_w)

@@ -51,6 +51,15 @@ def test_gptaq_rows_absorb_drift_by_least_squares(alpha):
             np.testing.assert_allclose(P[p, p + 1:], ref, rtol=1e-9, atol=1e-12)
 
 
+def test_gptaq_rows_subset_equals_full():
+    d = 40
+    U = O.inverse_cholesky_factor(O.damp(spd(d, 4, cond=1e2)))
+    D = rng(5).standard_normal((d, d))
+    rows = [0, 7, 23, 39]
+    np.testing.assert_allclose(O.gptaq_correction(D, U, 0.5, rows),
+                               O.gptaq_correction(D, U, 0.5)[rows], rtol=1e-12, atol=1e-15)
+
+
 def _token_problem(n, d_in, d_out, seed, lam_bar=0.5, drift=0.1):
     """Explicit tokens X, drift dX, and the damped H~ = X^T X + lam_bar I formed by appending
     sqrt(lam_bar) I as extra tokens (with zero drift), so D = dX^T X is unchanged."""
