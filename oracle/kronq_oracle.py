@@ -36,16 +36,16 @@ R13 traces are reported before and after BiIP; the sensitivity score uses post-B
 R14 bit allocation: exhaustive search minimising sum_l s_l (2^b_l - 1)^-2 under a
     parameter-weighted average-bit budget, ties to the lexicographically smallest vector.
 R15 the reported loss is taken in the original space with undamped H_X, H_G.
-R16 drift correction (Prop. 1, Algorithm 2): the paper's L with inv(H~) = L L^T is the
+R19 drift correction (Prop. 1, Algorithm 2): the paper's L with inv(H~) = L L^T is the
     transpose of the upper U of R3, so P = alpha ((D U^T) . M_U) U, where M_U is the STRICTLY
     upper mask (Prop. 1 says strictly, Algorithm 2's comment drops the word). Row p of P is then
     alpha D[p, p+1:] inv(H~[p+1:, p+1:]), which is the least-squares absorption of column p's
     drift by the columns after it. D is the token-major dX^T X (dX = X~ - X).
-R17 the W in the drift term of the sweep is the column as it stands when it is quantised; in
+R20 the W in the drift term of the sweep is the column as it stands when it is quantised; in
     the trailing update the block's columns enter with those same values, so that the lazy batch
     equals the per-column update of eq. kronq_update. (Read literally, Algorithm 2's trailing
     update would use the block after its sweep, which holds the quantised values.)
-R18 alpha is an input; 1 is the value for which the update is the exact least-squares
+R21 alpha is an input; 1 is the value for which the update is the exact least-squares
     absorption. The paper leaves alpha's value to GPTAQ.
 """
 from __future__ import annotations
@@ -276,7 +276,7 @@ def inverse_cholesky_factor(Hd) -> np.ndarray:
 
 def gptaq_correction(D, U, alpha: float = 1.0, rows=None) -> np.ndarray:
     """The drift correction of Prop. 1 and Algorithm 2's third line,
-    P = alpha ((D L) . M_U) L^T with L = U^T (readings R16, R18): strictly upper triangular.
+    P = alpha ((D L) . M_U) L^T with L = U^T (readings R19, R21): strictly upper triangular.
     ``rows`` (optional) returns only those rows of P, each from the same row of D."""
     D = np.asarray(D, dtype=np.float64)
     U = np.asarray(U, dtype=np.float64)
@@ -325,7 +325,7 @@ def obs_unblocked(W, U, bits: int, group: int = 128, P=None):
     """Sequential OBS: for each column p, quantise it (group parameters taken at the group's
     first column from the current W), form the scaled error e_p = (w_p - w_hat_p) / U_pp and
     subtract e_p U_{p, p:} from the columns p onward; with the drift correction P also add
-    w_p P_{p, p:}, w_p being column p before it is quantised (eq. kronq_update; R17). Column p
+    w_p P_{p, p:}, w_p being column p before it is quantised (eq. kronq_update; R20). Column p
     then holds w_hat_p.
 
     Returns dict(codes, scales, zeros, err, w_hat, W) with W the final compensated matrix."""
@@ -353,7 +353,7 @@ def obs_unblocked(W, U, bits: int, group: int = 128, P=None):
 def obs_blocked(W, U, bits: int, group: int = 128, block: int = 128, P=None):
     """Algorithm 2: in-block sequential updates restricted to the block, then one trailing
     update W[:, i+B:] -= E U[i:i+B, i+B:] - W_blk P[i:i+B, i+B:] per block (lazy batch), where
-    W_blk holds the block's columns as they stood when each was quantised (R17). P = None is
+    W_blk holds the block's columns as they stood when each was quantised (R20). P = None is
     the P = 0 case."""
     W = as_f64(W).copy()
     U = np.asarray(U, dtype=np.float64)

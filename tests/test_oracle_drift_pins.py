@@ -115,7 +115,7 @@ def test_zero_drift_is_the_plain_sweep():
 
 @pytest.mark.parametrize("block,group", [(128, 128), (32, 128), (64, 256), (128, 256), (64, 64)])
 def test_blocked_equals_unblocked_with_drift(block, group):
-    # the lazy batch (reading R17: block columns as they stood when quantised) changes nothing
+    # the lazy batch (reading R20: block columns as they stood when quantised) changes nothing
     r = rng(7)
     W = r.standard_normal((30, 256)) * 0.02
     H = O.damp(spd(256, 8, cond=1e3))
