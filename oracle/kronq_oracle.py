@@ -59,7 +59,7 @@ __all__ = [
     "rescale_factors", "hadamard", "rht_matrix", "rht_rows",
     "biip_forward", "biip_revert", "damp", "inverse_cholesky_factor", "gptaq_correction",
     "group_params", "quantize", "obs_unblocked", "obs_blocked", "kfac_loss", "kronq_objective",
-    "allocate_bits", "count_avg_bits",
+    "allocate_bits", "count_avg_bits", "dequantize", "online_matvec", "pack_codes",
     "RESCALE_IN", "RESCALE_OUT", "ROT_IN", "ROT_OUT", "BIIP",
 ]
 
@@ -383,6 +383,45 @@ def obs_blocked(W, U, bits: int, group: int = 128, block: int = 128, P=None):
             if P is not None:
                 W[:, j_end:] += Wq @ P[i:j_end, j_end:]
     return {"codes": codes, "scales": scales, "zeros": zeros, "err": err, "w_hat": w_hat, "W": W}
+
+
+# ----------------------------------------------------------------------------------------------
+# Inference with the quantised layer  (Sec. 3.2 and 4.2: the rotations are applied online; Alg. 2
+# last line gives the original-space weights; Limitations: O(d log d) online reversion)
+# ----------------------------------------------------------------------------------------------
+def dequantize(codes, scales, zeros, group: int) -> np.ndarray:
+    """W_hat' = scale * (q - zero) per row and group (the rotated-space dequantised weights)."""
+    codes = np.asarray(codes, dtype=np.float64)
+    s = np.repeat(np.asarray(scales, dtype=np.float64), group, axis=1)
+    z = np.repeat(np.asarray(zeros, dtype=np.float64), group, axis=1)
+    return s * (codes - z)
+
+
+def online_matvec(W_rot, sx, sg, V, U, x) -> np.ndarray:
+    """y = S_G^-1 U^T W_rot V S_X^-1 x for the columns of x [d_in x B], applied factor by factor
+    from the right (the original-space product of Alg. 2's last line without forming it)."""
+    x = np.asarray(x, dtype=np.float64)
+    xr = V @ (x / np.asarray(sx, dtype=np.float64)[:, None])
+    yr = np.asarray(W_rot, dtype=np.float64) @ xr
+    return (U.T @ yr) / np.asarray(sg, dtype=np.float64)[:, None]
+
+
+def pack_codes(codes, bits: int) -> np.ndarray:
+    """Storage format of the codes: each run of 32 consecutive codes of a row becomes a
+    32*bits-bit little-endian string (code j at bits [j*bits, (j+1)*bits)), held in `bits`
+    uint32 words. Returns uint32 [d_out x d_in*bits/32]."""
+    codes = np.asarray(codes, dtype=np.uint64)
+    d_out, d_in = codes.shape
+    if d_in % 32:
+        raise ValueError("d_in must be a multiple of 32")
+    out = np.zeros((d_out, d_in * bits // 32), dtype=np.uint64)
+    for j in range(d_in):
+        pos = (j // 32) * 32 * bits + (j % 32) * bits  # bit position in the row
+        w, off = pos // 32, pos % 32
+        out[:, w] |= (codes[:, j] << np.uint64(off)) & np.uint64(0xFFFFFFFF)
+        if off + bits > 32:
+            out[:, w + 1] |= codes[:, j] >> np.uint64(32 - off)
+    return out.astype(np.uint32)
 
 
 # ----------------------------------------------------------------------------------------------

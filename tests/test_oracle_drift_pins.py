@@ -175,3 +175,4 @@ def test_per_channel_rtn_when_hessian_is_diagonal():
         srt = np.sort(dist, axis=1)
         tie = srt[:, 1] - srt[:, 0] < 1e-15
         assert np.all((res["codes"][:, c] == np.argmin(dist, axis=1)) | tie)
+
