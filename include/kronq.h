@@ -87,6 +87,7 @@ extern "C" {
 #define KRONQ_OP_ROTATE_DRIFT 7  /* kronq_rotate_drift: d_in */
 #define KRONQ_OP_GPTAQ 8         /* kronq_gptaq_correction: d as d_in */
 #define KRONQ_OP_OBS_DRIFT 9     /* kronq_obs_quantize_layer_drift: d_out, d_in */
+#define KRONQ_OP_ONLINE 10       /* kronq_online_matvec: d_out, d_in, batch as n_rows */
 
 /* Bytes of scratch the operation needs for these sizes. For KRONQ_OP_COV pass the covariance
  * dimension d as d_in and the token count as n_rows (d_out ignored); for KRONQ_OP_CHOL pass
@@ -224,6 +225,43 @@ int kronq_obs_quantize_layer_drift(float* W, int64_t d_out, int64_t d_in, int64_
                                    int bits, int group, int block, uint8_t* codes, float* scales,
                                    float* zeros, float* err, float* W_hat, void* ws,
                                    size_t ws_bytes, void* stream);
+
+/* ---- 7. inference with the quantised layer (Sec. 3.2, 4.2; Limitations; Alg. 2 last line) ----
+ * The rotations are applied online around a matvec on the packed codes:
+ *   y = S_G^-1 U^T W_hat' V S_X^-1 x,   W_hat' = scale * (code - zero) per row and group,
+ * i.e. the original-space dequantised layer, without forming it.
+ *
+ * kronq_pack_codes: codes uint8 [d_out x ldq] (from the sweep) -> packed uint32 [d_out x ldp]:
+ * each run of 32 consecutive codes of a row becomes one 32 * bits-bit little-endian string
+ * (code j at bits [j * bits, (j + 1) * bits)) in `bits` words; ldp >= d_in * bits / 32.
+ * bits in {2, 3, 4, 8}; d_in a multiple of 32; packed 4-byte aligned. */
+int kronq_pack_codes(const uint8_t* codes, int64_t d_out, int64_t d_in, int64_t ldq, int bits,
+                     uint32_t* packed, int64_t ldp, void* stream);
+
+/* mul[j] = sign[j] / s[j] (a NULL sign or s counts as 1): the multipliers of the online
+ * transforms, mul_in from (sx, sign_in) and mul_out from (sg, sign_out). mul: device fp32 [d],
+ * 16-byte aligned. */
+int kronq_online_factors(const float* s, const int8_t* sign, int64_t d, float* mul, void* stream);
+
+/* y[b] = diag(mul_out) T_out W_hat' T_in diag(mul_in) x[b] for b < batch, where
+ * T_in = V diag(sign_in)^-1 (the Hadamard factor (Q28_in (x) H) / sqrt(m), with KRONQ_ROT_IN) and
+ * T_out = (Q28_out^T (x) H) / sqrt(m) (with KRONQ_ROT_OUT); with the factors of
+ * kronq_online_factors this is S_G^-1 U^T W_hat' V S_X^-1 x. Other flag bits of KRONQ_BIIP are
+ * accepted and ignored (the rescaling is inside mul_in, mul_out).
+ *   packed  device uint32 [d_out x ldp] from kronq_pack_codes; 16-byte aligned, ldp % 4 == 0.
+ *   scales, zeros  device fp32 [d_out x ldsz], one per row and group (group a multiple of 128
+ *           dividing d_in; d_in: per-channel).
+ *   mul_in [d_in], mul_out [d_out]  device fp32, 16-byte aligned, or NULL (1).
+ *   q28_in, q28_out  as for kronq_rotate, required when that side rotates a 28 * 2^k dimension.
+ *   x       device [batch x ldx], KRONQ_BF16 or KRONQ_FP32, 16-byte aligned rows.
+ *   y       device fp32 [batch x ldy], 16-byte aligned, ldy % 4 == 0.
+ *   1 <= batch <= 4, batch * d_in <= 32768, d_out <= 32768. Workspace: KRONQ_OP_ONLINE. */
+int kronq_online_matvec(const uint32_t* packed, int64_t ldp, const float* scales,
+                        const float* zeros, int64_t ldsz, int bits, int group, int64_t d_out,
+                        int64_t d_in, const float* mul_in, const float* mul_out,
+                        const float* q28_in, const float* q28_out, int flags, const void* x,
+                        int x_dtype, int64_t ldx, int64_t batch, float* y, int64_t ldy, void* ws,
+                        size_t ws_bytes, void* stream);
 
 /* ---- 6. K-FAC loss (Sec. 4.1 eq. kron_obj) -----------------------------------------------
  * loss = tr(H_G dW H_X dW^T) = sum_ij (H_G dW)_ij (dW H_X)_ij with dW = W - W_hat (W_hat NULL:

@@ -117,6 +117,23 @@ int rotate_launch(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64
 size_t rotate_drift_ws_bytes(int64_t d);
 int rotate_drift_launch(float* D, int64_t d, int64_t ldd, const float* sx, const int8_t* sign,
                         const float* q28, int flags, void* ws, hipStream_t s);
+// B vectors (rows of src) -> diag(post_col) T diag(pre_col) x, T the randomised Hadamard factor of
+// order n (transposed with q_trans) when transform, else the identity
+int rotate_vectors(const void* src, int dtype, int64_t lds, float* dst, int64_t ldd, int64_t rows,
+                   int64_t n, const float* pre_col, const float* post_col, bool transform,
+                   const float* q28, bool q_trans, hipStream_t s);
+// mul = sign / s (sign NULL: 1; s NULL: 1)
+int inverse_multipliers(const float* sv, const int8_t* sign, int64_t n, float* mul, hipStream_t s);
+// online inference: packed codes and the packed-code GEMV
+int pack_codes_launch(const uint8_t* codes, int64_t d_out, int64_t d_in, int64_t ldq, int bits,
+                      uint32_t* packed, int64_t ldp, hipStream_t s);
+size_t online_ws_bytes(int64_t d_out, int64_t d_in, int64_t batch);
+int online_matvec_launch(const uint32_t* packed, int64_t ldp, const float* scales,
+                         const float* zeros, int64_t ldsz, int bits, int group, int64_t d_out,
+                         int64_t d_in, const float* mul_in, const float* mul_out,
+                         const float* q28_in, const float* q28_out, int flags, const void* x,
+                         int x_dtype, int64_t ldx, int64_t batch, float* y, int64_t ldy, void* ws,
+                         hipStream_t s);
 // fp32 GEMM on MFMA: C = alpha * op(A) op(B) + beta * C
 enum GemmFlags : int {
   GEMM_TA = 1,          // op(A) = A^T (A stored [K x M])

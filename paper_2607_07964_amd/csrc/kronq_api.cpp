@@ -90,6 +90,8 @@ size_t kronq_workspace_bytes(int op, int64_t d_out, int64_t d_in, int64_t n_rows
       return kq::gptaq_ws_bytes(d_in);
     case KRONQ_OP_OBS_DRIFT:
       return kq::obs_ws_bytes(d_out, d_in, true);
+    case KRONQ_OP_ONLINE:
+      return kq::online_ws_bytes(d_out, d_in, n_rows);
     case KRONQ_OP_ROTATE:
       return kq::rotate_ws_bytes(d_out, d_in);
     case KRONQ_OP_CHOL:
@@ -265,6 +267,80 @@ int kronq_obs_quantize_layer_drift(float* W, int64_t d_out, int64_t d_in, int64_
   KQ_REQUIRE(P, KRONQ_ERR_INVALID_ARG, "P is NULL");
   return obs_common(W, d_out, d_in, ldw, U, ldu, P, ldp, bits, group, block, codes, scales, zeros,
                     err, W_hat, ws, ws_bytes, stream);
+}
+
+int kronq_pack_codes(const uint8_t* codes, int64_t d_out, int64_t d_in, int64_t ldq, int bits,
+                     uint32_t* packed, int64_t ldp, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(bits == 2 || bits == 3 || bits == 4 || bits == 8, KRONQ_ERR_UNSUPPORTED,
+             "bits must be 2, 3, 4 or 8");
+  KQ_REQUIRE(codes && packed && aligned(packed, 4), KRONQ_ERR_INVALID_ARG, "bad pointer");
+  KQ_REQUIRE(d_out >= 1 && d_in >= 32 && d_in % 32 == 0, KRONQ_ERR_SHAPE,
+             "need d_out >= 1 and d_in a positive multiple of 32");
+  KQ_REQUIRE(ldq >= d_in && ldp >= d_in * bits / 32, KRONQ_ERR_INVALID_ARG,
+             "bad leading dimension");
+  return kq::pack_codes_launch(codes, d_out, d_in, ldq, bits, packed, ldp, as_stream(stream));
+}
+
+int kronq_online_factors(const float* s, const int8_t* sign, int64_t d, float* mul, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(d >= 1 && mul && aligned(mul, 16), KRONQ_ERR_INVALID_ARG,
+             "mul must be a 16-byte aligned device pointer and d >= 1");
+  KQ_REQUIRE(!s || aligned(s, 4), KRONQ_ERR_INVALID_ARG, "misaligned s");
+  return kq::inverse_multipliers(s, sign, d, mul, as_stream(stream));
+}
+
+int kronq_online_matvec(const uint32_t* packed, int64_t ldp, const float* scales,
+                        const float* zeros, int64_t ldsz, int bits, int group, int64_t d_out,
+                        int64_t d_in, const float* mul_in, const float* mul_out,
+                        const float* q28_in, const float* q28_out, int flags, const void* x,
+                        int x_dtype, int64_t ldx, int64_t batch, float* y, int64_t ldy, void* ws,
+                        size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE((flags & ~KRONQ_BIIP) == 0, KRONQ_ERR_INVALID_ARG, "unknown flag bits 0x%x",
+             flags & ~KRONQ_BIIP);
+  KQ_REQUIRE(bits == 2 || bits == 3 || bits == 4 || bits == 8, KRONQ_ERR_UNSUPPORTED,
+             "bits must be 2, 3, 4 or 8");
+  KQ_REQUIRE(d_out >= 1 && d_in >= 128 && d_out <= (int64_t(1) << 24), KRONQ_ERR_INVALID_ARG,
+             "bad sizes");
+  KQ_REQUIRE(group >= 128 && group % 128 == 0 && d_in % group == 0, KRONQ_ERR_SHAPE,
+             "group must be a multiple of 128 dividing d_in");
+  KQ_REQUIRE(batch >= 1 && batch <= 4 && batch * d_in <= 32768, KRONQ_ERR_UNSUPPORTED,
+             "1 <= batch <= 4 and batch * d_in <= 32768 (the activations are held in LDS)");
+  KQ_REQUIRE(packed && aligned(packed, 16) && ldp % 4 == 0 && ldp >= d_in * bits / 32,
+             KRONQ_ERR_INVALID_ARG,
+             "packed must be 16-byte aligned with ldp >= d_in * bits / 32, divisible by 4");
+  KQ_REQUIRE(scales && zeros && aligned(scales, 4) && aligned(zeros, 4) && ldsz >= d_in / group,
+             KRONQ_ERR_INVALID_ARG, "bad scales or zeros");
+  KQ_REQUIRE(!mul_in || aligned(mul_in, 16), KRONQ_ERR_INVALID_ARG, "mul_in must be 16-byte aligned");
+  KQ_REQUIRE(!mul_out || aligned(mul_out, 16), KRONQ_ERR_INVALID_ARG,
+             "mul_out must be 16-byte aligned");
+  KQ_REQUIRE(x && valid_dtype(x_dtype) && ldx >= d_in && aligned(x, 16) &&
+                 ldx % (x_dtype == KRONQ_BF16 ? 8 : 4) == 0,
+             KRONQ_ERR_INVALID_ARG,
+             "x must be 16-byte aligned with ldx divisible by 8 (bf16) or 4 (fp32)");
+  KQ_REQUIRE(y && aligned(y, 16) && ldy >= d_out && ldy % 4 == 0, KRONQ_ERR_INVALID_ARG,
+             "y must be 16-byte aligned with ldy >= d_out divisible by 4");
+  if (flags & KRONQ_ROT_IN) {
+    const kq::RotDim r = kq::rot_dim(d_in);
+    KQ_REQUIRE(r.ok && d_in <= kMaxRotDim, KRONQ_ERR_UNSUPPORTED,
+               "input dimension %lld is not 2^k or 28*2^k", (long long)d_in);
+    KQ_REQUIRE(!r.has28 || (q28_in && aligned(q28_in, 4)), KRONQ_ERR_INVALID_ARG,
+               "input dimension 28 * 2^k needs the 28 x 28 factor");
+  }
+  if (flags & KRONQ_ROT_OUT) {
+    const kq::RotDim r = kq::rot_dim(d_out);
+    KQ_REQUIRE(r.ok && d_out <= kMaxRotDim, KRONQ_ERR_UNSUPPORTED,
+               "output dimension %lld is not 2^k or 28*2^k", (long long)d_out);
+    KQ_REQUIRE(!r.has28 || (q28_out && aligned(q28_out, 4)), KRONQ_ERR_INVALID_ARG,
+               "output dimension 28 * 2^k needs the 28 x 28 factor");
+  }
+  KQ_REQUIRE(d_out <= kMaxRotDim, KRONQ_ERR_UNSUPPORTED,
+             "d_out > %lld: an output vector must fit the LDS", (long long)kMaxRotDim);
+  KQ_TRY(check_ws(ws, ws_bytes, kq::online_ws_bytes(d_out, d_in, batch)));
+  return kq::online_matvec_launch(packed, ldp, scales, zeros, ldsz, bits, group, d_out, d_in,
+                                  mul_in, mul_out, q28_in, q28_out, flags, x, x_dtype, ldx, batch,
+                                  y, ldy, ws, as_stream(stream));
 }
 
 int kronq_layer_loss(const void* W, int w_dtype, int64_t ldw, const float* W_hat,

@@ -505,6 +505,22 @@ int col_transform(const float* src, int64_t lds_, float* dst, int64_t ldd, int64
 
 }  // namespace
 
+// rows of src (B vectors of length n) -> diag(post_col) T diag(pre_col) x, with T the randomised
+// Hadamard factor of order n (its transpose with q_trans) or the identity
+int rotate_vectors(const void* src, int dtype, int64_t lds_, float* dst, int64_t ldd, int64_t rows,
+                   int64_t n, const float* pre_col, const float* post_col, bool transform,
+                   const float* q28, bool q_trans, hipStream_t s) {
+  return launch_row_pass(src, dtype, lds_, dst, ldd, rows, n, nullptr, pre_col, nullptr, post_col,
+                         transform, rot_dim(n), q28, q_trans, s, "online_rot_pass");
+}
+
+// mul = sign / s (sign == nullptr: 1)
+int inverse_multipliers(const float* sv, const int8_t* sign, int64_t n, float* mul,
+                        hipStream_t s) {
+  return launch("online_factors", inv_factors, dim3(unsigned(cdiv(n, 256))), dim3(256), 0, s, n,
+                sv, sign, mul);
+}
+
 size_t rotate_drift_ws_bytes(int64_t d) {
   if (d <= 0) return 0;
   return align256(size_t(d) * sizeof(float)) + 256;

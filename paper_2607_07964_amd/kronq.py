@@ -22,7 +22,7 @@ RESCALE_IN, RESCALE_OUT, ROT_IN, ROT_OUT, INVERSE = 1, 2, 4, 8, 16
 HX_ONLY, SX_GIVEN = 32, 64
 BIIP = RESCALE_IN | RESCALE_OUT | ROT_IN | ROT_OUT
 OP_COV, OP_ROTATE, OP_CHOL, OP_OBS, OP_LOSS = 1, 2, 3, 4, 5
-OP_CROSS, OP_ROTATE_DRIFT, OP_GPTAQ, OP_OBS_DRIFT = 6, 7, 8, 9
+OP_CROSS, OP_ROTATE_DRIFT, OP_GPTAQ, OP_OBS_DRIFT, OP_ONLINE = 6, 7, 8, 9, 10
 ERRORS = {0: "OK", -1: "INVALID_ARG", -2: "SHAPE", -3: "NOT_PD", -4: "HIP", -5: "WORKSPACE",
           -6: "UNSUPPORTED"}
 
@@ -31,7 +31,8 @@ EXPORTS = (
     "kronq_traces", "kronq_rotate", "kronq_cholesky_inv", "kronq_obs_quantize_layer",
     "kronq_layer_loss", "kronq_allocate_bits", "kronq_profile_enable", "kronq_profile_only",
     "kronq_profile_reset", "kronq_profile_read", "kronq_accumulate_cross", "kronq_rotate_drift",
-    "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift",
+    "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift", "kronq_pack_codes",
+    "kronq_online_factors", "kronq_online_matvec",
 )
 
 
@@ -64,6 +65,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_gptaq_correction": (I, [P, I64, I64, P, I64, F, P, I64, P, SZ, P]),
         "kronq_obs_quantize_layer_drift": (I, [P, I64, I64, I64, P, I64, P, I64, I, I, I, P, P, P,
                                                P, P, P, SZ, P]),
+        "kronq_pack_codes": (I, [P, I64, I64, I64, I, P, I64, P]),
+        "kronq_online_factors": (I, [P, P, I64, P, P]),
+        "kronq_online_matvec": (I, [P, I64, P, P, I64, I, I, I64, I64, P, P, P, P, I, P, I, I64,
+                                    I64, P, I64, P, SZ, P]),
         "kronq_traces": (I, [P, I64, I64, P, I64, I64, P, P]),
         "kronq_rotate": (I, [P, I, I64, P, I64, I64, I64, P, I64, P, I64, P, P, P, P, P, P, I, P,
                              SZ, P]),
@@ -271,6 +276,55 @@ def kronq_obs_quantize_layer_drift(W: torch.Tensor, U: torch.Tensor, P: torch.Te
         _ptr(codes), _ptr(scales), _ptr(zeros), _ptr(err), _ptr(W_hat), _ptr(ws), ws.numel(),
         _stream(W.device))
     _check(rc, "kronq_obs_quantize_layer_drift")
+
+
+def kronq_pack_codes(codes: torch.Tensor, bits: int, packed: Optional[torch.Tensor] = None
+                     ) -> torch.Tensor:
+    """Packed uint32 storage [d_out x d_in * bits / 32] (as int32) of uint8 codes."""
+    _dev(codes, packed)
+    d_out, d_in = codes.shape
+    if packed is None:
+        packed = torch.empty(d_out, d_in * bits // 32, dtype=torch.int32, device=codes.device)
+    rc = load().kronq_pack_codes(_ptr(codes), d_out, d_in, _ld(codes), bits, _ptr(packed),
+                                 _ld(packed), _stream(codes.device))
+    _check(rc, "kronq_pack_codes")
+    return packed
+
+
+def kronq_online_factors(s: Optional[torch.Tensor], sign: Optional[torch.Tensor], d: int,
+                         mul: Optional[torch.Tensor] = None, device=None) -> torch.Tensor:
+    """mul = sign / s (the multipliers of the online transforms)."""
+    _dev(s, sign, mul)
+    dev = device or (s if s is not None else sign).device
+    if mul is None:
+        mul = torch.empty(d, dtype=torch.float32, device=dev)
+    rc = load().kronq_online_factors(_ptr(s), _ptr(sign), d, _ptr(mul), _stream(mul.device))
+    _check(rc, "kronq_online_factors")
+    return mul
+
+
+def kronq_online_matvec(packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor,
+                        bits: int, group: int, d_in: int, mul_in: Optional[torch.Tensor],
+                        mul_out: Optional[torch.Tensor], q28_in: Optional[torch.Tensor],
+                        q28_out: Optional[torch.Tensor], x: torch.Tensor,
+                        y: Optional[torch.Tensor] = None, flags: int = BIIP,
+                        ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """y = diag(mul_out) T_out W_hat' T_in diag(mul_in) x for the rows of x [batch x d_in]."""
+    _dev(packed, scales, zeros, mul_in, mul_out, q28_in, q28_out, x, y)
+    d_out = packed.shape[0]
+    if x.dim() == 1:
+        x = x.view(1, -1)
+    batch = x.shape[0]
+    if y is None:
+        y = torch.empty(batch, d_out, dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = workspace(OP_ONLINE, d_out, d_in, batch, x.device)
+    rc = load().kronq_online_matvec(
+        _ptr(packed), _ld(packed), _ptr(scales), _ptr(zeros), _ld(scales), bits, group, d_out,
+        d_in, _ptr(mul_in), _ptr(mul_out), _ptr(q28_in), _ptr(q28_out), flags, _ptr(x),
+        _dtype_code(x), _ld(x), batch, _ptr(y), _ld(y), _ptr(ws), ws.numel(), _stream(x.device))
+    _check(rc, "kronq_online_matvec")
+    return y
 
 
 def kronq_layer_loss(W: torch.Tensor, W_hat: Optional[torch.Tensor], HX: torch.Tensor,
