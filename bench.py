@@ -7,6 +7,8 @@ rotations of W, H_X, H_G), traces, damping + inverse-Cholesky factor, lazy-block
 group quantisation. Default workload: the LLaMA-3-8B q_proj shape, W 4096 x 4096, 262144 tokens
 (128 x 2048), 4-bit, group 128. --drift adds the drift correction (KronQ+GPTAQ: D = dX^T X, its
 BiIP, P and the drift-corrected sweep); --group sets the quantisation group (0: per-channel).
+--online times the inference side instead: one decode matvec of the quantised layer with the
+rotations applied online (kronq_online_matvec), against a dense bf16 GEMV of the same shape.
 
 The JSON line carries
   * roofline: the covariance syrk (the dominant kernel; with --drift the drift statistic's
@@ -98,6 +100,90 @@ def cpu_baseline(spec, rot_in, rot_out, n_sample: int, X_dev, G_dev, W_dev, dX_d
     }
 
 
+def online_bench(args, spec, dev) -> int:
+    """Decode matvec of a quantised layer (online rotations + packed-code GEMV), batch 1."""
+    import torch
+
+    import synth
+    from paper_2607_07964_amd import kronq as K
+    from paper_2607_07964_amd import layer as L
+
+    d_out, d_in, bits = spec.d_out, spec.d_in, spec.bits
+    group = args.group if args.group > 0 else d_in
+    g = torch.Generator(device=dev)
+    g.manual_seed(spec.seed)
+    codes = torch.randint(0, 2 ** bits, (d_out, d_in), generator=g, device=dev, dtype=torch.uint8)
+    scales = torch.rand(d_out, d_in // group, generator=g, device=dev) * 0.01 + 0.005
+    zeros = torch.randint(0, 2 ** bits, (d_out, d_in // group), generator=g,
+                          device=dev).float()
+    ri = synth.rotation_params(d_in, spec.seed, spec.name + ":in")
+    ro = synth.rotation_params(d_out, spec.seed, spec.name + ":out")
+    rin = L.RotParams.to_device(ri.sign, ri.q28, dev)
+    rout = L.RotParams.to_device(ro.sign, ro.q28, dev)
+    sx = torch.rand(d_in, generator=g, device=dev) + 0.5
+    sg = torch.rand(d_out, generator=g, device=dev) + 0.5
+    mul_in = K.kronq_online_factors(sx, rin.sign, d_in)
+    mul_out = K.kronq_online_factors(sg, rout.sign, d_out)
+    packed = K.kronq_pack_codes(codes, bits)
+    x = torch.randn(1, d_in, generator=g, device=dev).to(torch.bfloat16)
+    y = torch.empty(1, d_out, device=dev)
+    ws = K.workspace(K.OP_ONLINE, d_out, d_in, 1, dev)
+    Wd = torch.randn(d_out, d_in, generator=g, device=dev).to(torch.bfloat16)  # dense baseline
+
+    def step():
+        K.kronq_online_matvec(packed, scales, zeros, bits, group, d_in, mul_in, mul_out, rin.q28,
+                              rout.q28, x, y, ws=ws)
+
+    def timed(fn, n):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    reps = max(args.steps, 1) * 100
+    warm = max(args.warmup, 1) * 20
+    for _ in range(warm):
+        step()
+    K.kronq_profile_only("online_gemv")
+    K.kronq_profile_reset()
+    K.kronq_profile_enable(True)
+    timed(step, reps)
+    K.kronq_profile_enable(False)
+    g_ms, g_n = K.kronq_profile_read("online_gemv")
+    gemv_ms = g_ms / max(g_n, 1)
+    ms = timed(step, reps)  # without the profiler's events around the GEMV
+    for _ in range(warm):
+        torch.nn.functional.linear(x, Wd)
+    dense_ms = timed(lambda: torch.nn.functional.linear(x, Wd), reps)
+    # algorithmic HBM bytes of the GEMV kernel: packed codes, scales and zeros, x' and y'
+    gbytes = d_out * d_in * bits / 8 + 2 * 4 * d_out * (d_in // group) + 4 * d_in + 4 * d_out
+    achieved = gbytes / (gemv_ms * 1e-3) / 1e9
+    print(f"[bench] online matvec {ms * 1e3:.2f} us (GEMV kernel {gemv_ms * 1e3:.2f} us), "
+          f"dense bf16 GEMV {dense_ms * 1e3:.2f} us", file=sys.stderr, flush=True)
+    out = {
+        "metric": "microseconds per decode matvec of a quantised layer (online rotations + "
+                  "packed-code GEMV, batch 1)",
+        "value": round(ms * 1e3, 3), "unit": "us", "n_gpus": 1, "steps": reps, "warmup": warm,
+        "ms_per_step": round(ms, 6), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": f"u{bits} codes, fp32 arithmetic", "data": "synthetic",
+        "config": {"workload": f"{spec.name} W {d_out}x{d_in}, {bits}-bit, group {group}, "
+                               f"decode batch 1", "d_out": d_out, "d_in": d_in, "bits": bits,
+                   "group": group, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": 8000.0,
+                     "unit": "GB/s", "frac": round(achieved / 8000.0, 4), "traffic": None,
+                     "kernel": "online_gemv", "launches": g_n,
+                     "avg_launch_ms": round(gemv_ms, 6)},
+        "dense_bf16_gemv_us": round(dense_ms * 1e3, 3),
+        "speedup_vs_dense_bf16": round(dense_ms / ms, 3),
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +201,8 @@ def main() -> int:
     ap.add_argument("--alpha", type=float, default=1.0, help="drift correction scaling")
     ap.add_argument("--group", type=int, default=128,
                     help="quantisation group (a multiple of 128 dividing d_in; 0: per-channel)")
+    ap.add_argument("--online", action="store_true",
+                    help="time the inference-side decode matvec of the quantised layer instead")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run 3 plain 1 GiB device copies (reference for counter scaling)")
     args = ap.parse_args()
@@ -141,6 +229,8 @@ def main() -> int:
         del src, dst
         print("[bench] calibration copies done: 3 x 1 GiB", file=sys.stderr, flush=True)
     spec = synth.workload(WORKLOADS[args.workload])
+    if args.online:
+        return online_bench(args, spec, dev)
     print(f"[bench] generating {spec.name}: W {spec.d_out}x{spec.d_in}, N={spec.n_tokens}",
           file=sys.stderr, flush=True)
     X = synth.gen_matrix(spec.x, dev)

@@ -170,36 +170,37 @@ __device__ __forceinline__ void hadamard_reg(float* x) {
       }
 }
 
-// One group of up to 3 butterfly stages (strides h, 2h, 4h) over a buffer of n floats in LDS,
-// segments of length m. `stride` is the LDS distance between consecutive vector elements.
+// One group of up to 3 butterfly stages (strides h, 2h, 4h; h = 2^lgh) over a buffer of n
+// floats in LDS (n <= 2^24, so 32-bit indices; shifts and masks instead of divisions).
 template <int R>
-__device__ __forceinline__ void fwht_stage_group(float* buf, int64_t n, int64_t h, int tid,
+__device__ __forceinline__ void fwht_stage_group(float* buf, int n, int lgh, int tid,
                                                  int nthreads) {
-  const int64_t groups = n / R;
-  for (int64_t q = tid; q < groups; q += nthreads) {
-    const int64_t base = (q / h) * (R * h) + (q % h);
+  const int groups = n / R, hm = (1 << lgh) - 1;
+  for (int q = tid; q < groups; q += nthreads) {
+    const int base = (q >> lgh) * (R << lgh) + (q & hm);
     float x[R];
 #pragma unroll
-    for (int k = 0; k < R; ++k) x[k] = buf[base + k * h];
+    for (int k = 0; k < R; ++k) x[k] = buf[base + (k << lgh)];
     hadamard_reg<R>(x);
 #pragma unroll
-    for (int k = 0; k < R; ++k) buf[base + k * h] = x[k];
+    for (int k = 0; k < R; ++k) buf[base + (k << lgh)] = x[k];
   }
 }
 
+// FWHT of every length-m segment (m a power of 2) of buf[0, n)
 __device__ void fwht_lds(float* buf, int64_t n, int64_t m, int tid, int nthreads) {
-  int64_t h = 1;
-  while (h < m) {
-    const int64_t left = m / h;
+  int lgh = 0;
+  while ((int64_t(1) << lgh) < m) {
+    const int64_t left = m >> lgh;
     if (left >= 8) {
-      fwht_stage_group<8>(buf, n, h, tid, nthreads);
-      h *= 8;
+      fwht_stage_group<8>(buf, int(n), lgh, tid, nthreads);
+      lgh += 3;
     } else if (left == 4) {
-      fwht_stage_group<4>(buf, n, h, tid, nthreads);
-      h *= 4;
+      fwht_stage_group<4>(buf, int(n), lgh, tid, nthreads);
+      lgh += 2;
     } else {
-      fwht_stage_group<2>(buf, n, h, tid, nthreads);
-      h *= 2;
+      fwht_stage_group<2>(buf, int(n), lgh, tid, nthreads);
+      lgh += 1;
     }
     __syncthreads();
   }
@@ -327,18 +328,20 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
     }
   }
   const int cw4 = CW / 4;
+  int lcw4 = 0;  // CW is a power of 2 (32, 64 or 256): shifts instead of divisions
+  while ((1 << lcw4) < cw4) ++lcw4;
   // load the L x CW tile: 8 independent float4 loads in flight per thread before they are
   // stored (one workgroup per CU at L = 1024, so latency must be hidden within the thread)
-  const int64_t n_items = L * cw4;
-  for (int64_t it0 = tid; it0 < n_items; it0 += 8 * CP_THREADS) {
+  const int n_items = int(L) * cw4;
+  for (int it0 = tid; it0 < n_items; it0 += 8 * CP_THREADS) {
     float4 x[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int64_t it = it0 + int64_t(u) * CP_THREADS;
+      const int it = it0 + u * CP_THREADS;
       x[u] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (it < n_items) {
-        const int64_t a = it / cw4;
-        const int c = int(it % cw4) * 4;
+        const int64_t a = it >> lcw4;
+        const int c = (it & (cw4 - 1)) * 4;
         const int64_t gr = row0 + a * n_lo;
         const int64_t gc = c0 + c;
         const float* p = src + gr * lds_;
@@ -354,23 +357,25 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int64_t it = it0 + int64_t(u) * CP_THREADS;
+      const int it = it0 + u * CP_THREADS;
       if (it < n_items)
-        *reinterpret_cast<float4*>(tile + (it / cw4) * CWP + int(it % cw4) * 4) = x[u];
+        *reinterpret_cast<float4*>(tile + (it >> lcw4) * CWP + (it & (cw4 - 1)) * 4) = x[u];
     }
   }
   __syncthreads();
   if (kind == 0) {
     // butterflies along a, items (group q, column c)
-    int64_t h = 1;
-    while (h < L) {
-      const int64_t left = L / h;
+    const int lcw = lcw4 + 2;
+    int lgh = 0;
+    while ((int64_t(1) << lgh) < L) {
+      const int64_t left = L >> lgh;
       const int R = left >= 8 ? 8 : (left == 4 ? 4 : 2);
-      const int64_t items = (L / R) * CW;
-      for (int64_t it = tid; it < items; it += CP_THREADS) {
-        const int64_t q = it / CW;
-        const int c = int(it % CW);
-        const int64_t base = (q / h) * (R * h) + (q % h);
+      const int h = 1 << lgh;
+      const int items = int(L / R) * CW;
+      for (int it = tid; it < items; it += CP_THREADS) {
+        const int q = it >> lcw;
+        const int c = it & (CW - 1);
+        const int base = (q >> lgh) * (R << lgh) + (q & (h - 1));
         float x[8];
         if (R == 8) {
 #pragma unroll
@@ -391,12 +396,12 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
           tile[(base + h) * CWP + c] = x[0] - x[1];
         }
       }
-      h *= R;
+      lgh += R == 8 ? 3 : (R == 4 ? 2 : 1);
       __syncthreads();
     }
-    for (int64_t it = tid; it < L * cw4; it += CP_THREADS) {
-      const int64_t a = it / cw4;
-      const int c = int(it % cw4) * 4;
+    for (int it = tid; it < n_items; it += CP_THREADS) {
+      const int64_t a = it >> lcw4;
+      const int c = (it & (cw4 - 1)) * 4;
       const int64_t gr = row0 + a * n_lo;
       const int64_t gc = c0 + c;
       float4 x = *reinterpret_cast<const float4*>(tile + a * CWP + c);
