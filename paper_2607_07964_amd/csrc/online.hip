@@ -11,8 +11,14 @@
 //   2. y' = W_hat' x': the packed-code GEMV, bound by the HBM reads of the codes.
 // Packed format: each run of 32 consecutive codes of a row is one 32 * bits-bit little-endian
 // string held in `bits` uint32 words.
-// GEMV: a workgroup takes 4 * RPW rows, RPW per wave, and stages x' (B x d_in fp32, B <= 4 per
-// launch) in LDS. Lane l
+// GEMV with 2- and 4-bit codes (online_gemv_int): the input transform also writes x' as
+// three byte digits per element, a 21-bit fixed point with one exponent per 32-column chunk
+// (relative precision 2^-21 of the chunk's largest value), in the byte order in which the GEMV
+// extracts codes from a packed word with one shift and one mask. Each code byte group then meets
+// the digits in three integer dot4 products with exact sums, about 1.1 instructions per code
+// against 3.5 for the fp32 dequantise-and-FMA, which made the GEMV ALU-bound.
+// GEMV with 3- and 8-bit codes (online_gemv): a workgroup takes 4 * RPW rows, RPW per wave, and
+// stages x' (B x d_in fp32, B <= 4 per launch) in LDS. Lane l
 // takes steps of 32 * UPL columns (UPL = 2 at 2 bits, so every code load is 16 bytes) at a
 // stride of 64 steps. A decode matvec moves little data per CU, so latency is the limit: a lane
 // requests the codes of up to MAXU steps of its RPW rows at once, before x' is staged, and only
@@ -223,15 +229,47 @@ int gemv_bits(int nb, const uint32_t* packed, int64_t ldp, const float* scales,
   return KRONQ_OK;
 }
 
+// Digits of x' for the integer GEMV: per chunk of 32 columns, X_j = rint(x'_j 2^(21 - e)) with
+// |x'_j| < 2^e over the chunk, split as X = d0 65536 + d1 256 + d2 (d0 = X >> 16 signed,
+// d1, d2 unsigned bytes). The bytes are stored in the order the GEMV extracts codes from a packed
+// word: digit dword (w, g) of a chunk holds the digits of the columns w * cpw + g + i * (8 / bits),
+// i = 0..3 (cpw = 32 / bits codes per word), in bytes i; a chunk has 3 x 8 such dwords. Also the
+// exponent e and the sum of the quantised chunk, sum_j X_j 2^(e - 21).
+__device__ __forceinline__ void emit_digits(float v, int64_t col, int lane32, int bits,
+                                            uint8_t* __restrict__ dig, int* __restrict__ dexp,
+                                            float* __restrict__ dsum) {
+  float mx = fabsf(v);
+#pragma unroll
+  for (int o = 1; o < 32; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 32));
+  // |v| < 2^e from the exponent field (chunks below 2^-100 are taken as zero)
+  const int e = max(int((__float_as_uint(mx) >> 23) & 0xFFu) - 126, -100);
+  const float up = __uint_as_float(uint32_t(127 + 21 - e) << 23);  // 2^(21 - e)
+  const int X = int(rintf(v * up));                                  // |X| <= 2^21
+  int sx = X;
+#pragma unroll
+  for (int o = 1; o < 32; o <<= 1) sx += __shfl_xor(sx, o, 32);
+  const int64_t c = col >> 5;
+  const int j = int(col & 31), cpw = 32 / bits, per = 8 / bits;
+  const int w = j / cpw, rem = j % cpw, g = rem % per, i = rem / per;
+  uint8_t* base = dig + c * 96 + (w * per + g) * 4 + i;
+  base[0] = uint8_t(X >> 16);   // d0, signed byte
+  base[32] = uint8_t(X >> 8);   // d1
+  base[64] = uint8_t(X);        // d2
+  if (lane32 == 0) {
+    dexp[c] = e;
+    dsum[c] = float(sx) / up;  // exact: a division by a power of two
+  }
+}
+
 // Transform of B vectors of order d = L m: out[b] = diag(post) (A (x) H_m) diag(pre) src[b] * norm
 // (A = Q28 or Q28^T when has28, else the Sylvester H_L). Workgroup (a, b): segment a of vector b.
+// With dig != nullptr (and m a multiple of 32) it also writes the digits of the result.
 template <typename T>
-__global__ __launch_bounds__(1024) void seg_transform(const T* __restrict__ src, int64_t lds_,
-                                                      float* __restrict__ dst, int64_t ldd, int L,
-                                                      int m, const float* __restrict__ pre,
-                                                      const float* __restrict__ post,
-                                                      const float* __restrict__ q28, int q_trans,
-                                                      int has28, float norm) {
+__global__ __launch_bounds__(1024) void seg_transform(
+    const T* __restrict__ src, int64_t lds_, float* __restrict__ dst, int64_t ldd, int L, int m,
+    const float* __restrict__ pre, const float* __restrict__ post, const float* __restrict__ q28,
+    int q_trans, int has28, float norm, uint8_t* __restrict__ dig, int* __restrict__ dexp,
+    float* __restrict__ dsum, int64_t ldc, int bits) {
   __shared__ float t[1024];
   __shared__ float arow[32];
   const int a = blockIdx.x, tid = threadIdx.x;
@@ -241,13 +279,18 @@ __global__ __launch_bounds__(1024) void seg_transform(const T* __restrict__ src,
                       : ((__popc(unsigned(a & tid)) & 1) ? -1.f : 1.f);
   __syncthreads();
   if (tid < m) {
+    float v[32];  // all L loads in flight before the first use
+#pragma unroll
+    for (int k = 0; k < 32; ++k)
+      if (k < L) {
+        const int64_t idx = int64_t(k) * m + tid;
+        v[k] = ld_f32(x, idx);
+        if (pre) v[k] *= pre[idx];
+      }
     float acc = 0.f;
-    for (int k = 0; k < L; ++k) {
-      const int64_t idx = int64_t(k) * m + tid;
-      float v = ld_f32(x, idx);
-      if (pre) v *= pre[idx];
-      acc = fmaf(arow[k], v, acc);
-    }
+#pragma unroll
+    for (int k = 0; k < 32; ++k)
+      if (k < L) acc = fmaf(arow[k], v[k], acc);
     t[tid] = acc;
   }
   __syncthreads();
@@ -255,9 +298,9 @@ __global__ __launch_bounds__(1024) void seg_transform(const T* __restrict__ src,
     const int h = 1 << lh;
     if (tid < m / 2) {
       const int i = ((tid >> lh) << (lh + 1)) + (tid & (h - 1));
-      const float u = t[i], v = t[i + h];
-      t[i] = u + v;
-      t[i + h] = u - v;
+      const float u = t[i], w = t[i + h];
+      t[i] = u + w;
+      t[i + h] = u - w;
     }
     __syncthreads();
   }
@@ -266,15 +309,147 @@ __global__ __launch_bounds__(1024) void seg_transform(const T* __restrict__ src,
     float v = t[tid] * norm;
     if (post) v *= post[idx];
     dst[int64_t(blockIdx.y) * ldd + idx] = v;
+    if (dig) {
+      const int64_t cb = int64_t(blockIdx.y) * ldc;  // chunks per vector
+      emit_digits(v, idx, tid & 31, bits, dig + cb * 96, dexp + cb, dsum + cb);
+    }
   }
 }
 
-// launch seg_transform for B rows of order d (identity scaling when !rotate)
+// digits of B fp32 vectors of length d (a multiple of 32) that no transform produced
+__global__ __launch_bounds__(256) void digitize(const float* __restrict__ src, int64_t d, int bits,
+                                                uint8_t* __restrict__ dig, int* __restrict__ dexp,
+                                                float* __restrict__ dsum, int64_t ldc) {
+  const int64_t col = int64_t(blockIdx.x) * 256 + threadIdx.x;  // d % 32 == 0: whole chunks
+  if (col - (threadIdx.x & 31) >= d) return;                     // uniform per 32 lanes
+  const int64_t b = blockIdx.y, cb = b * ldc;
+  emit_digits(src[b * d + col], col, int(threadIdx.x & 31), bits, dig + cb * 96, dexp + cb,
+              dsum + cb);
+}
+
+// Packed-code GEMV with the activations as digits (2- and 4-bit codes): per chunk of 32 columns
+// and row, the code bytes of each packed word (groups g: (word >> bits g) & byte mask) meet the
+// digit dwords in three dot4 products (d0 signed, d1 and d2 unsigned), exact integer sums, and
+// sum_j q_j x'_j = 2^(e - 21) (65536 I0 + 256 I1 + I2).
+template <int BITS, int NB, int RPW>
+__global__ __launch_bounds__(256) void online_gemv_int(
+    const uint32_t* __restrict__ packed, int64_t ldp, const float* __restrict__ scales,
+    const float* __restrict__ zeros, int64_t ldsz, int group, int64_t d_out, int64_t d_in,
+    const uint32_t* __restrict__ dig, const int* __restrict__ dexp,
+    const float* __restrict__ dsum, float* __restrict__ yr, int64_t ldyr) {
+  constexpr int UPL = BITS == 2 ? 2 : 1;  // chunks per lane step (16-byte code loads)
+  constexpr int PER = 8 / BITS;           // byte groups per code word
+  constexpr uint32_t BM = BITS == 2 ? 0x03030303u : 0x0F0F0F0Fu;
+  extern __shared__ __attribute__((aligned(16))) uint32_t sm[];
+  const int64_t nch = d_in / 32;
+  uint32_t* sd = sm;                                   // NB x nch x 24 digit dwords
+  int* se = reinterpret_cast<int*>(sm + NB * nch * 24);  // NB x nch exponents
+  float* ss = reinterpret_cast<float*>(se + NB * nch);  // NB x nch chunk sums
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t row0 = (int64_t(blockIdx.x) * 4 + wave) * RPW;
+  const int64_t steps = nch / UPL;
+  float acc[RPW][NB];
+#pragma unroll
+  for (int r = 0; r < RPW; ++r)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[r][b] = 0.f;
+  for (int64_t base = 0; base < steps; base += 128) {  // 2 lane steps per chunk of work
+    uint32_t w[2][RPW][4];  // 16 bytes of codes per row and lane step
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int64_t st = base + lane + 64 * q;
+      if (st < steps) {
+#pragma unroll
+        for (int r = 0; r < RPW; ++r) {
+          const int64_t row = row0 + r < d_out ? row0 + r : d_out - 1;
+          const uint4 v = *reinterpret_cast<const uint4*>(packed + row * ldp + st * 4);
+          w[q][r][0] = v.x, w[q][r][1] = v.y, w[q][r][2] = v.z, w[q][r][3] = v.w;
+        }
+      }
+    }
+    if (base == 0) {  // the same for every thread of the workgroup
+      for (int64_t i = tid; i < NB * nch * 6; i += 256)
+        reinterpret_cast<uint4*>(sd)[i] = reinterpret_cast<const uint4*>(dig)[i];
+      for (int64_t i = tid; i < NB * nch; i += 256) {
+        se[i] = dexp[i];
+        ss[i] = dsum[i];
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int64_t st = base + lane + 64 * q;
+      if (st < steps) {
+#pragma unroll
+        for (int u = 0; u < UPL; ++u) {
+          const int64_t c = st * UPL + u, g = (c * 32) / group;
+          float sc[RPW], ze[RPW];
+#pragma unroll
+          for (int r = 0; r < RPW; ++r) {
+            const int64_t row = row0 + r < d_out ? row0 + r : d_out - 1;
+            sc[r] = scales[row * ldsz + g];
+            ze[r] = zeros[row * ldsz + g];
+          }
+#pragma unroll
+          for (int b = 0; b < NB; ++b) {
+            const uint32_t* dd = sd + (b * nch + c) * 24;
+            uint32_t d0[8], d1[8], d2[8];
+#pragma unroll
+            for (int k = 0; k < 8; k += 4) {
+              const uint4 x0 = *reinterpret_cast<const uint4*>(dd + k);
+              const uint4 x1 = *reinterpret_cast<const uint4*>(dd + 8 + k);
+              const uint4 x2 = *reinterpret_cast<const uint4*>(dd + 16 + k);
+              d0[k] = x0.x, d0[k + 1] = x0.y, d0[k + 2] = x0.z, d0[k + 3] = x0.w;
+              d1[k] = x1.x, d1[k + 1] = x1.y, d1[k + 2] = x1.z, d1[k + 3] = x1.w;
+              d2[k] = x2.x, d2[k + 1] = x2.y, d2[k + 2] = x2.z, d2[k + 3] = x2.w;
+            }
+            const float e = __uint_as_float(uint32_t(127 - 21 + se[b * nch + c]) << 23);
+            const float xs = ss[b * nch + c];
+#pragma unroll
+            for (int r = 0; r < RPW; ++r) {
+              int i0 = 0;
+              uint32_t i1 = 0u, i2 = 0u;
+#pragma unroll
+              for (int wi = 0; wi < BITS; ++wi) {  // the chunk's code words
+                const uint32_t word = w[q][r][u * BITS + wi];
+#pragma unroll
+                for (int gg = 0; gg < PER; ++gg) {
+                  const uint32_t by = (word >> (BITS * gg)) & BM;
+                  const int slot = wi * PER + gg;
+                  i0 = __builtin_amdgcn_sdot4(int(by), int(d0[slot]), i0, false);
+                  i1 = __builtin_amdgcn_udot4(by, d1[slot], i1, false);
+                  i2 = __builtin_amdgcn_udot4(by, d2[slot], i2, false);
+                }
+              }
+              const float dot =
+                  e * fmaf(float(i0), 65536.f, fmaf(float(i1), 256.f, float(i2)));
+              acc[r][b] = fmaf(sc[r], fmaf(-ze[r], xs, dot), acc[r][b]);
+            }
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < RPW; ++r)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      float v = acc[r][b];
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+      if (lane == 0 && row0 + r < d_out) yr[b * ldyr + row0 + r] = v;
+    }
+}
+
+// launch seg_transform for B rows of order d (identity scaling when !rotate); with dig, also the
+// digits of the result (for chunk-aligned segments, else by a separate pass)
 int seg_transform_launch(const void* src, int dtype, int64_t lds_, float* dst, int64_t ldd,
                          int64_t batch, int64_t d, const float* pre, const float* post,
-                         bool rotate, const float* q28, bool q_trans, hipStream_t s) {
-  int L, m, has28 = 0;
-  float norm;
+                         bool rotate, const float* q28, bool q_trans, hipStream_t s,
+                         uint8_t* dig = nullptr, int* dexp = nullptr, float* dsum = nullptr,
+                         int bits = 0) {
+  int L = 0, m = 0, has28 = 0;
+  float norm = 1.f;
   const RotDim rd = rot_dim(d);
   if (rotate && rd.has28) {
     L = 28, m = int(rd.m), has28 = 1;
@@ -282,18 +457,65 @@ int seg_transform_launch(const void* src, int dtype, int64_t lds_, float* dst, i
   } else if (rotate) {
     m = int(d < 1024 ? d : 1024), L = int(d / m);
     norm = float(1.0 / std::sqrt(double(d)));
-  } else {  // no rotation: L = 1 segment of d <= 1024, or the identity as L x m with A = I
-    return rotate_vectors(src, dtype, lds_, dst, ldd, batch, d, pre, post, false, nullptr, false,
-                          s);
   }
-  const dim3 grid(static_cast<unsigned>(L), static_cast<unsigned>(batch));
-  if (dtype == KRONQ_BF16)
-    return launch("online_transform", seg_transform<uint16_t>, grid, dim3(1024), 0, s,
-                  static_cast<const uint16_t*>(src), lds_, dst, ldd, L, m, pre, post, q28,
-                  int(q_trans), has28, norm);
-  return launch("online_transform", seg_transform<float>, grid, dim3(1024), 0, s,
-                static_cast<const float*>(src), lds_, dst, ldd, L, m, pre, post, q28,
-                int(q_trans), has28, norm);
+  const int64_t nch = d / 32;
+  const bool fused = dig && rotate && m % 32 == 0;
+  if (!rotate) {
+    KQ_TRY(rotate_vectors(src, dtype, lds_, dst, ldd, batch, d, pre, post, false, nullptr, false,
+                          s));
+  } else {
+    const dim3 grid(static_cast<unsigned>(L), static_cast<unsigned>(batch));
+    uint8_t* dg = fused ? dig : nullptr;
+    if (dtype == KRONQ_BF16)
+      KQ_TRY(launch("online_transform", seg_transform<uint16_t>, grid, dim3(1024), 0, s,
+                    static_cast<const uint16_t*>(src), lds_, dst, ldd, L, m, pre, post, q28,
+                    int(q_trans), has28, norm, dg, dexp, dsum, nch, bits));
+    else
+      KQ_TRY(launch("online_transform", seg_transform<float>, grid, dim3(1024), 0, s,
+                    static_cast<const float*>(src), lds_, dst, ldd, L, m, pre, post, q28,
+                    int(q_trans), has28, norm, dg, dexp, dsum, nch, bits));
+  }
+  if (dig && !fused)
+    KQ_TRY(launch("online_digitize", digitize,
+                  dim3(static_cast<unsigned>(cdiv(d, 256)), static_cast<unsigned>(batch)),
+                  dim3(256), 0, s, static_cast<const float*>(dst), d, bits, dig, dexp, dsum,
+                  nch));
+  return KRONQ_OK;
+}
+
+// the integer GEMV over the batch in chunks of 4, 2 and 1 vectors
+template <int BITS>
+int gemv_int(int nb, const uint32_t* packed, int64_t ldp, const float* scales,
+             const float* zeros, int64_t ldsz, int group, int64_t d_out, int64_t d_in,
+             const uint8_t* dig, const int* dexp, const float* dsum, float* yr, hipStream_t s) {
+  const int64_t nch = d_in / 32;
+  int b = 0;
+  while (b < nb) {
+    const int k = nb - b >= 4 ? 4 : (nb - b >= 2 ? 2 : 1);
+    const uint32_t* dg = reinterpret_cast<const uint32_t*>(dig + int64_t(b) * nch * 96);
+    const int* de = dexp + int64_t(b) * nch;
+    const float* ds = dsum + int64_t(b) * nch;
+    float* y = yr + int64_t(b) * d_out;
+    const size_t lds = size_t(k) * size_t(nch) * (96 + 8);
+    // rows per wave (measured on the 70B up_proj shape): 4 for one vector of 2-bit codes when
+    // that still gives 512 workgroups, else 2
+    const bool four = BITS == 2 && k == 1 && cdiv(d_out, 16) >= 512;
+    const dim3 grid(static_cast<unsigned>(cdiv(d_out, four ? 16 : 8)));
+#define KQ_GEMV_INT(NB_, RPW_)                                                                 \
+  launch("online_gemv", online_gemv_int<BITS, NB_, RPW_>, grid, dim3(256), lds, s, packed, ldp, \
+         scales, zeros, ldsz, group, d_out, d_in, dg, de, ds, y, d_out)
+    if (k == 4)
+      KQ_TRY(KQ_GEMV_INT(4, 2));
+    else if (k == 2)
+      KQ_TRY(KQ_GEMV_INT(2, 2));
+    else if (four)
+      KQ_TRY(KQ_GEMV_INT(1, 4));
+    else
+      KQ_TRY(KQ_GEMV_INT(1, 2));
+#undef KQ_GEMV_INT
+    b += k;
+  }
+  return KRONQ_OK;
 }
 
 }  // namespace
@@ -320,8 +542,10 @@ int pack_codes_launch(const uint8_t* codes, int64_t d_out, int64_t d_in, int64_t
 
 size_t online_ws_bytes(int64_t d_out, int64_t d_in, int64_t batch) {
   if (d_out <= 0 || d_in <= 0 || batch <= 0) return 0;
+  const size_t nch = size_t(batch) * size_t(d_in / 32);
   return align256(size_t(batch) * size_t(d_in) * sizeof(float)) +
-         align256(size_t(batch) * size_t(d_out) * sizeof(float)) + 256;
+         align256(size_t(batch) * size_t(d_out) * sizeof(float)) + align256(nch * 96) +
+         2 * align256(nch * 4) + 256;
 }
 
 int online_matvec_launch(const uint32_t* packed, int64_t ldp, const float* scales,
@@ -333,20 +557,28 @@ int online_matvec_launch(const uint32_t* packed, int64_t ldp, const float* scale
   Carver cv(ws);
   float* xr = cv.take<float>(size_t(batch) * size_t(d_in));
   float* yr = cv.take<float>(size_t(batch) * size_t(d_out));
+  const size_t nch = size_t(batch) * size_t(d_in / 32);
+  uint8_t* dig = cv.take<uint8_t>(nch * 96);
+  int* dexp = cv.take<int>(nch);
+  float* dsum = cv.take<float>(nch);
   const int nb = int(batch);
-  // x' = V S_X^-1 x
+  const bool integer = bits == 2 || bits == 4;  // codes that fill whole bytes of a word
+  // x' = V S_X^-1 x (and its digits for the integer GEMV)
   KQ_TRY(seg_transform_launch(x, x_dtype, ldx, xr, d_in, batch, d_in, mul_in, nullptr,
-                              (flags & KRONQ_ROT_IN) != 0, q28_in, false, s));
+                              (flags & KRONQ_ROT_IN) != 0, q28_in, false, s,
+                              integer ? dig : nullptr, dexp, dsum, bits));
   // y' = W_hat' x'
   switch (bits) {
     case 2:
-      KQ_TRY(gemv_bits<2>(nb, packed, ldp, scales, zeros, ldsz, group, d_out, d_in, xr, yr, s));
+      KQ_TRY(gemv_int<2>(nb, packed, ldp, scales, zeros, ldsz, group, d_out, d_in, dig, dexp,
+                         dsum, yr, s));
       break;
     case 3:
       KQ_TRY(gemv_bits<3>(nb, packed, ldp, scales, zeros, ldsz, group, d_out, d_in, xr, yr, s));
       break;
     case 4:
-      KQ_TRY(gemv_bits<4>(nb, packed, ldp, scales, zeros, ldsz, group, d_out, d_in, xr, yr, s));
+      KQ_TRY(gemv_int<4>(nb, packed, ldp, scales, zeros, ldsz, group, d_out, d_in, dig, dexp,
+                         dsum, yr, s));
       break;
     default:
       KQ_TRY(gemv_bits<8>(nb, packed, ldp, scales, zeros, ldsz, group, d_out, d_in, xr, yr, s));
