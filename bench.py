@@ -100,6 +100,31 @@ def cpu_baseline(spec, rot_in, rot_out, n_sample: int, X_dev, G_dev, W_dev, dX_d
     }
 
 
+def cpu_baseline_online(codes, scales, zeros, group, sx, sg, rot_in, rot_out, x):
+    """The float64 oracle's decode matvec: dequantise the codes, then x -> V S_X^-1 x -> W_hat' .
+    -> S_G^-1 U^T . with dense V and U (built once, outside the timing)."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+    c, s, z = codes.cpu().numpy(), scales.cpu().numpy(), zeros.cpu().numpy()
+    sx64, sg64 = sx.cpu().double().numpy(), sg.cpu().double().numpy()
+    x64 = x.float().cpu().double().numpy().T
+    V = O.rht_matrix(c.shape[1], rot_in.sign, rot_in.q28)
+    U = O.rht_matrix(c.shape[0], rot_out.sign, rot_out.q28)
+    reps = 3 if c.size <= 1 << 26 else 1  # about 2 s and 6 s per call at 4096^2 and 28672 x 8192
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        O.online_matvec(O.dequantize(c, s, z, group), sx64, sg64, V, U, x64)
+    t = (time.perf_counter() - t0) / reps
+    return {"value": round(t * 1e6, 1), "unit": "us", "cores": int(cores), "kind": "oracle",
+            "sample": f"float64 oracle: dequantisation and the online matvec with dense V and U "
+                      f"at full size, batch 1, mean of {reps} calls ({t * reps:.2f} s)"}
+
+
 def online_bench(args, spec, dev) -> int:
     """Decode matvec of a quantised layer (online rotations + packed-code GEMV), batch 1."""
     import torch
@@ -162,6 +187,7 @@ def online_bench(args, spec, dev) -> int:
     # algorithmic HBM bytes of the GEMV kernel: packed codes, scales and zeros, x' and y'
     gbytes = d_out * d_in * bits / 8 + 2 * 4 * d_out * (d_in // group) + 4 * d_in + 4 * d_out
     achieved = gbytes / (gemv_ms * 1e-3) / 1e9
+    int_path = bits in (2, 4)  # the GEMV on integer dot products; 3- and 8-bit codes use fp32
     print(f"[bench] online matvec {ms * 1e3:.2f} us (GEMV kernel {gemv_ms * 1e3:.2f} us), "
           f"dense bf16 GEMV {dense_ms * 1e3:.2f} us", file=sys.stderr, flush=True)
     out = {
@@ -169,17 +195,22 @@ def online_bench(args, spec, dev) -> int:
                   "packed-code GEMV, batch 1)",
         "value": round(ms * 1e3, 3), "unit": "us", "n_gpus": 1, "steps": reps, "warmup": warm,
         "ms_per_step": round(ms, 6), "higher_is_better": False, "scaling": "weak",
-        "vs_baseline": None, "dtype": f"u{bits} codes, fp32 arithmetic", "data": "synthetic",
+        "vs_baseline": None, "dtype": (f"u{bits} codes, i8 dot products (21-bit fixed-point "
+                                        f"activations) with fp32 combine" if int_path else
+                                        f"u{bits} codes, fp32 arithmetic"), "data": "synthetic",
         "config": {"workload": f"{spec.name} W {d_out}x{d_in}, {bits}-bit, group {group}, "
                                f"decode batch 1", "d_out": d_out, "d_in": d_in, "bits": bits,
                    "group": group, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": 8000.0,
                      "unit": "GB/s", "frac": round(achieved / 8000.0, 4), "traffic": None,
-                     "kernel": "online_gemv", "launches": g_n,
+                     "kernel": "online_gemv_int" if int_path else "online_gemv",
+                     "launches": g_n,
                      "avg_launch_ms": round(gemv_ms, 6)},
         "dense_bf16_gemv_us": round(dense_ms * 1e3, 3),
         "speedup_vs_dense_bf16": round(dense_ms / ms, 3),
     }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_online(codes, scales, zeros, group, sx, sg, ri, ro, x)
     print(json.dumps(out), flush=True)
     return 0
 
