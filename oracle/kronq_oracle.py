@@ -47,6 +47,19 @@ R20 the W in the drift term of the sweep is the column as it stands when it is q
     update would use the block after its sweep, which holds the quantised values.)
 R21 alpha is an input; 1 is the value for which the update is the exact least-squares
     absorption. The paper leaves alpha's value to GPTAQ.
+R22 packed codes: each run of 32 consecutive codes of a row is one 32*b-bit little-endian
+    string (code j at bits [j*b, (j+1)*b)) held in b uint32 words.
+R23 the online product is the original-space layer S_G^-1 U^T W_hat' V S_X^-1 x, applied factor
+    by factor.
+R24 CV_in and CV_out are population coefficients of variation (std / mean, std over n, not
+    n - 1) of the column norms ||W_:,j|| and the row norms ||W_i,:|| (norms, not squared).
+R25 mu(H) = sqrt(d) max |Q_ij| over the eigenvector matrix Q (unit columns) of the symmetric H.
+    Within a repeated eigenvalue Q is not unique and neither is mu; comparisons are made where
+    the maximising eigenvector belongs to a simple, separated eigenvalue.
+R26 Prop. 2 and the optimality table: h_i = [H_G]_ii and a_i = ||W_i,:||^2 of the layer before
+    BiIP; D holds the pivots the natural-order sweep sees, D_p = 1 / [inv(H~[p:, p:])]_00 for the
+    damped post-BiIP H~ (the paper's "LDL diagonal"); the nearest-rounding row takes tr(H~) of
+    the same matrix. A channel with h_i a_i = 0 takes s_i = 1 (as R10).
 """
 from __future__ import annotations
 
@@ -60,6 +73,8 @@ __all__ = [
     "biip_forward", "biip_revert", "damp", "inverse_cholesky_factor", "gptaq_correction",
     "group_params", "quantize", "obs_unblocked", "obs_blocked", "kfac_loss", "kronq_objective",
     "allocate_bits", "count_avg_bits", "dequantize", "online_matvec", "pack_codes",
+    "incoherence", "norm_cv", "eigenvectors", "hessian_incoherence", "sweep_pivots",
+    "rescale_objective", "rescale_gain", "proxy_loss_factors",
     "RESCALE_IN", "RESCALE_OUT", "ROT_IN", "ROT_OUT", "BIIP",
 ]
 
@@ -472,3 +487,83 @@ def allocate_bits(scores, weights, choices=(2, 3, 4), avg_bits: float = 3.0):
 def count_avg_bits(bits) -> float:
     """Count-weighted average bit width (the 'Avg bits' column of the mixed-precision table)."""
     return float(np.mean(np.asarray(bits, dtype=np.float64)))
+
+
+# ----------------------------------------------------------------------------------------------
+# Diagnostics  (Sec. 2.3 eq. incoherence_measure; Sec. 4.2 with Fig. 2; Prop. 2 eq. biip-bound,
+# appendix A.3 and the optimality table)
+# ----------------------------------------------------------------------------------------------
+def incoherence(M) -> float:
+    """mu(M) = sqrt(rows * cols) max_ij |M_ij| / ||M||_F (eq. incoherence_measure, left)."""
+    M = as_f64(M)
+    r, c = M.shape
+    return float(np.sqrt(r * c) * np.max(np.abs(M)) / np.sqrt(np.sum(M * M)))
+
+
+def norm_cv(M) -> tuple[float, float]:
+    """(CV_in, CV_out): coefficient of variation of the column norms and of the row norms
+    (Fig. 2b; reading R24)."""
+    M = as_f64(M)
+
+    def cv(n):
+        mean = np.mean(n)
+        return float(np.sqrt(np.mean((n - mean) ** 2)) / mean)
+
+    return cv(np.sqrt(np.sum(M * M, axis=0))), cv(np.sqrt(np.sum(M * M, axis=1)))
+
+
+def eigenvectors(H) -> tuple[np.ndarray, np.ndarray]:
+    """Eigenvalues and the eigenvector matrix Q (unit columns) of the symmetric H (LAPACK)."""
+    return np.linalg.eigh(np.asarray(H, dtype=np.float64))
+
+
+def hessian_incoherence(H) -> float:
+    """mu(H) = sqrt(d) max_ij |Q_ij| (eq. incoherence_measure, right; reading R25)."""
+    _, Q = eigenvectors(H)
+    return float(np.sqrt(H.shape[0]) * np.max(np.abs(Q)))
+
+
+def sweep_pivots(Hd, U=None) -> np.ndarray:
+    """D_p = 1 / [inv(H~[p:, p:])]_00, the pivots the natural-order sweep divides by (R26).
+    [inv(H~[p:, p:])]_00 = U_pp^2 for the factor of R3, so the diagonal of that factor is used
+    (``U`` if given, else the oracle's own factor of Hd)."""
+    U = inverse_cholesky_factor(Hd) if U is None else np.asarray(U, dtype=np.float64)
+    return 1.0 / np.diag(U) ** 2
+
+
+def _powered_ratio(h, a, alpha: float) -> np.ndarray:
+    h, a = np.asarray(h, dtype=np.float64), np.asarray(a, dtype=np.float64)
+    ok = (h > 0) & (a > 0)
+    s = np.ones_like(h)
+    s[ok] = (h[ok] / a[ok]) ** alpha
+    return s
+
+
+def rescale_objective(h, a, alpha: float) -> float:
+    """(sum_i h_i / s_i^2)(sum_i s_i^2 a_i) for s_i = (h_i / a_i)^alpha: the rescaling-dependent
+    factor of the expected loss in Prop. 2 (eq. biip-bound; the exponent sweep of appendix A.3)."""
+    h, a = np.asarray(h, dtype=np.float64), np.asarray(a, dtype=np.float64)
+    s2 = _powered_ratio(h, a, alpha) ** 2
+    return float(np.sum(h / s2) * np.sum(s2 * a))
+
+
+def rescale_gain(h, a) -> float:
+    """rho = (sum_i sqrt(h_i a_i))^2 / (sum_i h_i sum_i a_i) (Prop. 2)."""
+    h, a = np.asarray(h, dtype=np.float64), np.asarray(a, dtype=np.float64)
+    return float(np.sum(np.sqrt(h * a)) ** 2 / (np.sum(h) * np.sum(a)))
+
+
+def proxy_loss_factors(HG, W, Hd, U=None) -> dict:
+    """The three rows of the optimality table for a layer: nearest rounding
+    (sum h)(sum a) tr(H~), GPTQ (sum h)(sum a) tr(D), KronQ (sum sqrt(h a))^2 tr(D), with
+    h = diag(H_G) and a the squared row norms of W before BiIP, H~ the damped post-BiIP H_X
+    (reading R26). Also rho and tr(D)."""
+    h = _diag(HG)
+    W = as_f64(W)
+    a = np.sum(W * W, axis=1)
+    trD = float(np.sum(sweep_pivots(Hd, U)))
+    trH = float(np.trace(np.asarray(Hd, dtype=np.float64)))
+    return {"nearest": float(np.sum(h) * np.sum(a) * trH),
+            "gptq": float(np.sum(h) * np.sum(a) * trD),
+            "kronq": float(np.sum(np.sqrt(h * a)) ** 2 * trD),
+            "rho": rescale_gain(h, a), "trD": trD, "trH": trH}
