@@ -9,6 +9,10 @@ group quantisation. Default workload: the LLaMA-3-8B q_proj shape, W 4096 x 4096
 BiIP, P and the drift-corrected sweep); --group sets the quantisation group (0: per-channel).
 --online times the inference side instead: one decode matvec of the quantised layer with the
 rotations applied online (kronq_online_matvec), against a dense bf16 GEMV of the same shape.
+--diagnostics times the diagnostics of the incoherence processing on the layer instead: mu(W) and
+the row/column norm variation for the original, input-side-processed and BiIP-processed weights,
+mu(H_X) and mu(H_G) before and after BiIP from Jacobi eigendecompositions, and the expected-loss
+factors of Prop. 2 with the rescale-exponent sweep.
 
 The JSON line carries
   * roofline: the covariance syrk (the dominant kernel; with --drift the drift statistic's
@@ -215,6 +219,140 @@ def online_bench(args, spec, dev) -> int:
     return 0
 
 
+def diag_bench(args, spec, dev) -> int:
+    """The layer's incoherence diagnostics (Sec. 2.3, Fig. 2, Prop. 2) on resident statistics."""
+    import torch
+
+    import synth
+    from paper_2607_07964_amd import kronq as K
+    from paper_2607_07964_amd import layer as L
+
+    d_out, d_in = spec.d_out, spec.d_in
+    print(f"[bench] diagnostics setup {spec.name}: W {d_out}x{d_in}, N={spec.n_tokens}",
+          file=sys.stderr, flush=True)
+    X = synth.gen_matrix(spec.x, dev)
+    G = synth.gen_matrix(spec.g, dev)
+    W0 = synth.gen_matrix(spec.w, dev)
+    ri = synth.rotation_params(d_in, spec.seed, spec.name + ":in")
+    ro = synth.rotation_params(d_out, spec.seed, spec.name + ":out")
+    rin = L.RotParams.to_device(ri.sign, ri.q28, dev)
+    rout = L.RotParams.to_device(ro.sign, ro.q28, dev)
+    st = L.LayerState.allocate(d_out, d_in, spec.n_tokens, dev)
+    L.covariances(st, X, G)
+    del X, G
+    HX0, HG0 = st.HX.clone(), st.HG.clone()
+    W_in = torch.empty(d_out, d_in, device=dev)  # input-side processing only (Fig. 2b middle)
+    sx, sg = torch.empty(d_in, device=dev), torch.empty(d_out, device=dev)
+    K.kronq_rotate(W0, W_in, st.HX.clone(), None, rin.sign, None, rin.q28, None, sx, sg,
+                   K.RESCALE_IN | K.ROT_IN, st.ws_rot)
+    L.biip(st, W0, rin, rout)
+    HX1, HG1 = st.HX.clone(), st.HG.clone()
+    K.kronq_cholesky_inv(st.HX, st.U, spec.damp, st.info, st.ws_chol)  # st.HX: damped H~
+    L.check(st)
+    alphas = (0.0, 0.125, 0.25, 0.375, 0.5)
+    dmax = max(d_in, d_out)
+    ws_e = K.workspace(K.OP_EIGH, 0, dmax, 0, dev)
+    ws_s = K.workspace(K.OP_STATS, max(d_out, dmax), max(d_in, dmax), 0, dev)
+    ws_p = K.workspace(K.OP_PROXY, d_out, d_in, 0, dev)
+    Qs = {d: torch.empty(d, d, device=dev) for d in {d_in, d_out}}
+    ev = {d: torch.empty(d, device=dev) for d in {d_in, d_out}}
+    stats = {k: torch.empty(5, dtype=torch.float64, device=dev)
+             for k in ("W0", "W_in", "W_biip", "HX0", "HG0", "HX1", "HG1")}
+    offs = {k: torch.empty(1, dtype=torch.float64, device=dev) for k in ("HX0", "HG0", "HX1", "HG1")}
+    proxy = torch.empty(6 + len(alphas), dtype=torch.float64, device=dev)
+    hs = {"HX0": HX0, "HG0": HG0, "HX1": HX1, "HG1": HG1}
+    torch.cuda.synchronize()
+
+    def step():
+        for k, M in (("W0", W0), ("W_in", W_in), ("W_biip", st.W)):
+            K.kronq_matrix_stats(M, stats[k], ws_s)
+        for k, H in hs.items():
+            d = H.shape[0]
+            K.kronq_eigh(H, args.sweeps, ev[d], Qs[d], offs[k], ws_e)
+            K.kronq_matrix_stats(Qs[d], stats[k], ws_s)
+        K.kronq_proxy_loss_factors(HG0, W0, st.HX, st.U, alphas, proxy, ws_p)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    dom = "diag_jacobi_apply"
+    K.kronq_profile_only(dom)
+    K.kronq_profile_reset()
+    K.kronq_profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    K.kronq_profile_enable(False)
+    dom_ms, dom_n = K.kronq_profile_read(dom)
+    ms = (t1 - t0) * 1e3 / max(args.steps, 1)
+    avg_ms = dom_ms / max(dom_n, 1)
+    # algorithmic bytes of one Jacobi round: read and write A and V (4 d^2 fp32), averaged over
+    # the launches of the four eigendecompositions (two of order d_in, two of order d_out)
+    nbytes = 16.0 * (d_in * d_in + d_out * d_out) / 2
+    achieved = nbytes / (avg_ms * 1e-3) / 1e9
+    st_np = {k: v.cpu().tolist() for k, v in stats.items()}
+    pr = proxy.cpu().tolist()
+    diag = {
+        "mu_W": {k: round(st_np[k][2], 4) for k in ("W0", "W_in", "W_biip")},
+        "cv_in": {k: round(st_np[k][3], 4) for k in ("W0", "W_in", "W_biip")},
+        "cv_out": {k: round(st_np[k][4], 4) for k in ("W0", "W_in", "W_biip")},
+        "mu_H_over_sqrt_d": {k: round(st_np[k][0], 4) for k in hs},  # max |Q_ij|
+        "eigh_offdiag_rel": {k: float(f"{v.item():.3g}") for k, v in offs.items()},
+        "proxy_factors": {"nearest": pr[0], "gptq": pr[1], "kronq": pr[2], "rho": pr[3]},
+        "rescale_sweep": {str(a): pr[6 + i] / pr[1] for i, a in enumerate(alphas)},
+    }
+    print(f"[bench] diagnostics pass {ms:.1f} ms; " + json.dumps(diag), file=sys.stderr, flush=True)
+    out = {
+        "metric": "seconds per layer diagnostic pass (mu(W), CV_in/CV_out for three weight "
+                  "states, mu(H_X), mu(H_G) before/after BiIP by Jacobi eigendecomposition, "
+                  "expected-loss factors)",
+        "value": round(ms / 1e3, 4), "unit": "s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 3), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp32 (rotations), fp64 (sums)", "data": "synthetic",
+        "config": {"workload": f"{spec.name} W {d_out}x{d_in}, N={spec.n_tokens}, "
+                               f"{args.sweeps} Jacobi sweeps", "d_out": d_out, "d_in": d_in,
+                   "sweeps": args.sweeps, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": 8000.0,
+                     "unit": "GB/s", "frac": round(achieved / 8000.0, 4), "traffic": None,
+                     "kernel": dom, "launches": dom_n, "avg_launch_ms": round(avg_ms, 5)},
+        "diagnostics": diag,
+    }
+    if not args.no_cpu_baseline:
+        import numpy as np
+
+        import oracle as O
+        try:
+            from threadpoolctl import threadpool_info
+            cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        except Exception:  # pragma: no cover
+            cores = len(os.sched_getaffinity(0))
+        print("[bench] timing the float64 oracle's diagnostics on the host", file=sys.stderr,
+              flush=True)
+        w0 = synth.bf16_bits(W0.cpu()) if W0.dtype == torch.bfloat16 else W0.cpu().numpy()
+        mats = [w0, W_in.cpu().numpy(), st.W.cpu().numpy()]
+        hcpu = [h.cpu().numpy() for h in hs.values()]
+        hg0, hd, u = HG0.cpu().numpy(), st.HX.cpu().numpy(), st.U.cpu().numpy()
+        t0 = time.perf_counter()
+        for M in mats:
+            O.incoherence(M)
+            O.norm_cv(M)
+        for H in hcpu:
+            O.hessian_incoherence(H)
+        f = O.proxy_loss_factors(hg0, w0, hd, u)
+        for a in alphas:
+            O.rescale_objective(np.diag(hg0), np.sum(O.as_f64(w0) ** 2, axis=1), a)
+        t = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(t, 3), "unit": "s", "cores": int(cores),
+                               "kind": "oracle",
+                               "sample": "float64 oracle: the whole diagnostic pass at full size "
+                                         "(LAPACK eigh for the four eigendecompositions)"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -234,6 +372,9 @@ def main() -> int:
                     help="quantisation group (a multiple of 128 dividing d_in; 0: per-channel)")
     ap.add_argument("--online", action="store_true",
                     help="time the inference-side decode matvec of the quantised layer instead")
+    ap.add_argument("--diagnostics", action="store_true",
+                    help="time the incoherence diagnostics of the layer instead")
+    ap.add_argument("--sweeps", type=int, default=12, help="Jacobi sweeps (--diagnostics)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run 3 plain 1 GiB device copies (reference for counter scaling)")
     args = ap.parse_args()
@@ -262,6 +403,8 @@ def main() -> int:
     spec = synth.workload(WORKLOADS[args.workload])
     if args.online:
         return online_bench(args, spec, dev)
+    if args.diagnostics:
+        return diag_bench(args, spec, dev)
     print(f"[bench] generating {spec.name}: W {spec.d_out}x{spec.d_in}, N={spec.n_tokens}",
           file=sys.stderr, flush=True)
     X = synth.gen_matrix(spec.x, dev)

@@ -88,6 +88,9 @@ extern "C" {
 #define KRONQ_OP_GPTAQ 8         /* kronq_gptaq_correction: d as d_in */
 #define KRONQ_OP_OBS_DRIFT 9     /* kronq_obs_quantize_layer_drift: d_out, d_in */
 #define KRONQ_OP_ONLINE 10       /* kronq_online_matvec: d_out, d_in, batch as n_rows */
+#define KRONQ_OP_STATS 11        /* kronq_matrix_stats: rows as d_out, cols as d_in */
+#define KRONQ_OP_EIGH 12         /* kronq_eigh: d as d_in */
+#define KRONQ_OP_PROXY 13        /* kronq_proxy_loss_factors: d_out, d_in */
 
 /* Bytes of scratch the operation needs for these sizes. For KRONQ_OP_COV pass the covariance
  * dimension d as d_in and the token count as n_rows (d_out ignored); for KRONQ_OP_CHOL pass
@@ -262,6 +265,52 @@ int kronq_online_matvec(const uint32_t* packed, int64_t ldp, const float* scales
                         const float* q28_in, const float* q28_out, int flags, const void* x,
                         int x_dtype, int64_t ldx, int64_t batch, float* y, int64_t ldy, void* ws,
                         size_t ws_bytes, void* stream);
+
+/* ---- 8. diagnostics of the incoherence processing ------------------------------------------
+ * (Sec. 2.3 eq. incoherence_measure; Sec. 4.2 and Fig. 2; Prop. 2 eq. biip-bound, appendix A.3
+ * and its optimality table.) Sums are taken in fp64; results land in device memory. */
+
+/* out[5] = {max |M_ij|, ||M||_F^2, mu(M) = sqrt(rows cols) max |M_ij| / ||M||_F, CV_in, CV_out}:
+ * CV_in and CV_out are the population coefficients of variation (std / mean) of the column
+ * norms ||M_:,j|| and of the row norms ||M_i,:|| (Fig. 2b; the norms, not their squares).
+ *   M    device [rows x ld], dtype KRONQ_BF16 or KRONQ_FP32, 4-byte aligned; rows, cols >= 1.
+ *   out  device double[5]. Workspace: KRONQ_OP_STATS (rows as d_out, cols as d_in). */
+int kronq_matrix_stats(const void* M, int dtype, int64_t rows, int64_t cols, int64_t ld,
+                       double* out, void* ws, size_t ws_bytes, void* stream);
+
+/* Eigendecomposition of the symmetric H (the eigenvector matrix Q of mu(H) = sqrt(d) max |Q_ij|,
+ * eq. incoherence_measure) by cyclic two-sided Jacobi rotations in fp32: each sweep applies
+ * every pair rotation once, in d - 1 rounds of d/2 disjoint rotations (round-robin order);
+ * a pair is skipped once |a_pq| <= 1e-7 sqrt(|a_pp a_qq|).
+ *   H      device fp32 [d x ldh], symmetric (read only; only one triangle needs to be exact).
+ *   sweeps 1..64 sweeps (8 to 14 suffice for d <= 8192 in fp32).
+ *   evals  device fp32 [d]: the eigenvalues, unsorted; Q device fp32 [d x ldq], column k the
+ *          unit eigenvector of evals[k]. Q must not overlap H.
+ *   off    device double[1]: ||offdiag(Q^T H Q)||_F / ||H||_F after the last sweep, the
+ *          convergence measure.
+ *   1 <= d <= 16384. Workspace: KRONQ_OP_EIGH (d as d_in): two d x d fp32 matrices. */
+int kronq_eigh(const float* H, int64_t d, int64_t ldh, int sweeps, float* evals, float* Q,
+               int64_t ldq, double* off, void* ws, size_t ws_bytes, void* stream);
+
+#define KRONQ_MAX_ALPHAS 16
+
+/* The expected-loss factors of Prop. 2 and the optimality table, for h_i = [H_G]_ii and
+ * a_i = ||W_i,:||^2 of the layer before BiIP, D_p = 1 / U_pp^2 the pivots the sweep divides by
+ * (U the inverse-Cholesky factor of the damped post-BiIP H~, so D_p = 1 / [inv(H~[p:,p:])]_00):
+ *   out[0] = (sum h)(sum a) tr(H~)       nearest rounding
+ *   out[1] = (sum h)(sum a) tr(D)        GPTQ
+ *   out[2] = (sum sqrt(h a))^2 tr(D)     KronQ
+ *   out[3] = rho = (sum sqrt(h a))^2 / ((sum h)(sum a)),  out[4] = tr(D),  out[5] = tr(H~)
+ *   out[6 + k] = (sum h / s^2)(sum s^2 a) tr(D) with s_i = (h_i / a_i)^alphas[k] (1 where
+ *                h_i a_i = 0): the exponent sweep, minimal at alpha = 1/4.
+ *   HG  device fp32 [d_out x ldg] (its diagonal is read); W device [d_out x ldw], w_dtype
+ *       KRONQ_BF16 or KRONQ_FP32; Hd, U device fp32 [d_in x ldh], [d_in x ldu] (diagonals).
+ *   alphas HOST double[n_alpha], 0 <= n_alpha <= KRONQ_MAX_ALPHAS; out device double[6 + n_alpha].
+ *   Workspace: KRONQ_OP_PROXY (d_out, d_in). */
+int kronq_proxy_loss_factors(const float* HG, int64_t d_out, int64_t ldg, const void* W,
+                             int w_dtype, int64_t ldw, int64_t d_in, const float* Hd, int64_t ldh,
+                             const float* U, int64_t ldu, const double* alphas, int n_alpha,
+                             double* out, void* ws, size_t ws_bytes, void* stream);
 
 /* ---- 6. K-FAC loss (Sec. 4.1 eq. kron_obj) -----------------------------------------------
  * loss = tr(H_G dW H_X dW^T) = sum_ij (H_G dW)_ij (dW H_X)_ij with dW = W - W_hat (W_hat NULL:

@@ -134,6 +134,18 @@ int online_matvec_launch(const uint32_t* packed, int64_t ldp, const float* scale
                          const float* q28_in, const float* q28_out, int flags, const void* x,
                          int x_dtype, int64_t ldx, int64_t batch, float* y, int64_t ldy, void* ws,
                          hipStream_t s);
+// diagnostics: matrix statistics, Jacobi eigendecomposition, expected-loss factors
+size_t matrix_stats_ws_bytes(int64_t rows, int64_t cols);
+int matrix_stats_launch(const void* M, int dtype, int64_t rows, int64_t cols, int64_t ld,
+                        double* out, void* ws, hipStream_t s);
+size_t eigh_ws_bytes(int64_t d);
+int eigh_launch(const float* H, int64_t d, int64_t ldh, int sweeps, float* evals, float* Q,
+                int64_t ldq, double* off, void* ws, hipStream_t s);
+size_t proxy_ws_bytes(int64_t d_out, int64_t d_in);
+int proxy_launch(const float* HG, int64_t ldg, const void* W, int w_dtype, int64_t ldw,
+                 int64_t d_out, int64_t d_in, const float* Hd, int64_t ldh, const float* U,
+                 int64_t ldu, const double* alphas, int n_alpha, double* out, void* ws,
+                 hipStream_t s);
 // fp32 GEMM on MFMA: C = alpha * op(A) op(B) + beta * C
 enum GemmFlags : int {
   GEMM_TA = 1,          // op(A) = A^T (A stored [K x M])

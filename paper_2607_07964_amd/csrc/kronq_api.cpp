@@ -92,6 +92,12 @@ size_t kronq_workspace_bytes(int op, int64_t d_out, int64_t d_in, int64_t n_rows
       return kq::obs_ws_bytes(d_out, d_in, true);
     case KRONQ_OP_ONLINE:
       return kq::online_ws_bytes(d_out, d_in, n_rows);
+    case KRONQ_OP_STATS:
+      return kq::matrix_stats_ws_bytes(d_out, d_in);
+    case KRONQ_OP_EIGH:
+      return kq::eigh_ws_bytes(d_in);
+    case KRONQ_OP_PROXY:
+      return kq::proxy_ws_bytes(d_out, d_in);
     case KRONQ_OP_ROTATE:
       return kq::rotate_ws_bytes(d_out, d_in);
     case KRONQ_OP_CHOL:
@@ -280,6 +286,56 @@ int kronq_pack_codes(const uint8_t* codes, int64_t d_out, int64_t d_in, int64_t 
   KQ_REQUIRE(ldq >= d_in && ldp >= d_in * bits / 32, KRONQ_ERR_INVALID_ARG,
              "bad leading dimension");
   return kq::pack_codes_launch(codes, d_out, d_in, ldq, bits, packed, ldp, as_stream(stream));
+}
+
+int kronq_matrix_stats(const void* M, int dtype, int64_t rows, int64_t cols, int64_t ld,
+                       double* out, void* ws, size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(M && valid_dtype(dtype) && aligned(M, 4), KRONQ_ERR_INVALID_ARG,
+             "M must be a 4-byte aligned KRONQ_BF16 or KRONQ_FP32 matrix");
+  KQ_REQUIRE(rows >= 1 && cols >= 1 && ld >= cols && rows <= (int64_t(1) << 31) &&
+                 cols <= (int64_t(1) << 31),
+             KRONQ_ERR_INVALID_ARG, "bad sizes");
+  KQ_REQUIRE(out && aligned(out, 8), KRONQ_ERR_INVALID_ARG, "out must be a double[5] device pointer");
+  KQ_TRY(check_ws(ws, ws_bytes, kq::matrix_stats_ws_bytes(rows, cols)));
+  return kq::matrix_stats_launch(M, dtype, rows, cols, ld, out, ws, as_stream(stream));
+}
+
+int kronq_eigh(const float* H, int64_t d, int64_t ldh, int sweeps, float* evals, float* Q,
+               int64_t ldq, double* off, void* ws, size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(d >= 1 && d <= 16384, KRONQ_ERR_UNSUPPORTED, "1 <= d <= 16384");
+  KQ_REQUIRE(sweeps >= 1 && sweeps <= 64, KRONQ_ERR_INVALID_ARG, "1 <= sweeps <= 64");
+  KQ_REQUIRE(H && aligned(H, 4) && ldh >= d, KRONQ_ERR_INVALID_ARG, "bad H");
+  KQ_REQUIRE(Q && aligned(Q, 4) && ldq >= d, KRONQ_ERR_INVALID_ARG, "bad Q");
+  KQ_REQUIRE(evals && aligned(evals, 4) && off && aligned(off, 8), KRONQ_ERR_INVALID_ARG,
+             "evals and off are required");
+  const char *h0 = reinterpret_cast<const char*>(H), *q0 = reinterpret_cast<const char*>(Q);
+  const size_t hb = (size_t(d - 1) * size_t(ldh) + size_t(d)) * 4;
+  const size_t qb = (size_t(d - 1) * size_t(ldq) + size_t(d)) * 4;
+  KQ_REQUIRE(q0 + qb <= h0 || h0 + hb <= q0, KRONQ_ERR_INVALID_ARG, "Q must not overlap H");
+  KQ_TRY(check_ws(ws, ws_bytes, kq::eigh_ws_bytes(d)));
+  return kq::eigh_launch(H, d, ldh, sweeps, evals, Q, ldq, off, ws, as_stream(stream));
+}
+
+int kronq_proxy_loss_factors(const float* HG, int64_t d_out, int64_t ldg, const void* W,
+                             int w_dtype, int64_t ldw, int64_t d_in, const float* Hd, int64_t ldh,
+                             const float* U, int64_t ldu, const double* alphas, int n_alpha,
+                             double* out, void* ws, size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(d_out >= 1 && d_in >= 1 && d_out <= (int64_t(1) << 31) && d_in <= (int64_t(1) << 31),
+             KRONQ_ERR_INVALID_ARG, "bad sizes");
+  KQ_REQUIRE(HG && aligned(HG, 4) && ldg >= d_out, KRONQ_ERR_INVALID_ARG, "bad H_G");
+  KQ_REQUIRE(W && valid_dtype(w_dtype) && aligned(W, 4) && ldw >= d_in, KRONQ_ERR_INVALID_ARG,
+             "bad W");
+  KQ_REQUIRE(Hd && aligned(Hd, 4) && ldh >= d_in, KRONQ_ERR_INVALID_ARG, "bad H~");
+  KQ_REQUIRE(U && aligned(U, 4) && ldu >= d_in, KRONQ_ERR_INVALID_ARG, "bad U");
+  KQ_REQUIRE(n_alpha >= 0 && n_alpha <= KRONQ_MAX_ALPHAS && (n_alpha == 0 || alphas),
+             KRONQ_ERR_INVALID_ARG, "0 <= n_alpha <= %d host exponents", KRONQ_MAX_ALPHAS);
+  KQ_REQUIRE(out && aligned(out, 8), KRONQ_ERR_INVALID_ARG, "out is required");
+  KQ_TRY(check_ws(ws, ws_bytes, kq::proxy_ws_bytes(d_out, d_in)));
+  return kq::proxy_launch(HG, ldg, W, w_dtype, ldw, d_out, d_in, Hd, ldh, U, ldu, alphas,
+                          n_alpha, out, ws, as_stream(stream));
 }
 
 int kronq_online_factors(const float* s, const int8_t* sign, int64_t d, float* mul, void* stream) {

@@ -23,6 +23,8 @@ HX_ONLY, SX_GIVEN = 32, 64
 BIIP = RESCALE_IN | RESCALE_OUT | ROT_IN | ROT_OUT
 OP_COV, OP_ROTATE, OP_CHOL, OP_OBS, OP_LOSS = 1, 2, 3, 4, 5
 OP_CROSS, OP_ROTATE_DRIFT, OP_GPTAQ, OP_OBS_DRIFT, OP_ONLINE = 6, 7, 8, 9, 10
+OP_STATS, OP_EIGH, OP_PROXY = 11, 12, 13
+MAX_ALPHAS = 16
 ERRORS = {0: "OK", -1: "INVALID_ARG", -2: "SHAPE", -3: "NOT_PD", -4: "HIP", -5: "WORKSPACE",
           -6: "UNSUPPORTED"}
 
@@ -32,7 +34,8 @@ EXPORTS = (
     "kronq_layer_loss", "kronq_allocate_bits", "kronq_profile_enable", "kronq_profile_only",
     "kronq_profile_reset", "kronq_profile_read", "kronq_accumulate_cross", "kronq_rotate_drift",
     "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift", "kronq_pack_codes",
-    "kronq_online_factors", "kronq_online_matvec",
+    "kronq_online_factors", "kronq_online_matvec", "kronq_matrix_stats", "kronq_eigh",
+    "kronq_proxy_loss_factors",
 )
 
 
@@ -69,6 +72,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_online_factors": (I, [P, P, I64, P, P]),
         "kronq_online_matvec": (I, [P, I64, P, P, I64, I, I, I64, I64, P, P, P, P, I, P, I, I64,
                                     I64, P, I64, P, SZ, P]),
+        "kronq_matrix_stats": (I, [P, I, I64, I64, I64, P, P, SZ, P]),
+        "kronq_eigh": (I, [P, I64, I64, I, P, P, I64, P, P, SZ, P]),
+        "kronq_proxy_loss_factors": (I, [P, I64, I64, P, I, I64, I64, P, I64, P, I64, P, I, P, P,
+                                         SZ, P]),
         "kronq_traces": (I, [P, I64, I64, P, I64, I64, P, P]),
         "kronq_rotate": (I, [P, I, I64, P, I64, I64, I64, P, I64, P, I64, P, P, P, P, P, P, I, P,
                              SZ, P]),
@@ -342,6 +349,63 @@ def kronq_layer_loss(W: torch.Tensor, W_hat: Optional[torch.Tensor], HX: torch.T
         d_out, d_in, _ptr(HX), _ld(HX), _ptr(HG), _ld(HG), _ptr(out), _ptr(ws), ws.numel(),
         _stream(W.device))
     _check(rc, "kronq_layer_loss")
+    return out
+
+
+def kronq_matrix_stats(M: torch.Tensor, out: Optional[torch.Tensor] = None,
+                       ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Device float64 [5]: max |M|, ||M||_F^2, mu(M), CV of the column norms, CV of the row
+    norms."""
+    _dev(M)
+    rows, cols = M.shape
+    if out is None:
+        out = torch.empty(5, dtype=torch.float64, device=M.device)
+    if ws is None:
+        ws = workspace(OP_STATS, rows, cols, 0, M.device)
+    rc = load().kronq_matrix_stats(_ptr(M), _dtype_code(M), rows, cols, _ld(M), _ptr(out),
+                                   _ptr(ws), ws.numel(), _stream(M.device))
+    _check(rc, "kronq_matrix_stats")
+    return out
+
+
+def kronq_eigh(H: torch.Tensor, sweeps: int = 12, evals: Optional[torch.Tensor] = None,
+               Q: Optional[torch.Tensor] = None, off: Optional[torch.Tensor] = None,
+               ws: Optional[torch.Tensor] = None):
+    """Jacobi eigendecomposition of the symmetric fp32 H: (evals, Q with unit eigenvector
+    columns, device float64 off-diagonal residual)."""
+    _dev(H)
+    d = H.shape[0]
+    if evals is None:
+        evals = torch.empty(d, device=H.device)
+    if Q is None:
+        Q = torch.empty(d, d, device=H.device)
+    if off is None:
+        off = torch.empty(1, dtype=torch.float64, device=H.device)
+    if ws is None:
+        ws = workspace(OP_EIGH, 0, d, 0, H.device)
+    rc = load().kronq_eigh(_ptr(H), d, _ld(H), int(sweeps), _ptr(evals), _ptr(Q), _ld(Q), _ptr(off),
+                           _ptr(ws), ws.numel(), _stream(H.device))
+    _check(rc, "kronq_eigh")
+    return evals, Q, off
+
+
+def kronq_proxy_loss_factors(HG: torch.Tensor, W: torch.Tensor, Hd: torch.Tensor, U: torch.Tensor,
+                             alphas=(), out: Optional[torch.Tensor] = None,
+                             ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Device float64 [6 + len(alphas)]: nearest, GPTQ and KronQ expected-loss factors, rho,
+    tr(D), tr(H~), then the exponent sweep."""
+    _dev(HG, W, Hd, U)
+    d_out, d_in = W.shape
+    n = len(alphas)
+    if out is None:
+        out = torch.empty(6 + n, dtype=torch.float64, device=W.device)
+    if ws is None:
+        ws = workspace(OP_PROXY, d_out, d_in, 0, W.device)
+    al = (ctypes.c_double * max(n, 1))(*[float(a) for a in alphas])
+    rc = load().kronq_proxy_loss_factors(
+        _ptr(HG), d_out, _ld(HG), _ptr(W), _dtype_code(W), _ld(W), d_in, _ptr(Hd), _ld(Hd), _ptr(U),
+        _ld(U), al, n, _ptr(out), _ptr(ws), ws.numel(), _stream(W.device))
+    _check(rc, "kronq_proxy_loss_factors")
     return out
 
 

@@ -147,6 +147,39 @@ def test_drift_and_group_argument_checks():
     assert rc == -1 and "alias" in msg
 
 
+def test_diagnostics_argument_checks():
+    lib = K.load()
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)
+    other = ctypes.c_void_p(1 << 28)
+    ws = ctypes.c_void_p(1 << 30)
+    assert K.kronq_workspace_bytes(K.OP_EIGH, 0, 4096, 0) >= 2 * 4096 * 4096 * 4
+    assert K.kronq_workspace_bytes(K.OP_STATS, 4096, 4096, 0) > 0
+    assert K.kronq_workspace_bytes(K.OP_PROXY, 4096, 4096, 0) > 0
+    assert K.kronq_workspace_bytes(K.OP_EIGH, 0, 0, 0) == 0
+    # stats: bad dtype, ld < cols, workspace too small
+    rc, _ = _err(lib.kronq_matrix_stats(fake, 3, 8, 8, 8, other, ws, 1 << 30, nul))
+    assert rc == -1
+    rc, _ = _err(lib.kronq_matrix_stats(fake, 2, 8, 8, 4, other, ws, 1 << 30, nul))
+    assert rc == -1
+    rc, msg = _err(lib.kronq_matrix_stats(fake, 2, 64, 64, 64, other, ws, 16, nul))
+    assert rc == -5 and "workspace" in msg
+    # eigh: Q overlapping H, too many sweeps, too large an order
+    rc, msg = _err(lib.kronq_eigh(fake, 64, 64, 10, other, ctypes.c_void_p((1 << 20) + 256), 64,
+                                  other, ws, 1 << 30, nul))
+    assert rc == -1 and "overlap" in msg
+    rc, _ = _err(lib.kronq_eigh(fake, 64, 64, 65, other, other, 64, other, ws, 1 << 30, nul))
+    assert rc == -1
+    rc, _ = _err(lib.kronq_eigh(fake, 20000, 20000, 10, other, other, 20000, other, ws, 1 << 40,
+                                nul))
+    assert rc == -6
+    # proxy factors: more exponents than the kernel's argument block holds
+    al = (ctypes.c_double * 17)(*([0.25] * 17))
+    rc, _ = _err(lib.kronq_proxy_loss_factors(fake, 8, 8, fake, 2, 8, 8, fake, 8, fake, 8, al, 17,
+                                              other, ws, 1 << 30, nul))
+    assert rc == -1
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_allocation_matches_oracle(seed):
     r = np.random.default_rng(seed)
