@@ -28,6 +28,7 @@
 #include <cmath>
 
 #include "kq_common.hpp"
+#include "kq_fwht.hpp"
 
 namespace kq {
 namespace {
@@ -257,7 +258,7 @@ __device__ __forceinline__ void emit_digits(float v, int64_t col, int lane32, in
   base[64] = uint8_t(X);        // d2
   if (lane32 == 0) {
     dexp[c] = e;
-    dsum[c] = float(sx) / up;  // exact: a division by a power of two
+    dsum[c] = float(sx) / up;  // |sx| <= 2^26: one rounding to fp32, then an exact scaling
   }
 }
 
@@ -441,6 +442,383 @@ __global__ __launch_bounds__(256) void online_gemv_int(
     }
 }
 
+// lane (lane ^ 1) and (lane ^ 2) of each quad (DPP quad_perm [1,0,3,2] and [2,3,0,1])
+__device__ __forceinline__ int quad_xor1(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+}
+__device__ __forceinline__ int quad_xor2(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+}
+
+// The digits (as emit_digits) of 8 consecutive elements j0 .. j0 + 7 of x' held by one lane: the
+// four lanes of a quad hold one 32-column chunk, so the chunk's largest magnitude and digit sum
+// take two DPP steps each.
+template <int BITS>
+__device__ __forceinline__ void emit_digits8(const float (&v)[8], int j0, uint8_t* __restrict__ dig,
+                                             int* __restrict__ dexp, float* __restrict__ dsum) {
+  constexpr int CPW = 32 / BITS, PER = 8 / BITS;
+  float mx = 0.f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) mx = fmaxf(mx, fabsf(v[k]));
+  mx = fmaxf(mx, __int_as_float(quad_xor1(__float_as_int(mx))));
+  mx = fmaxf(mx, __int_as_float(quad_xor2(__float_as_int(mx))));
+  const int e = max(int((__float_as_uint(mx) >> 23) & 0xFFu) - 126, -100);
+  const float up = __uint_as_float(uint32_t(127 + 21 - e) << 23);  // 2^(21 - e)
+  const int c = j0 >> 5, jc = j0 & 31;
+  int sx = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int X = int(rintf(v[k] * up));  // |X| <= 2^21
+    sx += X;
+    const int col = jc + k, w = col / CPW, rem = col % CPW, g = rem % PER, i = rem / PER;
+    uint8_t* base = dig + c * 96 + (w * PER + g) * 4 + i;
+    base[0] = uint8_t(X >> 16);
+    base[32] = uint8_t(X >> 8);
+    base[64] = uint8_t(X);
+  }
+  sx += quad_xor1(sx);
+  sx += quad_xor2(sx);
+  if (jc == 0) {
+    dexp[c] = e;
+    dsum[c] = float(sx) / up;
+  }
+}
+
+// ---- one vector, 2- and 4-bit codes: the persistent GEMV -------------------------------------
+// A workgroup first puts the digits of x' in LDS, then walks its row blocks (4 * RPW rows each:
+// blockIdx.x, + gridDim.x, ...) in tiles of 128 lane steps, issuing the code, scale and zero
+// loads of the next tile before the dot products of the current one. Every load is issued
+// unconditionally (indices clamped into range), so the wait for a tile's loads counts exactly
+// the next tile's. With FUSE the workgroup computes x' itself: x and the multipliers are
+// requested before the first tile's codes, so the transform (the Sylvester FWHT of a
+// power-of-two d_in, or the scaling alone) runs while the codes are in flight; it is repeated
+// by every workgroup, which costs less than a separate launch at these sizes.
+// 8 consecutive activations as loaded (16-byte loads), widened to fp32 later
+template <typename T>
+struct RawX;
+template <>
+struct RawX<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = reinterpret_cast<const float4*>(p)[0];
+    b = reinterpret_cast<const float4*>(p)[1];
+  }
+  __device__ __forceinline__ void widen(float* v) const {
+    v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w, v[4] = b.x, v[5] = b.y, v[6] = b.z, v[7] = b.w;
+  }
+};
+template <>
+struct RawX<uint16_t> {
+  uint4 a;
+  __device__ __forceinline__ void load(const uint16_t* p) { a = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ void widen(float* v) const {
+    const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      v[2 * k] = __uint_as_float(w[k] << 16);
+      v[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
+    }
+  }
+};
+
+template <int BITS, int RPW>
+struct TileRegs {
+  uint32_t w[2][RPW][4];
+  float sc[2][RPW], ze[2][RPW];
+};
+
+// tile (k, b): row block blockIdx.x + k * gridDim.x, lane steps [128 b, 128 b + 128)
+template <int BITS, int RPW>
+__device__ __forceinline__ void load_tile(TileRegs<BITS, RPW>& T, int k, int b, int steps,
+                                          int wave, int lane,
+                                          const uint32_t* __restrict__ packed, int64_t ldp,
+                                          const float* __restrict__ scales,
+                                          const float* __restrict__ zeros, int64_t ldsz,
+                                          unsigned spg, int64_t d_out) {
+  const int64_t rb = blockIdx.x + int64_t(k) * gridDim.x;
+  const int64_t row0 = (rb * 4 + wave) * RPW;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    int st = b * 128 + lane + 64 * q;
+    st = st < steps ? st : steps - 1;
+    const int64_t g = unsigned(st) / spg;  // spg lane steps per quantisation group
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      const int64_t row = row0 + r < d_out ? row0 + r : d_out - 1;
+      const uint4 v = *reinterpret_cast<const uint4*>(packed + row * ldp + int64_t(st) * 4);
+      T.w[q][r][0] = v.x, T.w[q][r][1] = v.y, T.w[q][r][2] = v.z, T.w[q][r][3] = v.w;
+      T.sc[q][r] = scales[row * ldsz + g];
+      T.ze[q][r] = zeros[row * ldsz + g];
+    }
+  }
+}
+
+template <int BITS, int RPW>
+__device__ __forceinline__ void tile_dots(const TileRegs<BITS, RPW>& T, int b, int steps,
+                                          int lane, const uint32_t* __restrict__ sd,
+                                          const int* __restrict__ se,
+                                          const float* __restrict__ ss, float (&acc)[RPW]) {
+  constexpr int UPL = BITS == 2 ? 2 : 1, PER = 8 / BITS;
+  constexpr uint32_t BM = BITS == 2 ? 0x03030303u : 0x0F0F0F0Fu;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int st = b * 128 + lane + 64 * q;
+    if (st < steps) {
+#pragma unroll
+      for (int u = 0; u < UPL; ++u) {
+        const int c = st * UPL + u;
+        const uint32_t* dd = sd + c * 24;
+        uint32_t d0[8], d1[8], d2[8];
+#pragma unroll
+        for (int k = 0; k < 8; k += 4) {
+          const uint4 x0 = *reinterpret_cast<const uint4*>(dd + k);
+          const uint4 x1 = *reinterpret_cast<const uint4*>(dd + 8 + k);
+          const uint4 x2 = *reinterpret_cast<const uint4*>(dd + 16 + k);
+          d0[k] = x0.x, d0[k + 1] = x0.y, d0[k + 2] = x0.z, d0[k + 3] = x0.w;
+          d1[k] = x1.x, d1[k + 1] = x1.y, d1[k + 2] = x1.z, d1[k + 3] = x1.w;
+          d2[k] = x2.x, d2[k + 1] = x2.y, d2[k + 2] = x2.z, d2[k + 3] = x2.w;
+        }
+        const float e = __uint_as_float(uint32_t(127 - 21 + se[c]) << 23);
+        const float xs = ss[c];
+#pragma unroll
+        for (int r = 0; r < RPW; ++r) {
+          int i0 = 0;
+          uint32_t i1 = 0u, i2 = 0u;
+#pragma unroll
+          for (int wi = 0; wi < BITS; ++wi) {
+            const uint32_t word = T.w[q][r][u * BITS + wi];
+#pragma unroll
+            for (int gg = 0; gg < PER; ++gg) {
+              const uint32_t by = (word >> (BITS * gg)) & BM;
+              const int slot = wi * PER + gg;
+              i0 = __builtin_amdgcn_sdot4(int(by), int(d0[slot]), i0, false);
+              i1 = __builtin_amdgcn_udot4(by, d1[slot], i1, false);
+              i2 = __builtin_amdgcn_udot4(by, d2[slot], i2, false);
+            }
+          }
+          const float dot = e * fmaf(float(i0), 65536.f, fmaf(float(i1), 256.f, float(i2)));
+          acc[r] = fmaf(T.sc[q][r], fmaf(-T.ze[q][r], xs, dot), acc[r]);
+        }
+      }
+    }
+  }
+}
+
+template <int RPW>
+__device__ __forceinline__ void flush_rows(float (&acc)[RPW], int k, int wave, int lane,
+                                           int64_t d_out, float* __restrict__ yr) {
+  const int64_t rb = blockIdx.x + int64_t(k) * gridDim.x;
+  const int64_t row0 = (rb * 4 + wave) * RPW;
+#pragma unroll
+  for (int r = 0; r < RPW; ++r) {
+    float v = acc[r];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    if (lane == 0 && row0 + r < d_out) yr[row0 + r] = v;
+    acc[r] = 0.f;
+  }
+}
+
+constexpr int FUSE_MAX_DIN = 8192;
+
+// LDS slot of element j of the staged x': 4 floats of padding after every 128, so that the
+// strided butterfly passes below hit distinct banks (a stride of 256 moves 8 banks)
+__device__ __forceinline__ int xslot(int j) { return j + ((j >> 7) << 2); }
+
+// stages [lo, lo + LB) of the FWHT of d = 256 * 2^LB staged elements: thread tid holds the 2^LB
+// elements whose other index bits spell tid, all in registers for the LB stages
+template <int LB>
+__device__ __forceinline__ void fwht_pass(float* xt, int lo, int tid) {
+  constexpr int E = 1 << LB;
+  const int base = (tid & ((1 << lo) - 1)) | ((tid >> lo) << (lo + LB));
+  float v[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) v[i] = xt[xslot(base + (i << lo))];
+  hadamard_reg<E>(v);
+#pragma unroll
+  for (int i = 0; i < E; ++i) xt[xslot(base + (i << lo))] = v[i];
+}
+
+// the stages of strides 8 .. d/2 of the FWHT of d = 2^k staged elements (those of strides 1, 2, 4
+// are applied in registers while staging), in groups of up to three stages per LDS round trip
+template <int R>
+__device__ __forceinline__ void stage_group_x(float* xt, int d, int lgh, int tid) {
+  const int hm = (1 << lgh) - 1;
+  for (int q = tid; q < d / R; q += 256) {
+    const int base = ((q >> lgh) * (R << lgh)) + (q & hm);
+    float v[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) v[i] = xt[xslot(base + (i << lgh))];
+    hadamard_reg<R>(v);
+#pragma unroll
+    for (int i = 0; i < R; ++i) xt[xslot(base + (i << lgh))] = v[i];
+  }
+}
+__device__ __forceinline__ void fwht_x(float* xt, int d, int tid) {
+  if (d == 8192) {  // stages 3-7 and 8-12, 32 elements per thread
+    fwht_pass<5>(xt, 3, tid);
+    __syncthreads();
+    fwht_pass<5>(xt, 8, tid);
+    __syncthreads();
+    return;
+  }
+  if (d == 4096) {  // stages 3-6, 7-10, then 11
+    fwht_pass<4>(xt, 3, tid);
+    __syncthreads();
+    fwht_pass<4>(xt, 7, tid);
+    __syncthreads();
+    stage_group_x<2>(xt, d, 11, tid);
+    __syncthreads();
+    return;
+  }
+  for (int lgh = 3; (1 << lgh) < d;) {
+    const int left = d >> lgh;
+    if (left >= 8) {
+      stage_group_x<8>(xt, d, lgh, tid);
+      lgh += 3;
+    } else if (left == 4) {
+      stage_group_x<4>(xt, d, lgh, tid);
+      lgh += 2;
+    } else {
+      stage_group_x<2>(xt, d, lgh, tid);
+      lgh += 1;
+    }
+    __syncthreads();
+  }
+}  // x and its multipliers held in registers: 32 per thread
+
+template <int BITS, int RPW, int FUSE, typename TX>
+__global__ __launch_bounds__(256) void online_gemv_p(
+    const uint32_t* __restrict__ packed, int64_t ldp, const float* __restrict__ scales,
+    const float* __restrict__ zeros, int64_t ldsz, int group, int64_t d_out, int64_t d_in,
+    const uint32_t* __restrict__ dig, const int* __restrict__ dexp,
+    const float* __restrict__ dsum, const TX* __restrict__ x, const float* __restrict__ mul,
+    int rotate, float norm, float* __restrict__ yr) {
+  extern __shared__ __attribute__((aligned(16))) uint32_t sm[];
+  constexpr int UPL = BITS == 2 ? 2 : 1;
+  const int nch = int(d_in / 32);
+  uint32_t* sd = sm;                                  // nch x 24 digit dwords
+  int* se = reinterpret_cast<int*>(sm + nch * 24);    // nch exponents
+  float* ss = reinterpret_cast<float*>(se + nch);     // nch chunk sums
+  float* xt = ss + nch;  // FUSE: d_in + d_in / 32 floats (slots xslot(j)), 16-byte aligned
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int steps = nch / UPL, nbase = (steps + 127) / 128;
+  const unsigned spg = unsigned(group / (32 * UPL));
+  const int64_t nblk = cdiv(d_out, 4 * RPW);
+  const int nrb = int((nblk - 1 - blockIdx.x) / gridDim.x + 1);  // row blocks (grid <= nblk)
+  // FUSE: x and the multipliers, 8 consecutive elements per thread and step, requested
+  // unconditionally (indices clamped; a missing mul reads x's first bytes and is not used) and
+  // widened only after the first tile's loads are out
+  RawX<TX> xr[FUSE ? 4 : 1];
+  float4 mr[FUSE ? 8 : 1];
+  if constexpr (FUSE) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int j0 = 8 * (tid + 256 * k), j = j0 < d_in ? j0 : 0;
+      xr[k].load(x + j);
+      const float4* mp = reinterpret_cast<const float4*>(mul ? mul + j : reinterpret_cast<const float*>(x));
+      mr[2 * k] = mp[0];
+      mr[2 * k + 1] = mp[1];
+    }
+  }
+  TileRegs<BITS, RPW> A, B;
+  load_tile(A, 0, 0, steps, wave, lane, packed, ldp, scales, zeros, ldsz, spg, d_out);
+  if constexpr (FUSE) {
+    // the butterflies of strides 1, 2, 4 on each thread's 8 consecutive values, in registers;
+    // the other stages in LDS; then the digits, a quad of lanes per 32-column chunk
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int j = 8 * (tid + 256 * k);
+      if (j < d_in) {
+        float v[8];
+        xr[k].widen(v);
+        const float m[8] = {mr[2 * k].x, mr[2 * k].y, mr[2 * k].z, mr[2 * k].w,
+                            mr[2 * k + 1].x, mr[2 * k + 1].y, mr[2 * k + 1].z, mr[2 * k + 1].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = mul ? v[e] * m[e] : v[e];
+        if (rotate) hadamard_reg<8>(v);
+        float4* dst = reinterpret_cast<float4*>(xt + xslot(j));  // 8 slots, no padding inside
+        dst[0] = make_float4(v[0], v[1], v[2], v[3]);
+        dst[1] = make_float4(v[4], v[5], v[6], v[7]);
+      }
+    }
+    __syncthreads();
+    if (rotate) fwht_x(xt, int(d_in), tid);  // each group ends with a barrier
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int j = 8 * (tid + 256 * k);
+      if (j < d_in) {  // uniform over each quad (d_in % 32 == 0)
+        const float4 a = reinterpret_cast<const float4*>(xt + xslot(j))[0];
+        const float4 b = reinterpret_cast<const float4*>(xt + xslot(j))[1];
+        const float v[8] = {a.x * norm, a.y * norm, a.z * norm, a.w * norm,
+                            b.x * norm, b.y * norm, b.z * norm, b.w * norm};
+        emit_digits8<BITS>(v, j, reinterpret_cast<uint8_t*>(sd), se, ss);
+      }
+    }
+  } else {
+    for (int i = tid; i < nch * 6; i += 256)
+      reinterpret_cast<uint4*>(sd)[i] = reinterpret_cast<const uint4*>(dig)[i];
+    for (int i = tid; i < nch; i += 256) {
+      se[i] = dexp[i];
+      ss[i] = dsum[i];
+    }
+  }
+  __syncthreads();
+  float acc[RPW];
+#pragma unroll
+  for (int r = 0; r < RPW; ++r) acc[r] = 0.f;
+  // tiles in (row block k, base b) order; (k1, b1) is the tile after (k, b), clamped to the last
+  int k = 0, b = 0;
+  auto next = [&](int& kk, int& bb) {
+    if (++bb == nbase) bb = 0, ++kk;
+    if (kk == nrb) kk = nrb - 1, bb = nbase - 1;
+  };
+  for (;;) {
+    int k1 = k, b1 = b;
+    next(k1, b1);
+    load_tile(B, k1, b1, steps, wave, lane, packed, ldp, scales, zeros, ldsz, spg, d_out);
+    tile_dots(A, b, steps, lane, sd, se, ss, acc);
+    if (b == nbase - 1) flush_rows(acc, k, wave, lane, d_out, yr);
+    if (k == nrb - 1 && b == nbase - 1) break;
+    k = k1, b = b1;
+    next(k1, b1);
+    load_tile(A, k1, b1, steps, wave, lane, packed, ldp, scales, zeros, ldsz, spg, d_out);
+    tile_dots(B, b, steps, lane, sd, se, ss, acc);
+    if (b == nbase - 1) flush_rows(acc, k, wave, lane, d_out, yr);
+    if (k == nrb - 1 && b == nbase - 1) break;
+    k = k1, b = b1;
+  }
+}
+
+// the persistent GEMV for one vector: row blocks of 4 * RPW rows dealt to about two workgroups
+// per CU (fewer where the LDS holds less), in equal shares
+template <int BITS>
+int gemv_pers(bool fuse, const uint32_t* packed, int64_t ldp, const float* scales,
+              const float* zeros, int64_t ldsz, int group, int64_t d_out, int64_t d_in,
+              const uint8_t* dig, const int* dexp, const float* dsum, const void* x, int x_dtype,
+              const float* mul, bool rotate, float* yr, hipStream_t s) {
+  constexpr int RPW = 4;
+  const int64_t nch = d_in / 32;
+  const size_t lds = size_t(nch) * (96 + 8) + (fuse ? size_t(d_in + d_in / 32) * 4 : 0);
+  const int64_t per_cu = lds <= 64 * 1024 ? 2 : 1;
+  const int64_t nblk = cdiv(d_out, 4 * RPW);
+  const int64_t iters = cdiv(nblk, 256 * per_cu);
+  const dim3 grid(static_cast<unsigned>(cdiv(nblk, iters)));
+  const float norm = rotate ? float(1.0 / std::sqrt(double(d_in))) : 1.f;
+  const uint32_t* dg = reinterpret_cast<const uint32_t*>(dig);
+  if (!fuse)
+    return launch("online_gemv", online_gemv_p<BITS, RPW, 0, float>, grid, dim3(256), lds, s,
+                  packed, ldp, scales, zeros, ldsz, group, d_out, d_in, dg, dexp, dsum,
+                  static_cast<const float*>(nullptr), mul, 0, norm, yr);
+  if (x_dtype == KRONQ_BF16)
+    return launch("online_gemv", online_gemv_p<BITS, RPW, 1, uint16_t>, grid, dim3(256), lds, s,
+                  packed, ldp, scales, zeros, ldsz, group, d_out, d_in, dg, dexp, dsum,
+                  static_cast<const uint16_t*>(x), mul, int(rotate), norm, yr);
+  return launch("online_gemv", online_gemv_p<BITS, RPW, 1, float>, grid, dim3(256), lds, s,
+                packed, ldp, scales, zeros, ldsz, group, d_out, d_in, dg, dexp, dsum,
+                static_cast<const float*>(x), mul, int(rotate), norm, yr);
+}
+
 // launch seg_transform for B rows of order d (identity scaling when !rotate); with dig, also the
 // digits of the result (for chunk-aligned segments, else by a separate pass)
 int seg_transform_launch(const void* src, int dtype, int64_t lds_, float* dst, int64_t ldd,
@@ -563,6 +941,22 @@ int online_matvec_launch(const uint32_t* packed, int64_t ldp, const float* scale
   float* dsum = cv.take<float>(nch);
   const int nb = int(batch);
   const bool integer = bits == 2 || bits == 4;  // codes that fill whole bytes of a word
+  const bool rot_in = (flags & KRONQ_ROT_IN) != 0;
+  if (integer && nb == 1) {  // decode: the persistent GEMV, with the input transform inside
+    const bool pow2 = (d_in & (d_in - 1)) == 0;
+    const bool fuse = d_in <= FUSE_MAX_DIN && (!rot_in || pow2);
+    if (!fuse)
+      KQ_TRY(seg_transform_launch(x, x_dtype, ldx, xr, d_in, batch, d_in, mul_in, nullptr, rot_in,
+                                  q28_in, false, s, dig, dexp, dsum, bits));
+    if (bits == 2)
+      KQ_TRY(gemv_pers<2>(fuse, packed, ldp, scales, zeros, ldsz, group, d_out, d_in, dig, dexp,
+                          dsum, x, x_dtype, mul_in, rot_in, yr, s));
+    else
+      KQ_TRY(gemv_pers<4>(fuse, packed, ldp, scales, zeros, ldsz, group, d_out, d_in, dig, dexp,
+                          dsum, x, x_dtype, mul_in, rot_in, yr, s));
+    return seg_transform_launch(yr, KRONQ_FP32, d_out, y, ldy, batch, d_out, nullptr, mul_out,
+                                (flags & KRONQ_ROT_OUT) != 0, q28_out, true, s);
+  }
   // x' = V S_X^-1 x (and its digits for the integer GEMV)
   KQ_TRY(seg_transform_launch(x, x_dtype, ldx, xr, d_in, batch, d_in, mul_in, nullptr,
                               (flags & KRONQ_ROT_IN) != 0, q28_in, false, s,

@@ -322,8 +322,9 @@ def kronq_online_matvec(packed: torch.Tensor, scales: torch.Tensor, zeros: torch
     if x.dim() == 1:
         x = x.view(1, -1)
     batch = x.shape[0]
-    if y is None:
-        y = torch.empty(batch, d_out, dtype=torch.float32, device=x.device)
+    if y is None:  # rows padded to a multiple of 4 floats (16-byte aligned rows)
+        y = torch.empty(batch, (d_out + 3) // 4 * 4, dtype=torch.float32,
+                        device=x.device)[:, :d_out]
     if ws is None:
         ws = workspace(OP_ONLINE, d_out, d_in, batch, x.device)
     rc = load().kronq_online_matvec(
