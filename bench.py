@@ -192,6 +192,7 @@ def online_bench(args, spec, dev) -> int:
     gbytes = d_out * d_in * bits / 8 + 2 * 4 * d_out * (d_in // group) + 4 * d_in + 4 * d_out
     achieved = gbytes / (gemv_ms * 1e-3) / 1e9
     int_path = bits in (2, 4)  # the GEMV on integer dot products; 3- and 8-bit codes use fp32
+    gemv_kernel = "online_gemv_p" if int_path else "online_gemv"  # one vector: persistent
     print(f"[bench] online matvec {ms * 1e3:.2f} us (GEMV kernel {gemv_ms * 1e3:.2f} us), "
           f"dense bf16 GEMV {dense_ms * 1e3:.2f} us", file=sys.stderr, flush=True)
     out = {
@@ -207,7 +208,7 @@ def online_bench(args, spec, dev) -> int:
                    "group": group, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": 8000.0,
                      "unit": "GB/s", "frac": round(achieved / 8000.0, 4), "traffic": None,
-                     "kernel": "online_gemv_int" if int_path else "online_gemv",
+                     "kernel": gemv_kernel,
                      "launches": g_n,
                      "avg_launch_ms": round(gemv_ms, 6)},
         "dense_bf16_gemv_us": round(dense_ms * 1e3, 3),
