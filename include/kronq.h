@@ -279,16 +279,19 @@ int kronq_matrix_stats(const void* M, int dtype, int64_t rows, int64_t cols, int
                        double* out, void* ws, size_t ws_bytes, void* stream);
 
 /* Eigendecomposition of the symmetric H (the eigenvector matrix Q of mu(H) = sqrt(d) max |Q_ij|,
- * eq. incoherence_measure) by cyclic two-sided Jacobi rotations in fp32: each sweep applies
- * every pair rotation once, in d - 1 rounds of d/2 disjoint rotations (round-robin order);
- * a pair is skipped once |a_pq| <= 1e-7 sqrt(|a_pp a_qq|).
- *   H      device fp32 [d x ldh], symmetric (read only; only one triangle needs to be exact).
- *   sweeps 1..64 sweeps (8 to 14 suffice for d <= 8192 in fp32).
+ * eq. incoherence_measure) by block Jacobi in fp32: the order is padded to a multiple of 64
+ * and split into blocks of 32 indices; a sweep visits every pair of blocks once (round-robin,
+ * d/32 - 1 rounds of disjoint pairs), diagonalising the pair's 64 x 64 submatrix by one cyclic
+ * sweep of scalar rotations (skipped once |a_pq| <= 1e-7 sqrt(|a_pp a_qq|)) and applying the
+ * accumulated rotation to the whole matrix and to the eigenvectors.
+ *   H      device fp32 [d x ldh], symmetric (read only; both triangles are read).
+ *   sweeps 1..64 sweeps (about 12 reach the fp32 floor at d = 4096).
  *   evals  device fp32 [d]: the eigenvalues, unsorted; Q device fp32 [d x ldq], column k the
  *          unit eigenvector of evals[k]. Q must not overlap H.
  *   off    device double[1]: ||offdiag(Q^T H Q)||_F / ||H||_F after the last sweep, the
  *          convergence measure.
- *   1 <= d <= 16384. Workspace: KRONQ_OP_EIGH (d as d_in): two d x d fp32 matrices. */
+ *   1 <= d <= 16384. Workspace: KRONQ_OP_EIGH (d as d_in): three N x N fp32 matrices,
+ *   N = d rounded up to a multiple of 64. */
 int kronq_eigh(const float* H, int64_t d, int64_t ldh, int sweeps, float* evals, float* Q,
                int64_t ldq, double* off, void* ws, size_t ws_bytes, void* stream);
 

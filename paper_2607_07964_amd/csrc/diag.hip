@@ -2,8 +2,9 @@
 // Fig. 2; Prop. 2 eq. biip-bound and the optimality table of appendix A.3):
 //  * matrix statistics: max |M_ij|, ||M||_F^2, mu(M), and the coefficients of variation of the
 //    column and row norms, in three deterministic passes (tiles, lines, one final workgroup);
-//  * the symmetric eigendecomposition behind mu(H), by cyclic two-sided Jacobi rotations in the
-//    round-robin order (n/2 disjoint rotations per round, n - 1 rounds per sweep);
+//  * the symmetric eigendecomposition behind mu(H), by block Jacobi: 64 x 64 subproblems of
+//    block pairs solved in LDS by scalar Jacobi rotations, their rotations applied to the whole
+//    matrix as 64 x 64 tile products, block pairs in round-robin order;
 //  * the expected-loss factors of Prop. 2 and the optimality table.
 // Sums are taken in fp64: every square of an fp32 value is exact there.
 #include <cmath>
@@ -146,119 +147,237 @@ __global__ __launch_bounds__(1024) void stat_final(const double* __restrict__ co
   }
 }
 
-// ---- Jacobi eigensolver ----------------------------------------------------------------------
-// Round r pairs the n (even) indices by the circle method: position 0 holds index 0, position
-// k >= 1 holds 1 + (k - 1 + r) mod (n - 1), and pair j joins positions j and n - 1 - j. Every
-// pair of indices meets once in n - 1 rounds.
-__device__ __forceinline__ int64_t rr_index(int64_t k, int64_t r, int64_t n) {
+// ---- block Jacobi eigensolver ----------------------------------------------------------------
+// The order-N matrix (N = d rounded up to a multiple of 64, zero padding) is split into nb = N/32
+// blocks of 32 indices. Round r of a sweep pairs the blocks by the circle method (position 0
+// holds block 0, position k >= 1 block 1 + (k - 1 + r) mod (nb - 1), pair j joins positions j
+// and nb - 1 - j), so every pair of blocks meets once in nb - 1 rounds. For each pair (P, Q) the
+// 64 x 64 principal submatrix S is diagonalised in LDS by cyclic scalar Jacobi rotations,
+// S = Z diag Z^T; then A <- J^T A J and V <- V J with J the block-diagonal (permuted) product of
+// the Z of all pairs of the round. Padding indices have zero rows and columns: their rotations
+// are skipped, so they never mix with real indices.
+constexpr int BJ = 32;  // block size
+constexpr int BT = 64;  // two blocks: the subproblem order and the tile of the update
+constexpr int TS = 68;  // padded LDS row of a tile
+// inner sweeps per block-pair visit at most: the outer sweeps revisit every pair, so one suffices
+// (measured: the same convergence per outer sweep as with two, at half the cost)
+constexpr int kInnerSweeps = 1;
+
+__device__ __forceinline__ int circle(int k, int r, int n) {
   return k == 0 ? 0 : 1 + (k - 1 + r) % (n - 1);
 }
-
-struct Rot {
-  int p, q;
-  float c, s, t;
-};
-
-// The rotation of every pair of round r, from the current matrix: J = [[c, s], [-s, c]] on
-// (p, q) with tau = (a_qq - a_pp) / (2 a_pq), t = sign(tau) / (|tau| + sqrt(1 + tau^2)),
-// c = 1 / sqrt(1 + t^2), s = t c zeroes a_pq (the symmetric 2 x 2 Schur decomposition).
-// Pairs with |a_pq| below 1e-7 sqrt(|a_pp a_qq|), or with the padding index d, are skipped.
-__global__ __launch_bounds__(256) void jacobi_params(const float* __restrict__ A, int64_t lda,
-                                                     int64_t d, int64_t n, int64_t r,
-                                                     Rot* __restrict__ rot) {
-  const int64_t j = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (j >= n / 2) return;
-  const int64_t p = rr_index(j, r, n), q = rr_index(n - 1 - j, r, n);
-  Rot o{int(p), int(q), 1.f, 0.f, 0.f};
-  if (p < d && q < d) {
-    const double app = A[p * lda + p], aqq = A[q * lda + q], apq = A[p * lda + q];
-    if (apq != 0. && fabs(apq) > 1e-7 * sqrt(fabs(app * aqq))) {
-      const double tau = (aqq - app) / (2. * apq);
-      const double t = (tau >= 0. ? 1. : -1.) / (fabs(tau) + sqrt(1. + tau * tau));
-      const double c = 1. / sqrt(1. + t * t);
-      o.c = float(c);
-      o.s = float(t * c);
-      o.t = float(t);
-    }
-  }
-  rot[j] = o;
+// global index of local index m < 64 of the block pair (P, Q)
+__device__ __forceinline__ int64_t pair_index(int m, int P, int Q) {
+  return int64_t(m < BJ ? P : Q) * BJ + (m & (BJ - 1));
 }
 
-// B = J^T A J for all pairs of the round and V <- V J. Thread (row pair k1, column pair k2)
-// computes the 2 x 2 block of B on rows (p1, q1) and columns (p2, q2), and the entries of V on
-// rows (p1, q1) and columns (p2, q2) (in place: no other thread touches them). The diagonal
-// blocks take the exact form: b_pp = a_pp - t a_pq, b_qq = a_qq + t a_pq, b_pq = b_qp = 0.
-__global__ __launch_bounds__(256) void jacobi_apply(const float* __restrict__ A, float* __restrict__ B,
-                                                    int64_t lda, float* __restrict__ V,
-                                                    int64_t ldv, int64_t d, int64_t np,
-                                                    const Rot* __restrict__ rot) {
-  __shared__ Rot rc[64], rr[4];
-  const int tid = threadIdx.x;
-  const int64_t k2 = int64_t(blockIdx.x) * 64 + (tid & 63);
-  const int64_t k1 = int64_t(blockIdx.y) * 4 + (tid >> 6);
-  if (tid < 64 && int64_t(blockIdx.x) * 64 + tid < np) rc[tid] = rot[blockIdx.x * 64 + tid];
-  if (tid >= 64 && tid < 68 && int64_t(blockIdx.y) * 4 + tid - 64 < np)
-    rr[tid - 64] = rot[blockIdx.y * 4 + tid - 64];
-  __syncthreads();
-  if (k1 >= np || k2 >= np) return;
-  const Rot R1 = rr[tid >> 6], R2 = rc[tid & 63];
-  const int64_t p1 = R1.p, q1 = R1.q, p2 = R2.p, q2 = R2.q;
-  const bool hp1 = p1 < d, hq1 = q1 < d, hp2 = p2 < d, hq2 = q2 < d;
-  if (k1 == k2) {
-    if (hp1 && hq1) {
-      const float app = A[p1 * lda + p1], aqq = A[q1 * lda + q1], apq = A[p1 * lda + q1];
-      const float aqp = A[q1 * lda + p1];
-      if (R1.t != 0.f) {
-        B[p1 * lda + p1] = app - R1.t * apq;
-        B[q1 * lda + q1] = aqq + R1.t * apq;
-        B[p1 * lda + q1] = 0.f;
-        B[q1 * lda + p1] = 0.f;
-      } else {
-        B[p1 * lda + p1] = app;
-        B[q1 * lda + q1] = aqq;
-        B[p1 * lda + q1] = apq;
-        B[q1 * lda + p1] = aqp;
+// The rotation J = [[c, s], [-s, c]] on (p, q) that zeroes s_pq (the symmetric 2 x 2 Schur step:
+// tau = (s_qq - s_pp) / (2 s_pq), t = sign(tau) / (|tau| + sqrt(1 + tau^2)), c = 1/sqrt(1+t^2),
+// s = t c), in fp32 (its accuracy sets the convergence rate only: whatever angle results is
+// applied as an orthogonal rotation); skipped (t = 0) when |s_pq| <= 1e-7 sqrt(|s_pp s_qq|). It
+// is applied in Rutishauser's form, (x, y) -> (x - s (y + r x), y + s (x - r y)) with
+// r = s / (1 + c): for small angles c rounds to 1 in fp32 and c x - s y would grow every norm by
+// about s^2 / 2.
+__device__ __forceinline__ void schur2(float spp, float sqq, float spq, float& sn, float& rr,
+                                       float& t) {
+  sn = 0.f, rr = 0.f, t = 0.f;
+  if (spq != 0.f && fabsf(spq) > 1e-7f * sqrtf(fabsf(spp)) * sqrtf(fabsf(sqq))) {
+    const float tau = (sqq - spp) / (2.f * spq);
+    t = (tau >= 0.f ? 1.f : -1.f) / (fabsf(tau) + sqrtf(fmaf(tau, tau, 1.f)));
+    const float c = 1.f / sqrtf(fmaf(t, t, 1.f));
+    sn = t * c;
+    rr = sn / (1.f + c);
+  }
+}
+// (x, y) <- (c x - s y, s x + c y)
+__device__ __forceinline__ void rot2(float& x, float& y, float sn, float rr) {
+  const float x0 = x, y0 = y;
+  x = x0 - sn * fmaf(rr, x0, y0);
+  y = y0 + sn * fmaf(-rr, y0, x0);
+}
+
+// One workgroup per block pair of round r: diagonalise S (inner sweeps until a sweep rotates
+// nothing, at most max_inner) and store its rotation Z (64 x 64, row-major) in zbuf[pair].
+__global__ __launch_bounds__(256) void bjac_solve(const float* __restrict__ A, int64_t lda, int nb,
+                                                  int r, int max_inner, float* __restrict__ zbuf) {
+  __shared__ float S[BT][BT + 1], Z[BT][BT + 1];
+  __shared__ float pr[BT / 2], ps[BT / 2], pt[BT / 2];
+  __shared__ int pp[BT / 2], pq[BT / 2], any_rot;
+  const int tid = threadIdx.x, j = blockIdx.x;
+  const int P = circle(j, r, nb), Q = circle(nb - 1 - j, r, nb);
+  for (int e = tid; e < BT * BT; e += 256) {
+    const int i = e >> 6, c = e & 63;
+    S[i][c] = A[pair_index(i, P, Q) * lda + pair_index(c, P, Q)];
+    Z[i][c] = i == c ? 1.f : 0.f;
+  }
+  for (int sw = 0; sw < max_inner; ++sw) {
+    if (tid == 0) any_rot = 0;
+    __syncthreads();
+    for (int rr = 0; rr < BT - 1; ++rr) {
+      if (tid < BT / 2) {
+        const int p = circle(tid, rr, BT), q = circle(BT - 1 - tid, rr, BT);
+        float sn, rr2, t;
+        schur2(S[p][p], S[q][q], S[p][q], sn, rr2, t);
+        pp[tid] = p, pq[tid] = q, pr[tid] = rr2, ps[tid] = sn, pt[tid] = t;
+        if (t != 0.f) any_rot = 1;
       }
-    } else if (hp1) {
-      B[p1 * lda + p1] = A[p1 * lda + p1];
-    } else if (hq1) {
-      B[q1 * lda + q1] = A[q1 * lda + q1];
+      __syncthreads();
+      // S <- J^T S J (the 2 x 2 block of row pair k1 and column pair k2) and Z <- Z J (row i,
+      // column pair k2), in place: the entries of different work items are disjoint, so all
+      // are read first, then rotated, then written (no load waits on an earlier store)
+      int bp1[4], bq1[4], bp2[4], bq2[4], zi[8], zp2[8], zq2[8];
+      float v[4][4], zv[8][2];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int bi = tid + 256 * u, k1 = bi >> 5, k2 = bi & 31;
+        bp1[u] = pp[k1], bq1[u] = pq[k1], bp2[u] = pp[k2], bq2[u] = pq[k2];
+        v[u][0] = S[bp1[u]][bp2[u]], v[u][1] = S[bp1[u]][bq2[u]];
+        v[u][2] = S[bq1[u]][bp2[u]], v[u][3] = S[bq1[u]][bq2[u]];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = tid + 256 * u, k2 = e & 31;
+        zi[u] = e >> 5, zp2[u] = pp[k2], zq2[u] = pq[k2];
+        zv[u][0] = Z[zi[u]][zp2[u]], zv[u][1] = Z[zi[u]][zq2[u]];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int bi = tid + 256 * u, k1 = bi >> 5, k2 = bi & 31;
+        if (k1 == k2) {  // diagonal block: the exact form
+          const float t = pt[k1], apq = v[u][1];
+          if (t != 0.f) {
+            v[u][0] -= t * apq;
+            v[u][3] += t * apq;
+            v[u][1] = 0.f;
+            v[u][2] = 0.f;
+          }
+        } else {
+          rot2(v[u][0], v[u][1], ps[k2], pr[k2]);  // columns: S J2
+          rot2(v[u][2], v[u][3], ps[k2], pr[k2]);
+          rot2(v[u][0], v[u][2], ps[k1], pr[k1]);  // rows: J1^T (S J2)
+          rot2(v[u][1], v[u][3], ps[k1], pr[k1]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int k2 = (tid + 256 * u) & 31;
+        rot2(zv[u][0], zv[u][1], ps[k2], pr[k2]);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        S[bp1[u]][bp2[u]] = v[u][0], S[bp1[u]][bq2[u]] = v[u][1];
+        S[bq1[u]][bp2[u]] = v[u][2], S[bq1[u]][bq2[u]] = v[u][3];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) Z[zi[u]][zp2[u]] = zv[u][0], Z[zi[u]][zq2[u]] = zv[u][1];
+      __syncthreads();
     }
-  } else {
-    const float a = hp1 && hp2 ? A[p1 * lda + p2] : 0.f;
-    const float b = hp1 && hq2 ? A[p1 * lda + q2] : 0.f;
-    const float e = hq1 && hp2 ? A[q1 * lda + p2] : 0.f;
-    const float f = hq1 && hq2 ? A[q1 * lda + q2] : 0.f;
-    const float a1 = R2.c * a - R2.s * b, b1 = R2.s * a + R2.c * b;  // columns: A J2
-    const float e1 = R2.c * e - R2.s * f, f1 = R2.s * e + R2.c * f;
-    if (hp1 && hp2) B[p1 * lda + p2] = R1.c * a1 - R1.s * e1;  // rows: J1^T (A J2)
-    if (hp1 && hq2) B[p1 * lda + q2] = R1.c * b1 - R1.s * f1;
-    if (hq1 && hp2) B[q1 * lda + p2] = R1.s * a1 + R1.c * e1;
-    if (hq1 && hq2) B[q1 * lda + q2] = R1.s * b1 + R1.c * f1;
+    const int rot = any_rot;
+    __syncthreads();  // every thread has read the flag before the next sweep clears it
+    if (!rot) break;
   }
-  // V <- V J2 on rows p1, q1
-  if (hp2 && hq2) {
-    if (hp1) {
-      const float vp = V[p1 * ldv + p2], vq = V[p1 * ldv + q2];
-      V[p1 * ldv + p2] = R2.c * vp - R2.s * vq;
-      V[p1 * ldv + q2] = R2.s * vp + R2.c * vq;
+  // unit columns: fp32 rotations leave each column's norm about 3e-8 too large on average, and
+  // over the rounds of many sweeps that bias would scale V's columns and A's eigenvalues
+  __shared__ float zs[BT];
+  if (tid < BT) {
+    double n2 = 0.;
+    for (int i = 0; i < BT; ++i) n2 = fma(double(Z[i][tid]), double(Z[i][tid]), n2);
+    zs[tid] = float(1. / sqrt(n2));
+  }
+  __syncthreads();
+  float* zo = zbuf + int64_t(j) * BT * BT;
+  for (int e = tid; e < BT * BT; e += 256) zo[e] = Z[e >> 6][e & 63] * zs[e & 63];
+}
+
+// out (64 x 64, 4 x 4 per thread) = X^T_or_not . Y from LDS tiles: trans selects X^T
+__device__ __forceinline__ void tile_mm(const float (*X)[TS], const float (*Y)[TS], bool trans,
+                                        int tid, float (&acc)[4][4]) {
+  const int r0 = (tid >> 4) * 4, c0 = (tid & 15) * 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) acc[i][jj] = 0.f;
+  for (int k = 0; k < BT; ++k) {
+    float x[4];
+    if (trans) {
+      const float4 v = *reinterpret_cast<const float4*>(&X[k][r0]);
+      x[0] = v.x, x[1] = v.y, x[2] = v.z, x[3] = v.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[i] = X[r0 + i][k];
     }
-    if (hq1) {
-      const float vp = V[q1 * ldv + p2], vq = V[q1 * ldv + q2];
-      V[q1 * ldv + p2] = R2.c * vp - R2.s * vq;
-      V[q1 * ldv + q2] = R2.s * vp + R2.c * vq;
+    const float4 y = *reinterpret_cast<const float4*>(&Y[k][c0]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[i][0] = fmaf(x[i], y.x, acc[i][0]);
+      acc[i][1] = fmaf(x[i], y.y, acc[i][1]);
+      acc[i][2] = fmaf(x[i], y.z, acc[i][2]);
+      acc[i][3] = fmaf(x[i], y.w, acc[i][3]);
     }
   }
 }
 
-// A = H (d x d, dense copy), V = I
-__global__ __launch_bounds__(256) void jacobi_init(const float* __restrict__ H, int64_t ldh,
-                                                   float* __restrict__ A, int64_t lda,
-                                                   float* __restrict__ V, int64_t ldv, int64_t d) {
+// Tile (x, y) of the round's update: for y < np, B[rows of pair y][cols of pair x] =
+// Z_y^T A[...][...] Z_x (from A, into the other buffer B); for y >= np, the 64 rows starting at
+// 64 (y - np) of V times Z_x, in place (the workgroup holds its tile in LDS before writing it).
+__global__ __launch_bounds__(256) void bjac_apply(const float* __restrict__ A, float* __restrict__ B,
+                                                  float* __restrict__ V, int64_t lda, int nb, int r,
+                                                  const float* __restrict__ zbuf) {
+  __shared__ __attribute__((aligned(16))) float X[BT][TS], Zt[BT][TS], W[BT][TS];
+  const int tid = threadIdx.x, np = nb / 2;
+  const int kx = blockIdx.x, ky = blockIdx.y;
+  const int P2 = circle(kx, r, nb), Q2 = circle(nb - 1 - kx, r, nb);
+  const bool vt = ky >= np;
+  int P1 = 0, Q1 = 0;
+  if (!vt) P1 = circle(ky, r, nb), Q1 = circle(nb - 1 - ky, r, nb);
+  const int64_t vrow0 = int64_t(ky - np) * BT;
+  for (int e = tid; e < BT * BT; e += 256) {
+    const int i = e >> 6, c = e & 63;
+    const int64_t row = vt ? vrow0 + i : pair_index(i, P1, Q1);
+    X[i][c] = (vt ? V : A)[row * lda + pair_index(c, P2, Q2)];
+    Zt[i][c] = zbuf[int64_t(kx) * BT * BT + e];
+  }
+  __syncthreads();
+  float acc[4][4];
+  tile_mm(X, Zt, false, tid, acc);  // X Z_x
+  const int r0 = (tid >> 4) * 4, c0 = (tid & 15) * 4;
+  if (vt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) V[(vrow0 + r0 + i) * lda + pair_index(c0 + jj, P2, Q2)] = acc[i][jj];
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) W[r0 + i][c0 + jj] = acc[i][jj];
+  __syncthreads();  // W complete; Zt free
+  for (int e = tid; e < BT * BT; e += 256) Zt[e >> 6][e & 63] = zbuf[int64_t(ky) * BT * BT + e];
+  __syncthreads();
+  tile_mm(Zt, W, true, tid, acc);  // Z_y^T (X Z_x)
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj)
+      B[pair_index(r0 + i, P1, Q1) * lda + pair_index(c0 + jj, P2, Q2)] = acc[i][jj];
+}
+
+// A = H padded with zeros to N x N, V = I (N x N)
+__global__ __launch_bounds__(256) void bjac_init(const float* __restrict__ H, int64_t ldh, int64_t d,
+                                                 float* __restrict__ A, float* __restrict__ V,
+                                                 int64_t N) {
   const int64_t i = blockIdx.y, j = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (j >= d) return;
-  A[i * lda + j] = H[i * ldh + j];
-  V[i * ldv + j] = i == j ? 1.f : 0.f;
+  if (j >= N) return;
+  A[i * N + j] = (i < d && j < d) ? H[i * ldh + j] : 0.f;
+  V[i * N + j] = i == j ? 1.f : 0.f;
+}
+
+// Q = the leading d x d block of V
+__global__ __launch_bounds__(256) void bjac_out(const float* __restrict__ V, int64_t N, int64_t d,
+                                                float* __restrict__ Q, int64_t ldq) {
+  const int64_t i = blockIdx.y, j = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (j < d) Q[i * ldq + j] = V[i * N + j];
 }
 
 // per-row fp64 sums of squares of A (off-diagonal only when off != 0)
@@ -404,45 +523,49 @@ int matrix_stats_launch(const void* M, int dtype, int64_t rows, int64_t cols, in
 
 size_t eigh_ws_bytes(int64_t d) {
   if (d <= 0) return 0;
-  const int64_t n = d + (d & 1);
-  return 2 * align256(size_t(d) * size_t(d) * 4) + align256(size_t(n / 2) * sizeof(Rot)) +
+  const int64_t N = cdiv(d, BT) * BT;
+  return 3 * align256(size_t(N) * size_t(N) * 4) + align256(size_t(N / BT) * BT * BT * 4) +
          2 * align256(size_t(d) * 8) + 256;
 }
 
 int eigh_launch(const float* H, int64_t d, int64_t ldh, int sweeps, float* evals, float* Q,
                 int64_t ldq, double* off, void* ws, hipStream_t s) {
   Carver cv(ws);
-  const int64_t n = d + (d & 1), np = n / 2;
-  float* A0 = cv.take<float>(size_t(d) * size_t(d));
-  float* A1 = cv.take<float>(size_t(d) * size_t(d));
-  Rot* rot = cv.take<Rot>(size_t(np));
+  const int64_t N = cdiv(d, BT) * BT;
+  const int nb = int(N / BJ), np = nb / 2;
+  float* A0 = cv.take<float>(size_t(N) * size_t(N));
+  float* A1 = cv.take<float>(size_t(N) * size_t(N));
+  float* V = cv.take<float>(size_t(N) * size_t(N));
+  float* zbuf = cv.take<float>(size_t(np) * BT * BT);
   double* hsq = cv.take<double>(size_t(d));
   double* osq = cv.take<double>(size_t(d));
-  KQ_TRY(launch("diag_jacobi_init", jacobi_init,
-                dim3(static_cast<unsigned>(cdiv(d, 256)), static_cast<unsigned>(d)), dim3(256), 0,
-                s, H, ldh, A0, d, Q, ldq, d));
+  KQ_TRY(launch("diag_bjac_init", bjac_init,
+                dim3(static_cast<unsigned>(cdiv(N, 256)), static_cast<unsigned>(N)), dim3(256), 0,
+                s, H, ldh, d, A0, V, N));
   KQ_TRY(launch("diag_row_squares", row_squares, dim3(static_cast<unsigned>(d)), dim3(256), 0,
-                s, static_cast<const float*>(A0), d, d, 0, hsq));
-  const dim3 pgrid(static_cast<unsigned>(cdiv(np, 256)));
-  const dim3 agrid(static_cast<unsigned>(cdiv(np, 64)), static_cast<unsigned>(cdiv(np, 4)));
+                s, static_cast<const float*>(A0), N, d, 0, hsq));
   float* cur = A0;
   float* nxt = A1;
   for (int sw = 0; sw < sweeps; ++sw) {
-    for (int64_t r = 0; r < n - 1; ++r) {
-      KQ_TRY(launch("diag_jacobi_params", jacobi_params, pgrid, dim3(256), 0, s,
-                    static_cast<const float*>(cur), d, d, n, r, rot));
-      KQ_TRY(launch("diag_jacobi_apply", jacobi_apply, agrid, dim3(256), 0, s,
-                    static_cast<const float*>(cur), nxt, d, Q, ldq, d, np,
-                    static_cast<const Rot*>(rot)));
+    for (int r = 0; r < nb - 1; ++r) {
+      KQ_TRY(launch("diag_bjac_solve", bjac_solve, dim3(static_cast<unsigned>(np)), dim3(256), 0,
+                    s, static_cast<const float*>(cur), N, nb, r, kInnerSweeps, zbuf));
+      KQ_TRY(launch("diag_bjac_apply", bjac_apply,
+                    dim3(static_cast<unsigned>(np), static_cast<unsigned>(np + N / BT)),
+                    dim3(256), 0, s, static_cast<const float*>(cur), nxt, V, N, nb, r,
+                    static_cast<const float*>(zbuf)));
       float* t = cur;
       cur = nxt;
       nxt = t;
     }
   }
+  KQ_TRY(launch("diag_bjac_out", bjac_out,
+                dim3(static_cast<unsigned>(cdiv(d, 256)), static_cast<unsigned>(d)), dim3(256), 0,
+                s, static_cast<const float*>(V), N, d, Q, ldq));
   KQ_TRY(launch("diag_row_squares", row_squares, dim3(static_cast<unsigned>(d)), dim3(256), 0,
-                s, static_cast<const float*>(cur), d, d, 1, osq));
+                s, static_cast<const float*>(cur), N, d, 1, osq));
   return launch("diag_jacobi_finish", jacobi_finish, dim3(1), dim3(1024), 0, s,
-                static_cast<const float*>(cur), d, d, static_cast<const double*>(hsq),
+                static_cast<const float*>(cur), N, d, static_cast<const double*>(hsq),
                 static_cast<const double*>(osq), evals, off);
 }
 
