@@ -20,6 +20,9 @@ The JSON line carries
     inside the timed region, algorithmic flops N d (d + 1) per launch, against the 2.5 PFLOP/s
     dense bf16 MFMA peak; HBM traffic from the committed rocprofv3 counter summary when it was
     taken on the current kernel source;
+  * shared_covariance: when the two-stream schedule runs the H_G covariance on part of the chip
+    beside the factorisation (a separately named launch of the same kernel), its time and its
+    fraction of the peak of the CUs it held; the roofline then covers the whole-chip H_X launch;
   * cpu_baseline: the float64 oracle on this host's cores on a bounded sample (the covariances
     on the first --cpu-tokens tokens, scaled linearly to N; every other step at full size).
 """
@@ -40,9 +43,9 @@ PEAK_BF16_TFLOPS = 2500.0
 # fp32 FMAs on the vector units without packed instructions: 256 CUs x 4 SIMDs x 16 lanes x
 # 2 flops x 2.4 GHz
 PEAK_FP32_VALU = 78.6
-TRAFFIC_FILES = {k: os.path.join(ROOT, "profiles", f"{k.replace('_mfma', '')}_traffic.json")
-                 for k in ("syrk_bf16_mfma", "cross_bf16_mfma")}
-KERNELS = ["syrk_bf16_mfma", "syrk_reduce", "cross_bf16_mfma", "cross_reduce", "traces",
+def traffic_file(kernel: str, workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"{kernel.replace('_mfma', '')}_{workload}_traffic.json")
+KERNELS = ["syrk_bf16_mfma", "syrk_bf16_mfma_shared", "syrk_reduce", "cross_bf16_mfma", "cross_reduce", "traces",
            "rot_w_norms", "rot_factors", "rot_inv_factors", "rot_row_pass", "fwht_col",
            "mix28_col", "chol_diag_shift", "chol_add_diag", "chol_reverse_copy",
            "chol_potrf_diag", "chol_trsm", "chol_syrk", "trtri_row", "trtri_put_diag",
@@ -56,10 +59,11 @@ def cov_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def traffic(kernel: str):
-    """HBM bytes per launch from the rocprofv3 FETCH_SIZE/WRITE_SIZE summary (or None)."""
-    path = TRAFFIC_FILES.get(kernel)
-    if path is None or not os.path.exists(path):
+def traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the rocprofv3 FETCH_SIZE/WRITE_SIZE summary of this kernel on
+    this workload (or None)."""
+    path = traffic_file(kernel, workload)
+    if not os.path.exists(path):
         return None
     t = json.load(open(path))
     if t.get("cov_source_sha256_16") != cov_source_hash():
@@ -441,7 +445,8 @@ def main() -> int:
     L.check(st)
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
-    K.kronq_profile_only(dominant)
+    SHARED = "syrk_bf16_mfma_shared"  # the H_G covariance on part of the chip (two streams)
+    K.kronq_profile_only(f"{dominant},{SHARED}")
     K.kronq_profile_reset()
     K.kronq_profile_enable(True)
     torch.cuda.synchronize()
@@ -452,23 +457,35 @@ def main() -> int:
     t1 = time.perf_counter()
     K.kronq_profile_enable(False)
     dom_ms, dom_n = K.kronq_profile_read(dominant)
+    sh_ms, sh_n = K.kronq_profile_read(SHARED)
     L.check(st)
     ms_step = (t1 - t0) * 1e3 / args.steps
     print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
 
     # dominant kernel roofline: algorithmic flops N d (d + 1) per covariance launch (averaged
-    # over the two covariances), 2 N d_in^2 for the drift statistic
+    # over the covariances run on the whole chip: both, or H_X alone when H_G ran beside the
+    # factorisation on part of the chip), 2 N d_in^2 for the drift statistic
+    fl_x = float(spec.n_tokens) * spec.d_in * (spec.d_in + 1)
+    fl_g = float(spec.n_tokens) * spec.d_out * (spec.d_out + 1)
     if args.drift:
         flops = 2.0 * spec.n_tokens * spec.d_in * spec.d_in
     else:
-        flops = float(spec.n_tokens) * (spec.d_in * (spec.d_in + 1) +
-                                        spec.d_out * (spec.d_out + 1)) / 2
+        flops = fl_x if sh_n else (fl_x + fl_g) / 2
     avg_ms = dom_ms / max(dom_n, 1)
     achieved = flops / (avg_ms * 1e-3) / 1e12
     roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": traffic(dominant), "kernel": dominant, "launches": dom_n,
+            "traffic": traffic(dominant, args.workload), "kernel": dominant, "launches": dom_n,
             "avg_launch_ms": round(avg_ms, 4)}
+    shared = None
+    if sh_n:
+        cus = L._cov_cus(dev, spec.n_tokens, spec.d_out, spec.d_in)
+        sh_avg = sh_ms / sh_n
+        sh_tf = fl_g / (sh_avg * 1e-3) / 1e12
+        part_peak = PEAK_BF16_TFLOPS * cus / torch.cuda.get_device_properties(dev).multi_processor_count
+        shared = {"kernel": SHARED, "cus": cus, "launches": sh_n, "avg_launch_ms": round(sh_avg, 4),
+                  "achieved": round(sh_tf, 2), "peak_of_its_cus": round(part_peak, 1),
+                  "frac_of_its_cus": round(sh_tf / part_peak, 4)}
 
     breakdown = None
     if args.breakdown:
@@ -507,6 +524,8 @@ def main() -> int:
                    "schedule": "one stream" if args.serial else "two streams"},
         "roofline": roof, "cpu_baseline": cpu,
     }
+    if shared is not None:
+        out["shared_covariance"] = shared
     if breakdown is not None:
         out["kernels_ms"] = breakdown
     print(json.dumps(out), flush=True)

@@ -115,6 +115,16 @@ int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, in
                          float* H, int64_t ldh, float alpha, float beta, void* ws,
                          size_t ws_bytes, void* stream);
 
+/* As kronq_accumulate_cov, with the bf16 interior-tile kernel holding at most max_cus compute
+ * units at once (persistent workgroups, one per CU, rounded down to a multiple of 8; 0: the
+ * whole chip). For a caller that runs latency-bound work on another stream meanwhile (the
+ * factorisation beside the H_G covariance): a covariance workgroup holds its CU for the whole
+ * of its tile, so without a cap the other stream's kernels wait for CUs. Results are identical
+ * to kronq_accumulate_cov. max_cus < 0: KRONQ_ERR_INVALID_ARG. */
+int kronq_accumulate_cov_limited(const void* A, int dtype, int64_t n_rows, int64_t d,
+                                 int64_t lda, float* H, int64_t ldh, float alpha, float beta,
+                                 int max_cus, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- 1b. drift statistic (Alg. 1 first line; eq. gptaq_obj) ------------------------------
  * C <- beta * C + alpha * A^T B for token-major A, B [n_rows x d] with the same leading
  * dimension ld; every entry of the d x d matrix C is written (it is not symmetric). With
@@ -341,8 +351,8 @@ int kronq_allocate_bits(const double* scores, const int64_t* weights, int n_laye
  * synchronises the recorded events and returns the summed milliseconds and the launch count
  * of the named kernel (0 if never launched). Not thread-safe; meant for benchmarks. */
 int kronq_profile_enable(int on);
-/* Restrict the profiler to launches of one kernel name (NULL or "": every kernel), so that
- * timing one kernel adds no events around the others. */
+/* Restrict the profiler to launches of the named kernels (one name or a comma-separated list;
+ * NULL or "": every kernel), so that timing them adds no events around the others. */
 int kronq_profile_only(const char* kernel);
 void kronq_profile_reset(void);
 int kronq_profile_read(const char* kernel, double* total_ms, int64_t* launches);

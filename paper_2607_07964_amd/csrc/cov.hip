@@ -269,12 +269,21 @@ __device__ __forceinline__ void gram_dma(const uint16_t* __restrict__ A,
                                          const uint16_t* __restrict__ B,
                                          int64_t n_rows, int64_t lda,
                                                         float* __restrict__ part, int n_slices,
-                                                        int64_t rows_per_slice, int T, int Tf) {
+                                                        int64_t rows_per_slice, int T, int Tf,
+                                                        int n_items) {
   __shared__ __attribute__((aligned(16))) uint32_t a0[SBUF], a1[SBUF], a2[SBUF], a3[SBUF];
   __shared__ __attribute__((aligned(16))) uint32_t b0[SBUF], b1[SBUF], b2[SBUF], b3[SBUF];
   uint32_t* const bufa[RING] = {a0, a1, a2, a3};
   uint32_t* const bufb[RING] = {b0, b1, b2, b3};
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid_launch = threadIdx.x;
+  // work items b = blockIdx.x, + gridDim.x, ...: one per workgroup unless the launch caps its
+  // workgroups (gridDim.x a multiple of 8 then, so that b % 8 stays the workgroup's XCD)
+  for (int item = int(blockIdx.x); item < n_items; item += int(gridDim.x)) {
+  // an opaque copy of the thread index per item: the lane-dependent addresses are then formed
+  // inside the loop, not hoisted out of it into hundreds of live (spilled) registers
+  int tid = tid_launch;
+  asm volatile("" : "+v"(tid));
+  const int wave = tid >> 6, lane = tid & 63;
   // work item: with S a multiple of 8, XCD x = b % 8 (workgroups are dealt round-robin over the
   // 8 XCDs) runs the tiles of its slices x, x + 8, ... one slice after another, so the
   // workgroups that run together on an XCD read the same tokens through its L2; otherwise
@@ -282,12 +291,12 @@ __device__ __forceinline__ void gram_dma(const uint16_t* __restrict__ A,
   const int ntile = CROSS ? Tf * Tf : Tf * (Tf + 1) / 2;
   int slice, rem;
   if ((n_slices & 7) == 0) {
-    const int kk = int(blockIdx.x >> 3);
-    slice = (kk / ntile) * 8 + int(blockIdx.x & 7);
+    const int kk = item >> 3;
+    slice = (kk / ntile) * 8 + (item & 7);
     rem = kk % ntile;
   } else {
-    slice = int(blockIdx.x) % n_slices;
-    rem = int(blockIdx.x) / n_slices;
+    slice = item % n_slices;
+    rem = item / n_slices;
   }
   // tile (I <= J; any I, J for cross) of sequence number rem: panels of PJ tile columns, within
   // a panel by rows, so that the 32 workgroups running together on an XCD form an 8 x 4 block of
@@ -468,6 +477,8 @@ __device__ __forceinline__ void gram_dma(const uint16_t* __restrict__ A,
         const int col = wn * 128 + bj * 32 + l32;
         out[row * TT + col] = acc[bi][bj][r];
       }
+  __syncthreads();  // the ring's last reads are done before the next item's loads overwrite it
+  }
 }
 
 // Sum the S partial tiles of one 64 x 64 sub-block and write H (and its mirror; cross: the
@@ -575,12 +586,16 @@ __global__ __launch_bounds__(256, 1) void cross_bf16_partial(KQ_GRAM_PARTIAL_ARG
 }
 #define KQ_GRAM_DMA_ARGS                                                                  \
   const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, int64_t n_rows, int64_t lda, \
-      float *__restrict__ part, int n_slices, int64_t rows_per_slice, int T, int Tf
+      float *__restrict__ part, int n_slices, int64_t rows_per_slice, int T, int Tf, int n_items
 __global__ __launch_bounds__(256, 1) void syrk_bf16_dma(KQ_GRAM_DMA_ARGS) {
-  gram_dma<false>(A, B, n_rows, lda, part, n_slices, rows_per_slice, T, Tf);
+  gram_dma<false>(A, B, n_rows, lda, part, n_slices, rows_per_slice, T, Tf, n_items);
+}
+// the same kernel for a launch that holds part of the chip (its own name in profiles)
+__global__ __launch_bounds__(256, 1) void syrk_bf16_dma_shared(KQ_GRAM_DMA_ARGS) {
+  gram_dma<false>(A, B, n_rows, lda, part, n_slices, rows_per_slice, T, Tf, n_items);
 }
 __global__ __launch_bounds__(256, 1) void cross_bf16_dma(KQ_GRAM_DMA_ARGS) {
-  gram_dma<true>(A, B, n_rows, lda, part, n_slices, rows_per_slice, T, Tf);
+  gram_dma<true>(A, B, n_rows, lda, part, n_slices, rows_per_slice, T, Tf, n_items);
 }
 #define KQ_GRAM_REDUCE_ARGS                                                                \
   const float *__restrict__ part, int n_slices, int T, int64_t d, float *__restrict__ H,   \
@@ -721,21 +736,30 @@ CovPlan cov_plan(int64_t n_rows, int64_t d, bool cross) {
 }
 
 // the bf16 pipeline shared by the covariance (B == nullptr) and the cross product
+// max_cus > 0: the interior-tile launch holds at most that many CUs at once (persistent
+// workgroups, one per CU, a multiple of 8), leaving the rest of the chip to other streams
 int gram_bf16(const uint16_t* A, const uint16_t* B, int64_t n_rows, int64_t d, int64_t lda,
-              float* H, int64_t ldh, float alpha, float beta, void* ws, hipStream_t s) {
+              float* H, int64_t ldh, float alpha, float beta, void* ws, int max_cus,
+              hipStream_t s) {
   const bool cross = B != nullptr;
   const CovPlan p = cov_plan(n_rows, d, cross);
   float* part = static_cast<float*>(ws);
   const int64_t full = cross ? int64_t(p.Tf) * p.Tf : int64_t(p.Tf) * (p.Tf + 1) / 2;
   // interior tiles, whole 32-token stages of every slice
   if (p.Tf > 0) {
-    const dim3 grid(unsigned(int64_t(p.S) * full));
+    const int64_t items = int64_t(p.S) * full;
+    int64_t wgs = items;
+    if (max_cus > 0 && items > max_cus) wgs = max_cus >= 8 ? (max_cus / 8) * 8 : max_cus;
+    const dim3 grid(static_cast<unsigned>(wgs));
     if (cross)
       KQ_TRY(launch("cross_bf16_mfma", cross_bf16_dma, grid, dim3(256), 0, s, A, B, n_rows,
-                    lda, part, p.S, p.rows_per_slice, p.T, p.Tf));
+                    lda, part, p.S, p.rows_per_slice, p.T, p.Tf, int(items)));
+    else if (wgs < items)
+      KQ_TRY(launch("syrk_bf16_mfma_shared", syrk_bf16_dma_shared, grid, dim3(256), 0, s, A, A,
+                    n_rows, lda, part, p.S, p.rows_per_slice, p.T, p.Tf, int(items)));
     else
       KQ_TRY(launch("syrk_bf16_mfma", syrk_bf16_dma, grid, dim3(256), 0, s, A, A, n_rows,
-                    lda, part, p.S, p.rows_per_slice, p.T, p.Tf));
+                    lda, part, p.S, p.rows_per_slice, p.T, p.Tf, int(items)));
   }
   // tiles of a ragged last channel block, same tokens
   const int64_t body_end = p.tail ? p.tail_begin : n_rows;
@@ -775,7 +799,8 @@ size_t cov_ws_bytes(int dtype, int64_t n_rows, int64_t d, bool cross) {
 }
 
 int cov_launch(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d, int64_t lda,
-               float* H, int64_t ldh, float alpha, float beta, void* ws, hipStream_t s) {
+               float* H, int64_t ldh, float alpha, float beta, void* ws, hipStream_t s,
+               int max_cus) {
   if (n_rows == 0) {
     return launch("cov_scale", scale_matrix, dim3(unsigned(cdiv(d, 256)), unsigned(d)), dim3(256),
                   0, s, H, d, ldh, beta);
@@ -787,7 +812,7 @@ int cov_launch(const void* A, const void* B, int dtype, int64_t n_rows, int64_t 
                   B ? static_cast<const float*>(B) : a, n_rows, d, lda, H, ldh, alpha, beta);
   }
   return gram_bf16(static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), n_rows, d,
-                   lda, H, ldh, alpha, beta, ws, s);
+                   lda, H, ldh, alpha, beta, ws, max_cus, s);
 }
 
 }  // namespace kq

@@ -101,8 +101,10 @@ RotDim rot_dim(int64_t d);
 // covariance
 // covariance (B == nullptr: H = A^T A, symmetric) or cross product (H = A^T B, all tiles)
 size_t cov_ws_bytes(int dtype, int64_t n_rows, int64_t d, bool cross = false);
+// max_cus > 0 caps the CUs the interior-tile launch holds at once (0: the whole chip)
 int cov_launch(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d, int64_t lda,
-               float* H, int64_t ldh, float alpha, float beta, void* ws, hipStream_t s);
+               float* H, int64_t ldh, float alpha, float beta, void* ws, hipStream_t s,
+               int max_cus = 0);
 // traces
 int traces_launch(const float* HX, int64_t d_in, int64_t ldx, const float* HG, int64_t d_out,
                   int64_t ldg, double* out3, hipStream_t s);

@@ -64,7 +64,19 @@ void clear_error() { g_err[0] = '\0'; }
 
 bool prof_on() { return g_prof; }
 
-bool prof_wants(const char* name) { return g_prof_only.empty() || g_prof_only == name; }
+// g_prof_only: empty (every kernel), or kernel names separated by commas
+bool prof_wants(const char* name) {
+  if (g_prof_only.empty()) return true;
+  const std::string n(name);
+  size_t b = 0;
+  while (b <= g_prof_only.size()) {
+    size_t e = g_prof_only.find(',', b);
+    if (e == std::string::npos) e = g_prof_only.size();
+    if (g_prof_only.compare(b, e - b, n) == 0 && e - b == n.size()) return true;
+    b = e + 1;
+  }
+  return false;
+}
 
 void prof_begin(const char* name, hipStream_t s) {
   (void)name;

@@ -114,7 +114,15 @@ size_t kronq_workspace_bytes(int op, int64_t d_out, int64_t d_in, int64_t n_rows
 int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
                          float* H, int64_t ldh, float alpha, float beta, void* ws,
                          size_t ws_bytes, void* stream) {
+  return kronq_accumulate_cov_limited(A, dtype, n_rows, d, lda, H, ldh, alpha, beta, 0, ws,
+                                      ws_bytes, stream);
+}
+
+int kronq_accumulate_cov_limited(const void* A, int dtype, int64_t n_rows, int64_t d,
+                                 int64_t lda, float* H, int64_t ldh, float alpha, float beta,
+                                 int max_cus, void* ws, size_t ws_bytes, void* stream) {
   kq::clear_error();
+  KQ_REQUIRE(max_cus >= 0, KRONQ_ERR_INVALID_ARG, "max_cus must be >= 0");
   KQ_REQUIRE(valid_dtype(dtype), KRONQ_ERR_INVALID_ARG, "dtype must be KRONQ_BF16 or KRONQ_FP32");
   KQ_REQUIRE(H, KRONQ_ERR_INVALID_ARG, "H is NULL");
   KQ_REQUIRE(n_rows >= 0 && d >= 1 && d <= 65535, KRONQ_ERR_INVALID_ARG,
@@ -131,7 +139,7 @@ int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, in
     KQ_TRY(check_ws(ws, ws_bytes, kq::cov_ws_bytes(dtype, n_rows, d)));
   }
   return kq::cov_launch(A, nullptr, dtype, n_rows, d, lda, H, ldh, alpha, beta, ws,
-                        as_stream(stream));
+                        as_stream(stream), max_cus);
 }
 
 int kronq_accumulate_cross(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d,

@@ -35,7 +35,7 @@ EXPORTS = (
     "kronq_profile_reset", "kronq_profile_read", "kronq_accumulate_cross", "kronq_rotate_drift",
     "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift", "kronq_pack_codes",
     "kronq_online_factors", "kronq_online_matvec", "kronq_matrix_stats", "kronq_eigh",
-    "kronq_proxy_loss_factors",
+    "kronq_proxy_loss_factors", "kronq_accumulate_cov_limited",
 )
 
 
@@ -63,6 +63,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_last_error": (ctypes.c_char_p, []),
         "kronq_version": (I, []),
         "kronq_accumulate_cov": (I, [P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
+        "kronq_accumulate_cov_limited": (I, [P, I, I64, I64, I64, P, I64, F, F, I, P, SZ, P]),
         "kronq_accumulate_cross": (I, [P, P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
         "kronq_rotate_drift": (I, [P, I64, I64, P, P, P, I, P, SZ, P]),
         "kronq_gptaq_correction": (I, [P, I64, I64, P, I64, F, P, I64, P, SZ, P]),
@@ -155,6 +156,22 @@ def kronq_accumulate_cov(A: torch.Tensor, H: torch.Tensor, alpha: float = 1.0, b
     rc = load().kronq_accumulate_cov(_ptr(A), _dtype_code(A), n, d, _ld(A), _ptr(H), _ld(H),
                                      alpha, beta, _ptr(ws), ws.numel(), _stream(A.device))
     _check(rc, "kronq_accumulate_cov")
+    return H
+
+
+def kronq_accumulate_cov_limited(A: torch.Tensor, H: torch.Tensor, max_cus: int,
+                                 alpha: float = 1.0, beta: float = 0.0,
+                                 ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """kronq_accumulate_cov holding at most ``max_cus`` compute units at once (0: all)."""
+    _dev(A, H)
+    n, d = A.shape
+    if ws is None:
+        ws = workspace(OP_COV, 0, d, n, A.device) if A.dtype == torch.bfloat16 else \
+            torch.empty(256, dtype=torch.uint8, device=A.device)
+    rc = load().kronq_accumulate_cov_limited(_ptr(A), _dtype_code(A), n, d, _ld(A), _ptr(H),
+                                             _ld(H), alpha, beta, int(max_cus), _ptr(ws),
+                                             ws.numel(), _stream(A.device))
+    _check(rc, "kronq_accumulate_cov_limited")
     return H
 
 

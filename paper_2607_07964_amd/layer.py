@@ -148,6 +148,28 @@ def solve(st: LayerState, bits: int, damp: float = 0.01, alpha: Optional[float] 
     sweep(st, bits, alpha)
 
 
+# Share of the compute units left free beside the H_G covariance in the two-stream schedule, for
+# the factorisation's latency-bound kernels (a covariance workgroup holds its CU for a whole
+# tile, so uncapped it starves them). The covariance loses less than the CUs it gives up, its
+# clock being power-limited on the full chip: on half the chip the 8B q_proj H_G takes 5.5 ms
+# instead of 4.1 ms. Worth it when the factorisation is not much shorter than that covariance:
+# measured per layer, q_proj 14.1 -> 12.0 ms (21.3 instead of 23.2 ms with the drift
+# correction); but the 70B up_proj's H_G (d = 28672) outlasts its factorisation (d = 8192) many
+# times over, and a cap there only slows it (260 -> 352 ms at half the chip). The estimate uses
+# rough rates: 1.1 PFLOP/s for a covariance, 20 TFLOP/s for the factorisation.
+FACTOR_SHARE = 0.5
+
+
+def _cov_cus(device, n_tokens: int, d_out: int, d_in: int) -> int:
+    """CUs the H_G covariance may hold beside the factorisation (0: no cap)."""
+    t_cov = float(n_tokens) * d_out * d_out / 1.1e15
+    t_factor = (2.0 / 3.0) * float(d_in) ** 3 / 2.0e13
+    if FACTOR_SHARE <= 0 or t_factor < 0.25 * t_cov:
+        return 0
+    cus = torch.cuda.get_device_properties(device).multi_processor_count
+    return max(8, int(cus * (1.0 - FACTOR_SHARE)))
+
+
 def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bits: int,
                    damp: float = 0.01, flags: int = K.BIIP, skip_x: bool = False,
                    overlap: bool = True, dX: Optional[torch.Tensor] = None, alpha: float = 1.0):
@@ -186,7 +208,10 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
     # issued the whole factorisation
     with torch.cuda.stream(st.side):
         st.side.wait_event(ev_x)
-        K.kronq_accumulate_cov(G, st.HG, 1.0, 0.0, st.ws_cov_g)
+        # the H_G covariance leaves part of the chip to the factorisation's latency-bound
+        # kernels (a covariance workgroup holds its CU for a whole tile)
+        K.kronq_accumulate_cov_limited(G, st.HG, _cov_cus(st.HG.device, G.shape[0], st.d_out,
+                                                          st.d_in), 1.0, 0.0, st.ws_cov_g)
         K.kronq_traces(None, st.HG, st.tr_pre)
         if drift:  # the third token contraction, also beside the factorisation
             drift_statistic(st, dX, X)
