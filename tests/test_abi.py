@@ -147,6 +147,18 @@ def test_drift_and_group_argument_checks():
     assert rc == -1 and "alias" in msg
 
 
+def test_cov_limited_argument_checks():
+    lib = K.load()
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)
+    rc, msg = _err(lib.kronq_accumulate_cov_limited(fake, 1, 100, 64, 64, fake, 64, 1.0, 0.0, -1,
+                                                    nul, 0, nul))
+    assert rc == -1 and "max_cus" in msg
+    rc, msg = _err(lib.kronq_accumulate_cov_limited(fake, 1, 1000, 64, 64, fake, 64, 1.0, 0.0, 8,
+                                                    nul, 16, nul))
+    assert rc == -5 and "workspace" in msg
+
+
 def test_diagnostics_argument_checks():
     lib = K.load()
     nul = ctypes.c_void_p(0)

@@ -81,6 +81,25 @@ def test_cov_chained_scaled_and_strided():
     assert rel_frob(to_np(H), ref) < TOL
 
 
+@pytest.mark.parametrize("max_cus", [8, 5, 24, 100000])
+def test_cov_limited_matches_uncapped(max_cus):
+    """The covariance holding at most max_cus CUs (persistent workgroups, several work items
+    each) gives the bits of the uncapped launch, and matches the oracle; 100000 exceeds the
+    work items (no cap), 5 is not a multiple of 8."""
+    n, d = 9000, 1280  # 5 x 5 channel blocks, 15 upper tiles, several token slices
+    spec = synth.small_spec(d, d, n, seed=17).x
+    X = synth.gen_matrix(spec, DEV)
+    H0 = torch.empty(d, d, device=DEV)
+    H1 = torch.full((d, d), float("nan"), device=DEV)
+    note(f"cov limited max_cus={max_cus}")
+    K.kronq_accumulate_cov(X, H0)
+    K.kronq_accumulate_cov_limited(X, H1, max_cus)
+    torch.cuda.synchronize()
+    assert torch.equal(H0, H1)
+    ref = O.covariance(oracle_view(synth.gen_matrix(spec)))
+    assert rel_frob(to_np(H1), ref) < TOL
+
+
 def test_cov_fp32_and_empty():
     s = synth.workload(1)
     X = synth.gen_matrix(s.x, DEV)
