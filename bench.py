@@ -521,7 +521,7 @@ def main() -> int:
                    "bits": spec.bits, "group": group, "block": 128, "damp": spec.damp,
                    "drift": bool(args.drift),
                    "parallelism": "single GPU",
-                   "schedule": "one stream" if args.serial else "two streams"},
+                   "schedule": L.schedule(st, spec.n_tokens, not args.serial)},
         "roofline": roof, "cpu_baseline": cpu,
     }
     if shared is not None:

@@ -170,6 +170,12 @@ def _cov_cus(device, n_tokens: int, d_out: int, d_in: int) -> int:
     return max(8, int(cus * (1.0 - FACTOR_SHARE)))
 
 
+def schedule(st: LayerState, n_tokens: int, overlap: bool = True) -> str:
+    """The schedule quantize_layer takes for this layer."""
+    cus = _cov_cus(st.HG.device, n_tokens, st.d_out, st.d_in) if overlap else 0
+    return f"two streams, H_G on {cus} CUs" if cus else "one stream"
+
+
 def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bits: int,
                    damp: float = 0.01, flags: int = K.BIIP, skip_x: bool = False,
                    overlap: bool = True, dX: Optional[torch.Tensor] = None, alpha: float = 1.0):
@@ -178,12 +184,19 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
 
     With ``overlap`` the work is split over two streams: the factorisation depends only on H_X
     and S_X, so it runs on the current stream right after H_X is rotated, while the second
-    stream accumulates H_G (after H_X is done, so the two covariances do not share the GPU),
-    then the drift statistic, and rotates W and H_G. P waits for the drift statistic, the sweep
-    for both streams."""
+    stream accumulates H_G (after H_X is done, so the two covariances do not share the GPU) on
+    part of the chip, leaving the rest to the factorisation, then the drift statistic, and
+    rotates W and H_G. P waits for the drift statistic, the sweep for both streams. Where the
+    factorisation is too short beside H_G for a chip share to pay (see _cov_cus), the layer
+    runs on one stream."""
     drift = dX is not None
     if drift and st.D is None:
         raise ValueError("the drift correction needs LayerState.allocate(..., drift=True)")
+    cov_cus = _cov_cus(st.HG.device, G.shape[0], st.d_out, st.d_in) if overlap else 0
+    if cov_cus == 0:
+        # without a chip share the factorisation's kernels starve beside the H_G covariance and
+        # slow it down (70B up_proj: 260 ms on two streams, 249 ms on one)
+        overlap = False
     if not overlap:
         covariances(st, X, G, skip_x)
         if drift:
@@ -210,8 +223,7 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
         st.side.wait_event(ev_x)
         # the H_G covariance leaves part of the chip to the factorisation's latency-bound
         # kernels (a covariance workgroup holds its CU for a whole tile)
-        K.kronq_accumulate_cov_limited(G, st.HG, _cov_cus(st.HG.device, G.shape[0], st.d_out,
-                                                          st.d_in), 1.0, 0.0, st.ws_cov_g)
+        K.kronq_accumulate_cov_limited(G, st.HG, cov_cus, 1.0, 0.0, st.ws_cov_g)
         K.kronq_traces(None, st.HG, st.tr_pre)
         if drift:  # the third token contraction, also beside the factorisation
             drift_statistic(st, dX, X)
