@@ -45,7 +45,7 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_FP32_VALU = 78.6
 def traffic_file(kernel: str, workload: str) -> str:
     return os.path.join(ROOT, "profiles", f"{kernel.replace('_mfma', '')}_{workload}_traffic.json")
-KERNELS = ["syrk_bf16_mfma", "syrk_bf16_mfma_shared", "syrk_reduce", "cross_bf16_mfma", "cross_reduce", "traces",
+KERNELS = ["cov_diag_partial", "cov_diag_final", "syrk_bf16_mfma", "syrk_bf16_mfma_shared", "syrk_reduce", "cross_bf16_mfma", "cross_reduce", "traces",
            "rot_w_norms", "rot_factors", "rot_inv_factors", "rot_row_pass", "fwht_col",
            "mix28_col", "chol_diag_shift", "chol_add_diag", "chol_reverse_copy",
            "chol_potrf_diag", "chol_trsm", "chol_syrk", "trtri_row", "trtri_put_diag",
@@ -379,6 +379,9 @@ def main() -> int:
                     help="per-kernel times of one extra step run on a single stream (stderr)")
     ap.add_argument("--serial", action="store_true",
                     help="time the single-stream schedule instead of the two-stream one")
+    ap.add_argument("--cov-cus", type=int, default=-1,
+                    help="CUs of the H_G covariance in the two-stream schedule (0: no cap; "
+                         "default: the library's policy)")
     ap.add_argument("--drift", action="store_true",
                     help="the drift-corrected path (KronQ+GPTAQ) with synthetic input drift")
     ap.add_argument("--alpha", type=float, default=1.0, help="drift correction scaling")
@@ -435,9 +438,11 @@ def main() -> int:
     dominant = "cross_bf16_mfma" if args.drift else "syrk_bf16_mfma"
     torch.cuda.synchronize()
 
+    cov_cus = None if args.cov_cus < 0 else args.cov_cus
+
     def step(overlap=not args.serial):
         L.quantize_layer(st, X, G, W0, rin, rout, spec.bits, spec.damp, overlap=overlap, dX=dX,
-                         alpha=args.alpha)
+                         alpha=args.alpha, cov_cus=cov_cus)
 
     for _ in range(args.warmup):
         step()
@@ -479,7 +484,8 @@ def main() -> int:
             "avg_launch_ms": round(avg_ms, 4)}
     shared = None
     if sh_n:
-        cus = L._cov_cus(dev, spec.n_tokens, spec.d_out, spec.d_in)
+        cus = cov_cus if cov_cus is not None else L._cov_cus(dev, spec.n_tokens, spec.d_out,
+                                                              spec.d_in)
         sh_avg = sh_ms / sh_n
         sh_tf = fl_g / (sh_avg * 1e-3) / 1e12
         part_peak = PEAK_BF16_TFLOPS * cus / torch.cuda.get_device_properties(dev).multi_processor_count
@@ -521,7 +527,7 @@ def main() -> int:
                    "bits": spec.bits, "group": group, "block": 128, "damp": spec.damp,
                    "drift": bool(args.drift),
                    "parallelism": "single GPU",
-                   "schedule": L.schedule(st, spec.n_tokens, not args.serial)},
+                   "schedule": L.schedule(st, spec.n_tokens, not args.serial, cov_cus)},
         "roofline": roof, "cpu_baseline": cpu,
     }
     if shared is not None:

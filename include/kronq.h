@@ -73,9 +73,21 @@ extern "C" {
  *                   H_G and sg are not touched.
  *   KRONQ_SX_GIVEN: sx is an input (from a KRONQ_HX_ONLY call with the same W_in); compute sg and
  *                   transform W and H_G; H_X is not touched (may be NULL).
- * HX_ONLY followed by SX_GIVEN gives exactly the result of one call without either flag. */
+ * HX_ONLY followed by SX_GIVEN gives exactly the result of one call without either flag.
+ * The H_G side splits the same way, so that W (which the sweep needs) does not wait for H_G:
+ *   KRONQ_HG_DIAG:  HG points at diag(H_G) only, d_out contiguous floats (ldg ignored; from
+ *                   kronq_cov_diag or any other source); sg comes from it, W (and H_X unless
+ *                   KRONQ_SX_GIVEN) is transformed, H_G is not. Not with KRONQ_HX_ONLY,
+ *                   KRONQ_SG_GIVEN or KRONQ_INVERSE.
+ *   KRONQ_SG_GIVEN: with KRONQ_SX_GIVEN only: sg is an input (from a KRONQ_HG_DIAG call);
+ *                   transform H_G only. W_in and W are not read (may be NULL; d_out and d_in
+ *                   still size the workspace).
+ * HX_ONLY, then SX_GIVEN | HG_DIAG with diag(H_G), then SX_GIVEN | SG_GIVEN gives exactly the
+ * result of one call without flags. */
 #define KRONQ_HX_ONLY 32
 #define KRONQ_SX_GIVEN 64
+#define KRONQ_HG_DIAG 128
+#define KRONQ_SG_GIVEN 256
 
 /* ---- workspace queries ------------------------------------------------------------------- */
 #define KRONQ_OP_COV 1
@@ -91,6 +103,7 @@ extern "C" {
 #define KRONQ_OP_STATS 11        /* kronq_matrix_stats: rows as d_out, cols as d_in */
 #define KRONQ_OP_EIGH 12         /* kronq_eigh: d as d_in */
 #define KRONQ_OP_PROXY 13        /* kronq_proxy_loss_factors: d_out, d_in */
+#define KRONQ_OP_COV_DIAG 14     /* kronq_cov_diag: d as d_in, tokens as n_rows */
 
 /* Bytes of scratch the operation needs for these sizes. For KRONQ_OP_COV pass the covariance
  * dimension d as d_in and the token count as n_rows (d_out ignored); for KRONQ_OP_CHOL pass
@@ -124,6 +137,19 @@ int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, in
 int kronq_accumulate_cov_limited(const void* A, int dtype, int64_t n_rows, int64_t d,
                                  int64_t lda, float* H, int64_t ldh, float alpha, float beta,
                                  int max_cus, void* ws, size_t ws_bytes, void* stream);
+
+/* ---- 1a. covariance diagonal (Sec. 4.1 eq. kfac; the h of eq. rescale) --------------------
+ * hdiag[j] = sum_t A[t][j]^2 = (A^T A)_jj for token-major A [n_rows x d], without the
+ * covariance: one read of A at HBM speed. Squares are summed in fp64 (exact products for bf16)
+ * and rounded once to fp32; the summation order is fixed, so the result is reproducible bit
+ * for bit. For a caller that needs a side's rescaling (KRONQ_HG_DIAG) before that side's
+ * covariance exists.
+ *   A      device, KRONQ_BF16 or KRONQ_FP32, rows of lda elements; A 16-byte aligned, lda
+ *          divisible by 8 (bf16) or 4 (fp32).
+ *   hdiag  device fp32 [d], written. n_rows = 0 writes zeros (A may then be NULL).
+ *   ws     kronq_workspace_bytes(KRONQ_OP_COV_DIAG, 0, d, n_rows) bytes. */
+int kronq_cov_diag(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
+                   float* hdiag, void* ws, size_t ws_bytes, void* stream);
 
 /* ---- 1b. drift statistic (Alg. 1 first line; eq. gptaq_obj) ------------------------------
  * C <- beta * C + alpha * A^T B for token-major A, B [n_rows x d] with the same leading
@@ -163,11 +189,13 @@ int kronq_traces(const float* HX, int64_t d_in, int64_t ldx, const float* HG, in
  *          (ldw_in divisible by 8 for bf16, by 4 for fp32); may alias W when fp32.
  *   W      device fp32 [d_out x ldw].
  *   HX     device fp32 [d_in x ldx] (forward; may be NULL for INVERSE).
- *   HG     device fp32 [d_out x ldg] or NULL; required by KRONQ_RESCALE_OUT.
+ *   HG     device fp32 [d_out x ldg] or NULL; required by KRONQ_RESCALE_OUT (with
+ *          KRONQ_HG_DIAG: fp32 [d_out], the diagonal only).
  *   sign_in/sign_out  device int8 (+1/-1) [d_in]/[d_out]; required when that side rotates.
  *   q28_in/q28_out    device fp32 [28 x 28] row-major; required iff that dimension is
  *                     28 * 2^k and rotates; ignored otherwise.
- *   sx/sg  device fp32 [d_in]/[d_out]: outputs (forward), inputs (inverse).
+ *   sx/sg  device fp32 [d_in]/[d_out]: outputs (forward), inputs (inverse; sx with
+ *          KRONQ_SX_GIVEN, sg with KRONQ_SG_GIVEN).
  * Rotated dimensions must be 2^k (k >= 1) or 28 * 2^k with 2^k <= 16384. */
 int kronq_rotate(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_t d_out,
                  int64_t d_in, int64_t ldw, float* HX, int64_t ldx, float* HG, int64_t ldg,

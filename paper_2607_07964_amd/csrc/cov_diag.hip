@@ -1,0 +1,131 @@
+// diag(A^T A) as column sums of squares (Sec. 4.1 eq. kfac; the diagonal that the rescaling of
+// eq. rescale reads), for a caller that needs a side's S before that side's covariance exists.
+#include <algorithm>
+
+#include "kq_common.hpp"
+
+namespace kq {
+namespace {
+// diag(A^T A) without the covariance: column sums of squares. A workgroup takes CSQ_COLS columns
+// of one chunk of rows; lane l of wave w reads 8 consecutive columns (one 16-byte load for bf16,
+// two for fp32) of rows w, w + 4, ... and sums their squares in fp64, so a bf16 input gives the
+// exact sum up to fp64 rounding. The four waves meet in LDS and the chunk's sums go to the
+// workspace; colsq_final adds the chunks in order and rounds once to fp32. No atomics: the
+// result does not depend on scheduling.
+constexpr int CSQ_COLS = 512;
+constexpr int CSQ_TARGET_WGS = 1024;  // about four resident workgroups per CU
+
+__device__ __forceinline__ void csq_load8(const uint16_t* p, int64_t n, float (&x)[8]) {
+  if (n >= 8) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(w[e] << 16);
+      x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = e < n ? __uint_as_float(uint32_t(p[e]) << 16) : 0.f;
+  }
+}
+__device__ __forceinline__ void csq_load8(const float* p, int64_t n, float (&x)[8]) {
+  if (n >= 8) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    x[0] = a.x, x[1] = a.y, x[2] = a.z, x[3] = a.w, x[4] = b.x, x[5] = b.y, x[6] = b.z, x[7] = b.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = e < n ? p[e] : 0.f;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void colsq_partial(const T* __restrict__ A, int64_t n_rows,
+                                                     int64_t d, int64_t lda, int64_t chunk_rows,
+                                                     double* __restrict__ part) {
+  __shared__ double red[3][CSQ_COLS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t c0 = int64_t(blockIdx.x) * CSQ_COLS + lane * 8;
+  const int64_t r0 = int64_t(blockIdx.y) * chunk_rows;
+  const int64_t r1 = min(n_rows, r0 + chunk_rows);
+  double acc[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+  if (c0 < d) {
+    const int64_t nc = d - c0;
+    int64_t r = r0 + wave;
+    // four rows in flight per wave before the first use
+    for (; r + 12 < r1; r += 16) {
+      float x[4][8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) csq_load8(A + (r + 4 * u) * lda + c0, nc, x[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fma(double(x[u][e]), double(x[u][e]), acc[e]);
+    }
+    for (; r < r1; r += 4) {
+      float x[8];
+      csq_load8(A + r * lda + c0, nc, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = fma(double(x[e]), double(x[e]), acc[e]);
+    }
+  }
+  if (wave > 0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) red[wave - 1][lane * 8 + e] = acc[e];
+  }
+  __syncthreads();
+  if (wave == 0 && c0 < d) {
+    double* out = part + int64_t(blockIdx.y) * d + c0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const double v = acc[e] + red[0][lane * 8 + e] + red[1][lane * 8 + e] + red[2][lane * 8 + e];
+      if (c0 + e < d) out[e] = v;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void colsq_final(const double* __restrict__ part, int n_chunks,
+                                                   int64_t d, float* __restrict__ out) {
+  const int64_t j = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (j >= d) return;
+  double v = 0.0;
+  for (int c = 0; c < n_chunks; ++c) v += part[int64_t(c) * d + j];
+  out[j] = float(v);
+}
+
+// row chunks of the column-square kernel: enough workgroups to fill the chip, at least 64 rows
+int64_t colsq_chunk_rows(int64_t n_rows, int64_t d) {
+  const int64_t col_blocks = cdiv(d, CSQ_COLS);
+  const int64_t want = std::max<int64_t>(1, CSQ_TARGET_WGS / col_blocks);
+  return std::max<int64_t>(64, cdiv(n_rows, want));
+}
+
+}  // namespace
+
+size_t cov_diag_ws_bytes(int64_t n_rows, int64_t d) {
+  if (n_rows <= 0 || d <= 0) return 256;
+  const int64_t chunks = cdiv(n_rows, colsq_chunk_rows(n_rows, d));
+  return align256(size_t(chunks) * size_t(d) * sizeof(double));
+}
+
+int cov_diag_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
+                    float* hdiag, void* ws, hipStream_t s) {
+  if (n_rows == 0)  // no chunks: the final kernel writes zeros
+    return launch("cov_diag_final", colsq_final, dim3(unsigned(cdiv(d, 256))), dim3(256), 0, s,
+                  static_cast<const double*>(nullptr), 0, d, hdiag);
+  const int64_t rows = colsq_chunk_rows(n_rows, d);
+  const int64_t chunks = cdiv(n_rows, rows);
+  double* part = static_cast<double*>(ws);
+  const dim3 grid(unsigned(cdiv(d, CSQ_COLS)), unsigned(chunks));
+  if (dtype == KRONQ_BF16)
+    KQ_TRY(launch("cov_diag_partial", colsq_partial<uint16_t>, grid, dim3(256), 0, s,
+                  static_cast<const uint16_t*>(A), n_rows, d, lda, rows, part));
+  else
+    KQ_TRY(launch("cov_diag_partial", colsq_partial<float>, grid, dim3(256), 0, s,
+                  static_cast<const float*>(A), n_rows, d, lda, rows, part));
+  return launch("cov_diag_final", colsq_final, dim3(unsigned(cdiv(d, 256))), dim3(256), 0, s,
+                static_cast<const double*>(part), int(chunks), d, hdiag);
+}
+
+}  // namespace kq

@@ -84,6 +84,8 @@ size_t kronq_workspace_bytes(int op, int64_t d_out, int64_t d_in, int64_t n_rows
       return kq::cov_ws_bytes(KRONQ_BF16, n_rows, d_in);
     case KRONQ_OP_CROSS:
       return kq::cov_ws_bytes(KRONQ_BF16, n_rows, d_in, true);
+    case KRONQ_OP_COV_DIAG:
+      return kq::cov_diag_ws_bytes(n_rows, d_in);
     case KRONQ_OP_ROTATE_DRIFT:
       return kq::rotate_drift_ws_bytes(d_in);
     case KRONQ_OP_GPTAQ:
@@ -142,6 +144,23 @@ int kronq_accumulate_cov_limited(const void* A, int dtype, int64_t n_rows, int64
                         as_stream(stream), max_cus);
 }
 
+int kronq_cov_diag(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
+                   float* hdiag, void* ws, size_t ws_bytes, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(valid_dtype(dtype), KRONQ_ERR_INVALID_ARG, "dtype must be KRONQ_BF16 or KRONQ_FP32");
+  KQ_REQUIRE(hdiag && aligned(hdiag, 4), KRONQ_ERR_INVALID_ARG, "hdiag is NULL or misaligned");
+  KQ_REQUIRE(n_rows >= 0 && d >= 1 && d <= (int64_t(1) << 24), KRONQ_ERR_INVALID_ARG,
+             "need n_rows >= 0 and 1 <= d <= 2^24");
+  if (n_rows > 0) {
+    KQ_REQUIRE(A, KRONQ_ERR_INVALID_ARG, "A is NULL");
+    KQ_REQUIRE(lda >= d, KRONQ_ERR_INVALID_ARG, "lda < d");
+    KQ_REQUIRE(aligned(A, 16) && lda % (dtype == KRONQ_BF16 ? 8 : 4) == 0, KRONQ_ERR_INVALID_ARG,
+               "A must be 16-byte aligned with lda divisible by 8 (bf16) or 4 (fp32)");
+    KQ_TRY(check_ws(ws, ws_bytes, kq::cov_diag_ws_bytes(n_rows, d)));
+  }
+  return kq::cov_diag_launch(A, dtype, n_rows, d, lda, hdiag, ws, as_stream(stream));
+}
+
 int kronq_accumulate_cross(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d,
                            int64_t ld, float* C, int64_t ldc, float alpha, float beta, void* ws,
                            size_t ws_bytes, void* stream) {
@@ -181,20 +200,29 @@ int kronq_rotate(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_
                  const float* q28_out, float* sx, float* sg, int flags, void* ws,
                  size_t ws_bytes, void* stream) {
   kq::clear_error();
-  const int known = KRONQ_BIIP | KRONQ_INVERSE | KRONQ_HX_ONLY | KRONQ_SX_GIVEN;
+  const int known = KRONQ_BIIP | KRONQ_INVERSE | KRONQ_HX_ONLY | KRONQ_SX_GIVEN |
+                    KRONQ_HG_DIAG | KRONQ_SG_GIVEN;
   KQ_REQUIRE((flags & ~known) == 0, KRONQ_ERR_INVALID_ARG, "unknown flag bits 0x%x",
              flags & ~known);
-  KQ_REQUIRE(W_in && valid_dtype(w_dtype), KRONQ_ERR_INVALID_ARG, "bad W_in");
-  KQ_REQUIRE(ldw_in >= d_in, KRONQ_ERR_INVALID_ARG, "ldw_in < d_in");
-  // W_in is read with 16-byte vector loads (8 bf16 or 4 fp32 values)
-  KQ_REQUIRE(aligned(W_in, 16) && ldw_in % (w_dtype == KRONQ_BF16 ? 8 : 4) == 0,
-             KRONQ_ERR_INVALID_ARG,
-             "W_in must be 16-byte aligned with ldw_in divisible by 8 (bf16) or 4 (fp32)");
   const bool inv = flags & KRONQ_INVERSE;
   const bool hx_only = flags & KRONQ_HX_ONLY, sx_given = flags & KRONQ_SX_GIVEN;
+  const bool hg_diag = flags & KRONQ_HG_DIAG, sg_given = flags & KRONQ_SG_GIVEN;
   KQ_REQUIRE(!(hx_only && sx_given) && !(inv && (hx_only || sx_given)), KRONQ_ERR_INVALID_ARG,
              "KRONQ_HX_ONLY, KRONQ_SX_GIVEN and KRONQ_INVERSE exclude each other");
-  if (!hx_only) KQ_TRY(check_f32_mat(W, d_out, d_in, ldw, "W"));
+  KQ_REQUIRE(!hg_diag || !(hx_only || sg_given || inv), KRONQ_ERR_INVALID_ARG,
+             "KRONQ_HG_DIAG excludes KRONQ_HX_ONLY, KRONQ_SG_GIVEN and KRONQ_INVERSE");
+  KQ_REQUIRE(!sg_given || sx_given, KRONQ_ERR_INVALID_ARG,
+             "KRONQ_SG_GIVEN needs KRONQ_SX_GIVEN");
+  if (!sg_given) {  // W_in is read (W_in is not touched by an H_G-only call)
+    KQ_REQUIRE(W_in && valid_dtype(w_dtype), KRONQ_ERR_INVALID_ARG, "bad W_in");
+    KQ_REQUIRE(ldw_in >= d_in, KRONQ_ERR_INVALID_ARG, "ldw_in < d_in");
+    // W_in is read with 16-byte vector loads (8 bf16 or 4 fp32 values)
+    KQ_REQUIRE(aligned(W_in, 16) && ldw_in % (w_dtype == KRONQ_BF16 ? 8 : 4) == 0,
+               KRONQ_ERR_INVALID_ARG,
+               "W_in must be 16-byte aligned with ldw_in divisible by 8 (bf16) or 4 (fp32)");
+  }
+  KQ_REQUIRE(d_out >= 1 && d_in >= 1, KRONQ_ERR_INVALID_ARG, "need d_out >= 1 and d_in >= 1");
+  if (!hx_only && !sg_given) KQ_TRY(check_f32_mat(W, d_out, d_in, ldw, "W"));
   KQ_REQUIRE(sx && aligned(sx, 4) && (hx_only || (sg && aligned(sg, 4))), KRONQ_ERR_INVALID_ARG,
              "sx and sg are required");
   if (inv) {
@@ -203,10 +231,14 @@ int kronq_rotate(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64_
                "W_in must be 16-byte aligned with ldw_in divisible by 4");
   } else {
     if (!sx_given) KQ_TRY(check_f32_mat(HX, d_in, d_in, ldx, "HX"));
-    if (HG && !hx_only) KQ_TRY(check_f32_mat(HG, d_out, d_out, ldg, "HG"));
+    if (hg_diag)
+      KQ_REQUIRE(!HG || aligned(HG, 4), KRONQ_ERR_INVALID_ARG, "diag(H_G) misaligned");
+    else if (HG && !hx_only)
+      KQ_TRY(check_f32_mat(HG, d_out, d_out, ldg, "HG"));
     KQ_REQUIRE(HG || hx_only || !(flags & KRONQ_RESCALE_OUT), KRONQ_ERR_INVALID_ARG,
                "KRONQ_RESCALE_OUT needs H_G");
-    KQ_REQUIRE(W_in != static_cast<const void*>(W) || w_dtype == KRONQ_FP32,
+    KQ_REQUIRE(!sg_given || HG, KRONQ_ERR_INVALID_ARG, "KRONQ_SG_GIVEN needs H_G");
+    KQ_REQUIRE(sg_given || W_in != static_cast<const void*>(W) || w_dtype == KRONQ_FP32,
                KRONQ_ERR_INVALID_ARG, "in-place rotation needs fp32 W");
   }
   if (flags & KRONQ_ROT_IN) KQ_TRY(check_rot_side(d_in, sign_in, q28_in, "input"));

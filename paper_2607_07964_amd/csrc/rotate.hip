@@ -546,8 +546,10 @@ int rotate_launch(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64
 
   // ---- forward (optionally split into the H_X half and the W / H_G half)
   const bool hx_only = flags & KRONQ_HX_ONLY, sx_given = flags & KRONQ_SX_GIVEN;
+  const bool hg_diag = flags & KRONQ_HG_DIAG, sg_given = flags & KRONQ_SG_GIVEN;
+  const bool do_w = !hx_only && !sg_given;  // W is transformed
   const bool need_norms = ((flags & KRONQ_RESCALE_IN) && !sx_given) ||
-                          ((flags & KRONQ_RESCALE_OUT) && !hx_only);
+                          ((flags & KRONQ_RESCALE_OUT) && do_w);
   if (need_norms) {
     if (w_dtype == KRONQ_BF16)
       KQ_TRY(launch("rot_w_norms", w_norms<uint16_t>, dim3(unsigned(nb)), dim3(256), 0, s,
@@ -561,13 +563,15 @@ int rotate_launch(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64
                   d_in, static_cast<const float*>(HX), ldx, static_cast<const double*>(colp), nb,
                   static_cast<const double*>(nullptr), rot_in ? sign_in : nullptr,
                   int((flags & KRONQ_RESCALE_IN) != 0), sx, mw_in, mh_in));
-  else
+  else if (do_w)
     KQ_TRY(launch("rot_factors", given_factors, dim3(unsigned(cdiv(d_in, 256))), dim3(256), 0, s,
                   d_in, static_cast<const float*>(sx), rot_in ? sign_in : nullptr, mw_in));
-  if (!hx_only) {
+  if (do_w) {
+    // with KRONQ_HG_DIAG, HG is the diagonal itself: a zero stride reads H[j] as H[j][j]
     KQ_TRY(launch("rot_factors", side_factors, dim3(unsigned(cdiv(d_out, 256))), dim3(256), 0, s,
-                  d_out, static_cast<const float*>(HG), ldg, static_cast<const double*>(nullptr),
-                  int64_t(0), static_cast<const double*>(rows), rot_out ? sign_out : nullptr,
+                  d_out, static_cast<const float*>(HG), hg_diag ? int64_t(0) : ldg,
+                  static_cast<const double*>(nullptr), int64_t(0),
+                  static_cast<const double*>(rows), rot_out ? sign_out : nullptr,
                   int((flags & KRONQ_RESCALE_OUT) != 0), sg, mw_out, mh_out));
     // W: rescale + signs + V side (row pass), then U side (column pass)
     KQ_TRY(launch_row_pass(W_in, w_dtype, ldw_in, W, ldw, d_out, d_in, mw_out, mw_in, nullptr,
@@ -580,8 +584,12 @@ int rotate_launch(const void* W_in, int w_dtype, int64_t ldw_in, float* W, int64
                            nullptr, rot_in, ri, q28_in, false, s, "rot_row_pass"));
     if (rot_in) KQ_TRY(col_transform(HX, ldx, HX, ldx, d_in, d_in, ri, q28_in, false, s));
   }
-  // H_G <- U S^-1 H_G S^-1 U^T
-  if (HG && !hx_only) {
+  // H_G <- U S^-1 H_G S^-1 U^T (with a given sg, the multipliers sign / s as side_factors
+  // forms them)
+  if (sg_given)
+    KQ_TRY(launch("rot_factors", inv_factors, dim3(unsigned(cdiv(d_out, 256))), dim3(256), 0, s,
+                  d_out, static_cast<const float*>(sg), rot_out ? sign_out : nullptr, mh_out));
+  if (HG && !hx_only && !hg_diag) {
     KQ_TRY(launch_row_pass(HG, KRONQ_FP32, ldg, HG, ldg, d_out, d_out, mh_out, mh_out, nullptr,
                            nullptr, rot_out, ro, q28_out, false, s, "rot_row_pass"));
     if (rot_out) KQ_TRY(col_transform(HG, ldg, HG, ldg, d_out, d_out, ro, q28_out, false, s));

@@ -19,11 +19,11 @@ LIB_PATH = os.path.join(_HERE, "libkronq.so")
 
 KRONQ_BF16, KRONQ_FP32 = 1, 2
 RESCALE_IN, RESCALE_OUT, ROT_IN, ROT_OUT, INVERSE = 1, 2, 4, 8, 16
-HX_ONLY, SX_GIVEN = 32, 64
+HX_ONLY, SX_GIVEN, HG_DIAG, SG_GIVEN = 32, 64, 128, 256
 BIIP = RESCALE_IN | RESCALE_OUT | ROT_IN | ROT_OUT
 OP_COV, OP_ROTATE, OP_CHOL, OP_OBS, OP_LOSS = 1, 2, 3, 4, 5
 OP_CROSS, OP_ROTATE_DRIFT, OP_GPTAQ, OP_OBS_DRIFT, OP_ONLINE = 6, 7, 8, 9, 10
-OP_STATS, OP_EIGH, OP_PROXY = 11, 12, 13
+OP_STATS, OP_EIGH, OP_PROXY, OP_COV_DIAG = 11, 12, 13, 14
 MAX_ALPHAS = 16
 ERRORS = {0: "OK", -1: "INVALID_ARG", -2: "SHAPE", -3: "NOT_PD", -4: "HIP", -5: "WORKSPACE",
           -6: "UNSUPPORTED"}
@@ -35,7 +35,7 @@ EXPORTS = (
     "kronq_profile_reset", "kronq_profile_read", "kronq_accumulate_cross", "kronq_rotate_drift",
     "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift", "kronq_pack_codes",
     "kronq_online_factors", "kronq_online_matvec", "kronq_matrix_stats", "kronq_eigh",
-    "kronq_proxy_loss_factors", "kronq_accumulate_cov_limited",
+    "kronq_proxy_loss_factors", "kronq_accumulate_cov_limited", "kronq_cov_diag",
 )
 
 
@@ -64,6 +64,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_version": (I, []),
         "kronq_accumulate_cov": (I, [P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
         "kronq_accumulate_cov_limited": (I, [P, I, I64, I64, I64, P, I64, F, F, I, P, SZ, P]),
+        "kronq_cov_diag": (I, [P, I, I64, I64, I64, P, P, SZ, P]),
         "kronq_accumulate_cross": (I, [P, P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
         "kronq_rotate_drift": (I, [P, I64, I64, P, P, P, I, P, SZ, P]),
         "kronq_gptaq_correction": (I, [P, I64, I64, P, I64, F, P, I64, P, SZ, P]),
@@ -175,6 +176,21 @@ def kronq_accumulate_cov_limited(A: torch.Tensor, H: torch.Tensor, max_cus: int,
     return H
 
 
+def kronq_cov_diag(A: torch.Tensor, out: Optional[torch.Tensor] = None,
+                   ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """diag(A^T A) as fp32 [d] (token-major A [N x d], bf16 or fp32), without the covariance."""
+    _dev(A, out)
+    n, d = A.shape
+    if out is None:
+        out = torch.empty(d, dtype=torch.float32, device=A.device)
+    if ws is None:
+        ws = workspace(OP_COV_DIAG, 0, d, n, A.device)
+    rc = load().kronq_cov_diag(_ptr(A), _dtype_code(A), n, d, _ld(A), _ptr(out), _ptr(ws),
+                               ws.numel(), _stream(A.device))
+    _check(rc, "kronq_cov_diag")
+    return out
+
+
 def kronq_traces(HX: Optional[torch.Tensor], HG: Optional[torch.Tensor],
                  out: Optional[torch.Tensor] = None):
     """Device float64 tensor [tr H_X, tr H_G, tr H_X * tr H_G] (a None side leaves its slot)."""
@@ -190,22 +206,28 @@ def kronq_traces(HX: Optional[torch.Tensor], HG: Optional[torch.Tensor],
     return out
 
 
-def kronq_rotate(W_in: torch.Tensor, W: Optional[torch.Tensor], HX: Optional[torch.Tensor],
+def kronq_rotate(W_in: Optional[torch.Tensor], W: Optional[torch.Tensor],
+                 HX: Optional[torch.Tensor],
                  HG: Optional[torch.Tensor], sign_in: Optional[torch.Tensor],
                  sign_out: Optional[torch.Tensor], q28_in: Optional[torch.Tensor],
                  q28_out: Optional[torch.Tensor], sx: torch.Tensor, sg: torch.Tensor,
                  flags: int = BIIP, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """BiIP forward (W <- U S_G W_in S_X V^T, H_X and H_G in place) or, with INVERSE, the revert."""
+    """BiIP forward (W <- U S_G W_in S_X V^T, H_X and H_G in place) or, with INVERSE, the revert.
+    With HG_DIAG, HG is the 1-D diagonal of H_G; with SG_GIVEN, W_in and W may be None (the
+    sizes then come from sg and sx)."""
     _dev(W_in, W, HX, HG, sign_in, sign_out, q28_in, q28_out, sx, sg)
-    d_out, d_in = W_in.shape
+    d_out, d_in = W_in.shape if W_in is not None else (sg.numel(), sx.numel())
+    dev = sx.device
     if ws is None:
-        ws = workspace(OP_ROTATE, d_out, d_in, 0, W_in.device)
+        ws = workspace(OP_ROTATE, d_out, d_in, 0, dev)
     rc = load().kronq_rotate(
-        _ptr(W_in), _dtype_code(W_in), _ld(W_in), _ptr(W), d_out, d_in,
+        _ptr(W_in), _dtype_code(W_in) if W_in is not None else KRONQ_FP32,
+        _ld(W_in) if W_in is not None else 0, _ptr(W), d_out, d_in,
         _ld(W) if W is not None else 0, _ptr(HX),
-        _ld(HX) if HX is not None else 0, _ptr(HG), _ld(HG) if HG is not None else 0,
+        _ld(HX) if HX is not None else 0, _ptr(HG),
+        _ld(HG) if HG is not None and HG.dim() == 2 else 0,
         _ptr(sign_in), _ptr(sign_out), _ptr(q28_in), _ptr(q28_out), _ptr(sx), _ptr(sg), flags,
-        _ptr(ws), ws.numel(), _stream(W_in.device))
+        _ptr(ws), ws.numel(), _stream(dev))
     _check(rc, "kronq_rotate")
     return W
 

@@ -46,11 +46,13 @@ class LayerState:
     zeros: torch.Tensor
     sx: torch.Tensor
     sg: torch.Tensor
+    hgd: torch.Tensor  # diag(H_G) from G (the S_G rescaling without waiting for H_G)
     tr_pre: torch.Tensor
     tr_post: torch.Tensor
     info: torch.Tensor
     ws_cov_x: torch.Tensor
     ws_cov_g: torch.Tensor
+    ws_diag: torch.Tensor
     ws_rot: torch.Tensor
     ws_chol: torch.Tensor
     ws_obs: torch.Tensor
@@ -86,11 +88,13 @@ class LayerState:
             scales=torch.empty(d_out, d_in // group, **f32),
             zeros=torch.empty(d_out, d_in // group, **f32),
             sx=torch.empty(d_in, **f32), sg=torch.empty(d_out, **f32),
+            hgd=torch.empty(d_out, **f32),
             tr_pre=torch.empty(3, dtype=torch.float64, device=device),
             tr_post=torch.empty(3, dtype=torch.float64, device=device),
             info=torch.empty(1, dtype=torch.int32, device=device),
             ws_cov_x=ws(K.OP_COV, 0, d_in, n_tokens, x_dtype),
             ws_cov_g=ws(K.OP_COV, 0, d_out, n_tokens, g_dtype),
+            ws_diag=K.workspace(K.OP_COV_DIAG, 0, d_out, n_tokens, device),
             ws_rot=ws(K.OP_ROTATE, d_out, d_in, 0), ws_chol=ws(K.OP_CHOL, 0, d_in, 0),
             ws_obs=ws(K.OP_OBS_DRIFT if drift else K.OP_OBS, d_out, d_in, 0),
             err=torch.empty(d_out, d_in, **f32) if keep_err else None,
@@ -101,7 +105,7 @@ class LayerState:
             ws_rdrift=ws(K.OP_ROTATE_DRIFT, 0, d_in, 0) if drift else None,
             ws_gptaq=ws(K.OP_GPTAQ, 0, d_in, 0) if drift else None,
             side=torch.cuda.Stream(device=device),  # default priority
-            ev=tuple(torch.cuda.Event() for _ in range(4)),
+            ev=tuple(torch.cuda.Event() for _ in range(5)),
         )
 
 
@@ -149,90 +153,111 @@ def solve(st: LayerState, bits: int, damp: float = 0.01, alpha: Optional[float] 
 
 
 # Share of the compute units left free beside the H_G covariance in the two-stream schedule, for
-# the factorisation's latency-bound kernels (a covariance workgroup holds its CU for a whole
-# tile, so uncapped it starves them). The covariance loses less than the CUs it gives up, its
-# clock being power-limited on the full chip: on half the chip the 8B q_proj H_G takes 5.5 ms
-# instead of 4.1 ms. Worth it when the factorisation is not much shorter than that covariance:
-# measured per layer, q_proj 14.1 -> 12.0 ms (21.3 instead of 23.2 ms with the drift
-# correction); but the 70B up_proj's H_G (d = 28672) outlasts its factorisation (d = 8192) many
-# times over, and a cap there only slows it (260 -> 352 ms at half the chip). The estimate uses
-# rough rates: 1.1 PFLOP/s for a covariance, 20 TFLOP/s for the factorisation.
+# the factorisation's and the sweep's latency-bound kernels (a covariance workgroup holds its CU
+# for a whole tile, so uncapped it starves them: the 8B q_proj takes 14.7 ms per layer uncapped,
+# 12.3 ms on half the chip). The covariance loses less than the CUs it gives up, its clock
+# being power-limited on the full chip: on half the chip the q_proj H_G takes 5.9 ms instead of
+# 4.1 ms. Half the chip where the factorisation is not much shorter than that covariance; an
+# eighth where H_G outlasts factorisation and sweep many times over (70B up_proj, d = 28672
+# against d = 8192: 238.7 ms per layer on 7/8 of the chip, 242.9 ms on 3/4, 247.7 ms on one
+# stream, 262.5 ms uncapped). The estimate uses rough rates: 1.1 PFLOP/s for a covariance,
+# 20 TFLOP/s for the factorisation.
 FACTOR_SHARE = 0.5
+FACTOR_SHARE_SHORT = 0.125
 
 
 def _cov_cus(device, n_tokens: int, d_out: int, d_in: int) -> int:
-    """CUs the H_G covariance may hold beside the factorisation (0: no cap)."""
+    """CUs the H_G covariance may hold beside the factorisation and the sweep."""
     t_cov = float(n_tokens) * d_out * d_out / 1.1e15
     t_factor = (2.0 / 3.0) * float(d_in) ** 3 / 2.0e13
-    if FACTOR_SHARE <= 0 or t_factor < 0.25 * t_cov:
-        return 0
+    share = FACTOR_SHARE if t_factor >= 0.25 * t_cov else FACTOR_SHARE_SHORT
     cus = torch.cuda.get_device_properties(device).multi_processor_count
-    return max(8, int(cus * (1.0 - FACTOR_SHARE)))
+    return max(8, int(cus * (1.0 - share)))
 
 
-def schedule(st: LayerState, n_tokens: int, overlap: bool = True) -> str:
+def schedule(st: LayerState, n_tokens: int, overlap: bool = True,
+             cov_cus: Optional[int] = None) -> str:
     """The schedule quantize_layer takes for this layer."""
-    cus = _cov_cus(st.HG.device, n_tokens, st.d_out, st.d_in) if overlap else 0
-    return f"two streams, H_G on {cus} CUs" if cus else "one stream"
+    if not overlap:
+        return "one stream"
+    if cov_cus is None:
+        cov_cus = _cov_cus(st.HG.device, n_tokens, st.d_out, st.d_in)
+    return f"two streams, H_G on {cov_cus} CUs" if cov_cus else "two streams, H_G uncapped"
+
+
+def biip_split(st: LayerState, W0: torch.Tensor, rin: RotParams, rout: RotParams,
+               flags: int = K.BIIP):
+    """Steps a3-a5 with S_G from ``st.hgd`` (diag(H_G) from G): pre traces, BiIP of W and H_X,
+    then of H_G, post traces. The same transforms as the two-stream schedule's split calls."""
+    K.kronq_traces(st.HX, st.HG, st.tr_pre)
+    K.kronq_rotate(W0, st.W, st.HX, st.hgd, rin.sign, rout.sign, rin.q28, rout.q28, st.sx, st.sg,
+                   flags | K.HG_DIAG, st.ws_rot)
+    K.kronq_rotate(None, None, None, st.HG, rin.sign, rout.sign, rin.q28, rout.q28, st.sx, st.sg,
+                   flags | K.SX_GIVEN | K.SG_GIVEN, st.ws_rot)
+    K.kronq_traces(st.HX, st.HG, st.tr_post)
 
 
 def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bits: int,
                    damp: float = 0.01, flags: int = K.BIIP, skip_x: bool = False,
-                   overlap: bool = True, dX: Optional[torch.Tensor] = None, alpha: float = 1.0):
+                   overlap: bool = True, dX: Optional[torch.Tensor] = None, alpha: float = 1.0,
+                   cov_cus: Optional[int] = None):
     """The whole hot path of one layer (enqueue only). ``dX`` (with buffers from
     ``allocate(drift=True)``) adds the drift correction with scaling ``alpha``.
 
-    With ``overlap`` the work is split over two streams: the factorisation depends only on H_X
-    and S_X, so it runs on the current stream right after H_X is rotated, while the second
-    stream accumulates H_G (after H_X is done, so the two covariances do not share the GPU) on
-    part of the chip, leaving the rest to the factorisation, then the drift statistic, and
-    rotates W and H_G. P waits for the drift statistic, the sweep for both streams. Where the
-    factorisation is too short beside H_G for a chip share to pay (see _cov_cus), the layer
-    runs on one stream."""
+    S_G needs only diag(H_G), which one read of G gives (kronq_cov_diag), so W is rescaled and
+    rotated without waiting for the H_G covariance, and the sweep never waits for it either.
+    With ``overlap`` the work is split over two streams after H_X: the current stream rotates
+    H_X, factors it and runs the sweep; the second stream takes diag(H_G) (beside the H_X
+    covariance), transforms W as soon as S_X exists, then (the drift statistic and) the H_G
+    covariance on ``cov_cus`` CUs (None: the policy of _cov_cus; 0: no cap), whose traces and
+    rotation end the layer. The current stream waits for the second at the end. Both schedules
+    give bit-identical results."""
     drift = dX is not None
     if drift and st.D is None:
         raise ValueError("the drift correction needs LayerState.allocate(..., drift=True)")
-    cov_cus = _cov_cus(st.HG.device, G.shape[0], st.d_out, st.d_in) if overlap else 0
-    if cov_cus == 0:
-        # without a chip share the factorisation's kernels starve beside the H_G covariance and
-        # slow it down (70B up_proj: 260 ms on two streams, 249 ms on one)
-        overlap = False
+    if overlap and cov_cus is None:
+        cov_cus = _cov_cus(st.HG.device, G.shape[0], st.d_out, st.d_in)
     if not overlap:
+        K.kronq_cov_diag(G, st.hgd, st.ws_diag)
         covariances(st, X, G, skip_x)
         if drift:
             drift_statistic(st, dX, X)
-        biip(st, W0, rin, rout, flags)
+        biip_split(st, W0, rin, rout, flags)
         if drift:
             drift_biip(st, rin, flags)
         solve(st, bits, damp, alpha if drift else None)
         return
     main = torch.cuda.current_stream(st.HX.device)
-    ev_x, ev_sx, ev_w, ev_d = st.ev
+    ev_x, ev_sx, ev_w, ev_d, ev_g = st.ev
+    ev_x.record(main)
+    with torch.cuda.stream(st.side):
+        st.side.wait_event(ev_x)  # ordered after the caller's earlier work on this stream
+        K.kronq_cov_diag(G, st.hgd, st.ws_diag)
     if not skip_x:
         K.kronq_accumulate_cov(X, st.HX, 1.0, 0.0, st.ws_cov_x)
     K.kronq_traces(st.HX, None, st.tr_pre)
-    ev_x.record(main)
     K.kronq_rotate(W0, None, st.HX, None, rin.sign, None, rin.q28, None, st.sx, st.sg,
                    flags | K.HX_ONLY, st.ws_rot)
     K.kronq_traces(st.HX, None, st.tr_post)
     ev_sx.record(main)
-    # the side stream's work is enqueued before the factorisation's ~160 launches, so that the
-    # H_G covariance is dispatched as soon as H_X is done rather than after the host has
-    # issued the whole factorisation
+    # the side stream's work is enqueued before the factorisation's ~160 launches, so that it
+    # is dispatched as soon as S_X exists rather than after the host has issued them
     with torch.cuda.stream(st.side):
-        st.side.wait_event(ev_x)
-        # the H_G covariance leaves part of the chip to the factorisation's latency-bound
-        # kernels (a covariance workgroup holds its CU for a whole tile)
-        K.kronq_accumulate_cov_limited(G, st.HG, cov_cus, 1.0, 0.0, st.ws_cov_g)
-        K.kronq_traces(None, st.HG, st.tr_pre)
-        if drift:  # the third token contraction, also beside the factorisation
+        st.side.wait_event(ev_sx)
+        K.kronq_rotate(W0, st.W, None, st.hgd, rin.sign, rout.sign, rin.q28, rout.q28, st.sx,
+                       st.sg, flags | K.SX_GIVEN | K.HG_DIAG, st.ws_rot)
+        ev_w.record(st.side)
+        if drift:  # the drift statistic first: the correction P waits for it
             drift_statistic(st, dX, X)
             ev_d.record(st.side)
-        st.side.wait_event(ev_sx)
-        K.kronq_rotate(W0, st.W, None, st.HG, rin.sign, rout.sign, rin.q28, rout.q28, st.sx,
-                       st.sg, flags | K.SX_GIVEN, st.ws_rot)
+        # the H_G covariance leaves part of the chip to the factorisation's and the sweep's
+        # latency-bound kernels (a covariance workgroup holds its CU for a whole tile)
+        K.kronq_accumulate_cov_limited(G, st.HG, cov_cus, 1.0, 0.0, st.ws_cov_g)
+        K.kronq_traces(None, st.HG, st.tr_pre)
+        K.kronq_rotate(None, None, None, st.HG, rin.sign, rout.sign, rin.q28, rout.q28, st.sx,
+                       st.sg, flags | K.SX_GIVEN | K.SG_GIVEN, st.ws_rot)
         K.kronq_traces(None, st.HG, st.tr_post)
-        ev_w.record(st.side)
+        ev_g.record(st.side)
     K.kronq_cholesky_inv(st.HX, st.U, damp, st.info, st.ws_chol)
     if drift:
         main.wait_event(ev_d)
@@ -245,6 +270,7 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
     else:
         K.kronq_obs_quantize_layer(st.W, st.U, bits, st.codes, st.scales, st.zeros, st.err, None,
                                    group=st.group, ws=st.ws_obs)
+    main.wait_event(ev_g)
 
 
 def check(st: LayerState):

@@ -159,6 +159,44 @@ def test_cov_limited_argument_checks():
     assert rc == -5 and "workspace" in msg
 
 
+def test_cov_diag_and_split_rotation_argument_checks():
+    lib = K.load()
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)
+    ws = ctypes.c_void_p(1 << 30)
+    assert K.kronq_workspace_bytes(K.OP_COV_DIAG, 0, 4096, 262144) >= 4096 * 8
+    # cov_diag: bad dtype, lda < d, bf16 lda not divisible by 8, workspace too small
+    rc, _ = _err(lib.kronq_cov_diag(fake, 3, 100, 64, 64, fake, ws, 1 << 30, nul))
+    assert rc == -1
+    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100, 64, 32, fake, ws, 1 << 30, nul))
+    assert rc == -1 and "lda" in msg
+    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100, 60, 60, fake, ws, 1 << 30, nul))
+    assert rc == -1 and "aligned" in msg
+    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100000, 64, 64, fake, ws, 16, nul))
+    assert rc == -5 and "workspace" in msg
+    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100, 64, 64, nul, ws, 1 << 30, nul))
+    assert rc == -1 and "hdiag" in msg
+
+    def rot(flags, W_in=fake, W=fake):
+        return _err(lib.kronq_rotate(W_in, 2, 128, W, 64, 128, 128, fake, 128, fake, 64, fake,
+                                     fake, nul, nul, fake, fake, flags, ws, 1 << 30, nul))
+    # HG_DIAG excludes HX_ONLY and SG_GIVEN; SG_GIVEN needs SX_GIVEN
+    for flags in (K.HG_DIAG | K.HX_ONLY, K.HG_DIAG | K.SX_GIVEN | K.SG_GIVEN,
+                  K.HG_DIAG | K.INVERSE):
+        rc, msg = rot(K.BIIP | flags)
+        assert rc == -1 and "HG_DIAG" in msg
+    rc, msg = rot(K.BIIP | K.SG_GIVEN)
+    assert rc == -1 and "SX_GIVEN" in msg
+    # an H_G-only call reads neither W_in nor W, but needs H_G
+    rc, msg = _err(lib.kronq_rotate(nul, 2, 0, nul, 64, 128, 0, nul, 0, nul, 64, fake, fake, nul,
+                                    nul, fake, fake, K.BIIP | K.SX_GIVEN | K.SG_GIVEN, ws,
+                                    1 << 30, nul))
+    assert rc == -1 and "H_G" in msg
+    # a W-transforming call still needs W_in
+    rc, msg = rot(K.BIIP | K.SX_GIVEN | K.HG_DIAG, W_in=nul)
+    assert rc == -1 and "W_in" in msg
+
+
 def test_diagnostics_argument_checks():
     lib = K.load()
     nul = ctypes.c_void_p(0)

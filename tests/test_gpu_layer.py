@@ -113,13 +113,17 @@ def test_overlapped_schedule_matches_single_stream():
     ro = synth.rotation_params(spec.d_out, spec.seed, spec.name + ":out")
     rin, rout = rot_device(ri), rot_device(ro)
     res = []
-    for overlap in (False, True):
+    # one stream; two streams with the policy's cap, without a cap, with a small cap
+    for overlap, cus in ((False, None), (True, None), (True, 0), (True, 16)):
         st = L.LayerState.allocate(spec.d_out, spec.d_in, spec.n_tokens, DEV)
-        note(f"layer overlap={overlap}")
+        note(f"layer overlap={overlap} cov_cus={cus}")
         for _ in range(2):  # twice: the second step reuses every buffer and event
-            L.quantize_layer(st, X, G, W0, rin, rout, spec.bits, spec.damp, overlap=overlap)
+            L.quantize_layer(st, X, G, W0, rin, rout, spec.bits, spec.damp, overlap=overlap,
+                             cov_cus=cus)
         L.check(st)
         torch.cuda.synchronize()
-        res.append([to_np(t) for t in (st.codes, st.W, st.U, st.tr_pre, st.tr_post, st.sx, st.sg)])
-    for a, b in zip(*res):
-        np.testing.assert_array_equal(a, b)
+        res.append([to_np(t) for t in (st.codes, st.W, st.U, st.HX, st.HG, st.tr_pre,
+                                       st.tr_post, st.sx, st.sg)])
+    for other in res[1:]:
+        for a, b in zip(res[0], other):
+            np.testing.assert_array_equal(a, b)

@@ -100,6 +100,43 @@ def test_cov_limited_matches_uncapped(max_cus):
     assert rel_frob(to_np(H1), ref) < TOL
 
 
+@pytest.mark.parametrize("n,d,bf16", [(1000, 300, True), (5000, 600, True), (64, 8, True),
+                                      (4099, 1030, True), (70, 257, True), (3000, 260, False),
+                                      (200000, 64, True), (2, 4096, True)])
+def test_cov_diag(n, d, bf16):
+    """diag(A^T A) from one read of A: fp64 sums of exact bf16 squares (fp32 squares are exact
+    in fp64 too), rounded once, so within one fp32 ulp of the oracle's diagonal; lda > d for
+    ragged d; a second call gives the same bits."""
+    dp = (d + 7) // 8 * 8
+    spec = synth.small_spec(dp, dp, n, seed=n + 3 * d).x
+    A = synth.gen_matrix(spec, DEV)
+    if not bf16:
+        g = torch.Generator().manual_seed(d)
+        A = (A.float() * (1.0 + 1e-3 * torch.randn(A.shape, generator=g)).to(DEV)).contiguous()
+    A = A[:, :d]
+    note(f"cov diag n={n} d={d} bf16={bf16}")
+    got = K.kronq_cov_diag(A)
+    again = K.kronq_cov_diag(A, out=torch.full((d,), float("nan"), device=DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(got, again)
+    ref = np.diag(O.covariance(oracle_view(A.cpu().contiguous())))
+    np.testing.assert_allclose(to_np(got), ref, rtol=1.2e-7, atol=0)
+
+
+def test_cov_diag_empty_and_matches_covariance():
+    spec = synth.small_spec(512, 512, 3000, seed=8).x
+    A = synth.gen_matrix(spec, DEV)
+    note("cov diag n_rows=0")
+    z = K.kronq_cov_diag(A[:0], out=torch.full((512,), 7.0, device=DEV))
+    H = torch.empty(512, 512, device=DEV)
+    K.kronq_accumulate_cov(A, H)
+    dg = K.kronq_cov_diag(A)
+    torch.cuda.synchronize()
+    assert torch.equal(z, torch.zeros(512, device=DEV))
+    # the covariance's diagonal (fp32 accumulation) agrees to its own rounding
+    np.testing.assert_allclose(to_np(torch.diagonal(H)), to_np(dg), rtol=2e-6)
+
+
 def test_cov_fp32_and_empty():
     s = synth.workload(1)
     X = synth.gen_matrix(s.x, DEV)
@@ -326,6 +363,47 @@ def test_rotate_split_equals_one_call():
         outs.append([to_np(t) for t in (Wd, HX, HG, sx, sg)])
     for a, b in zip(*outs):
         np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("d_out,d_in,flags", [(448, 512, K.BIIP), (2048, 896, K.BIIP),
+                                              (448, 256, K.RESCALE_OUT | K.ROT_OUT),
+                                              (256, 256, K.RESCALE_IN | K.RESCALE_OUT)])
+def test_rotate_hg_split_equals_one_call(d_out, d_in, flags):
+    """H_X half, then W with S_G from diag(H_G) (HG_DIAG), then H_G from the given sg
+    (SG_GIVEN) -- the sweep no longer waits for H_G -- gives the one-call result bit for bit
+    when the diagonal passed is H_G's own; also HG_DIAG without SX_GIVEN (W and H_X at once)."""
+    s, W, hx, hg, ri, ro = _rot_problem(d_out, d_in, 21)
+    rin, rout = rot_device(ri), rot_device(ro)
+    Wb = W.to(DEV)
+    outs = []
+    for mode in ("one", "three", "two"):
+        HX, HG = f32(hx), f32(hg)
+        hgd = torch.diagonal(HG).contiguous()
+        Wd = torch.full((d_out, d_in), float("nan"), device=DEV)
+        sx = torch.empty(d_in, device=DEV)
+        sg = torch.empty(d_out, device=DEV)
+        note(f"rotate H_G split mode={mode} {d_out}x{d_in} flags={flags}")
+        if mode == "one":
+            K.kronq_rotate(Wb, Wd, HX, HG, rin.sign, rout.sign, rin.q28, rout.q28, sx, sg, flags)
+        else:
+            if mode == "three":
+                K.kronq_rotate(Wb, None, HX, None, rin.sign, None, rin.q28, None, sx, sg,
+                               flags | K.HX_ONLY)
+                K.kronq_rotate(Wb, Wd, None, hgd, rin.sign, rout.sign, rin.q28, rout.q28, sx, sg,
+                               flags | K.SX_GIVEN | K.HG_DIAG)
+            else:
+                K.kronq_rotate(Wb, Wd, HX, hgd, rin.sign, rout.sign, rin.q28, rout.q28, sx, sg,
+                               flags | K.HG_DIAG)
+            hg_before = HG.clone()
+            K.kronq_rotate(None, None, None, HG, rin.sign, rout.sign, rin.q28, rout.q28, sx, sg,
+                           flags | K.SX_GIVEN | K.SG_GIVEN)
+            torch.cuda.synchronize()
+            assert not torch.equal(HG, hg_before) or not (flags & (K.RESCALE_OUT | K.ROT_OUT))
+        torch.cuda.synchronize()
+        outs.append([to_np(t) for t in (Wd, HX, HG, sx, sg)])
+    for other in outs[1:]:
+        for a, b in zip(outs[0], other):
+            np.testing.assert_array_equal(a, b)
 
 
 def test_traces_split_across_calls():
