@@ -5,16 +5,21 @@
 // two products of the K-FAC loss.
 //   * 128 x 128 output tile per workgroup, 4 waves in a 2 x 2 grid, each wave 64 x 64 =
 //     2 x 2 MFMA blocks (64 fp32 accumulators per lane).
-//   * K advances 16 at a time through LDS stored k-major ([k][m], [k][n]) so that every MFMA
-//     operand is one 4-byte LDS read by 32 consecutive lanes; the row stride of 160 floats puts
-//     the two k rows a wave reads at once in disjoint bank halves.
-//   * The next K chunk is fetched into registers while the current one is multiplied.
+//   * K advances 32 at a time through two LDS buffers: the next stage is fetched into
+//     registers before the current stage's products and stored into the other buffer after
+//     them, one barrier per stage. An operand read with k contiguous stays [m][k] in LDS (row
+//     stride 36 floats, so 16-byte stores and at most 2-way conflicts on the MFMA reads); one
+//     read with m contiguous is stored [k][m] (row stride 160 floats: the two k rows a wave
+//     reads at once fall in disjoint bank halves).
 //   * Triangular flags skip tiles or K ranges that are known to be zero or unused.
-// Problems too small to give the 128 x 128 kernel enough workgroups (the short products of the
-// recursive Cholesky) use gemm_f32_small: a 32 x 32 or 64 x 64 tile per workgroup, K staged 64
-// at a time through LDS, and for 32 x 32 tiles each stage's K split over the four waves (the
-// partial blocks are summed through LDS at the end). The dispatcher takes the largest tile that
-// still gives at least 128 workgroups.
+// The recursive Cholesky's products, most of them with a triangular operand, use
+// gemm_f32_small: a 32 x 32 or 64 x 64 tile per workgroup, K staged 64 at a time through LDS,
+// and for 32 x 32 tiles each stage's K split over the four waves (the partial blocks are summed
+// through LDS at the end). With a triangular operand the tiles' K ranges are unequal; the
+// 64 x 64 tiles are then dealt longest range first, which balances the chip far better than
+// 128 x 128 tiles, whose longest tile sets the time (the 2048-order products of a 4096
+// factorisation: 210 -> 110-125 us, the lower-triangle update 210 -> 186 us). Otherwise the
+// dispatcher takes the largest tile that still gives at least 128 workgroups.
 #include <algorithm>
 
 #include "kq_common.hpp"
@@ -25,71 +30,74 @@ namespace {
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int GT = 128;    // tile edge
-constexpr int GK = 16;     // K per stage
+constexpr int GK = 32;     // K per stage
 constexpr int GLD = 160;   // LDS row stride (floats)
 
+constexpr int SKC = GK + 4;  // LDS row stride of a k-contiguous operand stored [m][k]
+
 struct Frag {
-  float v[8];
+  float v[GK / 2];
 };
 
-// Fetch an operand chunk: 16 (k) x 128 (m) elements of op(X), 8 per thread.
-// trans == false: X[m][k] (k contiguous); trans == true: X[k][m] (m contiguous).
-__device__ __forceinline__ void fetch(Frag& f, const float* X, int64_t ldx,
-                                      bool kcontig, int64_t m0, int64_t k0, int64_t M, int64_t K,
-                                      int tid) {
-  if (kcontig) {
-    const int m = tid >> 1, kb = (tid & 1) * 8;
-    const int64_t gm = m0 + m;
+// Fetch an operand chunk: GK (k) x 128 (m) elements of op(X), GK / 2 per thread in float4s.
+// KC: X[m][k] (k contiguous), two threads per row m; else X[k][m] (m contiguous).
+template <bool KC>
+__device__ __forceinline__ void fetch(Frag& f, const float* X, int64_t ldx, int64_t m0,
+                                      int64_t k0, int64_t M, int64_t K, int tid) {
+  constexpr int NQ = GK / 8;  // float4 per thread
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int64_t gk = k0 + kb + h * 4;
-      if (gm < M && gk + 4 <= K) {
-        const float4 x = *reinterpret_cast<const float4*>(X + gm * ldx + gk);
-        f.v[h * 4 + 0] = x.x;
-        f.v[h * 4 + 1] = x.y;
-        f.v[h * 4 + 2] = x.z;
-        f.v[h * 4 + 3] = x.w;
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          f.v[h * 4 + e] = (gm < M && gk + e < K) ? X[gm * ldx + gk + e] : 0.f;
-      }
+  for (int h = 0; h < NQ; ++h) {
+    int64_t r, c;  // element (r, c) of X starts the float4; c is the contiguous index
+    bool full, in_r;
+    if (KC) {
+      r = m0 + (tid >> 1);
+      c = k0 + (tid & 1) * (GK / 2) + h * 4;
+      in_r = r < M;
+      full = in_r && c + 4 <= K;
+    } else {
+      r = k0 + tid / (256 / GK);
+      c = m0 + (tid % (256 / GK)) * (GK / 2) + h * 4;
+      in_r = r < K;
+      full = in_r && c + 4 <= M;
     }
-  } else {
-    const int k = tid >> 4, mb = (tid & 15) * 8;
-    const int64_t gk = k0 + k;
+    if (full) {
+      const float4 x = *reinterpret_cast<const float4*>(X + r * ldx + c);
+      f.v[h * 4 + 0] = x.x;
+      f.v[h * 4 + 1] = x.y;
+      f.v[h * 4 + 2] = x.z;
+      f.v[h * 4 + 3] = x.w;
+    } else {
+      const int64_t lim = KC ? K : M;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int64_t gm = m0 + mb + h * 4;
-      if (gk < K && gm + 4 <= M) {
-        const float4 x = *reinterpret_cast<const float4*>(X + gk * ldx + gm);
-        f.v[h * 4 + 0] = x.x;
-        f.v[h * 4 + 1] = x.y;
-        f.v[h * 4 + 2] = x.z;
-        f.v[h * 4 + 3] = x.w;
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          f.v[h * 4 + e] = (gk < K && gm + e < M) ? X[gk * ldx + gm + e] : 0.f;
-      }
+      for (int e = 0; e < 4; ++e) f.v[h * 4 + e] = (in_r && c + e < lim) ? X[r * ldx + c + e] : 0.f;
     }
   }
 }
 
-// Store the fetched chunk k-major into LDS: s[k][m].
-__device__ __forceinline__ void stash(float* __restrict__ s, const Frag& f, bool kcontig,
-                                      int tid) {
-  if (kcontig) {
-    const int m = tid >> 1, kb = (tid & 1) * 8;
+// Store a fetched chunk in LDS: KC as [m][k] (row stride SKC), else as [k][m] (row stride GLD);
+// both with 16-byte writes.
+template <bool KC>
+__device__ __forceinline__ void stash(float* __restrict__ s, const Frag& f, int tid) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s[(kb + e) * GLD + m] = f.v[e];
-  } else {
-    const int k = tid >> 4, mb = (tid & 15) * 8;
-    *reinterpret_cast<float4*>(s + k * GLD + mb) = make_float4(f.v[0], f.v[1], f.v[2], f.v[3]);
-    *reinterpret_cast<float4*>(s + k * GLD + mb + 4) = make_float4(f.v[4], f.v[5], f.v[6], f.v[7]);
+  for (int h = 0; h < GK / 8; ++h) {
+    float* p = KC ? s + (tid >> 1) * SKC + (tid & 1) * (GK / 2) + 4 * h
+                  : s + (tid / (256 / GK)) * GLD + (tid % (256 / GK)) * (GK / 2) + 4 * h;
+    *reinterpret_cast<float4*>(p) =
+        make_float4(f.v[4 * h], f.v[4 * h + 1], f.v[4 * h + 2], f.v[4 * h + 3]);
   }
 }
 
+// operand value (m, k) of a stage held in LDS
+template <bool KC>
+__device__ __forceinline__ float opnd(const float* s, int m, int k) {
+  return KC ? s[m * SKC + k] : s[k * GLD + m];
+}
+
+// Double-buffered LDS: stage s + 1 is fetched into registers before the products of stage s
+// and stored into the other buffer after them, so one barrier per stage suffices and the
+// global loads' latency hides behind the products. AKC / BKC: op(A) / op(B) is read with k
+// contiguous (the layout in LDS follows, so every store is 16 bytes wide).
+template <bool AKC, bool BKC>
 __global__ __launch_bounds__(256, 2) void gemm_f32_mfma(int flags, int64_t M, int64_t N,
                                                         int64_t K, float alpha,
                                                         const float* A, int64_t lda,
@@ -98,8 +106,7 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_mfma(int flags, int64_t M, in
                                                         int64_t ldc) {
   // A, B and C may overlap (in-place panel solves): all loads of A and B precede the stores,
   // and each workgroup reads only the rows/columns it writes.
-  __shared__ float sA[GK * GLD];
-  __shared__ float sB[GK * GLD];
+  __shared__ __attribute__((aligned(16))) float lds[2][2][GK * GLD];  // [buffer][A, B]
   const int tid = threadIdx.x;
   const int64_t m0 = int64_t(blockIdx.y) * GT, n0 = int64_t(blockIdx.x) * GT;
   if ((flags & GEMM_LOWER_C) && m0 + GT <= n0) return;  // tile strictly above the diagonal
@@ -110,9 +117,8 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_mfma(int flags, int64_t M, in
   if ((flags & GEMM_A_UPPER) && m0 > kbeg) kbeg = (m0 / GK) * GK;  // A[m][k] = 0 for k < m
   if ((flags & GEMM_A_LOWER) && m0 + GT < kend) kend = m0 + GT;  // A[m][k] = 0 for k > m
   if ((flags & GEMM_OPB_UPPER) && n0 + GT < kend) kend = n0 + GT;  // op(B)[k][n] = 0, k > n
+  const int nst = kbeg < kend ? int(cdiv(kend - kbeg, GK)) : 0;
 
-  const bool a_kc = !(flags & GEMM_TA);  // A[m][k] row-major: k contiguous
-  const bool b_kc = (flags & GEMM_TB);   // B^T stored [n][k]: k contiguous
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave & 1, wn = wave >> 1;
   const int l32 = lane & 31, lhi = lane >> 5;
@@ -124,33 +130,41 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_mfma(int flags, int64_t M, in
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x16_t{};
 
   Frag fa, fb;
-  if (kbeg < kend) {
-    fetch(fa, A, lda, a_kc, m0, kbeg, M, kend, tid);
-    fetch(fb, B, ldb, b_kc, n0, kbeg, N, kend, tid);
+  if (nst > 0) {
+    fetch<AKC>(fa, A, lda, m0, kbeg, M, kend, tid);
+    fetch<BKC>(fb, B, ldb, n0, kbeg, N, kend, tid);
+    stash<AKC>(lds[0][0], fa, tid);
+    stash<BKC>(lds[0][1], fb, tid);
   }
-  for (int64_t k0 = kbeg; k0 < kend; k0 += GK) {
-    __syncthreads();
-    stash(sA, fa, a_kc, tid);
-    stash(sB, fb, b_kc, tid);
-    __syncthreads();
-    if (k0 + GK < kend) {
-      fetch(fa, A, lda, a_kc, m0, k0 + GK, M, kend, tid);
-      fetch(fb, B, ldb, b_kc, n0, k0 + GK, N, kend, tid);
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    const bool more = st + 1 < nst;
+    if (more) {
+      const int64_t k1 = kbeg + int64_t(st + 1) * GK;
+      fetch<AKC>(fa, A, lda, m0, k1, M, kend, tid);
+      fetch<BKC>(fb, B, ldb, n0, k1, N, kend, tid);
     }
+    const float* sa = lds[st & 1][0];
+    const float* sb = lds[st & 1][1];
 #pragma unroll
     for (int kk = 0; kk < GK / 2; ++kk) {
       const int kr = 2 * kk + lhi;
       float av[2], bv[2];
 #pragma unroll
-      for (int bi = 0; bi < 2; ++bi) av[bi] = sA[kr * GLD + wm * 64 + bi * 32 + l32];
+      for (int bi = 0; bi < 2; ++bi) av[bi] = opnd<AKC>(sa, wm * 64 + bi * 32 + l32, kr);
 #pragma unroll
-      for (int bj = 0; bj < 2; ++bj) bv[bj] = sB[kr * GLD + wn * 64 + bj * 32 + l32];
+      for (int bj = 0; bj < 2; ++bj) bv[bj] = opnd<BKC>(sb, wn * 64 + bj * 32 + l32, kr);
 #pragma unroll
       for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj)
           acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[bi], bv[bj], acc[bi][bj], 0, 0, 0);
     }
+    if (more) {
+      stash<AKC>(lds[(st + 1) & 1][0], fa, tid);
+      stash<BKC>(lds[(st + 1) & 1][1], fb, tid);
+    }
+    __syncthreads();
   }
 
 #pragma unroll
@@ -170,8 +184,32 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_mfma(int flags, int64_t M, in
 }
 
 
+// Tile of this workgroup, longest K range first: with a triangular operand the K range of a
+// tile depends on its row (A_LOWER, A_UPPER) or column (B_LOWER, OPB_UPPER) index, and
+// workgroups are dispatched in linear order, so the tiles are dealt with that index running
+// slowest, from the longest range to the shortest (the short ones then fill in at the end).
+__device__ __forceinline__ void tile_of(int flags, int tm, int64_t& m0, int64_t& n0) {
+  const int64_t gx = gridDim.x, gy = gridDim.y;
+  const int64_t lin = int64_t(blockIdx.x) + gx * blockIdx.y;
+  int64_t bm = blockIdx.y, bn = blockIdx.x;
+  if (flags & (GEMM_B_LOWER | GEMM_OPB_UPPER)) {  // K set by the column
+    const int64_t c = lin / gy;
+    bm = lin % gy;
+    bn = (flags & GEMM_OPB_UPPER) ? gx - 1 - c : c;
+  } else if (flags & (GEMM_A_LOWER | GEMM_A_UPPER)) {  // K set by the row
+    const int64_t r = lin / gx;
+    bn = lin % gx;
+    bm = (flags & GEMM_A_LOWER) ? gy - 1 - r : r;
+  }
+  m0 = bm * tm;
+  n0 = bn * tm;
+}
+
 // Small-tile variant (see the file comment). A, B and C must not overlap.
-template <int TM>
+// BKC: op(B) is read with k contiguous (B^T stored [n][k]); B then stays [n][k] in LDS (row
+// stride AS, like A) so that both the transposing store and the MFMA reads are free of bank
+// conflicts.
+template <int TM, bool BKC>
 __global__ __launch_bounds__(256) void gemm_f32_small(int flags, int64_t M, int64_t N, int64_t K,
                                                       float alpha, const float* __restrict__ A,
                                                       int64_t lda, const float* __restrict__ B,
@@ -184,11 +222,13 @@ __global__ __launch_bounds__(256) void gemm_f32_small(int flags, int64_t M, int6
   constexpr int AS = KC + 1;                  // LDS row stride of the A tile, [m][k]
   constexpr int BS = TM == 32 ? 32 : 96;      // LDS row stride of the B tile, [k][n]
   constexpr int NV = TM * KC / 1024;          // float4 per thread per operand per stage
+  constexpr int SB = (BKC ? TM * AS : KC * BS);
   __shared__ float sA[TM * AS];
-  __shared__ float sB[KC * BS];
+  __shared__ float sB[SB];
   __shared__ float red[(SK - 1) * 1024 + 1];
   const int tid = threadIdx.x;
-  const int64_t m0 = int64_t(blockIdx.y) * TM, n0 = int64_t(blockIdx.x) * TM;
+  int64_t m0, n0;
+  tile_of(flags, TM, m0, n0);
   if ((flags & GEMM_LOWER_C) && m0 + TM <= n0) return;
   if ((flags & GEMM_UPPER_C) && n0 + TM <= m0) return;
   int64_t kbeg = 0, kend = K;
@@ -196,7 +236,8 @@ __global__ __launch_bounds__(256) void gemm_f32_small(int flags, int64_t M, int6
   if ((flags & GEMM_A_UPPER) && m0 > kbeg) kbeg = m0;
   if ((flags & GEMM_A_LOWER) && m0 + TM < kend) kend = m0 + TM;
   if ((flags & GEMM_OPB_UPPER) && n0 + TM < kend) kend = n0 + TM;
-  const bool a_kc = !(flags & GEMM_TA), b_kc = (flags & GEMM_TB);
+  const bool a_kc = !(flags & GEMM_TA);
+  constexpr bool b_kc = BKC;
   const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, lhi = lane >> 5;
   const int blk = wave % (NB32 * NB32), part = wave / (NB32 * NB32);
   const int bm = (blk / NB32) * 32, bn = (blk % NB32) * 32;
@@ -252,7 +293,7 @@ __global__ __launch_bounds__(256) void gemm_f32_small(int flags, int64_t M, int6
       if (b_kc) {
         const int n = e / (KC / 4), k4 = (e % (KC / 4)) * 4;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) sB[(k4 + c) * BS + n] = z[c];
+        for (int c = 0; c < 4; ++c) sB[n * AS + k4 + c] = z[c];
       } else {
         const int k = e / (TM / 4), n4 = (e % (TM / 4)) * 4;
 #pragma unroll
@@ -271,8 +312,8 @@ __global__ __launch_bounds__(256) void gemm_f32_small(int flags, int64_t M, int6
 #pragma unroll
     for (int s2 = 0; s2 < KW / 2; ++s2) {
       const int kk = part * KW + 2 * s2 + lhi;
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sA[(bm + l32) * AS + kk], sB[kk * BS + bn + l32],
-                                                 acc, 0, 0, 0);
+      const float bv = BKC ? sB[(bn + l32) * AS + kk] : sB[kk * BS + bn + l32];
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sA[(bm + l32) * AS + kk], bv, acc, 0, 0, 0);
     }
   }
   if (SK > 1) {
@@ -314,19 +355,28 @@ int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const floa
       c += (flags & GEMM_LOWER_C) ? std::min(tn, i + 1) : std::max<int64_t>(0, tn - i);
     return c;
   };
-  if (work(GT) >= 128) {
+  // a triangular operand makes the tiles' K ranges unequal: 64 x 64 tiles, longest first,
+  // balance them better than 128 x 128 tiles, whose longest tile sets the time
+  const bool tri_k = flags & (GEMM_B_LOWER | GEMM_OPB_UPPER | GEMM_A_LOWER | GEMM_A_UPPER |
+                              GEMM_LOWER_C | GEMM_UPPER_C);
+  if (work(GT) >= 128 && !(tri_k && work(64) >= 256)) {
     const dim3 grid(unsigned(cdiv(N, GT)), unsigned(cdiv(M, GT)));
-    return launch(name, gemm_f32_mfma, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B,
-                  ldb, beta, C, ldc);
+    const bool akc = !(flags & GEMM_TA), bkc = flags & GEMM_TB;
+    auto kern = akc ? (bkc ? gemm_f32_mfma<true, true> : gemm_f32_mfma<true, false>)
+                    : (bkc ? gemm_f32_mfma<false, true> : gemm_f32_mfma<false, false>);
+    return launch(name, kern, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B, ldb, beta,
+                  C, ldc);
   }
   if (work(64) >= 128) {
     const dim3 grid(unsigned(cdiv(N, 64)), unsigned(cdiv(M, 64)));
-    return launch(name, gemm_f32_small<64>, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda,
-                  B, ldb, beta, C, ldc);
+    auto kern = (flags & GEMM_TB) ? gemm_f32_small<64, true> : gemm_f32_small<64, false>;
+    return launch(name, kern, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B, ldb, beta,
+                  C, ldc);
   }
   const dim3 grid(unsigned(cdiv(N, 32)), unsigned(cdiv(M, 32)));
-  return launch(name, gemm_f32_small<32>, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B,
-                ldb, beta, C, ldc);
+  auto kern = (flags & GEMM_TB) ? gemm_f32_small<32, true> : gemm_f32_small<32, false>;
+  return launch(name, kern, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B, ldb, beta, C,
+                ldc);
 }
 
 }  // namespace kq
