@@ -48,7 +48,7 @@ def traffic_file(kernel: str, workload: str) -> str:
 KERNELS = ["cov_diag_partial", "cov_diag_final", "syrk_bf16_mfma", "syrk_bf16_mfma_shared", "syrk_reduce", "cross_bf16_mfma", "cross_reduce", "traces",
            "rot_w_norms", "rot_factors", "rot_inv_factors", "rot_row_pass", "fwht_col",
            "mix28_col", "chol_diag_shift", "chol_add_diag", "chol_reverse_copy",
-           "chol_potrf_diag", "chol_trsm", "chol_syrk", "trtri_row", "trtri_put_diag",
+           "chol_potrf_diag", "chol_trsm", "chol_syrk_trtri_row",
            "trtri_update", "chol_reverse_out", "gptaq_d_ut", "gptaq_t_u", "gptaq_mask",
            "obs_split_u", "obs_split_p", "obs_group_params", "obs_sweep", "obs_trailing_update"]
 WORKLOADS = {"q_proj": 2, "down_proj": 3, "up_proj_70b": 4}

@@ -6,13 +6,16 @@
 //   2. L and X = L^-1 together, recursively on [[M11, .], [M21, M22]] split at a multiple of 128:
 //        factor and invert M11 (X11 = L11^-1);
 //        L21 = M21 X11^T                  (written to the X21 slot, which is still free);
-//        M22 -= L21 L21^T                 (lower tiles only);
+//        M22 -= L21 L21^T                 (lower tiles only) and T = L21 X11 (scratch kept
+//                                          until the last step), both in one launch;
 //        factor and invert M22 (X22);
-//        X21 = -X22 (L21 X11)             (through a scratch product, then over L21).
+//        X21 = -X22 T                     (over L21).
 //      Leaves of at most 128 columns are factored and inverted in LDS by one workgroup; every
-//      other step is a fp32 MFMA GEMM, so the large updates have a long K;
+//      other step is a fp32 MFMA GEMM, so the large updates have a long K. Three dependent
+//      launches per split: the chain of small ones, not the flops, sets the time at d = 4096;
 //   3. U[i][j] = X[d-1-i][d-1-j] for i <= j, 0 below the diagonal.
 // A non-positive pivot sets *info to its 1-based column in the original order (first failure).
+#include <algorithm>
 #include <cmath>
 
 #include "kq_common.hpp"
@@ -269,8 +272,17 @@ int64_t ld_for(int64_t d) { return ((d + 63) / 64) * 64; }
 // split of an n-column block: the first h columns, a multiple of NB, about half
 int64_t split_at(int64_t n) { return (cdiv(n, NB) / 2) * NB; }
 
+// Scratch floats the recursion below needs for an n-column block: a node keeps its product
+// T (r x h) until its last step, while the second child's recursion runs after it.
+int64_t chol_scratch(int64_t n) {
+  if (n <= NB) return 0;
+  const int64_t h = split_at(n), r = n - h;
+  return std::max(chol_scratch(h), r * h + chol_scratch(r));
+}
+
 // L and L^-1 of the block [n0, n0 + n) of M; the lower part of the same block of X receives
-// L^-1 (zeros on the upper part of the diagonal leaves), T is scratch of split rows x cols.
+// L^-1 (zeros on the upper part of the diagonal leaves). T is scratch of tcap floats (at least
+// chol_scratch(n)).
 int chol_rec(float* M, float* X, float* T, int64_t tcap, int64_t ld, int64_t n0, int64_t n,
              int64_t d, int* info, hipStream_t s) {
   if (n <= NB)
@@ -287,12 +299,13 @@ int chol_rec(float* M, float* X, float* T, int64_t tcap, int64_t ld, int64_t n0,
   // L21 = M21 X11^T (op(B) = X11^T is upper triangular)
   KQ_TRY(gemm_f32(GEMM_TB | GEMM_OPB_UPPER, r, h, h, 1.f, M21, ld, X11, ld, 0.f, X21, ld, s,
                   "chol_trsm"));
-  // M22 -= L21 L21^T
-  KQ_TRY(gemm_f32(GEMM_TB | GEMM_LOWER_C, r, r, h, -1.f, X21, ld, X21, ld, 1.f, M22, ld, s,
-                  "chol_syrk"));
-  KQ_TRY(chol_rec(M, X, T, tcap, ld, n0 + h, r, d, info, s));
-  // T = L21 X11, then X21 = -X22 T
-  KQ_TRY(gemm_f32(GEMM_B_LOWER, r, h, h, 1.f, X21, ld, X11, ld, 0.f, T, h, s, "trtri_row"));
+  // in one launch (both need only L21 and X11): M22 -= L21 L21^T (lower tiles only) and
+  // T = L21 X11 (X11 lower triangular)
+  const GemmProb syrk{GEMM_TB | GEMM_LOWER_C, r, r, h, -1.f, X21, ld, X21, ld, 1.f, M22, ld};
+  const GemmProb row{GEMM_B_LOWER, r, h, h, 1.f, X21, ld, X11, ld, 0.f, T, h};
+  KQ_TRY(gemm_f32_dual(syrk, row, s, "chol_syrk_trtri_row"));
+  KQ_TRY(chol_rec(M, X, T + r * h, tcap - r * h, ld, n0 + h, r, d, info, s));
+  // X21 = -X22 T
   return gemm_f32(GEMM_A_LOWER, r, h, r, -1.f, X22, ld, T, h, 0.f, X21, ld, s, "trtri_update");
 }
 
@@ -301,19 +314,17 @@ int chol_rec(float* M, float* X, float* T, int64_t tcap, int64_t ld, int64_t n0,
 size_t chol_ws_bytes(int64_t d) {
   if (d <= 0) return 0;
   const int64_t ld = ld_for(d);
-  const int64_t h = split_at(d);
   return 2 * align256(size_t(d) * ld * sizeof(float)) +
-         align256(size_t(d - h) * size_t(h > 0 ? h : 1) * sizeof(float)) + 256;
+         align256(size_t(std::max<int64_t>(1, chol_scratch(d))) * sizeof(float)) + 256;
 }
 
 int chol_launch(float* H, int64_t d, int64_t ldh, float damp_rel, float* U, int64_t ldu,
                 int* info, void* ws, hipStream_t s) {
   const int64_t ld = ld_for(d);
-  const int64_t h = split_at(d);
   Carver cv(ws);
   float* M = cv.take<float>(size_t(d) * ld);
   float* X = cv.take<float>(size_t(d) * ld);
-  const int64_t tcap = (d - h) * (h > 0 ? h : 1);
+  const int64_t tcap = std::max<int64_t>(1, chol_scratch(d));
   float* T = cv.take<float>(size_t(tcap));
   float* shift = cv.take<float>(1);
 

@@ -184,15 +184,30 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_mfma(int flags, int64_t M, in
 }
 
 
-// Tile of this workgroup, longest K range first: with a triangular operand the K range of a
+// Tiles of a product on a tm-edge grid (gx x gy tiles): with LOWER_C / UPPER_C on a square grid
+// only the tiles that touch that triangle are enumerated.
+__host__ __device__ inline int64_t tile_count(int flags, int64_t gx, int64_t gy) {
+  if ((flags & (GEMM_LOWER_C | GEMM_UPPER_C)) && gx == gy) return gx * (gx + 1) / 2;
+  return gx * gy;
+}
+
+// Tile number lin of a product -> its corner. Triangular outputs are enumerated row by row
+// (LOWER_C) or column by column (UPPER_C). Otherwise, with a triangular operand the K range of a
 // tile depends on its row (A_LOWER, A_UPPER) or column (B_LOWER, OPB_UPPER) index, and
-// workgroups are dispatched in linear order, so the tiles are dealt with that index running
-// slowest, from the longest range to the shortest (the short ones then fill in at the end).
-__device__ __forceinline__ void tile_of(int flags, int tm, int64_t& m0, int64_t& n0) {
-  const int64_t gx = gridDim.x, gy = gridDim.y;
-  const int64_t lin = int64_t(blockIdx.x) + gx * blockIdx.y;
-  int64_t bm = blockIdx.y, bn = blockIdx.x;
-  if (flags & (GEMM_B_LOWER | GEMM_OPB_UPPER)) {  // K set by the column
+// workgroups are dispatched in order, so the tiles are dealt with that index running slowest,
+// from the longest range to the shortest (the short ones then fill in at the end).
+__device__ __forceinline__ void tile_from(int flags, int64_t lin, int64_t gx, int64_t gy,
+                                          int tm, int64_t& m0, int64_t& n0) {
+  int64_t bm = lin / gx, bn = lin % gx;
+  if ((flags & (GEMM_LOWER_C | GEMM_UPPER_C)) && gx == gy) {
+    // lin = i (i + 1) / 2 + j with j <= i
+    int64_t i = int64_t((sqrt(8.0 * double(lin) + 1.0) - 1.0) * 0.5);
+    while (i * (i + 1) / 2 > lin) --i;
+    while ((i + 1) * (i + 2) / 2 <= lin) ++i;
+    const int64_t j = lin - i * (i + 1) / 2;
+    bm = (flags & GEMM_LOWER_C) ? i : j;
+    bn = (flags & GEMM_LOWER_C) ? j : i;
+  } else if (flags & (GEMM_B_LOWER | GEMM_OPB_UPPER)) {  // K set by the column
     const int64_t c = lin / gy;
     bm = lin % gy;
     bn = (flags & GEMM_OPB_UPPER) ? gx - 1 - c : c;
@@ -205,16 +220,23 @@ __device__ __forceinline__ void tile_of(int flags, int tm, int64_t& m0, int64_t&
   n0 = bn * tm;
 }
 
-// Small-tile variant (see the file comment). A, B and C must not overlap.
+template <int TM>
+struct SmallLds {
+  static constexpr int KC = 64, AS = KC + 1, BS = TM == 32 ? 32 : 96;
+  static constexpr int SK = 4 / ((TM / 32) * (TM / 32));
+  static constexpr int A = TM * AS;
+  static constexpr int B = TM * AS > KC * BS ? TM * AS : KC * BS;  // either B layout
+  static constexpr int R = (SK - 1) * 1024 + 1;
+};
+
+// One tile of the small-tile product (see the file comment). A, B and C must not overlap.
 // BKC: op(B) is read with k contiguous (B^T stored [n][k]); B then stays [n][k] in LDS (row
 // stride AS, like A) so that both the transposing store and the MFMA reads are free of bank
 // conflicts.
 template <int TM, bool BKC>
-__global__ __launch_bounds__(256) void gemm_f32_small(int flags, int64_t M, int64_t N, int64_t K,
-                                                      float alpha, const float* __restrict__ A,
-                                                      int64_t lda, const float* __restrict__ B,
-                                                      int64_t ldb, float beta,
-                                                      float* __restrict__ C, int64_t ldc) {
+__device__ __forceinline__ void small_tile(const GemmProb& p, int64_t m0, int64_t n0,
+                                           float* __restrict__ sA, float* __restrict__ sB,
+                                           float* __restrict__ red) {
   constexpr int KC = 64;                      // K per stage
   constexpr int NB32 = TM / 32;               // 32 x 32 blocks per tile edge
   constexpr int SK = 4 / (NB32 * NB32);       // waves per block (split of each stage's K)
@@ -223,12 +245,14 @@ __global__ __launch_bounds__(256) void gemm_f32_small(int flags, int64_t M, int6
   constexpr int BS = TM == 32 ? 32 : 96;      // LDS row stride of the B tile, [k][n]
   constexpr int NV = TM * KC / 1024;          // float4 per thread per operand per stage
   constexpr int SB = (BKC ? TM * AS : KC * BS);
-  __shared__ float sA[TM * AS];
-  __shared__ float sB[SB];
-  __shared__ float red[(SK - 1) * 1024 + 1];
+  (void)SB;
+  const int flags = p.flags;
+  const int64_t M = p.M, N = p.N, K = p.K, lda = p.lda, ldb = p.ldb, ldc = p.ldc;
+  const float alpha = p.alpha, beta = p.beta;
+  const float* __restrict__ A = p.A;
+  const float* __restrict__ B = p.B;
+  float* __restrict__ C = p.C;
   const int tid = threadIdx.x;
-  int64_t m0, n0;
-  tile_of(flags, TM, m0, n0);
   if ((flags & GEMM_LOWER_C) && m0 + TM <= n0) return;
   if ((flags & GEMM_UPPER_C) && n0 + TM <= m0) return;
   int64_t kbeg = 0, kend = K;
@@ -339,27 +363,65 @@ __global__ __launch_bounds__(256) void gemm_f32_small(int flags, int64_t M, int6
   }
 }
 
+
+template <int TM, bool BKC>
+__global__ __launch_bounds__(256) void gemm_f32_small(GemmProb p, int64_t gx, int64_t gy) {
+  __shared__ float sA[SmallLds<TM>::A];
+  __shared__ float sB[SmallLds<TM>::B];
+  __shared__ float red[SmallLds<TM>::R];
+  int64_t m0, n0;
+  tile_from(p.flags, blockIdx.x, gx, gy, TM, m0, n0);
+  small_tile<TM, BKC>(p, m0, n0, sA, sB, red);
+}
+
+// Two independent products in one launch (the first problem's tiles first): one dependent
+// launch fewer where the recursion has two products with the same inputs ready.
+template <int TM, bool BKC1, bool BKC2>
+__global__ __launch_bounds__(256) void gemm_f32_dual(GemmProb p1, int64_t gx1, int64_t gy1,
+                                                     int64_t n1, GemmProb p2, int64_t gx2,
+                                                     int64_t gy2) {
+  __shared__ float sA[SmallLds<TM>::A];
+  __shared__ float sB[SmallLds<TM>::B];
+  __shared__ float red[SmallLds<TM>::R];
+  int64_t m0, n0;
+  const int64_t lin = blockIdx.x;
+  if (lin < n1) {
+    tile_from(p1.flags, lin, gx1, gy1, TM, m0, n0);
+    small_tile<TM, BKC1>(p1, m0, n0, sA, sB, red);
+  } else {
+    tile_from(p2.flags, lin - n1, gx2, gy2, TM, m0, n0);
+    small_tile<TM, BKC2>(p2, m0, n0, sA, sB, red);
+  }
+}
+
+}  // namespace
+
+namespace {
+
+// workgroups that do work for a tile edge t
+int64_t work(int flags, int64_t M, int64_t N, int64_t t) {
+  const int64_t tm = cdiv(M, t), tn = cdiv(N, t);
+  if (!(flags & (GEMM_LOWER_C | GEMM_UPPER_C))) return tm * tn;
+  int64_t c = 0;
+  for (int64_t i = 0; i < tm; ++i)
+    c += (flags & GEMM_LOWER_C) ? std::min(tn, i + 1) : std::max<int64_t>(0, tn - i);
+  return c;
+}
+
+// tile edge of the small-tile kernel for a product: 64 when that still gives enough workgroups
+int small_edge(int flags, int64_t M, int64_t N) { return work(flags, M, N, 64) >= 128 ? 64 : 32; }
+
 }  // namespace
 
 int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
              hipStream_t s, const char* name) {
   if (M <= 0 || N <= 0) return KRONQ_OK;
-  // workgroups that do work for a tile edge t (LOWER_C drops the tiles above the diagonal,
-  // UPPER_C those below it)
-  auto work = [&](int64_t t) {
-    const int64_t tm = cdiv(M, t), tn = cdiv(N, t);
-    if (!(flags & (GEMM_LOWER_C | GEMM_UPPER_C))) return tm * tn;
-    int64_t c = 0;
-    for (int64_t i = 0; i < tm; ++i)
-      c += (flags & GEMM_LOWER_C) ? std::min(tn, i + 1) : std::max<int64_t>(0, tn - i);
-    return c;
-  };
-  // a triangular operand makes the tiles' K ranges unequal: 64 x 64 tiles, longest first,
-  // balance them better than 128 x 128 tiles, whose longest tile sets the time
-  const bool tri_k = flags & (GEMM_B_LOWER | GEMM_OPB_UPPER | GEMM_A_LOWER | GEMM_A_UPPER |
-                              GEMM_LOWER_C | GEMM_UPPER_C);
-  if (work(GT) >= 128 && !(tri_k && work(64) >= 256)) {
+  // a triangular operand or output makes the tiles' work unequal: 64 x 64 tiles, longest
+  // first, balance them better than 128 x 128 tiles, whose longest tile sets the time
+  const bool tri = flags & (GEMM_B_LOWER | GEMM_OPB_UPPER | GEMM_A_LOWER | GEMM_A_UPPER |
+                            GEMM_LOWER_C | GEMM_UPPER_C);
+  if (work(flags, M, N, GT) >= 128 && !(tri && work(flags, M, N, 64) >= 256)) {
     const dim3 grid(unsigned(cdiv(N, GT)), unsigned(cdiv(M, GT)));
     const bool akc = !(flags & GEMM_TA), bkc = flags & GEMM_TB;
     auto kern = akc ? (bkc ? gemm_f32_mfma<true, true> : gemm_f32_mfma<true, false>)
@@ -367,16 +429,39 @@ int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const floa
     return launch(name, kern, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B, ldb, beta,
                   C, ldc);
   }
-  if (work(64) >= 128) {
-    const dim3 grid(unsigned(cdiv(N, 64)), unsigned(cdiv(M, 64)));
-    auto kern = (flags & GEMM_TB) ? gemm_f32_small<64, true> : gemm_f32_small<64, false>;
-    return launch(name, kern, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B, ldb, beta,
-                  C, ldc);
+  const GemmProb p{flags, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc};
+  const int t = small_edge(flags, M, N);
+  const int64_t gx = cdiv(N, t), gy = cdiv(M, t);
+  const dim3 grid(unsigned(tile_count(flags, gx, gy)));
+  const bool bkc = flags & GEMM_TB;
+  if (t == 64)
+    return launch(name, bkc ? gemm_f32_small<64, true> : gemm_f32_small<64, false>, grid,
+                  dim3(256), 0, s, p, gx, gy);
+  return launch(name, bkc ? gemm_f32_small<32, true> : gemm_f32_small<32, false>, grid, dim3(256),
+                0, s, p, gx, gy);
+}
+
+int gemm_f32_dual(const GemmProb& p1, const GemmProb& p2, hipStream_t s, const char* name) {
+  if (p1.M <= 0 || p1.N <= 0) return gemm_f32(p2.flags, p2.M, p2.N, p2.K, p2.alpha, p2.A, p2.lda,
+                                              p2.B, p2.ldb, p2.beta, p2.C, p2.ldc, s, name);
+  if (p2.M <= 0 || p2.N <= 0) return gemm_f32(p1.flags, p1.M, p1.N, p1.K, p1.alpha, p1.A, p1.lda,
+                                              p1.B, p1.ldb, p1.beta, p1.C, p1.ldc, s, name);
+  // one tile edge for both: 64 when the two together give enough workgroups
+  const int64_t w64 = work(p1.flags, p1.M, p1.N, 64) + work(p2.flags, p2.M, p2.N, 64);
+  const int t = w64 >= 128 ? 64 : 32;
+  const int64_t gx1 = cdiv(p1.N, t), gy1 = cdiv(p1.M, t), gx2 = cdiv(p2.N, t),
+                gy2 = cdiv(p2.M, t);
+  const int64_t n1 = tile_count(p1.flags, gx1, gy1), n2 = tile_count(p2.flags, gx2, gy2);
+  const dim3 grid(unsigned(n1 + n2));
+  const bool b1 = p1.flags & GEMM_TB, b2 = p2.flags & GEMM_TB;
+  if (t == 64) {
+    auto kern = b1 ? (b2 ? gemm_f32_dual<64, true, true> : gemm_f32_dual<64, true, false>)
+                   : (b2 ? gemm_f32_dual<64, false, true> : gemm_f32_dual<64, false, false>);
+    return launch(name, kern, grid, dim3(256), 0, s, p1, gx1, gy1, n1, p2, gx2, gy2);
   }
-  const dim3 grid(unsigned(cdiv(N, 32)), unsigned(cdiv(M, 32)));
-  auto kern = (flags & GEMM_TB) ? gemm_f32_small<32, true> : gemm_f32_small<32, false>;
-  return launch(name, kern, grid, dim3(256), 0, s, flags, M, N, K, alpha, A, lda, B, ldb, beta, C,
-                ldc);
+  auto kern = b1 ? (b2 ? gemm_f32_dual<32, true, true> : gemm_f32_dual<32, true, false>)
+                 : (b2 ? gemm_f32_dual<32, false, true> : gemm_f32_dual<32, false, false>);
+  return launch(name, kern, grid, dim3(256), 0, s, p1, gx1, gy1, n1, p2, gx2, gy2);
 }
 
 }  // namespace kq

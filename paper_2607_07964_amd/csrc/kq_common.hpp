@@ -182,6 +182,22 @@ int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th,
 int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
              hipStream_t s, const char* name = "gemm_f32_mfma");
+// one product C = alpha op(A) op(B) + beta C with the GEMM_* flags
+struct GemmProb {
+  int flags;
+  int64_t M, N, K;
+  float alpha;
+  const float* A;
+  int64_t lda;
+  const float* B;
+  int64_t ldb;
+  float beta;
+  float* C;
+  int64_t ldc;
+};
+// two independent products in one launch (small-tile kernel; the outputs must not overlap
+// each other or the inputs)
+int gemm_f32_dual(const GemmProb& p1, const GemmProb& p2, hipStream_t s, const char* name);
 // Cholesky inverse factor
 size_t chol_ws_bytes(int64_t d);
 int chol_launch(float* H, int64_t d, int64_t ldh, float damp_rel, float* U, int64_t ldu,
