@@ -147,9 +147,12 @@ int kronq_accumulate_cov_limited(const void* A, int dtype, int64_t n_rows, int64
  *   A      device, KRONQ_BF16 or KRONQ_FP32, rows of lda elements; A 16-byte aligned, lda
  *          divisible by 8 (bf16) or 4 (fp32).
  *   hdiag  device fp32 [d], written. n_rows = 0 writes zeros (A may then be NULL).
+ *   max_cus  0: enough workgroups to fill the chip; > 0: at most max(max_cus, ceil(d / 512))
+ *          workgroups, for a caller that runs latency-bound work beside it (the result is the
+ *          same either way up to the order of the fp64 sums). < 0: KRONQ_ERR_INVALID_ARG.
  *   ws     kronq_workspace_bytes(KRONQ_OP_COV_DIAG, 0, d, n_rows) bytes. */
 int kronq_cov_diag(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
-                   float* hdiag, void* ws, size_t ws_bytes, void* stream);
+                   float* hdiag, int max_cus, void* ws, size_t ws_bytes, void* stream);
 
 /* ---- 1b. drift statistic (Alg. 1 first line; eq. gptaq_obj) ------------------------------
  * C <- beta * C + alpha * A^T B for token-major A, B [n_rows x d] with the same leading

@@ -53,13 +53,15 @@ __global__ __launch_bounds__(256) void colsq_partial(const T* __restrict__ A, in
   if (c0 < d) {
     const int64_t nc = d - c0;
     int64_t r = r0 + wave;
-    // four rows in flight per wave before the first use
-    for (; r + 12 < r1; r += 16) {
-      float x[4][8];
+    // U rows in flight per wave before the first use (16 KB per wave for bf16), so that a
+    // launch bounded to a few workgroups still keeps enough loads outstanding
+    constexpr int U = sizeof(T) == 2 ? 16 : 8;
+    for (; r + 4 * (U - 1) < r1; r += 4 * U) {
+      float x[U][8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) csq_load8(A + (r + 4 * u) * lda + c0, nc, x[u]);
+      for (int u = 0; u < U; ++u) csq_load8(A + (r + 4 * u) * lda + c0, nc, x[u]);
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < U; ++u)
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] = fma(double(x[u][e]), double(x[u][e]), acc[e]);
     }
@@ -89,15 +91,26 @@ __global__ __launch_bounds__(256) void colsq_final(const double* __restrict__ pa
                                                    int64_t d, float* __restrict__ out) {
   const int64_t j = int64_t(blockIdx.x) * 256 + threadIdx.x;
   if (j >= d) return;
+  // chunks added in order; loaded eight at a time so that the loads overlap
   double v = 0.0;
-  for (int c = 0; c < n_chunks; ++c) v += part[int64_t(c) * d + j];
+  int c = 0;
+  for (; c + 8 <= n_chunks; c += 8) {
+    double t[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) t[q] = part[int64_t(c + q) * d + j];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v += t[q];
+  }
+  for (; c < n_chunks; ++c) v += part[int64_t(c) * d + j];
   out[j] = float(v);
 }
 
-// row chunks of the column-square kernel: enough workgroups to fill the chip, at least 64 rows
-int64_t colsq_chunk_rows(int64_t n_rows, int64_t d) {
+// row chunks of the column-square kernel: enough workgroups to fill the chip (or at most
+// max_wgs of them, but never fewer than one chunk per column block), at least 64 rows each
+int64_t colsq_chunk_rows(int64_t n_rows, int64_t d, int max_wgs = 0) {
   const int64_t col_blocks = cdiv(d, CSQ_COLS);
-  const int64_t want = std::max<int64_t>(1, CSQ_TARGET_WGS / col_blocks);
+  const int64_t target = max_wgs > 0 ? std::min(max_wgs, CSQ_TARGET_WGS) : CSQ_TARGET_WGS;
+  const int64_t want = std::max<int64_t>(1, target / col_blocks);
   return std::max<int64_t>(64, cdiv(n_rows, want));
 }
 
@@ -110,11 +123,11 @@ size_t cov_diag_ws_bytes(int64_t n_rows, int64_t d) {
 }
 
 int cov_diag_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
-                    float* hdiag, void* ws, hipStream_t s) {
+                    float* hdiag, int max_cus, void* ws, hipStream_t s) {
   if (n_rows == 0)  // no chunks: the final kernel writes zeros
     return launch("cov_diag_final", colsq_final, dim3(unsigned(cdiv(d, 256))), dim3(256), 0, s,
                   static_cast<const double*>(nullptr), 0, d, hdiag);
-  const int64_t rows = colsq_chunk_rows(n_rows, d);
+  const int64_t rows = colsq_chunk_rows(n_rows, d, max_cus);
   const int64_t chunks = cdiv(n_rows, rows);
   double* part = static_cast<double*>(ws);
   const dim3 grid(unsigned(cdiv(d, CSQ_COLS)), unsigned(chunks));

@@ -108,7 +108,7 @@ int cov_launch(const void* A, const void* B, int dtype, int64_t n_rows, int64_t 
 // diag(A^T A) as column sums of squares (fp64 sums, one rounding to fp32)
 size_t cov_diag_ws_bytes(int64_t n_rows, int64_t d);
 int cov_diag_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
-                    float* hdiag, void* ws, hipStream_t s);
+                    float* hdiag, int max_cus, void* ws, hipStream_t s);
 // traces
 int traces_launch(const float* HX, int64_t d_in, int64_t ldx, const float* HG, int64_t d_out,
                   int64_t ldg, double* out3, hipStream_t s);

@@ -145,8 +145,9 @@ int kronq_accumulate_cov_limited(const void* A, int dtype, int64_t n_rows, int64
 }
 
 int kronq_cov_diag(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
-                   float* hdiag, void* ws, size_t ws_bytes, void* stream) {
+                   float* hdiag, int max_cus, void* ws, size_t ws_bytes, void* stream) {
   kq::clear_error();
+  KQ_REQUIRE(max_cus >= 0, KRONQ_ERR_INVALID_ARG, "max_cus must be >= 0");
   KQ_REQUIRE(valid_dtype(dtype), KRONQ_ERR_INVALID_ARG, "dtype must be KRONQ_BF16 or KRONQ_FP32");
   KQ_REQUIRE(hdiag && aligned(hdiag, 4), KRONQ_ERR_INVALID_ARG, "hdiag is NULL or misaligned");
   KQ_REQUIRE(n_rows >= 0 && d >= 1 && d <= (int64_t(1) << 24), KRONQ_ERR_INVALID_ARG,
@@ -158,7 +159,7 @@ int kronq_cov_diag(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t 
                "A must be 16-byte aligned with lda divisible by 8 (bf16) or 4 (fp32)");
     KQ_TRY(check_ws(ws, ws_bytes, kq::cov_diag_ws_bytes(n_rows, d)));
   }
-  return kq::cov_diag_launch(A, dtype, n_rows, d, lda, hdiag, ws, as_stream(stream));
+  return kq::cov_diag_launch(A, dtype, n_rows, d, lda, hdiag, max_cus, ws, as_stream(stream));
 }
 
 int kronq_accumulate_cross(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d,

@@ -129,8 +129,17 @@ __global__ void side_factors(int64_t n, const float* __restrict__ H, int64_t ldh
     if (direct) {
       a = direct[j];
     } else {
+      // partials added in order; loaded eight at a time so that the loads overlap
       a = 0.0;
-      for (int64_t p = 0; p < n_part; ++p) a += part[p * n + j];
+      int64_t p = 0;
+      for (; p + 8 <= n_part; p += 8) {
+        double t[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) t[q] = part[(p + q) * n + j];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) a += t[q];
+      }
+      for (; p < n_part; ++p) a += part[p * n + j];
     }
     const double h = H[j * ldh + j];
     if (a > 0.0 && h > 0.0) s = float(sqrt(sqrt(h / a)));

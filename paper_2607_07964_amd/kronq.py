@@ -64,7 +64,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_version": (I, []),
         "kronq_accumulate_cov": (I, [P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
         "kronq_accumulate_cov_limited": (I, [P, I, I64, I64, I64, P, I64, F, F, I, P, SZ, P]),
-        "kronq_cov_diag": (I, [P, I, I64, I64, I64, P, P, SZ, P]),
+        "kronq_cov_diag": (I, [P, I, I64, I64, I64, P, I, P, SZ, P]),
         "kronq_accumulate_cross": (I, [P, P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
         "kronq_rotate_drift": (I, [P, I64, I64, P, P, P, I, P, SZ, P]),
         "kronq_gptaq_correction": (I, [P, I64, I64, P, I64, F, P, I64, P, SZ, P]),
@@ -177,16 +177,17 @@ def kronq_accumulate_cov_limited(A: torch.Tensor, H: torch.Tensor, max_cus: int,
 
 
 def kronq_cov_diag(A: torch.Tensor, out: Optional[torch.Tensor] = None,
-                   ws: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """diag(A^T A) as fp32 [d] (token-major A [N x d], bf16 or fp32), without the covariance."""
+                   ws: Optional[torch.Tensor] = None, max_cus: int = 0) -> torch.Tensor:
+    """diag(A^T A) as fp32 [d] (token-major A [N x d], bf16 or fp32), without the covariance;
+    ``max_cus`` > 0 bounds its workgroups."""
     _dev(A, out)
     n, d = A.shape
     if out is None:
         out = torch.empty(d, dtype=torch.float32, device=A.device)
     if ws is None:
         ws = workspace(OP_COV_DIAG, 0, d, n, A.device)
-    rc = load().kronq_cov_diag(_ptr(A), _dtype_code(A), n, d, _ld(A), _ptr(out), _ptr(ws),
-                               ws.numel(), _stream(A.device))
+    rc = load().kronq_cov_diag(_ptr(A), _dtype_code(A), n, d, _ld(A), _ptr(out), int(max_cus),
+                               _ptr(ws), ws.numel(), _stream(A.device))
     _check(rc, "kronq_cov_diag")
     return out
 

@@ -164,6 +164,10 @@ def solve(st: LayerState, bits: int, damp: float = 0.01, alpha: Optional[float] 
 # 20 TFLOP/s for the factorisation.
 FACTOR_SHARE = 0.5
 FACTOR_SHARE_SHORT = 0.125
+# (Measured alternatives on q_proj, 11.5 ms with this schedule: starting H_G right after H_X
+# and transforming W on a third stream, 12.0 ms -- H_G then slows the rotation of H_X and the
+# start of the factorisation; diag(H_G) on 64 CUs beside the factorisation instead of beside
+# the H_X covariance, 12.0 ms -- starved by the H_G covariance, it took 5.1 ms.)
 
 
 def _cov_cus(device, n_tokens: int, d_out: int, d_in: int) -> int:

@@ -166,16 +166,18 @@ def test_cov_diag_and_split_rotation_argument_checks():
     ws = ctypes.c_void_p(1 << 30)
     assert K.kronq_workspace_bytes(K.OP_COV_DIAG, 0, 4096, 262144) >= 4096 * 8
     # cov_diag: bad dtype, lda < d, bf16 lda not divisible by 8, workspace too small
-    rc, _ = _err(lib.kronq_cov_diag(fake, 3, 100, 64, 64, fake, ws, 1 << 30, nul))
+    rc, _ = _err(lib.kronq_cov_diag(fake, 3, 100, 64, 64, fake, 0, ws, 1 << 30, nul))
     assert rc == -1
-    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100, 64, 32, fake, ws, 1 << 30, nul))
+    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100, 64, 32, fake, 0, ws, 1 << 30, nul))
     assert rc == -1 and "lda" in msg
-    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100, 60, 60, fake, ws, 1 << 30, nul))
+    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100, 60, 60, fake, 0, ws, 1 << 30, nul))
     assert rc == -1 and "aligned" in msg
-    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100000, 64, 64, fake, ws, 16, nul))
+    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100000, 64, 64, fake, 0, ws, 16, nul))
     assert rc == -5 and "workspace" in msg
-    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100, 64, 64, nul, ws, 1 << 30, nul))
+    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100, 64, 64, nul, 0, ws, 1 << 30, nul))
     assert rc == -1 and "hdiag" in msg
+    rc, msg = _err(lib.kronq_cov_diag(fake, 1, 100, 64, 64, fake, -1, ws, 1 << 30, nul))
+    assert rc == -1 and "max_cus" in msg
 
     def rot(flags, W_in=fake, W=fake):
         return _err(lib.kronq_rotate(W_in, 2, 128, W, 64, 128, 128, fake, 128, fake, 64, fake,

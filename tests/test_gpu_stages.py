@@ -117,10 +117,12 @@ def test_cov_diag(n, d, bf16):
     note(f"cov diag n={n} d={d} bf16={bf16}")
     got = K.kronq_cov_diag(A)
     again = K.kronq_cov_diag(A, out=torch.full((d,), float("nan"), device=DEV))
+    few = K.kronq_cov_diag(A, max_cus=8)  # fewer, longer chunks
     torch.cuda.synchronize()
     assert torch.equal(got, again)
     ref = np.diag(O.covariance(oracle_view(A.cpu().contiguous())))
     np.testing.assert_allclose(to_np(got), ref, rtol=1.2e-7, atol=0)
+    np.testing.assert_allclose(to_np(few), ref, rtol=1.2e-7, atol=0)
 
 
 def test_cov_diag_empty_and_matches_covariance():
