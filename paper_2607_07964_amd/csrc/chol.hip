@@ -83,12 +83,11 @@ __device__ __forceinline__ void mfma_block(float* C, int ldc, const float* A, in
   }
 }
 
-// One 32-column panel of the diagonal-block factorisation (see potrf_diag), then the rank-32
-// update of the lower blocks of the rest of the block.
+// One 32-column panel of the diagonal-block factorisation (see potrf_diag), by one wave.
 template <int c0>
-__device__ __forceinline__ void panel_step(float* a, float* colbuf, float* dummy, int64_t kb,
-                                           int64_t d, int* info, int wave, int lane) {
-  if (wave == 0) {
+__device__ __forceinline__ void panel_factor(float* a, float* colbuf, float* dummy, int64_t kb,
+                                             int64_t d, int* info, int lane) {
+  {
     const int r0 = c0 + lane, r1 = c0 + 64 + lane;
     const bool ok0 = r0 < NB, ok1 = r1 < NB;  // r1 < NB only for c0 < 64
     float v0[32], v1[32];
@@ -111,7 +110,7 @@ __device__ __forceinline__ void panel_step(float* a, float* colbuf, float* dummy
       }
       const float piv = raw[j];
       if (!(piv > 0.f) && first_bad == 32) first_bad = j;  // also catches NaN; a select
-      const float rl = rsqrtf(piv);
+      const float rl = __builtin_amdgcn_rsqf(piv);  // pivots are normal or the factor fails
       const float ljj = piv * rl;
       const float l0 = v0[j] * rl, l1 = v1[j] * rl;
       // A[i][k] -= L[i][j] L[k][j] = (l_i rl) raw_k
@@ -137,18 +136,31 @@ __device__ __forceinline__ void panel_step(float* a, float* colbuf, float* dummy
     if (lane == 0 && first_bad < 32 && kb + c0 + first_bad < d)
       atomicCAS(info, 0, int(d - (kb + c0 + first_bad)));
   }
-  __syncthreads();
-  const int c1 = c0 + 32, nb = (NB - c1) / 32;
-  if (nb > 0) {
-    // lower 32-blocks (bi >= bj) of A22 -= P P^T, P = L[c1:, c0:c0+32]
-    for (int t = wave; t < nb * (nb + 1) / 2; t += 4) {
-      int bi = 0, rem = t;
-      while (rem > bi) rem -= ++bi;
-      const int bj = rem;
-      mfma_block(a + (c1 + 32 * bi) * DLD + c1 + 32 * bj, DLD, a + (c1 + 32 * bi) * DLD + c0,
-                 DLD, a + (c1 + 32 * bj) * DLD + c0, DLD, true, 32, -1.f, 1.f, lane);
+}
+
+// A[bi][bj] -= L[bi][p] L[bj][p]^T for 32 x 32 blocks of the diagonal block, one wave
+__device__ __forceinline__ void upd_block(float* a, int bi, int bj, int p, int lane) {
+  mfma_block(a + 32 * bi * DLD + 32 * bj, DLD, a + 32 * bi * DLD + 32 * p, DLD,
+             a + 32 * bj * DLD + 32 * p, DLD, true, 32, -1.f, 1.f, lane);
+}
+
+// Y_pp = L_pp^-1 for the 32 x 32 diagonal block p, one wave: lane c solves column c by forward
+// substitution (a multiplication by the reciprocal of L_ii, not a division)
+__device__ __forceinline__ void inv_block(const float* a, float* y, int p,
+                                          int lane) {
+  const int b0 = 32 * p;
+  if (lane < 32) {
+    float x[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      float s = (i == lane) ? 1.f : 0.f;
+#pragma unroll
+      for (int k = 0; k < i; ++k) s = fmaf(-a[(b0 + i) * DLD + b0 + k], x[k], s);
+      x[i] = s * __builtin_amdgcn_rcpf(a[(b0 + i) * DLD + b0 + i]);
+      __builtin_amdgcn_sched_barrier(0);  // read one row of L at a time
     }
-    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 32; ++i) y[(b0 + i) * DLD + b0 + lane] = x[i];
   }
 }
 
@@ -160,7 +172,9 @@ __device__ __forceinline__ void panel_step(float* a, float* colbuf, float* dummy
 //     rows is published once through a 64-float LDS buffer and read back as broadcasts, and the
 //     1 / L_jj scaling is folded into the per-row coefficient, so each column costs one LDS
 //     round trip and one FMA per remaining entry;
-//   * rank-32 update of the lower blocks of the rest of the block by all four waves (MFMA).
+//   * rank-32 updates of the lower 32 x 32 blocks right of the panel (MFMA), the next panel's
+//     block column first; the rest, and the inverse of the panel's diagonal block, run on the
+//     other waves while wave 0 factors the next panel.
 // Inverse Y = L^-1 by recursive doubling, inv([[A, 0], [B, C]]) = [[A^-1, 0], [-C^-1 B A^-1, C^-1]]:
 //   32 x 32 diagonal blocks (one wave each, columns by forward substitution), then 64, then 128.
 // Writes Linv_kk, with exact zeros above the diagonal, to X (M itself is left as read).
@@ -172,7 +186,8 @@ __global__ __launch_bounds__(256) void potrf_diag(const float* __restrict__ M, i
   float* const y = lds + NB * DLD;      // Y = L^-1
   float* const tb = lds + 2 * NB * DLD; // product scratch (a dummy store target in the panels)
   __shared__ __attribute__((aligned(16))) float colbuf[64];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: per-wave branches
   const bool full = bs == NB;
   if (full) {
     float4 q[NB * NB / 1024];
@@ -199,27 +214,43 @@ __global__ __launch_bounds__(256) void potrf_diag(const float* __restrict__ M, i
     y[(o + i) * DLD + o + 32 + j] = 0.f;
   }
   __syncthreads();
-  panel_step<0>(a, colbuf, tb, kb, d, info, wave, lane);
-  panel_step<32>(a, colbuf, tb, kb, d, info, wave, lane);
-  panel_step<64>(a, colbuf, tb, kb, d, info, wave, lane);
-  panel_step<96>(a, colbuf, tb, kb, d, info, wave, lane);
-  // inverse: 32 x 32 diagonal blocks, wave w takes block w; lane c solves column c
-  {
-    const int b0 = wave * 32;
-    if (lane < 32) {
-      float x[32];
-#pragma unroll
-      for (int i = 0; i < 32; ++i) {
-        float s = (i == lane) ? 1.f : 0.f;
-#pragma unroll
-        for (int k = 0; k < i; ++k) s = fmaf(-a[(b0 + i) * DLD + b0 + k], x[k], s);
-        x[i] = s / a[(b0 + i) * DLD + b0 + i];
-        __builtin_amdgcn_sched_barrier(0);  // read one row of L at a time
-      }
-#pragma unroll
-      for (int i = 0; i < 32; ++i) y[(b0 + i) * DLD + b0 + lane] = x[i];
-    }
+  // Panels with a one-block lookahead: before panel p + 1 its block column gets panel p's
+  // update from all waves; then wave 0 factors panel p + 1 while the other waves apply panel
+  // p's update to the blocks further right and invert the diagonal block of panel p.
+  if (wave == 0) panel_factor<0>(a, colbuf, tb, kb, d, info, lane);
+  __syncthreads();
+  if (wave < 3) upd_block(a, 1 + wave, 1, 0, lane);  // block column 1 from panel 0
+  __syncthreads();
+  if (wave == 0) {
+    panel_factor<32>(a, colbuf, tb, kb, d, info, lane);
+  } else if (wave == 1) {
+    inv_block(a, y, 0, lane);
+  } else if (wave == 2) {
+    upd_block(a, 2, 2, 0, lane);
+    upd_block(a, 3, 3, 0, lane);
+  } else {
+    upd_block(a, 3, 2, 0, lane);
   }
+  __syncthreads();
+  if (wave < 2) upd_block(a, 2 + wave, 2, 1, lane);  // block column 2 from panel 1
+  __syncthreads();
+  if (wave == 0) {
+    panel_factor<64>(a, colbuf, tb, kb, d, info, lane);
+  } else if (wave == 1) {
+    inv_block(a, y, 1, lane);
+  } else if (wave == 2) {
+    upd_block(a, 3, 3, 1, lane);
+  }
+  __syncthreads();
+  if (wave == 0) upd_block(a, 3, 3, 2, lane);  // block column 3 from panel 2
+  __syncthreads();
+  if (wave == 0) {
+    panel_factor<96>(a, colbuf, tb, kb, d, info, lane);
+  } else if (wave == 1) {
+    inv_block(a, y, 2, lane);
+  }
+  __syncthreads();
+  if (wave == 0) inv_block(a, y, 3, lane);
   __syncthreads();
   // 64: Y10 = -Y11 (L10 Y00) for the block pairs at 0 and 64, one wave each
   if (wave < 2) {
