@@ -210,11 +210,11 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
 
     S_G needs only diag(H_G), which one read of G gives (kronq_cov_diag), so W is rescaled and
     rotated without waiting for the H_G covariance, and the sweep never waits for it either.
-    With ``overlap`` the work is split over two streams after H_X: the current stream rotates
-    H_X, factors it and runs the sweep; the second stream takes diag(H_G) (beside the H_X
-    covariance), transforms W as soon as S_X exists, then (the drift statistic and) the H_G
-    covariance on ``cov_cus`` CUs (None: the policy of _cov_cus; 0: no cap), whose traces and
-    rotation end the layer. The current stream waits for the second at the end. Both schedules
+    With ``overlap`` diag(H_G) and H_X come first, then the work is split over two streams: the
+    current stream rotates H_X, factors it and runs the sweep; the second stream transforms W
+    as soon as S_X exists, then takes (the drift statistic and) the H_G covariance on
+    ``cov_cus`` CUs (None: the policy of _cov_cus; 0: no cap), whose traces and rotation end
+    the layer. The current stream waits for the second at the end. Both schedules
     give bit-identical results."""
     drift = dX is not None
     if drift and st.D is None:
@@ -232,11 +232,10 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
         solve(st, bits, damp, alpha if drift else None)
         return
     main = torch.cuda.current_stream(st.HX.device)
-    ev_x, ev_sx, ev_w, ev_d, ev_g = st.ev
-    ev_x.record(main)
-    with torch.cuda.stream(st.side):
-        st.side.wait_event(ev_x)  # ordered after the caller's earlier work on this stream
-        K.kronq_cov_diag(G, st.hgd, st.ws_diag)
+    _, ev_sx, ev_w, ev_d, ev_g = st.ev
+    # diag(H_G) first and alone (0.3 ms at q_proj): beside the compute-bound H_X covariance it
+    # took 0.7 ms and slowed that covariance by more than its own time alone
+    K.kronq_cov_diag(G, st.hgd, st.ws_diag)
     if not skip_x:
         K.kronq_accumulate_cov(X, st.HX, 1.0, 0.0, st.ws_cov_x)
     K.kronq_traces(st.HX, None, st.tr_pre)
