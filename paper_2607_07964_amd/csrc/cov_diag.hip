@@ -7,13 +7,13 @@
 namespace kq {
 namespace {
 // diag(A^T A) without the covariance: column sums of squares. A workgroup takes CSQ_COLS columns
-// of one chunk of rows; lane l of wave w reads 8 consecutive columns (one 16-byte load for bf16,
-// two for fp32) of rows w, w + 4, ... and sums their squares in fp64, so a bf16 input gives the
-// exact sum up to fp64 rounding. The four waves meet in LDS and the chunk's sums go to the
-// workspace; colsq_final adds the chunks in order and rounds once to fp32. No atomics: the
-// result does not depend on scheduling.
-constexpr int CSQ_COLS = 512;
-constexpr int CSQ_TARGET_WGS = 1024;  // about four resident workgroups per CU
+// of one chunk of rows: thread t owns 16 consecutive columns, so each row is read as one
+// contiguous stretch of up to 8 KB (bf16) by the whole workgroup, with several rows in flight
+// per thread. Squares are summed in fp64 (a bf16 input gives the exact sum up to fp64
+// rounding); each chunk's sums go to the workspace and colsq_final adds the chunks in a fixed
+// order and rounds once to fp32. No atomics: the result does not depend on scheduling.
+constexpr int CSQ_COLS = 4096;        // 256 threads x 16 columns
+constexpr int CSQ_TARGET_WGS = 512;   // two resident workgroups per CU
 
 __device__ __forceinline__ void csq_load8(const uint16_t* p, int64_t n, float (&x)[8]) {
   if (n >= 8) {
@@ -44,65 +44,70 @@ template <typename T>
 __global__ __launch_bounds__(256) void colsq_partial(const T* __restrict__ A, int64_t n_rows,
                                                      int64_t d, int64_t lda, int64_t chunk_rows,
                                                      double* __restrict__ part) {
-  __shared__ double red[3][CSQ_COLS];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t c0 = int64_t(blockIdx.x) * CSQ_COLS + lane * 8;
+  const int64_t c0 = int64_t(blockIdx.x) * CSQ_COLS + int64_t(threadIdx.x) * 16;
   const int64_t r0 = int64_t(blockIdx.y) * chunk_rows;
   const int64_t r1 = min(n_rows, r0 + chunk_rows);
-  double acc[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
-  if (c0 < d) {
-    const int64_t nc = d - c0;
-    int64_t r = r0 + wave;
-    // U rows in flight per wave before the first use (16 KB per wave for bf16), so that a
-    // launch bounded to a few workgroups still keeps enough loads outstanding
-    constexpr int U = sizeof(T) == 2 ? 16 : 8;
-    for (; r + 4 * (U - 1) < r1; r += 4 * U) {
-      float x[U][8];
+  if (c0 >= d) return;
+  const int64_t nc = d - c0;
+  double acc[16];
 #pragma unroll
-      for (int u = 0; u < U; ++u) csq_load8(A + (r + 4 * u) * lda + c0, nc, x[u]);
+  for (int e = 0; e < 16; ++e) acc[e] = 0.0;
+  constexpr int U = sizeof(T) == 2 ? 8 : 4;  // rows in flight per thread
+  int64_t r = r0;
+  for (; r + U <= r1; r += U) {
+    float x[U][16];
 #pragma unroll
-      for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
+      float lo[8], hi[8];
+      csq_load8(A + (r + u) * lda + c0, nc, lo);
+      csq_load8(A + (r + u) * lda + c0 + 8, nc - 8, hi);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = fma(double(x[u][e]), double(x[u][e]), acc[e]);
+      for (int e = 0; e < 8; ++e) x[u][e] = lo[e], x[u][8 + e] = hi[e];
     }
-    for (; r < r1; r += 4) {
-      float x[8];
-      csq_load8(A + r * lda + c0, nc, x);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] = fma(double(x[e]), double(x[e]), acc[e]);
-    }
-  }
-  if (wave > 0) {
+    for (int u = 0; u < U; ++u)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) red[wave - 1][lane * 8 + e] = acc[e];
+      for (int e = 0; e < 16; ++e) acc[e] = fma(double(x[u][e]), double(x[u][e]), acc[e]);
   }
-  __syncthreads();
-  if (wave == 0 && c0 < d) {
-    double* out = part + int64_t(blockIdx.y) * d + c0;
+  for (; r < r1; ++r) {
+    float lo[8], hi[8];
+    csq_load8(A + r * lda + c0, nc, lo);
+    csq_load8(A + r * lda + c0 + 8, nc - 8, hi);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const double v = acc[e] + red[0][lane * 8 + e] + red[1][lane * 8 + e] + red[2][lane * 8 + e];
-      if (c0 + e < d) out[e] = v;
+      acc[e] = fma(double(lo[e]), double(lo[e]), acc[e]);
+      acc[8 + e] = fma(double(hi[e]), double(hi[e]), acc[8 + e]);
     }
   }
+  double* out = part + int64_t(blockIdx.y) * d + c0;
+#pragma unroll
+  for (int e = 0; e < 16; ++e)
+    if (e < nc) out[e] = acc[e];
 }
 
+// hdiag[j] = sum of the chunks' partials of column j: a workgroup takes 64 columns, thread
+// (g, c) adds the chunks g, g + 4, g + 8, ... of column c in order (eight loads in flight),
+// and the four groups are added in order through LDS
 __global__ __launch_bounds__(256) void colsq_final(const double* __restrict__ part, int n_chunks,
                                                    int64_t d, float* __restrict__ out) {
-  const int64_t j = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (j >= d) return;
-  // chunks added in order; loaded eight at a time so that the loads overlap
+  __shared__ double red[4][64];
+  const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int64_t j = int64_t(blockIdx.x) * 64 + c;
   double v = 0.0;
-  int c = 0;
-  for (; c + 8 <= n_chunks; c += 8) {
-    double t[8];
+  if (j < d) {
+    int k = g;
+    for (; k + 28 < n_chunks; k += 32) {
+      double t[8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) t[q] = part[int64_t(c + q) * d + j];
+      for (int q = 0; q < 8; ++q) t[q] = part[int64_t(k + 4 * q) * d + j];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) v += t[q];
+      for (int q = 0; q < 8; ++q) v += t[q];
+    }
+    for (; k < n_chunks; k += 4) v += part[int64_t(k) * d + j];
   }
-  for (; c < n_chunks; ++c) v += part[int64_t(c) * d + j];
-  out[j] = float(v);
+  red[g][c] = v;
+  __syncthreads();
+  if (g == 0 && j < d) out[j] = float(((red[0][c] + red[1][c]) + red[2][c]) + red[3][c]);
 }
 
 // row chunks of the column-square kernel: enough workgroups to fill the chip (or at most
@@ -125,7 +130,7 @@ size_t cov_diag_ws_bytes(int64_t n_rows, int64_t d) {
 int cov_diag_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
                     float* hdiag, int max_cus, void* ws, hipStream_t s) {
   if (n_rows == 0)  // no chunks: the final kernel writes zeros
-    return launch("cov_diag_final", colsq_final, dim3(unsigned(cdiv(d, 256))), dim3(256), 0, s,
+    return launch("cov_diag_final", colsq_final, dim3(unsigned(cdiv(d, 64))), dim3(256), 0, s,
                   static_cast<const double*>(nullptr), 0, d, hdiag);
   const int64_t rows = colsq_chunk_rows(n_rows, d, max_cus);
   const int64_t chunks = cdiv(n_rows, rows);
@@ -137,7 +142,7 @@ int cov_diag_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t
   else
     KQ_TRY(launch("cov_diag_partial", colsq_partial<float>, grid, dim3(256), 0, s,
                   static_cast<const float*>(A), n_rows, d, lda, rows, part));
-  return launch("cov_diag_final", colsq_final, dim3(unsigned(cdiv(d, 256))), dim3(256), 0, s,
+  return launch("cov_diag_final", colsq_final, dim3(unsigned(cdiv(d, 64))), dim3(256), 0, s,
                 static_cast<const double*>(part), int(chunks), d, hdiag);
 }
 
