@@ -155,9 +155,9 @@ def solve(st: LayerState, bits: int, damp: float = 0.01, alpha: Optional[float] 
 # Share of the compute units left free beside the H_G covariance in the two-stream schedule, for
 # the factorisation's and the sweep's latency-bound kernels (a covariance workgroup holds its CU
 # for a whole tile, so uncapped it starves them: the 8B q_proj takes 14.7 ms per layer uncapped,
-# 12.3 ms on half the chip). The covariance loses less than the CUs it gives up, its clock
-# being power-limited on the full chip: on half the chip the q_proj H_G takes 5.9 ms instead of
-# 4.1 ms. Half the chip where the factorisation is not much shorter than that covariance; an
+# 11.5 ms on half the chip). The covariance loses less than the CUs it gives up, its clock
+# being power-limited on the full chip: on half the chip the q_proj H_G takes 5.5-6.1 ms instead
+# of 4.1 ms. Half the chip where the factorisation is not much shorter than that covariance; an
 # eighth where H_G outlasts factorisation and sweep many times over (70B up_proj, d = 28672
 # against d = 8192: 238.7 ms per layer on 7/8 of the chip, 242.9 ms on 3/4, 247.7 ms on one
 # stream, 262.5 ms uncapped). The estimate uses rough rates: 1.1 PFLOP/s for a covariance,
