@@ -2,11 +2,12 @@
 // with or without the drift correction P; Alg. 2).
 //
 // Per block of 128 columns:
-//   * sweep kernel: rows are independent given U, so each row is one 16-lane group of a wave
-//     (4 rows per wave, 16 rows per workgroup) and each lane keeps 8 consecutive columns of the
-//     block in registers. Column j: the owning lane quantises it and forms the scaled error
-//     e_j = (w_j - w_hat_j) / U_jj, one DPP row broadcast hands e_j to the other 15 lanes, and
-//     every lane applies it to its 8 columns with U[j, its columns] read from the workgroup's
+//   * sweep kernel: rows are independent given U, so each row is one 8-lane group of a wave
+//     (8 rows per wave, 32 rows per workgroup; with the drift correction 16-lane groups) and
+//     each lane keeps 16 (8) consecutive columns of the block in registers. Column j: the
+//     owning lane quantises it and forms the scaled error e_j = (w_j - w_hat_j) / U_jj, a DPP
+//     broadcast (two for 8-lane groups, one per half of a 16-lane DPP row) hands e_j to the
+//     rest of the group, and every lane applies it to its columns with U[j, its columns] read from the workgroup's
 //     LDS copy of the 128 x 128 block of U (upper triangular, so columns already done are left
 //     alone). With the drift correction a second broadcast hands out w_j as it stood before
 //     quantisation and every lane adds w_j P[j, its columns] from an LDS copy of the block of P
@@ -42,17 +43,32 @@ namespace kq {
 namespace {
 
 constexpr int OB = 128;          // block (and the smallest group)
-constexpr int LPR = 16;          // lanes per row
-constexpr int CPL = OB / LPR;    // columns per lane
-constexpr int RPW = 64 / LPR;    // rows per wave
-constexpr int RPG = 4 * RPW;     // rows per workgroup (4 waves)
+// Lanes per row of the sweep kernel: 8 (16 columns per lane) without the drift correction, 16
+// (8 columns per lane) with it, whose second broadcast and P block would not fit the registers
+// of 16 columns. 8 lanes halve the instructions per row: beside the H_G covariance, two waves
+// per SIMD, the sweep's 32 blocks at q_proj take 2.75 ms instead of 3.2 ms (alone 1.8 against
+// 1.67 ms).
+template <bool DRIFT>
+struct SweepLayout {
+  static constexpr int LPR = DRIFT ? 16 : 8;  // lanes per row
+  static constexpr int CPL = OB / LPR;        // columns per lane
+  static constexpr int RPW = 64 / LPR;        // rows per wave
+  static constexpr int RPG = 4 * RPW;         // rows per workgroup (4 waves)
+};
 constexpr int GRP = 4;           // blocks per group of the two-level lazy update (at most)
 
-// v broadcast from lane `src` of each 16-lane row to the whole row (DPP row_newbcast)
-template <int src>
+// v broadcast from lane `src` of each LPR-lane row group to the whole group (DPP row_newbcast
+// over a 16-lane DPP row; for 8-lane groups one per half of it, selected by the bank mask)
+template <int LPR, int src>
 __device__ __forceinline__ float row_bcast(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x150 + src, 0xF, 0xF,
-                                                    false));
+  const int x = __float_as_int(v);
+  if constexpr (LPR == 16) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x150 + src, 0xF, 0xF, false));
+  } else {
+    static_assert(LPR == 8, "row groups of 8 or 16 lanes");
+    const int lo = __builtin_amdgcn_update_dpp(x, x, 0x150 + src, 0xF, 0x3, false);
+    return __int_as_float(__builtin_amdgcn_update_dpp(lo, x, 0x150 + 8 + src, 0xF, 0xC, false));
+  }
 }
 
 struct SweepArgs {
@@ -66,8 +82,12 @@ struct SweepArgs {
 
 // one column of the sweep: j = 8 * OWN + S (compile-time)
 template <bool DRIFT, int OWN, int S>
-__device__ __forceinline__ void sweep_col(float (&w)[CPL], float (&ev)[CPL], float (&xv)[CPL],
-                                          uint32_t (&qc)[CPL], const SweepArgs& a) {
+__device__ __forceinline__ void sweep_col(float (&w)[SweepLayout<DRIFT>::CPL],
+                                          float (&ev)[SweepLayout<DRIFT>::CPL],
+                                          float (&xv)[SweepLayout<DRIFT>::CPL],
+                                          uint32_t (&qc)[SweepLayout<DRIFT>::CPL],
+                                          const SweepArgs& a) {
+  constexpr int LPR = SweepLayout<DRIFT>::LPR, CPL = SweepLayout<DRIFT>::CPL;
   constexpr int j = OWN * CPL + S;
   const float x = w[S];
   const float t = x * a.inv_s;
@@ -82,51 +102,48 @@ __device__ __forceinline__ void sweep_col(float (&w)[CPL], float (&ev)[CPL], flo
     qc[S] = uint32_t(q);
     if (DRIFT) xv[S] = x;
   }
-  const float eb = row_bcast<OWN>(e);
-  const float4 u0 = *reinterpret_cast<const float4*>(a.ub + j * OB + a.cb);
-  const float4 u1 = *reinterpret_cast<const float4*>(a.ub + j * OB + a.cb + 4);
-  w[0] = fmaf(-eb, u0.x, w[0]);
-  w[1] = fmaf(-eb, u0.y, w[1]);
-  w[2] = fmaf(-eb, u0.z, w[2]);
-  w[3] = fmaf(-eb, u0.w, w[3]);
-  w[4] = fmaf(-eb, u1.x, w[4]);
-  w[5] = fmaf(-eb, u1.y, w[5]);
-  w[6] = fmaf(-eb, u1.z, w[6]);
-  w[7] = fmaf(-eb, u1.w, w[7]);
+  const float eb = row_bcast<LPR, OWN>(e);
+#pragma unroll
+  for (int h = 0; h < CPL / 4; ++h) {
+    const float4 u = *reinterpret_cast<const float4*>(a.ub + j * OB + a.cb + 4 * h);
+    w[4 * h + 0] = fmaf(-eb, u.x, w[4 * h + 0]);
+    w[4 * h + 1] = fmaf(-eb, u.y, w[4 * h + 1]);
+    w[4 * h + 2] = fmaf(-eb, u.z, w[4 * h + 2]);
+    w[4 * h + 3] = fmaf(-eb, u.w, w[4 * h + 3]);
+  }
   if (DRIFT) {  // + w_j P[j, its columns], w_j as it stood before quantisation
-    const float xb = row_bcast<OWN>(x);
-    const float4 p0 = *reinterpret_cast<const float4*>(a.pb + j * OB + a.cb);
-    const float4 p1 = *reinterpret_cast<const float4*>(a.pb + j * OB + a.cb + 4);
-    w[0] = fmaf(xb, p0.x, w[0]);
-    w[1] = fmaf(xb, p0.y, w[1]);
-    w[2] = fmaf(xb, p0.z, w[2]);
-    w[3] = fmaf(xb, p0.w, w[3]);
-    w[4] = fmaf(xb, p1.x, w[4]);
-    w[5] = fmaf(xb, p1.y, w[5]);
-    w[6] = fmaf(xb, p1.z, w[6]);
-    w[7] = fmaf(xb, p1.w, w[7]);
+    const float xb = row_bcast<LPR, OWN>(x);
+#pragma unroll
+    for (int h = 0; h < CPL / 4; ++h) {
+      const float4 pv = *reinterpret_cast<const float4*>(a.pb + j * OB + a.cb + 4 * h);
+      w[4 * h + 0] = fmaf(xb, pv.x, w[4 * h + 0]);
+      w[4 * h + 1] = fmaf(xb, pv.y, w[4 * h + 1]);
+      w[4 * h + 2] = fmaf(xb, pv.z, w[4 * h + 2]);
+      w[4 * h + 3] = fmaf(xb, pv.w, w[4 * h + 3]);
+    }
   }
 }
 
-template <bool DRIFT, int OWN>
-__device__ __forceinline__ void sweep_lane_cols(float (&w)[CPL], float (&ev)[CPL],
-                                                float (&xv)[CPL], uint32_t (&qc)[CPL],
+template <bool DRIFT, int OWN, int... S>
+__device__ __forceinline__ void sweep_lane_cols(std::integer_sequence<int, S...>,
+                                                float (&w)[SweepLayout<DRIFT>::CPL],
+                                                float (&ev)[SweepLayout<DRIFT>::CPL],
+                                                float (&xv)[SweepLayout<DRIFT>::CPL],
+                                                uint32_t (&qc)[SweepLayout<DRIFT>::CPL],
                                                 const SweepArgs& a) {
-  sweep_col<DRIFT, OWN, 0>(w, ev, xv, qc, a);
-  sweep_col<DRIFT, OWN, 1>(w, ev, xv, qc, a);
-  sweep_col<DRIFT, OWN, 2>(w, ev, xv, qc, a);
-  sweep_col<DRIFT, OWN, 3>(w, ev, xv, qc, a);
-  sweep_col<DRIFT, OWN, 4>(w, ev, xv, qc, a);
-  sweep_col<DRIFT, OWN, 5>(w, ev, xv, qc, a);
-  sweep_col<DRIFT, OWN, 6>(w, ev, xv, qc, a);
-  sweep_col<DRIFT, OWN, 7>(w, ev, xv, qc, a);
+  (sweep_col<DRIFT, OWN, S>(w, ev, xv, qc, a), ...);
 }
 
 template <bool DRIFT, int... OWN>
-__device__ __forceinline__ void sweep_all(std::integer_sequence<int, OWN...>, float (&w)[CPL],
-                                          float (&ev)[CPL], float (&xv)[CPL], uint32_t (&qc)[CPL],
+__device__ __forceinline__ void sweep_all(std::integer_sequence<int, OWN...>,
+                                          float (&w)[SweepLayout<DRIFT>::CPL],
+                                          float (&ev)[SweepLayout<DRIFT>::CPL],
+                                          float (&xv)[SweepLayout<DRIFT>::CPL],
+                                          uint32_t (&qc)[SweepLayout<DRIFT>::CPL],
                                           const SweepArgs& a) {
-  (sweep_lane_cols<DRIFT, OWN>(w, ev, xv, qc, a), ...);
+  (sweep_lane_cols<DRIFT, OWN>(std::make_integer_sequence<int, SweepLayout<DRIFT>::CPL>{}, w, ev,
+                               xv, qc, a),
+   ...);
 }
 
 // (scale, zero) of a group from its range, the same float64 steps as the oracle's reading
@@ -183,8 +200,10 @@ __global__ __launch_bounds__(256) void obs_sweep(
   __shared__ __attribute__((aligned(16))) float pb[DRIFT ? OB * OB : 4];  // P[c0 + j][c0 + k]
   __shared__ float rinv[OB];                                   // 1 / U_jj
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int LPR = SweepLayout<DRIFT>::LPR, CPL = SweepLayout<DRIFT>::CPL;
+  constexpr int RPW = SweepLayout<DRIFT>::RPW, RPG = SweepLayout<DRIFT>::RPG;
   const int sub = lane & (LPR - 1), cb = sub * CPL;
-  const int64_t row = int64_t(blockIdx.x) * RPG + wave * RPW + (lane >> 4);
+  const int64_t row = int64_t(blockIdx.x) * RPG + wave * RPW + lane / LPR;
   const bool live = row < d_out;
   const int64_t rr = live ? row : d_out - 1;  // rows past the end recompute the last row
 
@@ -198,10 +217,10 @@ __global__ __launch_bounds__(256) void obs_sweep(
   }
   if (tid < OB) rinv[tid] = 1.f / U[(c0 + tid) * ldu + c0 + tid];
   float w[CPL];
-  {
-    const float4 a = *reinterpret_cast<const float4*>(W + rr * ldw + c0 + cb);
-    const float4 b = *reinterpret_cast<const float4*>(W + rr * ldw + c0 + cb + 4);
-    w[0] = a.x, w[1] = a.y, w[2] = a.z, w[3] = a.w, w[4] = b.x, w[5] = b.y, w[6] = b.z, w[7] = b.w;
+#pragma unroll
+  for (int h = 0; h < CPL / 4; ++h) {
+    const float4 v = *reinterpret_cast<const float4*>(W + rr * ldw + c0 + cb + 4 * h);
+    w[4 * h] = v.x, w[4 * h + 1] = v.y, w[4 * h + 2] = v.z, w[4 * h + 3] = v.w;
   }
   float scale, fzero;
   if (given) {  // a wider group: parameters taken at its first block by obs_group_params
@@ -239,24 +258,19 @@ __global__ __launch_bounds__(256) void obs_sweep(
   float wh[CPL];
 #pragma unroll
   for (int c = 0; c < CPL; ++c) wh[c] = scale * (float(qc[c]) - fzero);
-  const float4 h0 = make_float4(wh[0], wh[1], wh[2], wh[3]);
-  const float4 h1 = make_float4(wh[4], wh[5], wh[6], wh[7]);
-  *reinterpret_cast<float4*>(W + row * ldw + c0 + cb) = h0;
-  *reinterpret_cast<float4*>(W + row * ldw + c0 + cb + 4) = h1;
-  if (W_hat) {
-    *reinterpret_cast<float4*>(W_hat + row * ldwh + c0 + cb) = h0;
-    *reinterpret_cast<float4*>(W_hat + row * ldwh + c0 + cb + 4) = h1;
+#pragma unroll
+  for (int h = 0; h < CPL / 4; ++h) {
+    const float4 hv = make_float4(wh[4 * h], wh[4 * h + 1], wh[4 * h + 2], wh[4 * h + 3]);
+    *reinterpret_cast<float4*>(W + row * ldw + c0 + cb + 4 * h) = hv;
+    if (W_hat) *reinterpret_cast<float4*>(W_hat + row * ldwh + c0 + cb + 4 * h) = hv;
+    *reinterpret_cast<float4*>(E + row * lde + cb + 4 * h) =
+        make_float4(ev[4 * h], ev[4 * h + 1], ev[4 * h + 2], ev[4 * h + 3]);
+    if (DRIFT)
+      *reinterpret_cast<float4*>(Xq + row * ldxq + cb + 4 * h) =
+          make_float4(xv[4 * h], xv[4 * h + 1], xv[4 * h + 2], xv[4 * h + 3]);
+    reinterpret_cast<uint32_t*>(codes + row * ldq + c0 + cb)[h] =
+        qc[4 * h] | (qc[4 * h + 1] << 8) | (qc[4 * h + 2] << 16) | (qc[4 * h + 3] << 24);
   }
-  *reinterpret_cast<float4*>(E + row * lde + cb) = make_float4(ev[0], ev[1], ev[2], ev[3]);
-  *reinterpret_cast<float4*>(E + row * lde + cb + 4) = make_float4(ev[4], ev[5], ev[6], ev[7]);
-  if (DRIFT) {
-    *reinterpret_cast<float4*>(Xq + row * ldxq + cb) = make_float4(xv[0], xv[1], xv[2], xv[3]);
-    *reinterpret_cast<float4*>(Xq + row * ldxq + cb + 4) = make_float4(xv[4], xv[5], xv[6], xv[7]);
-  }
-  uint2 pk;
-  pk.x = qc[0] | (qc[1] << 8) | (qc[2] << 16) | (qc[3] << 24);
-  pk.y = qc[4] | (qc[5] << 8) | (qc[6] << 16) | (qc[7] << 24);
-  *reinterpret_cast<uint2*>(codes + row * ldq + c0 + cb) = pk;
 }
 
 // Blocks per lazy group for a quantisation group of `group` columns: a group's parameters need
@@ -290,7 +304,8 @@ int obs_launch(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* 
   const int lz = lazy_blocks(d_in, group);
   KQ_REQUIRE(lz > 0, KRONQ_ERR_UNSUPPORTED, "group %d not supported for d_in %lld", group,
              (long long)d_in);
-  const unsigned grid = unsigned(cdiv(d_out, RPG));
+  const unsigned grid = unsigned(cdiv(d_out, drift ? SweepLayout<true>::RPG
+                                                   : SweepLayout<false>::RPG));
   Carver cv(ws);
   float* Ews = cv.take<float>(size_t(d_out) * GRP * OB);
   uint16_t* Uth = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
