@@ -7,12 +7,12 @@
 namespace kq {
 namespace {
 // diag(A^T A) without the covariance: column sums of squares. A workgroup takes CSQ_COLS columns
-// of one chunk of rows: thread t owns 16 consecutive columns, so each row is read as one
+// of one chunk of rows: thread t owns 16 of them (two runs of 8), so each row is read as one
 // contiguous stretch of up to 8 KB (bf16) by the whole workgroup, with several rows in flight
 // per thread. Squares are summed in fp64 (a bf16 input gives the exact sum up to fp64
 // rounding); each chunk's sums go to the workspace and colsq_final adds the chunks in a fixed
 // order and rounds once to fp32. No atomics: the result does not depend on scheduling.
-constexpr int CSQ_COLS = 4096;        // 256 threads x 16 columns
+constexpr int CSQ_COLS = 4096;        // 256 threads x 2 x 8 columns
 constexpr int CSQ_TARGET_WGS = 512;   // two resident workgroups per CU
 
 __device__ __forceinline__ void csq_load8(const uint16_t* p, int64_t n, float (&x)[8]) {
@@ -44,45 +44,66 @@ template <typename T>
 __global__ __launch_bounds__(256) void colsq_partial(const T* __restrict__ A, int64_t n_rows,
                                                      int64_t d, int64_t lda, int64_t chunk_rows,
                                                      double* __restrict__ part) {
-  const int64_t c0 = int64_t(blockIdx.x) * CSQ_COLS + int64_t(threadIdx.x) * 16;
+  // thread t owns columns c_lo + 0..7 and c_lo + 2048 + 0..7, so that each load instruction of
+  // a wave reads 1 KB (bf16) without gaps
+  const int64_t c_lo = int64_t(blockIdx.x) * CSQ_COLS + int64_t(threadIdx.x) * 8;
+  const int64_t c_hi = c_lo + CSQ_COLS / 2;
   const int64_t r0 = int64_t(blockIdx.y) * chunk_rows;
   const int64_t r1 = min(n_rows, r0 + chunk_rows);
-  if (c0 >= d) return;
-  const int64_t nc = d - c0;
+  if (c_lo >= d) return;
+  const int64_t n_lo = d - c_lo, n_hi = d - c_hi;  // n_hi <= 0: no high half
   double acc[16];
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.0;
   constexpr int U = sizeof(T) == 2 ? 8 : 4;  // rows in flight per thread
   int64_t r = r0;
-  for (; r + U <= r1; r += U) {
-    float x[U][16];
+  // whole column blocks, or a block whose first half is whole and second half empty (tests
+  // uniform over the workgroup): every load is a full 16-byte load, with no per-lane branch
+  // between the loads and their use, so all U rows are in flight at once
+  const int64_t b0 = int64_t(blockIdx.x) * CSQ_COLS;
+  if (b0 + CSQ_COLS <= d) {
+    for (; r + U <= r1; r += U) {
+      float x[U][16];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float lo[8], hi[8];
-      csq_load8(A + (r + u) * lda + c0, nc, lo);
-      csq_load8(A + (r + u) * lda + c0 + 8, nc - 8, hi);
+      for (int u = 0; u < U; ++u) {
+        float lo[8], hi[8];
+        csq_load8(A + (r + u) * lda + c_lo, 8, lo);
+        csq_load8(A + (r + u) * lda + c_hi, 8, hi);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[u][e] = lo[e], x[u][8 + e] = hi[e];
+        for (int e = 0; e < 8; ++e) x[u][e] = lo[e], x[u][8 + e] = hi[e];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[e] = fma(double(x[u][e]), double(x[u][e]), acc[e]);
     }
+  } else if (b0 + CSQ_COLS / 2 == d) {
+    for (; r + U <= r1; r += U) {
+      float x[U][8];
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+      for (int u = 0; u < U; ++u) csq_load8(A + (r + u) * lda + c_lo, 8, x[u]);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[e] = fma(double(x[u][e]), double(x[u][e]), acc[e]);
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fma(double(x[u][e]), double(x[u][e]), acc[e]);
+    }
   }
   for (; r < r1; ++r) {
     float lo[8], hi[8];
-    csq_load8(A + r * lda + c0, nc, lo);
-    csq_load8(A + r * lda + c0 + 8, nc - 8, hi);
+    csq_load8(A + r * lda + c_lo, n_lo, lo);
+    csq_load8(A + r * lda + c_hi, n_hi, hi);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       acc[e] = fma(double(lo[e]), double(lo[e]), acc[e]);
       acc[8 + e] = fma(double(hi[e]), double(hi[e]), acc[8 + e]);
     }
   }
-  double* out = part + int64_t(blockIdx.y) * d + c0;
+  double* out = part + int64_t(blockIdx.y) * d;
 #pragma unroll
-  for (int e = 0; e < 16; ++e)
-    if (e < nc) out[e] = acc[e];
+  for (int e = 0; e < 8; ++e) {
+    if (e < n_lo) out[c_lo + e] = acc[e];
+    if (e < n_hi) out[c_hi + e] = acc[8 + e];
+  }
 }
 
 // hdiag[j] = sum of the chunks' partials of column j: a workgroup takes 64 columns, thread

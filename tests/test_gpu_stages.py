@@ -102,11 +102,13 @@ def test_cov_limited_matches_uncapped(max_cus):
 
 @pytest.mark.parametrize("n,d,bf16", [(1000, 300, True), (5000, 600, True), (64, 8, True),
                                       (4099, 1030, True), (70, 257, True), (3000, 260, False),
-                                      (200000, 64, True), (2, 4096, True)])
+                                      (200000, 64, True), (2, 4096, True), (3001, 2048, True),
+                                      (1000, 6144, True), (2000, 4096, False)])
 def test_cov_diag(n, d, bf16):
     """diag(A^T A) from one read of A: fp64 sums of exact bf16 squares (fp32 squares are exact
     in fp64 too), rounded once, so within one fp32 ulp of the oracle's diagonal; lda > d for
-    ragged d; a second call gives the same bits."""
+    ragged d; whole 4096-column blocks, a half block (2048, 6144) and ragged blocks; a second
+    call gives the same bits."""
     dp = (d + 7) // 8 * 8
     spec = synth.small_spec(dp, dp, n, seed=n + 3 * d).x
     A = synth.gen_matrix(spec, DEV)
