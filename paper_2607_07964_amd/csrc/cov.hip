@@ -508,23 +508,39 @@ __device__ __forceinline__ void gram_reduce(const float* __restrict__ part, int 
   const int tid = threadIdx.x;
   const int c4 = (tid & 15) * 4;
   const int rb = tid >> 4;
+  // slices added in order; four slices of the four rows (16 loads) in flight at a time
   float v[4][4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int r = rb + 16 * k;
-    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-    for (int s = 0; s < n_slices; ++s) {
-      const float4 x = *reinterpret_cast<const float4*>(
-          part + (int64_t(s) * npos + pos) * (TT * TT) + (sr + r) * TT + sc + c4);
-      s0 += x.x;
-      s1 += x.y;
-      s2 += x.z;
-      s3 += x.w;
+  for (int k = 0; k < 4; ++k) v[k][0] = v[k][1] = v[k][2] = v[k][3] = 0.f;
+  const float* base = part + int64_t(pos) * (TT * TT) + (sr + rb) * TT + sc + c4;
+  const int64_t slice = npos * (TT * TT);
+  int s = 0;
+  for (; s + 4 <= n_slices; s += 4) {
+    float4 x[4][4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        x[k][q] = *reinterpret_cast<const float4*>(base + (s + q) * slice + 16 * k * TT);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[k][0] += x[k][q].x;
+        v[k][1] += x[k][q].y;
+        v[k][2] += x[k][q].z;
+        v[k][3] += x[k][q].w;
+      }
+  }
+  for (; s < n_slices; ++s) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float4 x = *reinterpret_cast<const float4*>(base + s * slice + 16 * k * TT);
+      v[k][0] += x.x;
+      v[k][1] += x.y;
+      v[k][2] += x.z;
+      v[k][3] += x.w;
     }
-    v[k][0] = s0;
-    v[k][1] = s1;
-    v[k][2] = s2;
-    v[k][3] = s3;
   }
   if (CROSS) {
 #pragma unroll
