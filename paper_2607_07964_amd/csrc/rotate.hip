@@ -80,20 +80,40 @@ __global__ __launch_bounds__(256) void w_norms(const T* __restrict__ W, int64_t 
   float rs[NORM_ROWS];
 #pragma unroll
   for (int r = 0; r < NORM_ROWS; ++r) rs[r] = 0.f;
+  // a block of NORM_ROWS whole rows of whole 8-column runs (tests uniform over the
+  // workgroup) loads without bounds branches, all NORM_ROWS loads of a thread in flight
+  // together; the sums are taken in the same order either way
+  const bool whole = (d_in & 7) == 0 && nr == NORM_ROWS;
   for (int64_t c0 = int64_t(tid) * 8; c0 < d_in; c0 += 256 * 8) {
     float cs[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (whole) {
+      float x[NORM_ROWS][8];
 #pragma unroll
-    for (int r = 0; r < NORM_ROWS; ++r) {
-      if (r < nr) {
-        float x[8];
-        load8_f32(W + (r0 + r) * ldw + c0, d_in - c0, x);
+      for (int r = 0; r < NORM_ROWS; ++r) load8_f32(W + (r0 + r) * ldw + c0, 8, x[r]);
+#pragma unroll
+      for (int r = 0; r < NORM_ROWS; ++r) {
         float t = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          cs[e] = fmaf(x[e], x[e], cs[e]);
-          t = fmaf(x[e], x[e], t);
+          cs[e] = fmaf(x[r][e], x[r][e], cs[e]);
+          t = fmaf(x[r][e], x[r][e], t);
         }
         rs[r] += t;
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < NORM_ROWS; ++r) {
+        if (r < nr) {
+          float x[8];
+          load8_f32(W + (r0 + r) * ldw + c0, d_in - c0, x);
+          float t = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            cs[e] = fmaf(x[e], x[e], cs[e]);
+            t = fmaf(x[e], x[e], t);
+          }
+          rs[r] += t;
+        }
       }
     }
     double* cp = col_part + int64_t(blockIdx.x) * d_in + c0;
