@@ -396,8 +396,8 @@ def main() -> int:
                     help="first run 3 plain 1 GiB device copies (reference for counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(see DESIGN.md for how the layer solve would shard).", file=sys.stderr)
+        print("bench.py runs on one GPU only: the layer solve has no multi-GPU path; "
+              "--gpus above 1 is not supported.", file=sys.stderr)
         return 2
 
     import torch

@@ -14,7 +14,7 @@ Paper references (arxiv 2607.07964, "KronQ"):
 * quantisation loop, Algorithm 2 (appendix B);
 * LDL loss identity, appendix A.3 eq. (app-decomp).
 
-Readings taken where the paper is silent or garbled (each also listed in the design doc):
+Readings taken where the paper is silent or garbled:
 
 R1  covariances are plain sums, H_X = X^T X, H_G = G^T G (token-major X, G).
 R3  the inverse-Cholesky factor is the UPPER U with inv(H~) = U^T U; the sweep uses rows of U

@@ -236,7 +236,7 @@ N_CAL = 128 * 2048  # calibration tokens: 128 sequences x 2048 (experimental set
 
 
 def workload(k: int, n_tokens: Optional[int] = None) -> LayerSpec:
-    """Single-layer workloads 1-4 (see the design doc for the table). ``n_tokens`` overrides N."""
+    """Single-layer workloads 1-4. ``n_tokens`` overrides N."""
     bf = torch.bfloat16
     if k == 1:
         return _layer("tiny256", 256, 256, n_tokens or 2048, 4, 0, "normal_x20", 1.0, 0.02,
