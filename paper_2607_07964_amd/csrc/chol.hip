@@ -60,6 +60,17 @@ __global__ void reverse_copy(const float* __restrict__ H, int64_t d, int64_t ldh
     M[i * ldm + j] = H[(d - 1 - i) * ldh + (d - 1 - j)];
 }
 
+// the same with four columns per thread (d divisible by 4; rows 16-byte aligned)
+__global__ void reverse_copy4(const float* __restrict__ H, int64_t d, int64_t ldh,
+                              float* __restrict__ M, int64_t ldm) {
+  const int64_t i = blockIdx.y;
+  for (int64_t j = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) * 4; j < d;
+       j += int64_t(gridDim.x) * blockDim.x * 4) {
+    const float4 h = *reinterpret_cast<const float4*>(H + (d - 1 - i) * ldh + (d - 4 - j));
+    *reinterpret_cast<float4*>(M + i * ldm + j) = make_float4(h.w, h.z, h.y, h.x);
+  }
+}
+
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // One 32 x 32 block C = alpha * A op(B) + beta * C on LDS arrays, by one wave on the fp32
@@ -298,6 +309,19 @@ __global__ void reverse_out(const float* __restrict__ X, int64_t ldm, int64_t d,
     U[i * ldu + j] = (j >= i) ? X[(d - 1 - i) * ldm + (d - 1 - j)] : 0.f;
 }
 
+// the same with four columns per thread (d divisible by 4; rows 16-byte aligned)
+__global__ void reverse_out4(const float* __restrict__ X, int64_t ldm, int64_t d,
+                             float* __restrict__ U, int64_t ldu) {
+  const int64_t i = blockIdx.y;
+  for (int64_t j = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) * 4; j < d;
+       j += int64_t(gridDim.x) * blockDim.x * 4) {
+    const float4 x = *reinterpret_cast<const float4*>(X + (d - 1 - i) * ldm + (d - 4 - j));
+    *reinterpret_cast<float4*>(U + i * ldu + j) =
+        make_float4(j >= i ? x.w : 0.f, j + 1 >= i ? x.z : 0.f, j + 2 >= i ? x.y : 0.f,
+                    j + 3 >= i ? x.x : 0.f);
+  }
+}
+
 int64_t ld_for(int64_t d) { return ((d + 63) / 64) * 64; }
 
 // split of an n-column block: the first h columns, a multiple of NB, about half
@@ -364,9 +388,18 @@ int chol_launch(float* H, int64_t d, int64_t ldh, float damp_rel, float* U, int6
   KQ_TRY(launch("chol_add_diag", add_diag, dim3(unsigned(cdiv(d, 256))), dim3(256), 0, s, H, d,
                 ldh, static_cast<const float*>(shift)));
   const unsigned gx = unsigned(cdiv(d, 256) < 64 ? cdiv(d, 256) : 64);
-  KQ_TRY(launch("chol_reverse_copy", reverse_copy, dim3(gx, unsigned(d)), dim3(256), 0, s,
-                static_cast<const float*>(H), d, ldh, M, ld));
+  const bool v4 = d % 4 == 0 && ldh % 4 == 0 && ldu % 4 == 0 && aligned(H, 16) && aligned(U, 16);
+  const unsigned gx4 = unsigned(cdiv(d, 1024) < 64 ? cdiv(d, 1024) : 64);
+  if (v4)
+    KQ_TRY(launch("chol_reverse_copy", reverse_copy4, dim3(gx4, unsigned(d)), dim3(256), 0, s,
+                  static_cast<const float*>(H), d, ldh, M, ld));
+  else
+    KQ_TRY(launch("chol_reverse_copy", reverse_copy, dim3(gx, unsigned(d)), dim3(256), 0, s,
+                  static_cast<const float*>(H), d, ldh, M, ld));
   KQ_TRY(chol_rec(M, X, T, tcap, ld, 0, d, d, info, s));
+  if (v4)
+    return launch("chol_reverse_out", reverse_out4, dim3(gx4, unsigned(d)), dim3(256), 0, s,
+                  static_cast<const float*>(X), ld, d, U, ldu);
   return launch("chol_reverse_out", reverse_out, dim3(gx, unsigned(d)), dim3(256), 0, s,
                 static_cast<const float*>(X), ld, d, U, ldu);
 }
