@@ -141,29 +141,57 @@ __global__ __launch_bounds__(256) void gemm_bf16x3_sub(
       }
 }
 
-// Ut_hi[n][k] + Ut_lo[n][k] = sgn U[k][n] (the three-term split of +-U^T), 32 x 32 tiles
-// through LDS
+// Ut_hi[n][k] + Ut_lo[n][k] = sgn U[k][n] (the three-term split of +-U^T), 64 x 64 tiles
+// through LDS: 16-byte loads of U rows, 8-byte stores of four bf16 of a Ut row. U is upper
+// triangular (strictly, for P) and the sweep's products read Ut[n][k] only for k < n, so tiles
+// wholly below that (k0 >= n0 + 64) are not written.
 __global__ __launch_bounds__(256) void split_transpose(const float* __restrict__ U, int64_t ldu,
                                                        int64_t d, uint16_t* __restrict__ Th,
                                                        uint16_t* __restrict__ Tl, int64_t ldt,
                                                        float sgn) {
-  __shared__ float t[32][33];
-  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
-  const int64_t k0 = int64_t(blockIdx.y) * 32, n0 = int64_t(blockIdx.x) * 32;
+  __shared__ float t[64][65];
+  const int64_t k0 = int64_t(blockIdx.y) * 64, n0 = int64_t(blockIdx.x) * 64;
+  if (k0 >= n0 + 64) return;
+  const int tid = threadIdx.x, q = (tid & 15) * 4, r = tid >> 4;  // 16 x 16
+  const bool whole = k0 + 64 <= d && n0 + 64 <= d;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int64_t k = k0 + ty + 8 * i, n = n0 + tx;
-    t[ty + 8 * i][tx] = (k < d && n < d) ? sgn * U[k * ldu + n] : 0.f;
+    const int kk = r + 16 * i;
+    const int64_t k = k0 + kk, n = n0 + q;
+    float4 v;
+    if (whole) {
+      v = *reinterpret_cast<const float4*>(U + k * ldu + n);
+    } else {
+      v.x = (k < d && n < d) ? U[k * ldu + n] : 0.f;
+      v.y = (k < d && n + 1 < d) ? U[k * ldu + n + 1] : 0.f;
+      v.z = (k < d && n + 2 < d) ? U[k * ldu + n + 2] : 0.f;
+      v.w = (k < d && n + 3 < d) ? U[k * ldu + n + 3] : 0.f;
+    }
+    t[kk][q] = sgn * v.x, t[kk][q + 1] = sgn * v.y, t[kk][q + 2] = sgn * v.z;
+    t[kk][q + 3] = sgn * v.w;
   }
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int64_t n = n0 + ty + 8 * i, k = k0 + tx;
-    if (n < d && k < d) {
-      const float x = t[tx][ty + 8 * i];
-      const uint32_t h = bf16_rne(x);
-      Th[n * ldt + k] = uint16_t(h);
-      Tl[n * ldt + k] = uint16_t(bf16_rne(x - bf16_to_f32(h)));
+    const int nn = r + 16 * i;
+    const int64_t n = n0 + nn, k = k0 + q;
+    uint32_t hi[4], lo[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float x = t[q + e][nn];
+      hi[e] = bf16_rne(x);
+      lo[e] = bf16_rne(x - bf16_to_f32(hi[e]));
+    }
+    if (whole) {
+      *reinterpret_cast<uint2*>(Th + n * ldt + k) = make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16));
+      *reinterpret_cast<uint2*>(Tl + n * ldt + k) = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
+    } else if (n < d) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (k + e < d) {
+          Th[n * ldt + k + e] = uint16_t(hi[e]);
+          Tl[n * ldt + k + e] = uint16_t(lo[e]);
+        }
     }
   }
 }
@@ -172,7 +200,7 @@ __global__ __launch_bounds__(256) void split_transpose(const float* __restrict__
 
 int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th, uint16_t* Tl,
                            int64_t ldt, hipStream_t s, bool neg) {
-  const dim3 grid(unsigned(cdiv(d, 32)), unsigned(cdiv(d, 32)));
+  const dim3 grid(unsigned(cdiv(d, 64)), unsigned(cdiv(d, 64)));
   return launch(neg ? "obs_split_p" : "obs_split_u", split_transpose, grid, dim3(256), 0, s, U,
                 ldu, d, Th, Tl, ldt, neg ? -1.f : 1.f);
 }
