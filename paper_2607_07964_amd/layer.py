@@ -164,10 +164,12 @@ def solve(st: LayerState, bits: int, damp: float = 0.01, alpha: Optional[float] 
 # 20 TFLOP/s for the factorisation.
 FACTOR_SHARE = 0.5
 FACTOR_SHARE_SHORT = 0.125
-# (Measured alternatives on q_proj, 11.5 ms with this schedule: starting H_G right after H_X
-# and transforming W on a third stream, 12.0 ms -- H_G then slows the rotation of H_X and the
-# start of the factorisation; diag(H_G) on 64 CUs beside the factorisation instead of beside
-# the H_X covariance, 12.0 ms -- starved by the H_G covariance, it took 5.1 ms.)
+# Measured alternatives (q_proj, alternating with this schedule in one run): H_G started
+# right after H_X with W transformed on the current stream, 11.58 against 11.40 ms; W on a third
+# stream with H_G starting once S_X exists, 11.12 against 11.06 ms; diag(H_G) beside the H_X
+# covariance slowed that covariance from 3.55 to 4.3 ms; on 64 CUs beside the factorisation it
+# took 5.1 ms, starved by H_G. With the drift correction, the drift statistic on the current
+# stream before the factorisation: 20.8 against 20.1 ms.
 
 
 def _cov_cus(device, n_tokens: int, d_out: int, d_in: int) -> int:
