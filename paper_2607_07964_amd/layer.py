@@ -166,7 +166,8 @@ FACTOR_SHARE = 0.5
 FACTOR_SHARE_SHORT = 0.125
 # Measured alternatives (q_proj, alternating with this schedule in one run): H_G started
 # right after H_X with W transformed on the current stream, 11.58 against 11.40 ms; W on a third
-# stream with H_G starting once S_X exists, 11.12 against 11.06 ms; diag(H_G) beside the H_X
+# stream with H_G starting once S_X exists, 11.12 against 11.06 ms; W on the current stream
+# with H_G starting once S_X exists, 11.18 against 11.10 ms; diag(H_G) beside the H_X
 # covariance slowed that covariance from 3.55 to 4.3 ms; on 64 CUs beside the factorisation it
 # took 5.1 ms, starved by H_G. With the drift correction, the drift statistic on the current
 # stream before the factorisation: 20.8 against 20.1 ms.
