@@ -43,14 +43,10 @@ PEAK_BF16_TFLOPS = 2500.0
 # fp32 FMAs on the vector units without packed instructions: 256 CUs x 4 SIMDs x 16 lanes x
 # 2 flops x 2.4 GHz
 PEAK_FP32_VALU = 78.6
+PEAK_FP32_MFMA = 157.3  # dense fp32 matrix-core peak
+PEAK_HBM_GBS = 8000.0
 def traffic_file(kernel: str, workload: str) -> str:
     return os.path.join(ROOT, "profiles", f"{kernel.replace('_mfma', '')}_{workload}_traffic.json")
-KERNELS = ["cov_diag_partial", "cov_diag_final", "syrk_bf16_mfma", "syrk_bf16_mfma_shared", "syrk_reduce", "cross_bf16_mfma", "cross_reduce", "traces",
-           "rot_w_norms", "rot_factors", "rot_inv_factors", "rot_row_pass", "fwht_col",
-           "mix28_col", "chol_diag_shift", "chol_add_diag", "chol_reverse_copy",
-           "chol_potrf_diag", "chol_trsm", "chol_syrk_trtri_row",
-           "trtri_update", "chol_reverse_out", "gptaq_d_ut", "gptaq_t_u", "gptaq_mask",
-           "obs_split_u", "obs_split_p", "obs_group_params", "obs_sweep", "obs_trailing_update"]
 WORKLOADS = {"q_proj": 2, "down_proj": 3, "up_proj_70b": 4}
 
 
@@ -102,7 +98,8 @@ def cpu_baseline(spec, rot_in, rot_out, n_sample: int, X_dev, G_dev, W_dev, dX_d
     t_rest = time.perf_counter() - t1
     scale = spec.n_tokens / n_sample
     return {
-        "value": t_cov * scale + t_rest, "unit": "s/layer", "cores": int(cores), "kind": "oracle",
+        "value": round(t_cov * scale + t_rest, 3), "unit": "s/layer", "cores": int(cores),
+        "kind": "oracle", "blas": blas_vendor(),
         "sample": (f"float64 oracle: covariances{' and drift statistic' if D is not None else ''} "
                    f"on the first {n_sample} of {spec.n_tokens} tokens "
                    f"({t_cov:.2f} s, scaled x{scale:g}); traces, BiIP with dense rotations, "
@@ -376,7 +373,10 @@ def main() -> int:
     ap.add_argument("--cpu-tokens", type=int, default=16384)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true",
-                    help="per-kernel times of one extra step run on a single stream (stderr)")
+                    help="add the per-kernel times of the profiled single-stream step")
+    ap.add_argument("--no-70b", action="store_true",
+                    help="leave out the 70B up_proj entry timed after the main workload")
+    ap.add_argument("--steps-70b", type=int, default=3, help="timed steps of the 70B entry")
     ap.add_argument("--serial", action="store_true",
                     help="time the single-stream schedule instead of the two-stream one")
     ap.add_argument("--cov-cus", type=int, default=-1,
@@ -422,6 +422,139 @@ def main() -> int:
         return online_bench(args, spec, dev)
     if args.diagnostics:
         return diag_bench(args, spec, dev)
+    out = layer_bench(args, spec, dev, args.steps, args.warmup, args.cpu_tokens)
+    if args.workload != "up_proj_70b" and not args.no_70b and not args.drift:
+        # the 70B-shaped layer in the same run: a few timed steps with its own roofline and a
+        # bounded oracle sample
+        spec70 = synth.workload(WORKLOADS["up_proj_70b"])
+        torch.cuda.empty_cache()
+        out["up_proj_70b"] = layer_bench(args, spec70, dev, args.steps_70b, 1, 1024,
+                                         brief=True)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+# Stages of the layer (SURVEY-style rows a1-a8) by kernel-name prefix, for the profiled
+# breakdown; the first matching prefix wins.
+STAGES = (
+    ("cov_diag", ("cov_diag_",)),
+    ("covariances", ("syrk_", "cov_scale")),
+    ("drift_statistic", ("cross_",)),
+    ("traces", ("traces",)),
+    ("biip", ("rot_", "fwht_", "mix28_")),
+    ("factor", ("chol_", "trtri_")),
+    ("gptaq", ("gptaq_", "obs_split_p")),
+    ("obs_sweep", ("obs_sweep", "obs_group_params")),
+    ("obs_update", ("obs_trailing_update", "obs_split_u")),
+)
+
+
+def stage_of(kernel: str) -> str:
+    for name, prefixes in STAGES:
+        if any(kernel.startswith(p) for p in prefixes):
+            return name
+    return "other"
+
+
+def stage_work(spec, drift: bool) -> dict:
+    """Algorithmic work per layer of each stage and the roofline it is held to: (amount, unit,
+    peak). Covariances N d (d + 1) flops each on bf16 MFMA; diag(H_G) one read of G; BiIP
+    2 passes x (read + write) x 4 B over W, H_X, H_G (the ideal is one pass); factor d^3 / 3 +
+    d^3 / 3 fp32 flops; sweep 9 B per weight; trailing update d_out d_in (d_in - 1) flops (bf16
+    MFMA, the algorithmic count of the fp32-accurate product)."""
+    n, do, di = float(spec.n_tokens), float(spec.d_out), float(spec.d_in)
+    w = {
+        "cov_diag": (2.0 * n * do, "B", PEAK_HBM_GBS * 1e9),
+        "covariances": (n * di * (di + 1) + n * do * (do + 1), "flop", PEAK_BF16_TFLOPS * 1e12),
+        "biip": (2 * 2 * 4.0 * (do * di + di * di + do * do), "B", PEAK_HBM_GBS * 1e9),
+        "factor": (2.0 * di ** 3 / 3.0, "flop", PEAK_FP32_MFMA * 1e12),
+        "obs_sweep": (9.0 * do * di, "B", PEAK_HBM_GBS * 1e9),
+        "obs_update": (do * di * (di - 1), "flop", PEAK_BF16_TFLOPS * 1e12),
+    }
+    if drift:
+        w["drift_statistic"] = (2.0 * n * di * di, "flop", PEAK_BF16_TFLOPS * 1e12)
+        w["gptaq"] = (2.0 * di ** 3 / 3.0, "flop", PEAK_FP32_MFMA * 1e12)
+    return w
+
+
+def blas_vendor() -> str:
+    import numpy as np
+    try:
+        b = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        return f"{b.get('name')} {b.get('version')}"
+    except Exception:  # pragma: no cover
+        return "unknown"
+
+
+def cpu_baseline_70b(spec, rot_in, rot_out, n_sample: int, X_dev, G_dev, W_dev,
+                     row_sample: int = 512, panel: int = 1024):
+    """The float64 oracle on a bounded sample of the 70B-shaped layer, each part scaled
+    linearly to the full layer: covariances of X and G on the first ``n_sample`` tokens (x N /
+    n_sample); the dense rotation of H_G timed on a ``panel``-column slice of both products
+    (x d_out / panel); the rotation of H_X, the factor, at full size; the blocked sweep of
+    ``row_sample`` rows of the rotated W (x d_out / row_sample)."""
+    import numpy as np
+    import oracle as O
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+
+    def view(t):
+        t = t.cpu()
+        return synth.bf16_bits(t) if str(t.dtype) == "torch.bfloat16" else t.numpy()
+
+    Xs, Gs, W = view(X_dev[:n_sample]), view(G_dev[:n_sample]), O.as_f64(view(W_dev))
+    ri = (rot_in.sign, rot_in.q28)
+    ro = (rot_out.sign, rot_out.q28)
+    t0 = time.perf_counter()
+    hx = O.covariance(Xs)
+    hg = O.covariance(Gs)
+    t_cov = time.perf_counter() - t0
+    rows = np.arange(row_sample)
+    t1 = time.perf_counter()
+    O.traces(hx, hg)
+    b = O.biip_forward_rows(W, hx, np.diag(hg), ri, ro, rows)
+    U = O.inverse_cholesky_factor(O.damp(b["HX"], spec.damp))
+    t_mid = time.perf_counter() - t1
+    t2 = time.perf_counter()
+    O.obs_blocked(b["W_rows"], U, spec.bits, 128, 128)
+    t_sweep = time.perf_counter() - t2
+    # U H_G' U^T on a panel of columns: (U (H_G' Ut[:, panel])) with the dense U
+    Ud = O.rht_matrix(spec.d_out, *ro)
+    hg1 = hg / np.outer(b["sg"], b["sg"])
+    t3 = time.perf_counter()
+    Ud @ (hg1 @ Ud[:panel].T)
+    t_rot = time.perf_counter() - t3
+    n_scale, r_scale, p_scale = spec.n_tokens / n_sample, spec.d_out / row_sample, \
+        spec.d_out / panel
+    total = t_cov * n_scale + t_mid + t_sweep * r_scale + t_rot * p_scale
+    return {
+        "value": round(total, 3), "unit": "s/layer", "cores": int(cores), "kind": "oracle",
+        "blas": blas_vendor(),
+        "sample": (f"float64 oracle, each part scaled linearly: covariances of X and G on the "
+                   f"first {n_sample} of {spec.n_tokens} tokens ({t_cov:.2f} s, x{n_scale:g}); "
+                   f"BiIP of H_X with dense V, factor and traces at full size ({t_mid:.2f} s); "
+                   f"dense U H_G U^T on {panel} of {spec.d_out} columns ({t_rot:.2f} s, "
+                   f"x{p_scale:g}); blocked sweep of {row_sample} of {spec.d_out} rows "
+                   f"({t_sweep:.2f} s, x{r_scale:g})"),
+    }
+
+
+def layer_bench(args, spec, dev, steps: int, warmup: int, cpu_tokens: int,
+                brief: bool = False) -> dict:
+    """Seconds per layer of one workload: ``warmup`` untimed steps, ``steps`` timed steps
+    (HIP events per step on the issuing stream, and the host clock around all of them), the
+    covariance launches timed by libkronq's profiler inside the timed region, then one profiled
+    single-stream step for the per-stage breakdown, then the oracle's bounded sample."""
+    import torch
+
+    import synth
+    from paper_2607_07964_amd import kronq as K
+    from paper_2607_07964_amd import layer as L
+
     print(f"[bench] generating {spec.name}: W {spec.d_out}x{spec.d_in}, N={spec.n_tokens}",
           file=sys.stderr, flush=True)
     X = synth.gen_matrix(spec.x, dev)
@@ -444,28 +577,36 @@ def main() -> int:
         L.quantize_layer(st, X, G, W0, rin, rout, spec.bits, spec.damp, overlap=overlap, dX=dX,
                          alpha=args.alpha, cov_cus=cov_cus)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     L.check(st)
-    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+    print(f"[bench] {spec.name}: warmup done ({warmup} steps)", file=sys.stderr, flush=True)
 
     SHARED = "syrk_bf16_mfma_shared"  # the H_G covariance on part of the chip (two streams)
     K.kronq_profile_only(f"{dominant},{SHARED}")
     K.kronq_profile_reset()
     K.kronq_profile_enable(True)
+    main = torch.cuda.current_stream()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    evs[0].record(main)
+    for i in range(steps):
         step()
+        evs[i + 1].record(main)  # the step ends with the issuing stream waiting for the other
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     K.kronq_profile_enable(False)
     dom_ms, dom_n = K.kronq_profile_read(dominant)
     sh_ms, sh_n = K.kronq_profile_read(SHARED)
     L.check(st)
-    ms_step = (t1 - t0) * 1e3 / args.steps
-    print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
+    ms_step = (t1 - t0) * 1e3 / steps
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+    med = sorted(per_step)[steps // 2] if steps % 2 else \
+        0.5 * sum(sorted(per_step)[steps // 2 - 1:steps // 2 + 1])
+    print(f"[bench] {spec.name}: timed {steps} steps: {ms_step:.3f} ms/step "
+          f"(median {med:.3f})", file=sys.stderr, flush=True)
 
     # dominant kernel roofline: algorithmic flops N d (d + 1) per covariance launch (averaged
     # over the covariances run on the whole chip: both, or H_X alone when H_G ran beside the
@@ -478,9 +619,11 @@ def main() -> int:
         flops = fl_x if sh_n else (fl_x + fl_g) / 2
     avg_ms = dom_ms / max(dom_n, 1)
     achieved = flops / (avg_ms * 1e-3) / 1e12
+    wl_key = next((k for k, v in WORKLOADS.items() if synth.workload(v).name == spec.name),
+                  spec.name)
     roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": traffic(dominant, args.workload), "kernel": dominant, "launches": dom_n,
+            "traffic": traffic(dominant, wl_key), "kernel": dominant, "launches": dom_n,
             "avg_launch_ms": round(avg_ms, 4)}
     shared = None
     if sh_n:
@@ -488,36 +631,66 @@ def main() -> int:
                                                               spec.d_in)
         sh_avg = sh_ms / sh_n
         sh_tf = fl_g / (sh_avg * 1e-3) / 1e12
-        part_peak = PEAK_BF16_TFLOPS * cus / torch.cuda.get_device_properties(dev).multi_processor_count
+        ncu = torch.cuda.get_device_properties(dev).multi_processor_count
+        part_peak = PEAK_BF16_TFLOPS * cus / ncu
         shared = {"kernel": SHARED, "cus": cus, "launches": sh_n, "avg_launch_ms": round(sh_avg, 4),
-                  "achieved": round(sh_tf, 2), "peak_of_its_cus": round(part_peak, 1),
+                  "achieved": round(sh_tf, 2), "frac_of_chip": round(sh_tf / PEAK_BF16_TFLOPS, 4),
+                  "peak_of_its_cus": round(part_peak, 1),
                   "frac_of_its_cus": round(sh_tf / part_peak, 4)}
 
-    breakdown = None
-    if args.breakdown:
-        K.kronq_profile_only(None)
-        K.kronq_profile_reset()
-        K.kronq_profile_enable(True)
-        step(overlap=False)
-        torch.cuda.synchronize()
-        K.kronq_profile_enable(False)
-        breakdown = {}
-        for k in KERNELS:
-            ms, n = K.kronq_profile_read(k)
-            if n:
-                breakdown[k] = {"ms": round(ms, 4), "launches": n}
-        print("[bench] per-kernel (one profiled step): " + json.dumps(breakdown), file=sys.stderr)
+    # per-stage breakdown: one profiled single-stream step (every launch bracketed by events)
+    K.kronq_profile_only(None)
+    K.kronq_profile_reset()
+    K.kronq_profile_enable(True)
+    step(overlap=False)
+    torch.cuda.synchronize()
+    K.kronq_profile_enable(False)
+    kern = {}
+    for k in K.kronq_profile_names():
+        ms, n = K.kronq_profile_read(k)
+        if n:
+            kern[k] = {"ms": round(ms, 4), "launches": n}
+    K.kronq_profile_reset()
+    work = stage_work(spec, bool(args.drift))
+    stages = {}
+    for k, v in kern.items():
+        sname = stage_of(k)
+        stages.setdefault(sname, 0.0)
+        stages[sname] += v["ms"]
+    bound_ms = 0.0
+    stage_out = {}
+    for sname, ms in stages.items():
+        ent = {"ms": round(ms, 4)}
+        if sname in work:
+            amount, unit, peak = work[sname]
+            b_ms = amount / peak * 1e3
+            if sname != "cov_diag":  # diag(H_G) is part of H_G's work: read early, not extra
+                bound_ms += b_ms
+            rate = amount / (ms * 1e-3)
+            ent.update({"bound_ms": round(b_ms, 4), "frac": round(b_ms / ms, 4),
+                        ("TFLOP/s" if unit == "flop" else "GB/s"):
+                            round(rate / (1e12 if unit == "flop" else 1e9), 2)})
+        stage_out[sname] = ent
+    roof["layer_bound_ms"] = round(bound_ms, 4)
+    roof["layer_frac"] = round(bound_ms / med, 4)
+    print(f"[bench] {spec.name}: stages (one single-stream step) " + json.dumps(stage_out),
+          file=sys.stderr, flush=True)
 
     cpu = None
     if not args.no_cpu_baseline:
-        print("[bench] timing the float64 oracle on the host (bounded sample)", file=sys.stderr,
-              flush=True)
-        cpu = cpu_baseline(spec, ri, ro, min(args.cpu_tokens, spec.n_tokens), X, G, W0, dX,
-                           args.alpha, group)
+        print(f"[bench] {spec.name}: timing the float64 oracle on the host (bounded sample)",
+              file=sys.stderr, flush=True)
+        if spec.d_out > 16384:
+            cpu = cpu_baseline_70b(spec, ri, ro, min(cpu_tokens, spec.n_tokens), X, G, W0)
+        else:
+            cpu = cpu_baseline(spec, ri, ro, min(cpu_tokens, spec.n_tokens), X, G, W0, dX,
+                               args.alpha, group)
+    del X, G, W0, dX, st
 
     out = {
         "metric": METRIC, "value": round(ms_step / 1e3, 6), "unit": "s/layer", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "steps": steps, "warmup": warmup, "ms_per_step": round(ms_step, 4),
+        "ms_median": round(med, 4), "step_ms": [round(x, 4) for x in per_step],
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16 (covariances, MFMA) + fp32 (rotations, factor, OBS)", "data": "synthetic",
         "config": {"workload": f"{spec.name} W {spec.d_out}x{spec.d_in}, N={spec.n_tokens} tokens, "
@@ -532,10 +705,14 @@ def main() -> int:
     }
     if shared is not None:
         out["shared_covariance"] = shared
-    if breakdown is not None:
-        out["kernels_ms"] = breakdown
-    print(json.dumps(out), flush=True)
-    return 0
+    out["stages_single_stream"] = stage_out
+    if args.breakdown:
+        out["kernels_ms"] = kern
+    if brief:
+        for k in ("metric", "n_gpus", "higher_is_better", "scaling", "vs_baseline", "dtype",
+                  "data"):
+            out.pop(k, None)
+    return out
 
 
 if __name__ == "__main__":

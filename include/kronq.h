@@ -387,6 +387,10 @@ int kronq_profile_enable(int on);
 int kronq_profile_only(const char* kernel);
 void kronq_profile_reset(void);
 int kronq_profile_read(const char* kernel, double* total_ms, int64_t* launches);
+/* Names of the kernels recorded since the last reset, comma-separated, into buf (capacity
+ * cap bytes, always NUL-terminated when cap > 0; truncated if short). Returns the length the
+ * full list needs, without the terminator. */
+int64_t kronq_profile_names(char* buf, size_t cap);
 
 #ifdef __cplusplus
 }

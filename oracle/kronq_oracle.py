@@ -70,7 +70,8 @@ import numpy as np
 __all__ = [
     "widen_bf16", "as_f64", "covariance", "covariance_diag", "cross_covariance", "traces",
     "rescale_factors", "hadamard", "rht_matrix", "rht_rows",
-    "biip_forward", "biip_revert", "damp", "inverse_cholesky_factor", "gptaq_correction",
+    "biip_forward", "biip_forward_rows", "biip_revert", "damp", "inverse_cholesky_factor",
+    "gptaq_correction",
     "group_params", "quantize", "obs_unblocked", "obs_blocked", "kfac_loss", "kronq_objective",
     "allocate_bits", "count_avg_bits", "dequantize", "online_matvec", "pack_codes",
     "incoherence", "norm_cv", "eigenvectors", "hessian_incoherence", "sweep_pivots",
@@ -264,6 +265,32 @@ def biip_forward(W, HX, HG, rot_in=None, rot_out=None, flags: int = BIIP, D=None
         "D": None if D1 is None else V @ D1 @ V.T,
         "sx": sx, "sg": sg, "V": V, "U": U,
     }
+
+
+def biip_forward_rows(W, HX, HG_diag, rot_in, rot_out, rows, flags: int = BIIP):
+    """Algorithm 1 for a layer whose output side is too large to rotate densely: the full
+    V H_X' V^T, but only the listed rows of W'' = U W' V^T (rows of U from ``rht_rows``) and the
+    post-BiIP traces. The output side enters only through diag(H_G) (S_G, eq. rescale) and
+    tr(U H_G' U^T) = tr(H_G') = sum_i H_G,ii / s^G_i^2 (an orthogonal similarity keeps the
+    trace). Returns dict(HX, W_rows, sx, sg, traces)."""
+    W = as_f64(W)
+    HX = np.asarray(HX, dtype=np.float64)
+    hg = _diag(HG_diag)
+    d_out, d_in = W.shape
+    sx, sg = rescale_factors(W, HX, hg, flags)
+    HX1 = HX / np.outer(sx, sx)
+    V = rht_matrix(d_in, *rot_in) if flags & ROT_IN else np.eye(d_in)
+    rows = np.asarray(rows, dtype=np.int64)
+    if flags & ROT_OUT:
+        Ur = rht_rows(d_out, rot_out[0], rot_out[1], rows)
+    else:
+        Ur = np.eye(d_out)[rows]
+    W1 = sg[:, None] * W * sx[None, :]
+    HX2 = V @ HX1 @ V.T
+    tx = float(np.trace(HX2))
+    tg = float(np.sum(hg / sg ** 2))
+    return {"HX": HX2, "W_rows": (Ur @ W1) @ V.T, "sx": sx, "sg": sg,
+            "traces": (tx, tg, tx * tg)}
 
 
 def biip_revert(W_hat, sx, sg, V, U) -> np.ndarray:

@@ -144,6 +144,20 @@ int kronq_profile_read(const char* kernel, double* total_ms, int64_t* launches) 
   return KRONQ_OK;
 }
 
+int64_t kronq_profile_names(char* buf, size_t cap) {
+  std::string all;
+  for (const auto& kv : kq::g_prof_tab) {
+    if (!all.empty()) all += ',';
+    all += kv.first;
+  }
+  if (buf && cap > 0) {
+    const size_t n = all.size() < cap - 1 ? all.size() : cap - 1;
+    std::memcpy(buf, all.data(), n);
+    buf[n] = '\0';
+  }
+  return static_cast<int64_t>(all.size());
+}
+
 int kronq_allocate_bits(const double* scores, const int64_t* weights, int n_layers,
                         const int* choices, int n_choices, double avg_bits, int* bits_out,
                         double* objective_out) {

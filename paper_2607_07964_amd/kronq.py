@@ -32,8 +32,8 @@ EXPORTS = (
     "kronq_workspace_bytes", "kronq_last_error", "kronq_version", "kronq_accumulate_cov",
     "kronq_traces", "kronq_rotate", "kronq_cholesky_inv", "kronq_obs_quantize_layer",
     "kronq_layer_loss", "kronq_allocate_bits", "kronq_profile_enable", "kronq_profile_only",
-    "kronq_profile_reset", "kronq_profile_read", "kronq_accumulate_cross", "kronq_rotate_drift",
-    "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift", "kronq_pack_codes",
+    "kronq_profile_reset", "kronq_profile_read", "kronq_profile_names", "kronq_accumulate_cross",
+    "kronq_rotate_drift",    "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift", "kronq_pack_codes",
     "kronq_online_factors", "kronq_online_matvec", "kronq_matrix_stats", "kronq_eigh",
     "kronq_proxy_loss_factors", "kronq_accumulate_cov_limited", "kronq_cov_diag",
 )
@@ -90,6 +90,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_profile_only": (I, [ctypes.c_char_p]),
         "kronq_profile_reset": (None, []),
         "kronq_profile_read": (I, [ctypes.c_char_p, P, P]),
+        "kronq_profile_names": (I64, [ctypes.c_char_p, SZ]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -484,3 +485,12 @@ def kronq_profile_read(kernel: str):
     _check(load().kronq_profile_read(kernel.encode(), ctypes.byref(ms), ctypes.byref(n)),
            "kronq_profile_read")
     return ms.value, n.value
+
+
+def kronq_profile_names() -> list:
+    """Kernel names recorded since the last reset."""
+    lib = load()
+    need = int(lib.kronq_profile_names(None, 0))
+    buf = ctypes.create_string_buffer(need + 1)
+    lib.kronq_profile_names(buf, need + 1)
+    return [n for n in buf.value.decode().split(",") if n]

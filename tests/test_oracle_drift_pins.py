@@ -176,3 +176,36 @@ def test_per_channel_rtn_when_hessian_is_diagonal():
         tie = srt[:, 1] - srt[:, 0] < 1e-15
         assert np.all((res["codes"][:, c] == np.argmin(dist, axis=1)) | tie)
 
+
+
+# ------------------------------------------------------------------------------ eq. gptaq_obj
+@pytest.mark.parametrize("kron_g", [False, True])
+def test_full_objective_equals_output_error_on_explicit_tokens(kron_g):
+    # eq. gptaq_obj: the drift-aware layer error ||W X~ - W_hat X||_F^2 on explicit tokens,
+    # X~ = X + dX, expands to the objective's two terms plus the constant ||W dX||_F^2, which
+    # does not depend on W_hat. With H_G = C^T C the output errors are weighted by C (each
+    # output channel mixed by the rows of C, the K-FAC weighting of eq. kron_obj). A flipped
+    # sign or a dropped factor 2 on the drift term breaks the equality.
+    r = rng(15)
+    n, d_out, d_in = 37, 6, 9
+    X = r.standard_normal((n, d_in))          # token-major: row t is token t's input
+    dX = 0.3 * r.standard_normal((n, d_in))
+    W = r.standard_normal((d_out, d_in))
+    W_hat = W + 0.2 * r.standard_normal((d_out, d_in))
+    C = r.standard_normal((11, d_out)) if kron_g else np.eye(d_out)
+    HX = X.T @ X
+    HG = C.T @ C
+    D = dX.T @ X                              # the drift statistic, token-major (reading R19)
+    Xt = X + dX
+    direct = 0.0
+    const = 0.0
+    for t in range(n):                        # token by token: y~_t - y_hat_t and W dx_t
+        e = C @ (W @ Xt[t] - W_hat @ X[t])
+        c = C @ (W @ dX[t])
+        direct += float(e @ e)
+        const += float(c @ c)
+    got = O.kronq_objective(W, W_hat, HX, HG, D)
+    np.testing.assert_allclose(got + const, direct, rtol=1e-11)
+    # without the drift statistic it is the plain K-FAC loss, the error without drift
+    plain = sum(float(np.sum((C @ ((W - W_hat) @ X[t])) ** 2)) for t in range(n))
+    np.testing.assert_allclose(O.kronq_objective(W, W_hat, HX, HG), plain, rtol=1e-11)

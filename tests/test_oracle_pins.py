@@ -232,6 +232,23 @@ def test_full_biip_loss_invariance_and_revert():
     np.testing.assert_allclose(back, W, rtol=1e-12, atol=1e-14)
 
 
+@pytest.mark.parametrize("shape,flags", [((28 * 4, 32), O.BIIP), ((64, 28 * 2), O.BIIP),
+                                         ((28 * 4, 32), O.RESCALE_IN | O.ROT_IN)])
+def test_biip_forward_rows_matches_dense(shape, flags):
+    # the sampled-row form used at full size: the same rotated H_X, the listed rows of the
+    # dense W'' and the post-BiIP traces of the dense matrices, with H_G given by its diagonal
+    d_out, d_in = shape
+    W, HX, HG, ri, ro = _rot_problem(d_out, d_in, 9)
+    dense = O.biip_forward(W, HX, HG, ri, ro, flags)
+    rows = [0, 5, d_out // 2, d_out - 1]
+    part = O.biip_forward_rows(W, HX, np.diag(HG), ri, ro, rows, flags)
+    np.testing.assert_allclose(part["HX"], dense["HX"], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(part["W_rows"], dense["W"][rows], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(part["traces"], O.traces(dense["HX"], dense["HG"]), rtol=1e-12)
+    np.testing.assert_array_equal(part["sx"], dense["sx"])
+    np.testing.assert_array_equal(part["sg"], dense["sg"])
+
+
 # ------------------------------------------------------------------------------------ O5/O6
 def test_damp():
     H = spd(6, 1)
