@@ -685,6 +685,7 @@ def layer_bench(args, spec, dev, steps: int, warmup: int, cpu_tokens: int,
         else:
             cpu = cpu_baseline(spec, ri, ro, min(cpu_tokens, spec.n_tokens), X, G, W0, dX,
                                args.alpha, group)
+    sched = L.schedule(st, spec.n_tokens, not args.serial, cov_cus)
     del X, G, W0, dX, st
 
     out = {
@@ -700,7 +701,7 @@ def layer_bench(args, spec, dev, steps: int, warmup: int, cpu_tokens: int,
                    "bits": spec.bits, "group": group, "block": 128, "damp": spec.damp,
                    "drift": bool(args.drift),
                    "parallelism": "single GPU",
-                   "schedule": L.schedule(st, spec.n_tokens, not args.serial, cov_cus)},
+                   "schedule": sched},
         "roofline": roof, "cpu_baseline": cpu,
     }
     if shared is not None:
