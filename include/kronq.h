@@ -154,6 +154,21 @@ int kronq_accumulate_cov_limited(const void* A, int dtype, int64_t n_rows, int64
 int kronq_cov_diag(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
                    float* hdiag, int max_cus, void* ws, size_t ws_bytes, void* stream);
 
+/* kronq_cov_diag without a workspace and without allocating, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc). Same arguments, kernels and result (bit for bit) as kronq_cov_diag. The chunk
+ * partials live in a fixed device array of KRONQ_NOALLOC_SCRATCH_BYTES inside the library, one
+ * copy per GPU, held until the process ends; its address on a device is taken once, on the
+ * first call for that device (the stream's device; the current one for the NULL stream). The
+ * call allocates nothing and calls no allocating routine. Every call on a GPU shares that
+ * GPU's array: calls that overlap on one GPU (other streams, other threads) race and must be
+ * ordered by the caller. Nothing in the array needs to start at zero: each call writes every
+ * partial it reads. Sizes whose partials exceed the array (for any d <= 2^21 they fit: at
+ * most 512 x 4096 partial sums) return KRONQ_ERR_WORKSPACE before anything is enqueued. */
+#define KRONQ_NOALLOC_SCRATCH_BYTES (16u << 20)
+int kronq_cov_diag_noalloc(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
+                           float* hdiag, int max_cus, void* stream);
+
 /* ---- 1b. drift statistic (Alg. 1 first line; eq. gptaq_obj) ------------------------------
  * C <- beta * C + alpha * A^T B for token-major A, B [n_rows x d] with the same leading
  * dimension ld; every entry of the d x d matrix C is written (it is not symmetric). With

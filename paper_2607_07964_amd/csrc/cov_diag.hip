@@ -1,8 +1,15 @@
 // diag(A^T A) as column sums of squares (Sec. 4.1 eq. kfac; the diagonal that the rescaling of
 // eq. rescale reads), for a caller that needs a side's S before that side's covariance exists.
 #include <algorithm>
+#include <mutex>
 
 #include "kq_common.hpp"
+
+// The chunk partials of kronq_cov_diag_noalloc: a fixed device array instead of a caller's
+// workspace (16 MiB on each GPU the library runs on, held until the process ends). Host code
+// never passes this name to a kernel: it stands for a host-side symbol, and each device's copy
+// has its own address, taken with hipGetSymbolAddress (cov_diag_scratch below).
+static __device__ __align__(256) double scratch[size_t(KRONQ_NOALLOC_SCRATCH_BYTES) / sizeof(double)];
 
 namespace kq {
 namespace {
@@ -146,6 +153,41 @@ size_t cov_diag_ws_bytes(int64_t n_rows, int64_t d) {
   if (n_rows <= 0 || d <= 0) return 256;
   const int64_t chunks = cdiv(n_rows, colsq_chunk_rows(n_rows, d));
   return align256(size_t(chunks) * size_t(d) * sizeof(double));
+}
+
+size_t cov_diag_need_bytes(int64_t n_rows, int64_t d, int max_cus) {
+  if (n_rows <= 0 || d <= 0) return 0;
+  const int64_t rows = colsq_chunk_rows(n_rows, d, max_cus);
+  return size_t(cdiv(n_rows, rows)) * size_t(d) * sizeof(double);
+}
+
+int cov_diag_scratch(hipStream_t s, void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* ptrs[kMaxDevices] = {};
+  int dev = 0;
+  if (s)
+    KQ_HIP(hipStreamGetDevice(s, &dev));
+  else
+    KQ_HIP(hipGetDevice(&dev));
+  KQ_REQUIRE(dev >= 0 && dev < kMaxDevices, KRONQ_ERR_HIP, "device ordinal %d out of range", dev);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptrs[dev]) {  // once per device, with that device current
+    int cur = 0;
+    KQ_HIP(hipGetDevice(&cur));
+    if (cur != dev) KQ_HIP(hipSetDevice(dev));
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p) {
+      set_error("hipGetSymbolAddress of the cov_diag scratch array failed: %s",
+                hipGetErrorString(e));
+      return KRONQ_ERR_HIP;
+    }
+    ptrs[dev] = p;
+  }
+  *out = ptrs[dev];
+  return KRONQ_OK;
 }
 
 int cov_diag_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,

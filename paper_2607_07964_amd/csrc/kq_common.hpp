@@ -107,6 +107,10 @@ int cov_launch(const void* A, const void* B, int dtype, int64_t n_rows, int64_t 
                int max_cus = 0);
 // diag(A^T A) as column sums of squares (fp64 sums, one rounding to fp32)
 size_t cov_diag_ws_bytes(int64_t n_rows, int64_t d);
+// bytes of chunk partials a cov_diag launch with these sizes uses, and the address of this
+// stream's device copy of the fixed scratch array of the no-allocation variant
+size_t cov_diag_need_bytes(int64_t n_rows, int64_t d, int max_cus);
+int cov_diag_scratch(hipStream_t s, void** out);
 int cov_diag_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
                     float* hdiag, int max_cus, void* ws, hipStream_t s);
 // traces

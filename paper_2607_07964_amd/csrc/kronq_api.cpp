@@ -31,6 +31,22 @@ int check_f32_mat(const float* p, int64_t rows, int64_t cols, int64_t ld, const 
 
 hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
+int check_cov_diag_args(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
+                        const float* hdiag, int max_cus) {
+  KQ_REQUIRE(max_cus >= 0, KRONQ_ERR_INVALID_ARG, "max_cus must be >= 0");
+  KQ_REQUIRE(valid_dtype(dtype), KRONQ_ERR_INVALID_ARG, "dtype must be KRONQ_BF16 or KRONQ_FP32");
+  KQ_REQUIRE(hdiag && aligned(hdiag, 4), KRONQ_ERR_INVALID_ARG, "hdiag is NULL or misaligned");
+  KQ_REQUIRE(n_rows >= 0 && d >= 1 && d <= (int64_t(1) << 24), KRONQ_ERR_INVALID_ARG,
+             "need n_rows >= 0 and 1 <= d <= 2^24");
+  if (n_rows > 0) {
+    KQ_REQUIRE(A, KRONQ_ERR_INVALID_ARG, "A is NULL");
+    KQ_REQUIRE(lda >= d, KRONQ_ERR_INVALID_ARG, "lda < d");
+    KQ_REQUIRE(aligned(A, 16) && lda % (dtype == KRONQ_BF16 ? 8 : 4) == 0, KRONQ_ERR_INVALID_ARG,
+               "A must be 16-byte aligned with lda divisible by 8 (bf16) or 4 (fp32)");
+  }
+  return KRONQ_OK;
+}
+
 constexpr int64_t kMaxRotDim = 32768;  // a transformed row must fit the 160 KB LDS
 
 int check_rot_side(int64_t d, const int8_t* sign, const float* q28, const char* side) {
@@ -147,19 +163,24 @@ int kronq_accumulate_cov_limited(const void* A, int dtype, int64_t n_rows, int64
 int kronq_cov_diag(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
                    float* hdiag, int max_cus, void* ws, size_t ws_bytes, void* stream) {
   kq::clear_error();
-  KQ_REQUIRE(max_cus >= 0, KRONQ_ERR_INVALID_ARG, "max_cus must be >= 0");
-  KQ_REQUIRE(valid_dtype(dtype), KRONQ_ERR_INVALID_ARG, "dtype must be KRONQ_BF16 or KRONQ_FP32");
-  KQ_REQUIRE(hdiag && aligned(hdiag, 4), KRONQ_ERR_INVALID_ARG, "hdiag is NULL or misaligned");
-  KQ_REQUIRE(n_rows >= 0 && d >= 1 && d <= (int64_t(1) << 24), KRONQ_ERR_INVALID_ARG,
-             "need n_rows >= 0 and 1 <= d <= 2^24");
-  if (n_rows > 0) {
-    KQ_REQUIRE(A, KRONQ_ERR_INVALID_ARG, "A is NULL");
-    KQ_REQUIRE(lda >= d, KRONQ_ERR_INVALID_ARG, "lda < d");
-    KQ_REQUIRE(aligned(A, 16) && lda % (dtype == KRONQ_BF16 ? 8 : 4) == 0, KRONQ_ERR_INVALID_ARG,
-               "A must be 16-byte aligned with lda divisible by 8 (bf16) or 4 (fp32)");
-    KQ_TRY(check_ws(ws, ws_bytes, kq::cov_diag_ws_bytes(n_rows, d)));
-  }
+  KQ_TRY(check_cov_diag_args(A, dtype, n_rows, d, lda, hdiag, max_cus));
+  if (n_rows > 0) KQ_TRY(check_ws(ws, ws_bytes, kq::cov_diag_ws_bytes(n_rows, d)));
   return kq::cov_diag_launch(A, dtype, n_rows, d, lda, hdiag, max_cus, ws, as_stream(stream));
+}
+
+int kronq_cov_diag_noalloc(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
+                           float* hdiag, int max_cus, void* stream) {
+  kq::clear_error();
+  KQ_TRY(check_cov_diag_args(A, dtype, n_rows, d, lda, hdiag, max_cus));
+  const size_t need = kq::cov_diag_need_bytes(n_rows, d, max_cus);
+  KQ_REQUIRE(need <= size_t(KRONQ_NOALLOC_SCRATCH_BYTES), KRONQ_ERR_WORKSPACE,
+             "kronq_cov_diag_noalloc: %zu bytes of partial sums needed (n_rows %lld, d %lld), "
+             "the fixed scratch array holds %zu",
+             need, (long long)n_rows, (long long)d, size_t(KRONQ_NOALLOC_SCRATCH_BYTES));
+  void* scratch = nullptr;
+  if (n_rows > 0) KQ_TRY(kq::cov_diag_scratch(as_stream(stream), &scratch));
+  return kq::cov_diag_launch(A, dtype, n_rows, d, lda, hdiag, max_cus, scratch,
+                             as_stream(stream));
 }
 
 int kronq_accumulate_cross(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d,

@@ -36,6 +36,7 @@ EXPORTS = (
     "kronq_rotate_drift",    "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift", "kronq_pack_codes",
     "kronq_online_factors", "kronq_online_matvec", "kronq_matrix_stats", "kronq_eigh",
     "kronq_proxy_loss_factors", "kronq_accumulate_cov_limited", "kronq_cov_diag",
+    "kronq_cov_diag_noalloc",
 )
 
 
@@ -65,6 +66,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_accumulate_cov": (I, [P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
         "kronq_accumulate_cov_limited": (I, [P, I, I64, I64, I64, P, I64, F, F, I, P, SZ, P]),
         "kronq_cov_diag": (I, [P, I, I64, I64, I64, P, I, P, SZ, P]),
+        "kronq_cov_diag_noalloc": (I, [P, I, I64, I64, I64, P, I, P]),
         "kronq_accumulate_cross": (I, [P, P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
         "kronq_rotate_drift": (I, [P, I64, I64, P, P, P, I, P, SZ, P]),
         "kronq_gptaq_correction": (I, [P, I64, I64, P, I64, F, P, I64, P, SZ, P]),
@@ -190,6 +192,17 @@ def kronq_cov_diag(A: torch.Tensor, out: Optional[torch.Tensor] = None,
     rc = load().kronq_cov_diag(_ptr(A), _dtype_code(A), n, d, _ld(A), _ptr(out), int(max_cus),
                                _ptr(ws), ws.numel(), _stream(A.device))
     _check(rc, "kronq_cov_diag")
+    return out
+
+
+def kronq_cov_diag_noalloc(A: torch.Tensor, out: torch.Tensor, max_cus: int = 0) -> torch.Tensor:
+    """kronq_cov_diag with the library's fixed device scratch array instead of a workspace:
+    nothing is allocated (``out`` fp32 [d] is the caller's). Overlapping calls on one GPU race."""
+    _dev(A, out)
+    n, d = A.shape
+    rc = load().kronq_cov_diag_noalloc(_ptr(A), _dtype_code(A), n, d, _ld(A), _ptr(out),
+                                       int(max_cus), _stream(A.device))
+    _check(rc, "kronq_cov_diag_noalloc")
     return out
 
 

@@ -199,6 +199,23 @@ def test_cov_diag_and_split_rotation_argument_checks():
     assert rc == -1 and "W_in" in msg
 
 
+def test_cov_diag_noalloc_checks_fail_before_any_launch():
+    lib = K.load()
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)
+    # the same argument checks as kronq_cov_diag
+    rc, _ = _err(lib.kronq_cov_diag_noalloc(fake, 3, 100, 64, 64, fake, 0, nul))
+    assert rc == -1
+    rc, msg = _err(lib.kronq_cov_diag_noalloc(fake, 1, 100, 64, 32, fake, 0, nul))
+    assert rc == -1 and "lda" in msg
+    rc, msg = _err(lib.kronq_cov_diag_noalloc(fake, 1, 100, 64, 64, nul, 0, nul))
+    assert rc == -1 and "hdiag" in msg
+    # partials beyond the fixed 16 MiB array: rejected with the workspace error, by size alone
+    d = 1 << 23
+    rc, msg = _err(lib.kronq_cov_diag_noalloc(fake, 1, 4096, d, d, fake, 0, nul))
+    assert rc == -5 and "scratch" in msg
+
+
 def test_diagnostics_argument_checks():
     lib = K.load()
     nul = ctypes.c_void_p(0)
