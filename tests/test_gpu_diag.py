@@ -90,6 +90,9 @@ def eigh_checks(H32, sweeps):
     tol = max(1e-5, 5e-7 * np.sqrt(sweeps * d))
     assert off < tol  # the off-diagonal mass left, relative: converged to rounding level
     # Weyl: each eigenvalue moves by at most the norm of the accumulated rounding perturbation
+    err = np.max(np.abs(np.sort(w) - wr))
+    print(f"eigh d={d}: max eigenvalue error {err:.3e} = {err / scale:.3e} max|lambda| = "
+          f"{err / np.linalg.norm(H):.3e} ||H||_F (tol {tol:.2e})")
     np.testing.assert_allclose(np.sort(w), wr, rtol=0, atol=tol * np.linalg.norm(H))
     assert np.linalg.norm(H @ Q - Q * w) / np.linalg.norm(H) < tol
     assert np.max(np.abs(Q.T @ Q - np.eye(d))) < tol
