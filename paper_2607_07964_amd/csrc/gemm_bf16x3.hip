@@ -11,6 +11,8 @@
 //     first over the K of the first pair, then over the K2 of the second;
 //     rows padded to 80 bytes so that the 16-byte operand reads of 8 consecutive lanes hit
 //     distinct banks; the next stage is fetched into registers during the MFMAs.
+#include <type_traits>
+
 #include "kq_common.hpp"
 
 namespace kq {
@@ -18,6 +20,7 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int BK = 32;      // K per stage
 constexpr int RS = 40;      // LDS row stride in bf16 (32 + 8 pad = 80 bytes)
@@ -141,6 +144,105 @@ __global__ __launch_bounds__(256) void gemm_bf16x3_sub(
       }
 }
 
+// C -= (Ah + Al)(Bh + Bl)^T ~ Al Bh^T + Ah Bl^T + Ah Bh^T with both operands split beforehand
+// into bf16 high and low parts and stored [row][k] (k contiguous): the OBS trailing update of
+// the P = 0 path, whose error block the sweep writes already split. The tiling of
+// gemm_bf16x3_sub (TM x TM per workgroup, 2 x 2 waves), with two LDS stages instead of one (one
+// barrier per stage) and every operand loaded as 16-byte chunks of bf16: the next stage is
+// fetched into registers during the current stage's MFMAs and written to the other buffer.
+template <int TM>
+__global__ __launch_bounds__(256) void gemm3_presplit_sub(
+    int64_t M, int64_t N, int64_t K, const uint16_t* __restrict__ Ah,
+    const uint16_t* __restrict__ Al, int64_t lda, const uint16_t* __restrict__ Bh,
+    const uint16_t* __restrict__ Bl, int64_t ldb, float* __restrict__ C, int64_t ldc) {
+  constexpr int NB = TM / 64;               // 32 x 32 blocks per wave edge (1 or 2)
+  constexpr int V = TM * BK / 8 / 256;      // 16-byte chunks of each array per thread per stage
+  __shared__ __attribute__((aligned(16))) uint16_t sA[2][2][TM * RS], sB[2][2][TM * RS];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave & 1, wn = wave >> 1, l32 = lane & 31, lhi = lane >> 5;
+  const int64_t m0 = int64_t(blockIdx.y) * TM, n0 = int64_t(blockIdx.x) * TM;
+  // this thread's 16-byte chunks: row r_v of the tile, k offset kc_v within the stage
+  int64_t oa[V], ob[V];
+  int so[V];
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    const int e = tid + 256 * v, r = e / (BK / 8), kc = (e % (BK / 8)) * 8;
+    const int64_t ra = m0 + r < M ? m0 + r : M - 1, rb = n0 + r < N ? n0 + r : N - 1;
+    oa[v] = ra * lda + kc;
+    ob[v] = rb * ldb + kc;
+    so[v] = r * RS + kc;
+  }
+  u32x4_t rah[V], ral[V], rbh[V], rbl[V];
+  f32x16_t acc[NB][NB];
+#pragma unroll
+  for (int a = 0; a < NB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[a][b] = f32x16_t{};
+  const int nst = int(K / BK);  // even: K is a multiple of 64
+#define KQ_FETCH(k0)                                                         \
+  _Pragma("unroll") for (int v = 0; v < V; ++v) {                            \
+    rah[v] = *reinterpret_cast<const u32x4_t*>(Ah + oa[v] + (k0));             \
+    ral[v] = *reinterpret_cast<const u32x4_t*>(Al + oa[v] + (k0));             \
+    rbh[v] = *reinterpret_cast<const u32x4_t*>(Bh + ob[v] + (k0));             \
+    rbl[v] = *reinterpret_cast<const u32x4_t*>(Bl + ob[v] + (k0));             \
+  }
+#define KQ_STASH(b)                                                          \
+  _Pragma("unroll") for (int v = 0; v < V; ++v) {                            \
+    *reinterpret_cast<u32x4_t*>(&sA[b][0][so[v]]) = rah[v];                    \
+    *reinterpret_cast<u32x4_t*>(&sA[b][1][so[v]]) = ral[v];                    \
+    *reinterpret_cast<u32x4_t*>(&sB[b][0][so[v]]) = rbh[v];                    \
+    *reinterpret_cast<u32x4_t*>(&sB[b][1][so[v]]) = rbl[v];                    \
+  }
+  // one stage from buffer B (compile-time), while the next stage (clamped to the last one at
+  // the end: a harmless reload) is fetched into registers and then written to the other buffer
+  auto stage = [&](auto bc, int st) {
+    constexpr int B = decltype(bc)::value;
+    __syncthreads();  // stage st is in LDS; the other buffer is free
+    const int64_t kn = int64_t(st + 1 < nst ? st + 1 : st) * BK;
+    KQ_FETCH(kn)
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int kc = ks * 16 + 8 * lhi;  // this lane's 8 k of the 16
+      bf16x8_t ah[NB], al[NB], bh[NB], bl[NB];
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const int m = wm * (TM / 2) + i * 32 + l32, n = wn * (TM / 2) + i * 32 + l32;
+        ah[i] = *reinterpret_cast<const bf16x8_t*>(&sA[B][0][m * RS + kc]);
+        al[i] = *reinterpret_cast<const bf16x8_t*>(&sA[B][1][m * RS + kc]);
+        bh[i] = *reinterpret_cast<const bf16x8_t*>(&sB[B][0][n * RS + kc]);
+        bl[i] = *reinterpret_cast<const bf16x8_t*>(&sB[B][1][n * RS + kc]);
+      }
+#pragma unroll
+      for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < NB; ++bj) {
+          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[bi], bh[bj], acc[bi][bj], 0, 0, 0);
+          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[bi], bl[bj], acc[bi][bj], 0, 0, 0);
+          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[bi], bh[bj], acc[bi][bj], 0, 0, 0);
+        }
+    }
+    KQ_STASH(1 - B)
+  };
+  KQ_FETCH(0)
+  KQ_STASH(0)
+  for (int st = 0; st < nst; st += 2) {
+    stage(std::integral_constant<int, 0>{}, st);
+    stage(std::integral_constant<int, 1>{}, st + 1);
+  }
+#undef KQ_FETCH
+#undef KQ_STASH
+#pragma unroll
+  for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < NB; ++bj)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t gm = m0 + wm * (TM / 2) + bi * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
+        const int64_t gn = n0 + wn * (TM / 2) + bj * 32 + l32;
+        if (gm < M && gn < N) C[gm * ldc + gn] -= acc[bi][bj][r];
+      }
+}
+
 // Ut_hi[n][k] + Ut_lo[n][k] = sgn U[k][n] (the three-term split of +-U^T), 64 x 64 tiles
 // through LDS: 16-byte loads of U rows, 8-byte stores of four bf16 of a Ut row. U is upper
 // triangular (strictly, for P) and the sweep's products read Ut[n][k] only for k < n, so tiles
@@ -203,6 +305,25 @@ int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th,
   const dim3 grid(unsigned(cdiv(d, 64)), unsigned(cdiv(d, 64)));
   return launch(neg ? "obs_split_p" : "obs_split_u", split_transpose, grid, dim3(256), 0, s, U,
                 ldu, d, Th, Tl, ldt, neg ? -1.f : 1.f);
+}
+
+int gemm_bf16x3_presplit_sub(int64_t M, int64_t N, int64_t K, const uint16_t* Ah,
+                             const uint16_t* Al, int64_t lda, const uint16_t* Bh,
+                             const uint16_t* Bl, int64_t ldb, float* C, int64_t ldc,
+                             hipStream_t s, const char* name) {
+  if (M <= 0 || N <= 0 || K <= 0) return KRONQ_OK;
+  KQ_REQUIRE(K % (2 * BK) == 0 && lda % 8 == 0 && ldb % 8 == 0 && aligned(Ah, 16) &&
+                 aligned(Al, 16) && aligned(Bh, 16) && aligned(Bl, 16),
+             KRONQ_ERR_INVALID_ARG,
+             "gemm_bf16x3_presplit_sub: K %% 64, lda %% 8, ldb %% 8 and 16-byte operands needed");
+  if (cdiv(M, 128) * cdiv(N, 128) >= 192) {
+    const dim3 grid(unsigned(cdiv(N, 128)), unsigned(cdiv(M, 128)));
+    return launch(name, gemm3_presplit_sub<128>, grid, dim3(256), 0, s, M, N, K, Ah, Al, lda, Bh,
+                  Bl, ldb, C, ldc);
+  }
+  const dim3 grid(unsigned(cdiv(N, 64)), unsigned(cdiv(M, 64)));
+  return launch(name, gemm3_presplit_sub<64>, grid, dim3(256), 0, s, M, N, K, Ah, Al, lda, Bh,
+                Bl, ldb, C, ldc);
 }
 
 int gemm_bf16x3_sub(int64_t M, int64_t N, const Bf16x3Pair& p1, const Bf16x3Pair& p2, float* C,

@@ -179,6 +179,11 @@ struct Bf16x3Pair {
 };
 int gemm_bf16x3_sub(int64_t M, int64_t N, const Bf16x3Pair& p1, const Bf16x3Pair& p2, float* C,
                     int64_t ldc, hipStream_t s, const char* name);
+// C -= (Ah + Al)(Bh + Bl)^T (three bf16 products) for operands split beforehand, [row][k]
+int gemm_bf16x3_presplit_sub(int64_t M, int64_t N, int64_t K, const uint16_t* Ah,
+                             const uint16_t* Al, int64_t lda, const uint16_t* Bh,
+                             const uint16_t* Bl, int64_t ldb, float* C, int64_t ldc,
+                             hipStream_t s, const char* name);
 // Th + Tl = sign * U^T split into bf16 high and low parts, [d x d] with row stride ldt
 // (sign = -1 when neg)
 int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th, uint16_t* Tl,

@@ -42,18 +42,29 @@
 namespace kq {
 namespace {
 
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// round-to-nearest-even fp32 -> bf16 bits (finite inputs)
+__device__ __forceinline__ uint32_t bf16_rne(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
 constexpr int OB = 128;          // block (and the smallest group)
-// Lanes per row of the sweep kernel: 8 (16 columns per lane) without the drift correction, 16
-// (8 columns per lane) with it, whose second broadcast and P block would not fit the registers
-// of 16 columns. 8 lanes halve the instructions per row: beside the H_G covariance, two waves
-// per SIMD, the sweep's 32 blocks at q_proj take 2.75 ms instead of 3.2 ms (alone 1.8 against
-// 1.67 ms).
-template <bool DRIFT>
+// Lanes per row of the sweep kernel, a template parameter: 8 (16 columns per lane, 8 rows per
+// wave) or 16 (8 columns per lane, 4 rows per wave). 8 lanes halve the instructions per row,
+// which matters when the rows are many and the sweep is throughput-bound (d_out = 28672, or on a
+// few CUs beside the H_G covariance); 16 lanes give twice the waves for a small d_out, whose
+// sweep is latency-bound (d_out = 4096 on the whole chip: 20.6 against 26.2 us per block). The
+// drift correction uses 16: its second broadcast and P block would not fit the registers of 16
+// columns.
+template <int L>
 struct SweepLayout {
-  static constexpr int LPR = DRIFT ? 16 : 8;  // lanes per row
-  static constexpr int CPL = OB / LPR;        // columns per lane
-  static constexpr int RPW = 64 / LPR;        // rows per wave
-  static constexpr int RPG = 4 * RPW;         // rows per workgroup (4 waves)
+  static constexpr int LPR = L;          // lanes per row
+  static constexpr int CPL = OB / L;     // columns per lane
+  static constexpr int RPW = 64 / L;     // rows per wave
+  static constexpr int RPG = 4 * RPW;    // rows per workgroup (4 waves)
 };
 constexpr int GRP = 4;           // blocks per group of the two-level lazy update (at most)
 
@@ -71,6 +82,15 @@ __device__ __forceinline__ float row_bcast(float v) {
   }
 }
 
+// an empty asm statement that reads and writes every element: its value must exist here
+template <int N>
+__device__ __forceinline__ void pin_regs(float (&w)[N]) {
+  static_assert(N % 4 == 0, "groups of four");
+#pragma unroll
+  for (int h = 0; h < N / 4; ++h)
+    asm volatile("" : "+v"(w[4 * h]), "+v"(w[4 * h + 1]), "+v"(w[4 * h + 2]), "+v"(w[4 * h + 3]));
+}
+
 struct SweepArgs {
   const float* ub;    // U block in LDS, [OB][OB]
   const float* pb;    // P block in LDS (drift only)
@@ -80,15 +100,29 @@ struct SweepArgs {
   double dscale;
 };
 
-// one column of the sweep: j = 8 * OWN + S (compile-time)
-template <bool DRIFT, int OWN, int S>
-__device__ __forceinline__ void sweep_col(float (&w)[SweepLayout<DRIFT>::CPL],
-                                          float (&ev)[SweepLayout<DRIFT>::CPL],
-                                          float (&xv)[SweepLayout<DRIFT>::CPL],
-                                          uint32_t (&qc)[SweepLayout<DRIFT>::CPL],
+// one column of the sweep: j = CPL * OWN + S (compile-time). uc / rc hold U[j, this lane's
+// columns] and 1 / U_jj, read from LDS during the previous column; this column issues the reads
+// for column j + 1 first, so that their latency is hidden behind its own work.
+template <bool DRIFT, int L, int OWN, int S>
+__device__ __forceinline__ void sweep_col(float (&w)[SweepLayout<L>::CPL],
+                                          float (&ev)[SweepLayout<L>::CPL],
+                                          float (&xv)[SweepLayout<L>::CPL],
+                                          uint32_t (&qc)[SweepLayout<L>::CPL],
+                                          float (&uc)[SweepLayout<L>::CPL], float& rc,
                                           const SweepArgs& a) {
-  constexpr int LPR = SweepLayout<DRIFT>::LPR, CPL = SweepLayout<DRIFT>::CPL;
+  constexpr int LPR = SweepLayout<L>::LPR, CPL = SweepLayout<L>::CPL;
   constexpr int j = OWN * CPL + S;
+  float un[CPL];
+  float rn = 0.f;
+  if constexpr (j + 1 < OB) {
+#pragma unroll
+    for (int h = 0; h < CPL / 4; ++h) {
+      const float4 u = *reinterpret_cast<const float4*>(a.ub + (j + 1) * OB + a.cb + 4 * h);
+      un[4 * h] = u.x, un[4 * h + 1] = u.y, un[4 * h + 2] = u.z, un[4 * h + 3] = u.w;
+    }
+    rn = a.rinv[j + 1];
+  }
+  __builtin_amdgcn_sched_barrier(0);  // the reads go out before this column's work
   const float x = w[S];
   const float t = x * a.inv_s;
   float qf = __builtin_rintf(t);
@@ -96,21 +130,19 @@ __device__ __forceinline__ void sweep_col(float (&w)[SweepLayout<DRIFT>::CPL],
   if (tie && a.sub == OWN) qf = float(__builtin_rint(double(x) / a.dscale));
   const float q = fminf(fmaxf(qf + a.fzero, 0.f), a.fmaxq);
   const float wh = a.scale * (q - a.fzero);
-  const float e = (x - wh) * a.rinv[j];
+  const float e = (x - wh) * rc;
   if (a.sub == OWN) {
     ev[S] = e;
     qc[S] = uint32_t(q);
     if (DRIFT) xv[S] = x;
   }
   const float eb = row_bcast<LPR, OWN>(e);
+  // the next column's update first: it is the one the next quantisation waits for
+  constexpr int nxt = (S + 1) % CPL;
+  w[nxt] = fmaf(-eb, uc[nxt], w[nxt]);
 #pragma unroll
-  for (int h = 0; h < CPL / 4; ++h) {
-    const float4 u = *reinterpret_cast<const float4*>(a.ub + j * OB + a.cb + 4 * h);
-    w[4 * h + 0] = fmaf(-eb, u.x, w[4 * h + 0]);
-    w[4 * h + 1] = fmaf(-eb, u.y, w[4 * h + 1]);
-    w[4 * h + 2] = fmaf(-eb, u.z, w[4 * h + 2]);
-    w[4 * h + 3] = fmaf(-eb, u.w, w[4 * h + 3]);
-  }
+  for (int c = 0; c < CPL; ++c)
+    if (c != nxt) w[c] = fmaf(-eb, uc[c], w[c]);
   if (DRIFT) {  // + w_j P[j, its columns], w_j as it stood before quantisation
     const float xb = row_bcast<LPR, OWN>(x);
 #pragma unroll
@@ -122,27 +154,44 @@ __device__ __forceinline__ void sweep_col(float (&w)[SweepLayout<DRIFT>::CPL],
       w[4 * h + 3] = fmaf(xb, pv.w, w[4 * h + 3]);
     }
   }
+  // the column's updates are applied here, as soon as e_j exists: left to itself the compiler
+  // sinks each column's FMAs to just before that column is quantised, which turns them into
+  // one long chain of dependent FMAs on the sweep's critical path (and keeps every e_j and U
+  // value live in registers). An empty asm that reads and writes every w pins them here.
+  pin_regs(w);
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) uc[c] = un[c];
+  rc = rn;
 }
 
-template <bool DRIFT, int OWN, int... S>
+template <bool DRIFT, int L, int OWN, int... S>
 __device__ __forceinline__ void sweep_lane_cols(std::integer_sequence<int, S...>,
-                                                float (&w)[SweepLayout<DRIFT>::CPL],
-                                                float (&ev)[SweepLayout<DRIFT>::CPL],
-                                                float (&xv)[SweepLayout<DRIFT>::CPL],
-                                                uint32_t (&qc)[SweepLayout<DRIFT>::CPL],
+                                                float (&w)[SweepLayout<L>::CPL],
+                                                float (&ev)[SweepLayout<L>::CPL],
+                                                float (&xv)[SweepLayout<L>::CPL],
+                                                uint32_t (&qc)[SweepLayout<L>::CPL],
+                                                float (&uc)[SweepLayout<L>::CPL], float& rc,
                                                 const SweepArgs& a) {
-  (sweep_col<DRIFT, OWN, S>(w, ev, xv, qc, a), ...);
+  (sweep_col<DRIFT, L, OWN, S>(w, ev, xv, qc, uc, rc, a), ...);
 }
 
-template <bool DRIFT, int... OWN>
+template <bool DRIFT, int L, int... OWN>
 __device__ __forceinline__ void sweep_all(std::integer_sequence<int, OWN...>,
-                                          float (&w)[SweepLayout<DRIFT>::CPL],
-                                          float (&ev)[SweepLayout<DRIFT>::CPL],
-                                          float (&xv)[SweepLayout<DRIFT>::CPL],
-                                          uint32_t (&qc)[SweepLayout<DRIFT>::CPL],
+                                          float (&w)[SweepLayout<L>::CPL],
+                                          float (&ev)[SweepLayout<L>::CPL],
+                                          float (&xv)[SweepLayout<L>::CPL],
+                                          uint32_t (&qc)[SweepLayout<L>::CPL],
                                           const SweepArgs& a) {
-  (sweep_lane_cols<DRIFT, OWN>(std::make_integer_sequence<int, SweepLayout<DRIFT>::CPL>{}, w, ev,
-                               xv, qc, a),
+  float uc[SweepLayout<L>::CPL];
+  constexpr int CPL = SweepLayout<L>::CPL;
+#pragma unroll
+  for (int h = 0; h < CPL / 4; ++h) {  // U row 0
+    const float4 u = *reinterpret_cast<const float4*>(a.ub + a.cb + 4 * h);
+    uc[4 * h] = u.x, uc[4 * h + 1] = u.y, uc[4 * h + 2] = u.z, uc[4 * h + 3] = u.w;
+  }
+  float rc = a.rinv[0];
+  (sweep_lane_cols<DRIFT, L, OWN>(std::make_integer_sequence<int, CPL>{}, w, ev, xv, qc, uc,
+                                  rc, a),
    ...);
 }
 
@@ -189,19 +238,69 @@ __global__ __launch_bounds__(256) void obs_group_params(const float* __restrict_
   }
 }
 
-template <bool DRIFT>
+// Pending updates of this block (the P = 0 sweep): the workgroup's rows of
+// W[:, c0 : c0 + OB] still owe sum_k E[row, k] U[kp0 + k, c0 + n] over the kpend columns of the
+// lazy group swept before this block. One 32 x 32 MFMA block per wave (its 32 of the block's
+// 128 columns, rows row0 .. row0 + 31), K in steps of 16, on the bf16 matrix cores with the
+// three-term split: the errors were written split by the sweep (Eph, Epl: [row][k]) and U^T
+// comes split ([n][k]). Operands go straight from global memory (L2) into the MFMA registers
+// (a lane's fragment is 8 contiguous k of one row or one column), a 128-column chunk's worth
+// requested at once. The result lands in dl[row - row0][column].
+__device__ __forceinline__ void pending_update(const uint16_t* __restrict__ Eph,
+                                               const uint16_t* __restrict__ Epl, int64_t ldep,
+                                               const uint16_t* __restrict__ Uth,
+                                               const uint16_t* __restrict__ Utl, int64_t ldut,
+                                               int64_t kp0, int kpend, int64_t c0,
+                                               int64_t row0, int64_t d_out, int wave, int lane,
+                                               float (*dl)[OB + 4]) {
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const int64_t ra = row0 + l32 < d_out ? row0 + l32 : d_out - 1;  // rows past the end: unused
+  const uint16_t* eh = Eph + ra * ldep + 8 * lhi;
+  const uint16_t* el = Epl + ra * ldep + 8 * lhi;
+  const int64_t n = c0 + wave * 32 + l32;
+  const uint16_t* bh = Uth + n * ldut + kp0 + 8 * lhi;
+  const uint16_t* bl = Utl + n * ldut + kp0 + 8 * lhi;
+  f32x16_t acc = {};
+  for (int k0 = 0; k0 < kpend; k0 += OB) {
+    bf16x8_t aha[OB / 16], ala[OB / 16], bha[OB / 16], bla[OB / 16];
+#pragma unroll
+    for (int ks = 0; ks < OB / 16; ++ks) {
+      const int kk = k0 + 16 * ks;
+      aha[ks] = *reinterpret_cast<const bf16x8_t*>(eh + kk);
+      ala[ks] = *reinterpret_cast<const bf16x8_t*>(el + kk);
+      bha[ks] = *reinterpret_cast<const bf16x8_t*>(bh + kk);
+      bla[ks] = *reinterpret_cast<const bf16x8_t*>(bl + kk);
+    }
+#pragma unroll
+    for (int ks = 0; ks < OB / 16; ++ks) {
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ala[ks], bha[ks], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aha[ks], bla[ks], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aha[ks], bha[ks], acc, 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) dl[8 * (r >> 2) + 4 * lhi + (r & 3)][wave * 32 + l32] = acc[r];
+}
+
+template <bool DRIFT, int L>
 __global__ __launch_bounds__(256) void obs_sweep(
     float* __restrict__ W, int64_t d_out, int64_t ldw, const float* __restrict__ U, int64_t ldu,
     const float* __restrict__ P, int64_t ldp, int64_t c0, int bits, uint8_t* __restrict__ codes,
     int64_t ldq, float* __restrict__ scales, float* __restrict__ zeros, int64_t ldsz, int64_t gi,
     int given, float* __restrict__ E, int64_t lde, float* __restrict__ Xq, int64_t ldxq,
-    float* __restrict__ W_hat, int64_t ldwh) {
+    float* __restrict__ W_hat, int64_t ldwh, uint16_t* __restrict__ Eh,
+    uint16_t* __restrict__ El, const uint16_t* __restrict__ Eph,
+    const uint16_t* __restrict__ Epl, int64_t ldes, const uint16_t* __restrict__ Uth,
+    const uint16_t* __restrict__ Utl, int64_t ldut, int64_t kp0, int kpend) {
   __shared__ __attribute__((aligned(16))) float ub[OB * OB];  // U[c0 + j][c0 + k]
   __shared__ __attribute__((aligned(16))) float pb[DRIFT ? OB * OB : 4];  // P[c0 + j][c0 + k]
   __shared__ float rinv[OB];                                   // 1 / U_jj
+  constexpr int LPR = SweepLayout<L>::LPR, CPL = SweepLayout<L>::CPL;
+  constexpr int RPW = SweepLayout<L>::RPW, RPG = SweepLayout<L>::RPG;
+  // pending update: 32 rows (one MFMA block; with 16 rows per workgroup the second half is
+  // computed and left unused)
+  __shared__ __attribute__((aligned(16))) float dl[DRIFT ? 1 : 32][OB + 4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  constexpr int LPR = SweepLayout<DRIFT>::LPR, CPL = SweepLayout<DRIFT>::CPL;
-  constexpr int RPW = SweepLayout<DRIFT>::RPW, RPG = SweepLayout<DRIFT>::RPG;
   const int sub = lane & (LPR - 1), cb = sub * CPL;
   const int64_t row = int64_t(blockIdx.x) * RPG + wave * RPW + lane / LPR;
   const bool live = row < d_out;
@@ -221,6 +320,19 @@ __global__ __launch_bounds__(256) void obs_sweep(
   for (int h = 0; h < CPL / 4; ++h) {
     const float4 v = *reinterpret_cast<const float4*>(W + rr * ldw + c0 + cb + 4 * h);
     w[4 * h] = v.x, w[4 * h + 1] = v.y, w[4 * h + 2] = v.z, w[4 * h + 3] = v.w;
+  }
+  if constexpr (!DRIFT) {
+    if (kpend > 0) {  // uniform over the launch
+      pending_update(Eph, Epl, ldes, Uth, Utl, ldut, kp0, kpend, c0, int64_t(blockIdx.x) * RPG,
+                     d_out, wave, lane, dl);
+      __syncthreads();
+      const int rl = wave * RPW + lane / LPR;
+#pragma unroll
+      for (int h = 0; h < CPL / 4; ++h) {
+        const float4 v = *reinterpret_cast<const float4*>(&dl[rl][cb + 4 * h]);
+        w[4 * h] -= v.x, w[4 * h + 1] -= v.y, w[4 * h + 2] -= v.z, w[4 * h + 3] -= v.w;
+      }
+    }
   }
   float scale, fzero;
   if (given) {  // a wider group: parameters taken at its first block by obs_group_params
@@ -248,7 +360,7 @@ __global__ __launch_bounds__(256) void obs_sweep(
   for (int c = 0; c < CPL; ++c) ev[c] = 0.f, xv[c] = 0.f, qc[c] = 0u;
   const SweepArgs args{ub,          pb,    rinv, sub, cb, scale, 1.f / scale, fzero,
                        float((1 << bits) - 1), double(scale)};
-  sweep_all<DRIFT>(std::make_integer_sequence<int, LPR>{}, w, ev, xv, qc, args);
+  sweep_all<DRIFT, L>(std::make_integer_sequence<int, LPR>{}, w, ev, xv, qc, args);
 
   if (!live) return;
   if (sub == 0 && !given) {
@@ -263,8 +375,22 @@ __global__ __launch_bounds__(256) void obs_sweep(
     const float4 hv = make_float4(wh[4 * h], wh[4 * h + 1], wh[4 * h + 2], wh[4 * h + 3]);
     *reinterpret_cast<float4*>(W + row * ldw + c0 + cb + 4 * h) = hv;
     if (W_hat) *reinterpret_cast<float4*>(W_hat + row * ldwh + c0 + cb + 4 * h) = hv;
-    *reinterpret_cast<float4*>(E + row * lde + cb + 4 * h) =
-        make_float4(ev[4 * h], ev[4 * h + 1], ev[4 * h + 2], ev[4 * h + 3]);
+    if (E)
+      *reinterpret_cast<float4*>(E + row * lde + cb + 4 * h) =
+          make_float4(ev[4 * h], ev[4 * h + 1], ev[4 * h + 2], ev[4 * h + 3]);
+    if (!DRIFT) {  // the errors split into bf16 high and low parts for the products after it
+      uint32_t hi[2], lo[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const uint32_t h0 = bf16_rne(ev[4 * h + 2 * e]), h1 = bf16_rne(ev[4 * h + 2 * e + 1]);
+        const uint32_t l0 = bf16_rne(ev[4 * h + 2 * e] - __uint_as_float(h0 << 16));
+        const uint32_t l1 = bf16_rne(ev[4 * h + 2 * e + 1] - __uint_as_float(h1 << 16));
+        hi[e] = h0 | (h1 << 16);
+        lo[e] = l0 | (l1 << 16);
+      }
+      *reinterpret_cast<uint2*>(Eh + row * ldes + cb + 4 * h) = make_uint2(hi[0], hi[1]);
+      *reinterpret_cast<uint2*>(El + row * ldes + cb + 4 * h) = make_uint2(lo[0], lo[1]);
+    }
     if (DRIFT)
       *reinterpret_cast<float4*>(Xq + row * ldxq + cb + 4 * h) =
           make_float4(xv[4 * h], xv[4 * h + 1], xv[4 * h + 2], xv[4 * h + 3]);
@@ -275,12 +401,28 @@ __global__ __launch_bounds__(256) void obs_sweep(
 
 // Blocks per lazy group for a quantisation group of `group` columns: a group's parameters need
 // its columns current when the sweep reaches it, which holds when it lies inside one lazy group
-// or starts one. 0 when the group is not supported.
+// or starts one. 0 when the group is not supported. (Drift path: the near updates are applied
+// after every block, so the whole lazy group is current.)
 int lazy_blocks(int64_t d_in, int group) {
   if (group < OB || group % OB != 0 || d_in % group != 0) return 0;
   const int m = group / OB;
   if (GRP % m == 0 || m % GRP == 0 || group == d_in) return GRP;
   for (int k = GRP - 1; k > 1; --k)
+    if (m % k == 0) return k;
+  return 1;
+}
+
+// Blocks per lazy group of the P = 0 sweep, whose pending updates reach a block only when the
+// sweep gets there: a quantisation group's columns are all current at its first block only if
+// that block starts a lazy group (then every earlier update has been applied to everything after
+// it). So the lazy group divides the quantisation group (up to LZMAX blocks); a group of one
+// block, or the whole row (parameters from the initial row), allows LZMAX.
+constexpr int LZMAX = 4;
+int lazy_blocks_pending(int64_t d_in, int group) {
+  if (group < OB || group % OB != 0 || d_in % group != 0) return 0;
+  const int m = group / OB;
+  if (m == 1 || group == d_in) return LZMAX;
+  for (int k = m < LZMAX ? m : LZMAX; k > 1; --k)
     if (m % k == 0) return k;
   return 1;
 }
@@ -291,76 +433,128 @@ int obs_group_ok(int64_t d_in, int group) { return lazy_blocks(d_in, group); }
 
 size_t obs_ws_bytes(int64_t d_out, int64_t d_in, bool drift) {
   if (d_out <= 0 || d_in <= 0) return 0;
-  const size_t per = align256(size_t(d_out) * GRP * OB * sizeof(float)) +
-                     2 * align256(size_t(d_in) * size_t(d_in) * sizeof(uint16_t));
-  return (drift ? 2 : 1) * per + 256;
+  const size_t split_u = 2 * align256(size_t(d_in) * size_t(d_in) * sizeof(uint16_t));
+  if (!drift)  // split errors of a lazy group, split U^T
+    return 2 * align256(size_t(d_out) * LZMAX * OB * sizeof(uint16_t)) + split_u + 256;
+  // errors and pre-quantisation values of a lazy group, split U^T and -P^T
+  return 2 * (align256(size_t(d_out) * GRP * OB * sizeof(float)) + split_u) + 256;
 }
+
+namespace {
+
+// P = 0: one sweep launch per block, which first applies the updates the block still owes to
+// the earlier blocks of its lazy group (pending_update), then one trailing product per lazy
+// group for everything after it.
+int obs_launch_pending(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* U,
+                       int64_t ldu, int bits, int group, uint8_t* codes, float* scales,
+                       float* zeros, float* err, float* W_hat, void* ws, hipStream_t s) {
+  const int64_t nblk = d_in / OB, ldsz = d_in / group;
+  const int lz = lazy_blocks_pending(d_in, group);
+  KQ_REQUIRE(lz > 0, KRONQ_ERR_UNSUPPORTED, "group %d not supported for d_in %lld", group,
+             (long long)d_in);
+  // 16 lanes per row for a small d_out (latency-bound sweep), 8 for a large one
+  const bool lanes16 = d_out <= 8192;
+  const unsigned grid =
+      unsigned(cdiv(d_out, lanes16 ? SweepLayout<16>::RPG : SweepLayout<8>::RPG));
+  Carver cv(ws);
+  // the lazy group's errors, split into bf16 high and low parts [row][LZMAX * OB]
+  const int64_t ldes = LZMAX * OB;
+  uint16_t* Eh = cv.take<uint16_t>(size_t(d_out) * ldes);
+  uint16_t* El = cv.take<uint16_t>(size_t(d_out) * ldes);
+  uint16_t* Uth = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
+  uint16_t* Utl = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
+  KQ_TRY(split_transpose_launch(U, ldu, d_in, Uth, Utl, d_in, s));
+  for (int64_t g0 = 0; g0 < nblk; g0 += lz) {
+    const int64_t gend = g0 + lz < nblk ? g0 + lz : nblk;
+    for (int64_t b = g0; b < gend; ++b) {
+      const int64_t c0 = b * OB, gi = c0 / group, eo = (b - g0) * OB;
+      const int given = group > OB;
+      if (given && c0 % group == 0)
+        KQ_TRY(launch("obs_group_params", obs_group_params, dim3(unsigned(cdiv(d_out, 4))),
+                      dim3(256), 0, s, static_cast<const float*>(W), d_out, ldw, c0,
+                      int64_t(group), bits, scales, zeros, ldsz, gi));
+      KQ_TRY(launch("obs_sweep", lanes16 ? obs_sweep<false, 16> : obs_sweep<false, 8>,
+                    dim3(grid), dim3(256), 0, s, W, d_out, ldw, U, ldu,
+                    static_cast<const float*>(nullptr), int64_t(0), c0, bits, codes, d_in,
+                    scales, zeros, ldsz, gi, given, err ? err + c0 : static_cast<float*>(nullptr),
+                    d_in, static_cast<float*>(nullptr), int64_t(0), W_hat, d_in, Eh + eo, El + eo,
+                    static_cast<const uint16_t*>(Eh), static_cast<const uint16_t*>(El), ldes,
+                    static_cast<const uint16_t*>(Uth), static_cast<const uint16_t*>(Utl), d_in,
+                    g0 * OB, int(eo)));
+    }
+    const int64_t rem = d_in - gend * OB;  // beyond the lazy group
+    if (rem > 0) {
+      // W[:, gend*OB :] -= E_group U[g0*OB : gend*OB, gend*OB :]
+      const int64_t K = (gend - g0) * OB, off = gend * OB * d_in + g0 * OB;
+      KQ_TRY(gemm_bf16x3_presplit_sub(d_out, rem, K, Eh, El, ldes, Uth + off, Utl + off, d_in,
+                                      W + gend * OB, ldw, s, "obs_trailing_update"));
+    }
+  }
+  return KRONQ_OK;
+}
+
+}  // namespace
 
 int obs_launch(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* U, int64_t ldu,
                int bits, int group, const float* P, int64_t ldp, uint8_t* codes, float* scales,
                float* zeros, float* err, float* W_hat, void* ws, hipStream_t s) {
-  const bool drift = P != nullptr;
+  if (P == nullptr)
+    return obs_launch_pending(W, d_out, d_in, ldw, U, ldu, bits, group, codes, scales, zeros,
+                              err, W_hat, ws, s);
+  // the drift correction: two-level lazy updates, near ones after every block
   const int64_t nblk = d_in / OB, ldsz = d_in / group;
   const int lz = lazy_blocks(d_in, group);
   KQ_REQUIRE(lz > 0, KRONQ_ERR_UNSUPPORTED, "group %d not supported for d_in %lld", group,
              (long long)d_in);
-  const unsigned grid = unsigned(cdiv(d_out, drift ? SweepLayout<true>::RPG
-                                                   : SweepLayout<false>::RPG));
+  const unsigned grid = unsigned(cdiv(d_out, SweepLayout<16>::RPG));
   Carver cv(ws);
   float* Ews = cv.take<float>(size_t(d_out) * GRP * OB);
   uint16_t* Uth = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
   uint16_t* Utl = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
-  float* Xws = drift ? cv.take<float>(size_t(d_out) * GRP * OB) : nullptr;
-  uint16_t* Pth = drift ? cv.take<uint16_t>(size_t(d_in) * size_t(d_in)) : nullptr;
-  uint16_t* Ptl = drift ? cv.take<uint16_t>(size_t(d_in) * size_t(d_in)) : nullptr;
-  // U^T (and -P^T) split once into bf16 high and low parts: the B operands of the trailing
+  float* Xws = cv.take<float>(size_t(d_out) * GRP * OB);
+  uint16_t* Pth = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
+  uint16_t* Ptl = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
+  // U^T and -P^T split once into bf16 high and low parts: the B operands of the trailing
   // updates
   KQ_TRY(split_transpose_launch(U, ldu, d_in, Uth, Utl, d_in, s));
-  if (drift) KQ_TRY(split_transpose_launch(P, ldp, d_in, Pth, Ptl, d_in, s, true));
+  KQ_TRY(split_transpose_launch(P, ldp, d_in, Pth, Ptl, d_in, s, true));
   const int64_t ldx = GRP * OB;
   for (int64_t g0 = 0; g0 < nblk; g0 += lz) {
     const int64_t gend = g0 + lz < nblk ? g0 + lz : nblk;
-    // errors of this lazy group's blocks: the caller's err (ld d_in) or the workspace
-    // (ld GRP * OB); pre-quantisation values (drift) always in the workspace
     float* Eg = err ? err + g0 * OB : Ews;
     const int64_t lde = err ? d_in : GRP * OB;
     for (int64_t b = g0; b < gend; ++b) {
       const int64_t c0 = b * OB;
       float* Eb = Eg + (b - g0) * OB;
-      float* Xb = drift ? Xws + (b - g0) * OB : nullptr;
+      float* Xb = Xws + (b - g0) * OB;
       const int64_t gi = c0 / group;
       const int given = group > OB;
       if (given && c0 % group == 0)
         KQ_TRY(launch("obs_group_params", obs_group_params, dim3(unsigned(cdiv(d_out, 4))),
                       dim3(256), 0, s, static_cast<const float*>(W), d_out, ldw, c0,
                       int64_t(group), bits, scales, zeros, ldsz, gi));
-      if (drift)
-        KQ_TRY(launch("obs_sweep", obs_sweep<true>, dim3(grid), dim3(256), 0, s, W, d_out, ldw, U,
-                      ldu, P, ldp, c0, bits, codes, d_in, scales, zeros, ldsz, gi, given, Eb, lde,
-                      Xb, ldx, W_hat, d_in));
-      else
-        KQ_TRY(launch("obs_sweep", obs_sweep<false>, dim3(grid), dim3(256), 0, s, W, d_out, ldw,
-                      U, ldu, P, ldp, c0, bits, codes, d_in, scales, zeros, ldsz, gi, given, Eb,
-                      lde, Xb, ldx, W_hat, d_in));
+      KQ_TRY(launch("obs_sweep", obs_sweep<true, 16>, dim3(grid), dim3(256), 0, s, W, d_out, ldw, U,
+                    ldu, P, ldp, c0, bits, codes, d_in, scales, zeros, ldsz, gi, given, Eb, lde,
+                    Xb, ldx, W_hat, d_in, static_cast<uint16_t*>(nullptr),
+                    static_cast<uint16_t*>(nullptr), static_cast<const uint16_t*>(nullptr),
+                    static_cast<const uint16_t*>(nullptr), int64_t(0),
+                    static_cast<const uint16_t*>(nullptr), static_cast<const uint16_t*>(nullptr),
+                    int64_t(0), int64_t(0), 0));
       const int64_t near = (gend - b - 1) * OB;  // rest of the lazy group
       if (near > 0) {
-        // W[:, c0+OB : gend*OB] -= E_b U[c0 : c0+OB, c0+OB : gend*OB] (- X_b P[...])
+        // W[:, c0+OB : gend*OB] -= E_b U[c0 : c0+OB, c0+OB : gend*OB] - X_b P[...]
         Bf16x3Pair pu{Eb, lde, Uth + (c0 + OB) * d_in + c0, Utl + (c0 + OB) * d_in + c0, d_in,
                       OB};
-        Bf16x3Pair pp;
-        if (drift)
-          pp = Bf16x3Pair{Xb, ldx, Pth + (c0 + OB) * d_in + c0, Ptl + (c0 + OB) * d_in + c0,
-                          d_in, OB};
+        Bf16x3Pair pp{Xb, ldx, Pth + (c0 + OB) * d_in + c0, Ptl + (c0 + OB) * d_in + c0, d_in,
+                      OB};
         KQ_TRY(gemm_bf16x3_sub(d_out, near, pu, pp, W + c0 + OB, ldw, s, "obs_trailing_update"));
       }
     }
     const int64_t rem = d_in - gend * OB;  // beyond the lazy group
     if (rem > 0) {
-      // W[:, gend*OB :] -= E_group U[g0*OB : gend*OB, gend*OB :] (- X_group P[...])
       const int64_t K = (gend - g0) * OB, off = gend * OB * d_in + g0 * OB;
       Bf16x3Pair pu{Eg, lde, Uth + off, Utl + off, d_in, K};
-      Bf16x3Pair pp;
-      if (drift) pp = Bf16x3Pair{Xws, ldx, Pth + off, Ptl + off, d_in, K};
+      Bf16x3Pair pp{Xws, ldx, Pth + off, Ptl + off, d_in, K};
       KQ_TRY(gemm_bf16x3_sub(d_out, rem, pu, pp, W + gend * OB, ldw, s, "obs_trailing_update"));
     }
   }
