@@ -54,11 +54,11 @@ __device__ __forceinline__ uint32_t bf16_rne(float x) {
 constexpr int OB = 128;          // block (and the smallest group)
 // Lanes per row of the sweep kernel, a template parameter: 8 (16 columns per lane, 8 rows per
 // wave) or 16 (8 columns per lane, 4 rows per wave). 8 lanes halve the instructions per row,
-// which matters when the rows are many and the sweep is throughput-bound (d_out = 28672, or on a
-// few CUs beside the H_G covariance); 16 lanes give twice the waves for a small d_out, whose
-// sweep is latency-bound (d_out = 4096 on the whole chip: 20.6 against 26.2 us per block). The
-// drift correction uses 16: its second broadcast and P block would not fit the registers of 16
-// columns.
+// which matters when the rows are many and the sweep is throughput-bound (d_out = 28672, or on
+// part of the chip beside the H_G covariance); 16 lanes give twice the waves for a small d_out,
+// whose sweep is latency-bound on the whole chip (d_out = 4096 alone: 20.6 against 26.2 us per
+// block). The drift correction uses 16: its second broadcast and P block would not fit the
+// registers of 16 columns.
 template <int L>
 struct SweepLayout {
   static constexpr int LPR = L;          // lanes per row
@@ -452,8 +452,10 @@ int obs_launch_pending(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const
   const int lz = lazy_blocks_pending(d_in, group);
   KQ_REQUIRE(lz > 0, KRONQ_ERR_UNSUPPORTED, "group %d not supported for d_in %lld", group,
              (long long)d_in);
-  // 16 lanes per row for a small d_out (latency-bound sweep), 8 for a large one
-  const bool lanes16 = d_out <= 8192;
+  // 16 lanes per row only for a small d_out: beside the H_G covariance the sweep has part of
+  // the chip, where the 16-lane layout's twice as many workgroups (one per CU) take two rounds
+  // (8B q_proj layer: 11.31-11.39 ms per layer with 8 lanes, 11.46-11.48 with 16)
+  const bool lanes16 = d_out <= 2048;
   const unsigned grid =
       unsigned(cdiv(d_out, lanes16 ? SweepLayout<16>::RPG : SweepLayout<8>::RPG));
   Carver cv(ws);
