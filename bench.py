@@ -543,6 +543,47 @@ def cpu_baseline_70b(spec, rot_in, rot_out, n_sample: int, X_dev, G_dev, W_dev,
     }
 
 
+def measured_peaks(X, dev) -> dict:
+    """The chip's measured ceilings next to the data-sheet figures: the bf16 MFMA rate of a
+    register-resident loop (kronq_probe_mfma_bf16) on the workload's own input values (the clock
+    is power-limited under MFMA load, and the limit depends on the data), and a plain 1 GiB
+    device copy (read + write bytes)."""
+    import torch
+    from paper_2607_07964_amd import kronq as K
+    out = {}
+    data = X.reshape(-1)[:4096].contiguous()
+    chk = torch.empty(2048, device=dev)
+    iters = 20000
+    K.kronq_probe_mfma_bf16(data, 200, chk)  # warm-up
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    best = None
+    for _ in range(3):
+        e0.record()
+        wgs = K.kronq_probe_mfma_bf16(data, iters, chk)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    tf = wgs * 4.0 * iters * 8 * 32768 / (best * 1e-3) / 1e12
+    out["bf16_mfma_tflops"] = round(tf, 1)
+    out["bf16_mfma_frac_of_spec"] = round(tf / PEAK_BF16_TFLOPS, 4)
+    out["bf16_mfma_data"] = "the first 4096 bf16 values of X"
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 5 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    out["hbm_copy_gbs"] = round(gbs, 1)
+    out["hbm_copy_frac_of_spec"] = round(gbs / PEAK_HBM_GBS, 4)
+    del src, dst
+    return out
+
+
 def layer_bench(args, spec, dev, steps: int, warmup: int, cpu_tokens: int,
                 brief: bool = False) -> dict:
     """Seconds per layer of one workload: ``warmup`` untimed steps, ``steps`` timed steps
@@ -583,6 +624,7 @@ def layer_bench(args, spec, dev, steps: int, warmup: int, cpu_tokens: int,
     L.check(st)
     print(f"[bench] {spec.name}: warmup done ({warmup} steps)", file=sys.stderr, flush=True)
 
+    peaks = None if brief else measured_peaks(X, dev)
     SHARED = "syrk_bf16_mfma_shared"  # the H_G covariance on part of the chip (two streams)
     K.kronq_profile_only(f"{dominant},{SHARED}")
     K.kronq_profile_reset()
@@ -671,6 +713,8 @@ def layer_bench(args, spec, dev, steps: int, warmup: int, cpu_tokens: int,
                         ("TFLOP/s" if unit == "flop" else "GB/s"):
                             round(rate / (1e12 if unit == "flop" else 1e9), 2)})
         stage_out[sname] = ent
+    if peaks is not None:
+        roof["frac_of_measured_peak"] = round(achieved / peaks["bf16_mfma_tflops"], 4)
     roof["layer_bound_ms"] = round(bound_ms, 4)
     roof["layer_frac"] = round(bound_ms / med, 4)
     print(f"[bench] {spec.name}: stages (one single-stream step) " + json.dumps(stage_out),
@@ -707,6 +751,8 @@ def layer_bench(args, spec, dev, steps: int, warmup: int, cpu_tokens: int,
     if shared is not None:
         out["shared_covariance"] = shared
     out["stages_single_stream"] = stage_out
+    if peaks is not None:
+        out["measured_peaks"] = peaks
     if args.breakdown:
         out["kernels_ms"] = kern
     if brief:

@@ -392,6 +392,21 @@ int kronq_allocate_bits(const double* scores, const int64_t* weights, int n_laye
                         const int* choices, int n_choices, double avg_bits, int* bits_out,
                         double* objective_out);
 
+/* ---- measured matrix-core ceiling (measurement support, not a step of the layer) ----------
+ * The clock of the chip is power-limited under matrix-core load, and the limit depends on the
+ * operand values; this measures the bf16 MFMA rate reachable on given data. Launches two
+ * workgroups of 4 waves per compute unit; each wave runs `iters` iterations of 8 independent
+ * v_mfma_f32_32x32x16_bf16 on 4 register fragments read once from `data`, with no memory
+ * access inside the loop. Time the launch on the stream; it performs
+ * (*workgroups) * 4 * iters * 8 * 32768 flops.
+ *   data        device bf16 [>= 4096], 16-byte aligned (the operand values).
+ *   iters       >= 1.
+ *   out         device fp32 [out_len]: one checksum per workgroup (keeps the loop alive).
+ *   workgroups  host int*, receives the workgroup count (2 x compute units); out_len must be at
+ *               least that, else KRONQ_ERR_INVALID_ARG before any launch. */
+int kronq_probe_mfma_bf16(const void* data, int iters, float* out, int64_t out_len,
+                          int* workgroups, void* stream);
+
 /* ---- profiler (hipEvent timing of every kernel launch, by kernel name) --------------------
  * While enabled, each launch is bracketed by two events on its stream. kronq_profile_read
  * synchronises the recorded events and returns the summed milliseconds and the launch count

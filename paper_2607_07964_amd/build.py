@@ -25,7 +25,7 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
 SOURCES = ["kq_runtime.cpp", "kronq_api.cpp", "cov.hip", "gemm_f32.hip", "gemm_bf16x3.hip", "rotate.hip",
-           "chol.hip", "obs.hip", "gptaq.hip", "online.hip", "diag.hip", "loss.hip", "cov_diag.hip"]
+           "chol.hip", "obs.hip", "gptaq.hip", "online.hip", "diag.hip", "loss.hip", "cov_diag.hip", "peaks.hip"]
 
 
 def _compile(src: str) -> str:

@@ -111,6 +111,8 @@ size_t cov_diag_ws_bytes(int64_t n_rows, int64_t d);
 // stream's device copy of the fixed scratch array of the no-allocation variant
 size_t cov_diag_need_bytes(int64_t n_rows, int64_t d, int max_cus);
 int cov_diag_scratch(hipStream_t s, void** out);
+// register-resident bf16 MFMA loop (measured ceiling); *workgroups receives the grid size
+int mfma_peak_launch(const uint16_t* data, int iters, float* out, int* workgroups, hipStream_t s);
 int cov_diag_launch(const void* A, int dtype, int64_t n_rows, int64_t d, int64_t lda,
                     float* hdiag, int max_cus, void* ws, hipStream_t s);
 // traces

@@ -183,6 +183,21 @@ int kronq_cov_diag_noalloc(const void* A, int dtype, int64_t n_rows, int64_t d, 
                              as_stream(stream));
 }
 
+int kronq_probe_mfma_bf16(const void* data, int iters, float* out, int64_t out_len,
+                          int* workgroups, void* stream) {
+  kq::clear_error();
+  KQ_REQUIRE(data && aligned(data, 16) && out && workgroups, KRONQ_ERR_INVALID_ARG,
+             "data (16-byte aligned), out and workgroups are required");
+  KQ_REQUIRE(iters >= 1, KRONQ_ERR_INVALID_ARG, "iters must be >= 1");
+  int dev = 0, cus = 0;
+  KQ_HIP(hipGetDevice(&dev));
+  KQ_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  KQ_REQUIRE(out_len >= 2 * int64_t(cus), KRONQ_ERR_INVALID_ARG,
+             "out holds %lld floats, %d needed", (long long)out_len, 2 * cus);
+  return kq::mfma_peak_launch(static_cast<const uint16_t*>(data), iters, out, workgroups,
+                              as_stream(stream));
+}
+
 int kronq_accumulate_cross(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d,
                            int64_t ld, float* C, int64_t ldc, float alpha, float beta, void* ws,
                            size_t ws_bytes, void* stream) {

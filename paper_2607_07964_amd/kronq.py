@@ -36,7 +36,7 @@ EXPORTS = (
     "kronq_rotate_drift",    "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift", "kronq_pack_codes",
     "kronq_online_factors", "kronq_online_matvec", "kronq_matrix_stats", "kronq_eigh",
     "kronq_proxy_loss_factors", "kronq_accumulate_cov_limited", "kronq_cov_diag",
-    "kronq_cov_diag_noalloc",
+    "kronq_cov_diag_noalloc", "kronq_probe_mfma_bf16",
 )
 
 
@@ -67,6 +67,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_accumulate_cov_limited": (I, [P, I, I64, I64, I64, P, I64, F, F, I, P, SZ, P]),
         "kronq_cov_diag": (I, [P, I, I64, I64, I64, P, I, P, SZ, P]),
         "kronq_cov_diag_noalloc": (I, [P, I, I64, I64, I64, P, I, P]),
+        "kronq_probe_mfma_bf16": (I, [P, I, P, I64, P, P]),
         "kronq_accumulate_cross": (I, [P, P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
         "kronq_rotate_drift": (I, [P, I64, I64, P, P, P, I, P, SZ, P]),
         "kronq_gptaq_correction": (I, [P, I64, I64, P, I64, F, P, I64, P, SZ, P]),
@@ -478,6 +479,19 @@ def kronq_allocate_bits(scores, weights, choices=(2, 3, 4), avg_bits: float = 3.
 
 
 # ------------------------------------------------------------------------------------ profiler
+def kronq_probe_mfma_bf16(data: torch.Tensor, iters: int, out: torch.Tensor) -> int:
+    """Launch the register-resident bf16 MFMA loop on ``data`` (bf16, >= 4096 elements) on the
+    current stream; returns the workgroup count (flops = wgs * 4 * iters * 8 * 32768)."""
+    _dev(data, out)
+    if data.dtype != torch.bfloat16 or data.numel() < 4096:
+        raise ValueError("data must be bf16 with at least 4096 elements")
+    wgs = ctypes.c_int()
+    rc = load().kronq_probe_mfma_bf16(_ptr(data), int(iters), _ptr(out), out.numel(),
+                                      ctypes.byref(wgs), _stream(data.device))
+    _check(rc, "kronq_probe_mfma_bf16")
+    return wgs.value
+
+
 def kronq_profile_enable(on: bool = True):
     _check(load().kronq_profile_enable(int(on)), "kronq_profile_enable")
 
