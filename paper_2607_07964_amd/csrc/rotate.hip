@@ -25,7 +25,7 @@ namespace {
 
 constexpr int RP_THREADS = 512;
 constexpr int CP_THREADS = 256;
-constexpr int CP_MAXL = 256;
+constexpr int CP_MAXL = 1024;
 constexpr int NORM_ROWS = 16;
 
 // ----------------------------------------------------------------------------- norms
@@ -220,7 +220,41 @@ __global__ __launch_bounds__(RP_THREADS) void row_pass(
       continue;
     }
     __syncthreads();  // previous row finished with buf
-    if ((n & 7) == 0) {  // 16-byte rows (checked by the API): 8 values per vector load
+    if (m >= 512) {
+      // whole 512-element chunks (m is a power of two >= 512, n = L m): a wave takes a chunk,
+      // 8 consecutive elements per lane, straight from global memory; the stages of strides
+      // 1, 2, 4 run in registers and those of strides 8 ... 256 across lanes (lane xor 1 ...
+      // 32), so the chunk reaches LDS with its first 9 stages done; the stages of strides
+      // >= 512 follow in LDS
+      const int wave = tid >> 6, lane = tid & 63;
+      for (int64_t c0 = int64_t(wave) * 512 + lane * 8; c0 < n; c0 += int64_t(RP_THREADS) * 8) {
+        float x[8];
+        load8_f32(s + c0, 8, x);
+        if (pre_col) {
+          const float4 p0 = *reinterpret_cast<const float4*>(pre_col + c0);
+          const float4 p1 = *reinterpret_cast<const float4*>(pre_col + c0 + 4);
+          x[0] *= pr * p0.x, x[1] *= pr * p0.y, x[2] *= pr * p0.z, x[3] *= pr * p0.w;
+          x[4] *= pr * p1.x, x[5] *= pr * p1.y, x[6] *= pr * p1.z, x[7] *= pr * p1.w;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[e] *= pr;
+        }
+        hadamard_reg<8>(x);
+#pragma unroll
+        for (int j = 0; j < 6; ++j) {
+          const bool upper = (lane >> j) & 1;  // holds the second element of each pair
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float y = __shfl_xor(x[e], 1 << j);
+            x[e] = upper ? y - x[e] : x[e] + y;
+          }
+        }
+        *reinterpret_cast<float4*>(buf + c0) = make_float4(x[0], x[1], x[2], x[3]);
+        *reinterpret_cast<float4*>(buf + c0 + 4) = make_float4(x[4], x[5], x[6], x[7]);
+      }
+      __syncthreads();
+      fwht_lds(buf, n, m, tid, RP_THREADS, 9);
+    } else if ((n & 7) == 0) {  // 16-byte rows (checked by the API): 8 values per vector load
       for (int64_t c0 = int64_t(tid) * 8; c0 < n; c0 += int64_t(RP_THREADS) * 8) {
         float x[8];
         load8_f32(s + c0, 8, x);
@@ -236,8 +270,10 @@ __global__ __launch_bounds__(RP_THREADS) void row_pass(
         buf[c] = x;
       }
     }
-    __syncthreads();
-    fwht_lds(buf, n, m, tid, RP_THREADS);
+    if (m < 512) {
+      __syncthreads();
+      fwht_lds(buf, n, m, tid, RP_THREADS);
+    }
     if (q28) {
       // output a * m + b = sum_k Q[a][k] buf[k * m + b]: one b per thread, its 28 inputs held in
       // registers, the rows of Q read as 16-byte broadcasts
@@ -284,7 +320,8 @@ __global__ __launch_bounds__(RP_THREADS) void row_pass(
 // Transform along the row axis. Rows are indexed r = hi * (L * n_lo) + a * n_lo + lo; for each
 // (hi, lo) and a strip of CW columns the L rows a = 0..L-1 are transformed:
 //   kind 0: H_L / sqrt(L) (FWHT);  kind 1: the 28-point factor Q (or Q^T), L = 28.
-__global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__ src, int64_t lds_,
+template <int NT>
+__global__ __launch_bounds__(NT) void col_pass(const float* __restrict__ src, int64_t lds_,
                                                        float* __restrict__ dst, int64_t ldd,
                                                        int64_t cols, int64_t L, int64_t n_lo,
                                                        int64_t n_groups, int CW, int kind,
@@ -302,7 +339,7 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
   const int64_t hi = g / n_lo, lo = g % n_lo;
   const int64_t row0 = hi * L * n_lo + lo;  // row of a = 0
   if (kind == 1) {
-    for (int i = tid; i < 28 * 28; i += CP_THREADS) {
+    for (int i = tid; i < 28 * 28; i += NT) {
       const int a = i / 28, b = i % 28;
       qs[i] = q_trans ? q28[b * 28 + a] : q28[i];
     }
@@ -313,11 +350,11 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
   // load the L x CW tile: 8 independent float4 loads in flight per thread before they are
   // stored (one workgroup per CU at L = 1024, so latency must be hidden within the thread)
   const int n_items = int(L) * cw4;
-  for (int it0 = tid; it0 < n_items; it0 += 8 * CP_THREADS) {
+  for (int it0 = tid; it0 < n_items; it0 += 8 * NT) {
     float4 x[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int it = it0 + u * CP_THREADS;
+      const int it = it0 + u * NT;
       x[u] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (it < n_items) {
         const int64_t a = it >> lcw4;
@@ -337,7 +374,7 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int it = it0 + u * CP_THREADS;
+      const int it = it0 + u * NT;
       if (it < n_items)
         *reinterpret_cast<float4*>(tile + (it >> lcw4) * CWP + (it & (cw4 - 1)) * 4) = x[u];
     }
@@ -352,7 +389,7 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
       const int R = left >= 8 ? 8 : (left == 4 ? 4 : 2);
       const int h = 1 << lgh;
       const int items = int(L / R) * CW;
-      for (int it = tid; it < items; it += CP_THREADS) {
+      for (int it = tid; it < items; it += NT) {
         const int q = it >> lcw;
         const int c = it & (CW - 1);
         const int base = (q >> lgh) * (R << lgh) + (q & (h - 1));
@@ -379,7 +416,7 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
       lgh += R == 8 ? 3 : (R == 4 ? 2 : 1);
       __syncthreads();
     }
-    for (int it = tid; it < n_items; it += CP_THREADS) {
+    for (int it = tid; it < n_items; it += NT) {
       const int64_t a = it >> lcw4;
       const int c = (it & (cw4 - 1)) * 4;
       const int64_t gr = row0 + a * n_lo;
@@ -401,7 +438,7 @@ __global__ __launch_bounds__(CP_THREADS) void col_pass(const float* __restrict__
   } else {
     // 28-point mix: out[a][c] = sum_k Q[a][k] tile[k][c]; one column per thread, its 28 inputs
     // in registers, the rows of Q read as 16-byte broadcasts
-    for (int c = tid; c < CW; c += CP_THREADS) {
+    for (int c = tid; c < CW; c += NT) {
       const int64_t gc = c0 + c;
       float x[28];
 #pragma unroll
@@ -446,15 +483,21 @@ int launch_col_step(const float* src, int64_t lds_, float* dst, int64_t ldd, int
                     int64_t cols, int64_t L, int64_t n_lo, int kind, const float* q28,
                     bool q_trans, hipStream_t s) {
   // strips of CW columns: 28-point mix 256 (one column per thread), FWHT 64 up to L = 256
-  // and 32 beyond (L = 1024: 1024 x 36 floats + the 28 x 28 factor = 150 KB of LDS)
+  // and 32 beyond (L = 1024: 1024 x 36 floats + the 28 x 28 factor = 150 KB of LDS, one
+  // workgroup per CU, so beyond L = 256 the workgroup has 1024 threads to keep enough loads in
+  // flight)
   const int CW = kind == 1 ? 256 : (L <= 256 ? 64 : 32);
   const int64_t n_groups = rows / L;
   const int64_t strips = cdiv(cols, CW);
   const size_t shmem = (size_t(L) * (CW + 4) + 28 * 28) * sizeof(float);
   const float norm = kind == 0 ? float(1.0 / std::sqrt(double(L))) : 1.f;
-  return launch(kind == 0 ? "fwht_col" : "mix28_col", col_pass, dim3(unsigned(n_groups * strips)),
-                dim3(CP_THREADS), shmem, s, src, lds_, dst, ldd, cols, L, n_lo, n_groups, CW,
-                kind, q28, int(q_trans), norm);
+  const char* name = kind == 0 ? "fwht_col" : "mix28_col";
+  const dim3 grid(unsigned(n_groups * strips));
+  if (kind == 0 && L > 256)
+    return launch(name, col_pass<1024>, grid, dim3(1024), shmem, s, src, lds_, dst, ldd, cols, L,
+                  n_lo, n_groups, CW, kind, q28, int(q_trans), norm);
+  return launch(name, col_pass<CP_THREADS>, grid, dim3(CP_THREADS), shmem, s, src, lds_, dst, ldd,
+                cols, L, n_lo, n_groups, CW, kind, q28, int(q_trans), norm);
 }
 
 // Full transform of every column (rows axis, length d): T = (Q (x) H_m) / sqrt(m).
