@@ -230,7 +230,9 @@ __device__ __forceinline__ void gram_partial(
 // during the previous half-stage, with the next half-stage's 16 reads issued two per MFMA over
 // its first eight MFMAs. Between the two halves of stage s, one raw s_barrier (after this wave's
 // own loads of stage s + 1 have landed, s_waitcnt vmcnt) both publishes stage s + 1 and frees
-// the buffer of stage s - 1, into which stage s + 3 is then issued. The steady state is unrolled
+// the buffer of stage s - 1. Stage s + 3's loads go out in two parts: its first operand in the
+// second half of stage s (into the buffer just freed), its second operand in the first half of
+// stage s + 1. The steady state is unrolled
 // over the four buffers with every index a constant and no branch, so the compiler places only
 // the waits the data needs; the last few stages run a checked copy of the same schedule.
 // A diagonal tile loads its block into both operand rings so that no buffer is chosen at run
@@ -239,6 +241,7 @@ typedef short v4s_t __attribute__((ext_vector_type(4)));
 #define KQ_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 constexpr int DK = 32;        // tokens per stage
 constexpr int RING = 4;       // stage buffers per operand
+static_assert(RING == 4, "four stage buffers: the steady state is unrolled over them");
 constexpr int PJ = 4;         // tile columns per panel of the tile order
 constexpr int SBUF = 4096;    // dwords per operand per stage
 
@@ -346,16 +349,19 @@ __device__ __forceinline__ void gram_dma(const uint16_t* __restrict__ A,
   }
   const uint16_t* Ai = A + t_begin * lda + int64_t(I) * TT;
   const uint16_t* Aj = (CROSS ? B : A) + t_begin * lda + int64_t(J) * TT;
-  auto issue = [&](int st, int b) {
+  // this wave's 4 loads of one operand (part 0: rows I, part 1: rows J) of stage st
+  auto issue_part = [&](int st, int b, int part) {
     const int64_t so = int64_t(st) * DK * lda;
+    const uint16_t* src = part ? Aj : Ai;
+    uint32_t* dst = part ? bufb[b] : bufa[b];
 #pragma unroll
     for (int k = 0; k < 4; ++k)
-      __builtin_amdgcn_global_load_lds(Ai + so + off[k], KQ_LDS(bufa[b] + (wave * 4 + k) * 256),
-                                       16, 0, 0);
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      __builtin_amdgcn_global_load_lds(Aj + so + off[k], KQ_LDS(bufb[b] + (wave * 4 + k) * 256),
-                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds(src + so + off[k], KQ_LDS(dst + (wave * 4 + k) * 256), 16,
+                                       0, 0);
+  };
+  auto issue = [&](int st, int b) {
+    issue_part(st, b, 0);
+    issue_part(st, b, 1);
   };
   const int wm = wave & 1, wn = wave >> 1;
   f32x16_t acc[4][4];
@@ -378,18 +384,6 @@ __device__ __forceinline__ void gram_dma(const uint16_t* __restrict__ A,
         acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][bi], fb[slot][bj],
                                                               acc[bi][bj], 0, 0, 0);
   };
-  // interleave pattern for one half-stage: 16 (MFMA, DS read) pairs
-  // the next half-stage's 16 operand reads go out two per MFMA over the first 8 MFMAs: a use of
-  // a transposing read's result waits for every outstanding LDS read, so they must all have
-  // landed by the start of the next half-stage
-  auto interleave = [&]() {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // two LDS reads
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-  };
   // this wave's loads of stage s + 1 are done when at most `newer` later stages are pending
   auto wait_newer = [&](int newer) {
     if (newer >= 3) wait_vm<24>();
@@ -397,42 +391,64 @@ __device__ __forceinline__ void gram_dma(const uint16_t* __restrict__ A,
     else if (newer == 1) wait_vm<8>();
     else wait_vm<0>();
   };
+  // steady state: stage s issues the rest of stage s + RING - 2 and the first half of stage
+  // s + RING - 1 unconditionally, no branches inside
+  const int s_main = n_st >= 2 * RING - 1 ? ((n_st - RING + 1) / RING) * RING : 0;
   if (n_st > 0) {
+    if (s_main > 0) {  // stages 0 .. RING - 3, and the first operand of stage RING - 2
 #pragma unroll
-    for (int p = 0; p < RING - 1; ++p)
-      if (p < n_st) issue(p, p);
-    wait_newer(min(RING - 2, n_st - 1));
+      for (int p = 0; p < RING - 2; ++p) issue(p, p);
+      issue_part(RING - 2, RING - 2, 0);
+      wait_vm<(RING - 3) * 8 + 4>();
+    } else {
+#pragma unroll
+      for (int p = 0; p < RING - 1; ++p)
+        if (p < n_st) issue(p, p);
+      wait_newer(min(RING - 2, n_st - 1));
+    }
     __builtin_amdgcn_s_barrier();
     frags(0, 0, 0);
   }
-  // steady state: stage s issues stage s + RING - 1 unconditionally, no branches inside
-  const int s_main = n_st >= 2 * RING - 1 ? ((n_st - RING + 1) / RING) * RING : 0;
-  auto body = [&](auto ucst, int s) {
-    constexpr int u = decltype(ucst)::value;
-    __builtin_amdgcn_sched_barrier(0);
-    frags(u, 1, 1);
-    mfmas(0);
-    interleave();
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vm<(RING - 3) * 8>();
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-    // second half-stage: the operand reads over the first 8 MFMAs, then this wave's 8 loads of
-    // stage s + 3 one per MFMA over the last 8 (a burst of loads right after the barrier, on
-    // top of the reads, measured 5-10% slower)
-    issue(s + RING - 1, (u + RING - 1) % RING);
-    frags((u + 1) % RING, 0, 0);
-    mfmas(1);
+  // Each half-stage: 16 MFMAs; the next half-stage's 16 operand reads two per MFMA over the
+  // first 8 (a use of a transposing read's result waits for every outstanding LDS read, so all
+  // must have landed by the next half-stage); 4 global-to-LDS loads over the last 8, one per two
+  // MFMAs. A stage's 8 loads are
+  // split over two half-stages (all 8 in one burst of 8 MFMAs queued behind each other in the
+  // address unit and held up the MFMAs behind them).
+  auto pattern = [&]() {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // two LDS reads
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < 4; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global-to-LDS load
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
     }
+  };
+  auto body = [&](auto ucst, int s) {
+    constexpr int u = decltype(ucst)::value;
+    __builtin_amdgcn_sched_barrier(0);
+    // first half-stage: the second operand of stage s + 2 (its buffer, that of stage s - 2, has
+    // been free since the barrier of stage s - 1)
+    issue_part(s + RING - 2, (u + RING - 2) % RING, 1);
+    frags(u, 1, 1);
+    mfmas(0);
+    pattern();
+    __builtin_amdgcn_sched_barrier(0);
+    // this wave's loads of stage s + 1 have landed when only those of stages s + 2 ..
+    // s + RING - 2 are newer
+    wait_vm<(RING - 3) * 8>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    // second half-stage: the first operand of stage s + 3 into the buffer of stage s - 1, whose
+    // last reads every wave finished before this barrier
+    issue_part(s + RING - 1, (u + RING - 1) % RING, 0);
+    frags((u + 1) % RING, 0, 0);
+    mfmas(1);
+    pattern();
     __builtin_amdgcn_sched_barrier(0);
   };
   for (int s0 = 0; s0 < s_main; s0 += RING) {
@@ -441,6 +457,9 @@ __device__ __forceinline__ void gram_dma(const uint16_t* __restrict__ A,
     body(std::integral_constant<int, 2>{}, s0 + 2);
     body(std::integral_constant<int, 3>{}, s0 + 3);
   }
+  // the second operand of stage s_main + RING - 2 (< n_st), so that the tail finds whole stages
+  // issued
+  if (s_main > 0) issue_part(s_main + RING - 2, (s_main + RING - 2) % RING, 1);
   // tail (the last few stages), with the bounds checks
   for (int s0 = s_main; s0 < n_st; s0 += RING) {
 #pragma unroll

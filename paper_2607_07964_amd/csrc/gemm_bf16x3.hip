@@ -246,11 +246,14 @@ __global__ __launch_bounds__(256) void gemm3_presplit_sub(
 // Ut_hi[n][k] + Ut_lo[n][k] = sgn U[k][n] (the three-term split of +-U^T), 64 x 64 tiles
 // through LDS: 16-byte loads of U rows, 8-byte stores of four bf16 of a Ut row. U is upper
 // triangular (strictly, for P) and the sweep's products read Ut[n][k] only for k < n, so tiles
-// wholly below that (k0 >= n0 + 64) are not written.
+// wholly below that (k0 >= n0 + 64) are not written. With Fh / Fl (d a multiple of 64) the same
+// values also go to a copy in MFMA-fragment order, the operand layout of the sweep's in-kernel
+// updates.
 __global__ __launch_bounds__(256) void split_transpose(const float* __restrict__ U, int64_t ldu,
                                                        int64_t d, uint16_t* __restrict__ Th,
                                                        uint16_t* __restrict__ Tl, int64_t ldt,
-                                                       float sgn) {
+                                                       float sgn, uint16_t* __restrict__ Fh,
+                                                       uint16_t* __restrict__ Fl) {
   __shared__ float t[64][65];
   const int64_t k0 = int64_t(blockIdx.y) * 64, n0 = int64_t(blockIdx.x) * 64;
   if (k0 >= n0 + 64) return;
@@ -285,8 +288,15 @@ __global__ __launch_bounds__(256) void split_transpose(const float* __restrict__
       lo[e] = bf16_rne(x - bf16_to_f32(hi[e]));
     }
     if (whole) {
-      *reinterpret_cast<uint2*>(Th + n * ldt + k) = make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16));
-      *reinterpret_cast<uint2*>(Tl + n * ldt + k) = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
+      const uint2 h2 = make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16));
+      const uint2 l2 = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
+      *reinterpret_cast<uint2*>(Th + n * ldt + k) = h2;
+      *reinterpret_cast<uint2*>(Tl + n * ldt + k) = l2;
+      if (Fh) {  // the MFMA-fragment copy (see split_frag_index)
+        const int64_t f = split_frag_index(n, k, d / 16);
+        *reinterpret_cast<uint2*>(Fh + f) = h2;
+        *reinterpret_cast<uint2*>(Fl + f) = l2;
+      }
     } else if (n < d) {
 #pragma unroll
       for (int e = 0; e < 4; ++e)
@@ -301,10 +311,12 @@ __global__ __launch_bounds__(256) void split_transpose(const float* __restrict__
 }  // namespace
 
 int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th, uint16_t* Tl,
-                           int64_t ldt, hipStream_t s, bool neg) {
+                           int64_t ldt, hipStream_t s, bool neg, uint16_t* Fh, uint16_t* Fl) {
+  KQ_REQUIRE(!Fh || (Fl && d % 64 == 0), KRONQ_ERR_INVALID_ARG,
+             "split_transpose: the fragment copy needs both planes and d %% 64 == 0");
   const dim3 grid(unsigned(cdiv(d, 64)), unsigned(cdiv(d, 64)));
   return launch(neg ? "obs_split_p" : "obs_split_u", split_transpose, grid, dim3(256), 0, s, U,
-                ldu, d, Th, Tl, ldt, neg ? -1.f : 1.f);
+                ldu, d, Th, Tl, ldt, neg ? -1.f : 1.f, Fh, Fl);
 }
 
 int gemm_bf16x3_presplit_sub(int64_t M, int64_t N, int64_t K, const uint16_t* Ah,

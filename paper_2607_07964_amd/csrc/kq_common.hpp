@@ -189,7 +189,17 @@ int gemm_bf16x3_presplit_sub(int64_t M, int64_t N, int64_t K, const uint16_t* Ah
 // Th + Tl = sign * U^T split into bf16 high and low parts, [d x d] with row stride ldt
 // (sign = -1 when neg)
 int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th, uint16_t* Tl,
-                           int64_t ldt, hipStream_t s, bool neg = false);
+                           int64_t ldt, hipStream_t s, bool neg = false, uint16_t* Fh = nullptr,
+                           uint16_t* Fl = nullptr);
+
+// Position of element (r, k) of a bf16 matrix kept in MFMA-fragment order for the operands of
+// v_mfma_f32_32x32x16_bf16: 32 rows x 16 k form one 1 KB unit in which lane
+// (r % 32) + 32 ((k % 16) / 8) holds its 8 consecutive k, so that a wave's fragment load is
+// one contiguous kilobyte; the units of a 32-row group follow each other along k (ksteps units
+// per group).
+__host__ __device__ inline int64_t split_frag_index(int64_t r, int64_t k, int64_t ksteps) {
+  return (((r >> 5) * ksteps + (k >> 4)) * 64 + (r & 31) + 32 * ((k >> 3) & 1)) * 8 + (k & 7);
+}
 int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
              hipStream_t s, const char* name = "gemm_f32_mfma");

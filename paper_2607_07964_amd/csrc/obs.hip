@@ -52,6 +52,7 @@ __device__ __forceinline__ uint32_t bf16_rne(float x) {
 }
 
 constexpr int OB = 128;          // block (and the smallest group)
+constexpr int LZMAX = 4;         // blocks per lazy group of the P = 0 sweep (at most)
 // Lanes per row of the sweep kernel, a template parameter: 8 (16 columns per lane, 8 rows per
 // wave) or 16 (8 columns per lane, 4 rows per wave). 8 lanes halve the instructions per row,
 // which matters when the rows are many and the sweep is throughput-bound (d_out = 28672, or on
@@ -242,44 +243,68 @@ __global__ __launch_bounds__(256) void obs_group_params(const float* __restrict_
 // W[:, c0 : c0 + OB] still owe sum_k E[row, k] U[kp0 + k, c0 + n] over the kpend columns of the
 // lazy group swept before this block. One 32 x 32 MFMA block per wave (its 32 of the block's
 // 128 columns, rows row0 .. row0 + 31), K in steps of 16, on the bf16 matrix cores with the
-// three-term split: the errors were written split by the sweep (Eph, Epl: [row][k]) and U^T
-// comes split ([n][k]). Operands go straight from global memory (L2) into the MFMA registers
-// (a lane's fragment is 8 contiguous k of one row or one column), a 128-column chunk's worth
-// requested at once. The result lands in dl[row - row0][column].
-__device__ __forceinline__ void pending_update(const uint16_t* __restrict__ Eph,
-                                               const uint16_t* __restrict__ Epl, int64_t ldep,
-                                               const uint16_t* __restrict__ Uth,
-                                               const uint16_t* __restrict__ Utl, int64_t ldut,
+// three-term split: the earlier blocks' errors (Efh, Efl) and U^T (Ufh, Ufl) come split and in
+// MFMA-fragment order (split_frag_index), so that each fragment load of a wave is one contiguous
+// kilobyte (row-major operands cost 32 cache lines per load, which made this step take as long
+// as the column sweep itself). K runs in 64-wide steps whose 16 fragment loads are requested one
+// step ahead of the step's 12 MFMAs, and the three products accumulate separately (three
+// independent MFMA chains, summed at the end). The result lands in dl[row - row0][column].
+constexpr int EKS = LZMAX * OB / 16;  // 16-k units per 32-row group of the errors
+__device__ __forceinline__ void pending_update(const uint16_t* __restrict__ Efh,
+                                               const uint16_t* __restrict__ Efl,
+                                               const uint16_t* __restrict__ Ufh,
+                                               const uint16_t* __restrict__ Ufl, int64_t d_in,
                                                int64_t kp0, int kpend, int64_t c0,
                                                int64_t row0, int64_t d_out, int wave, int lane,
                                                float (*dl)[OB + 4]) {
+  constexpr int KS = 64;  // k per step
   const int l32 = lane & 31, lhi = lane >> 5;
   const int64_t ra = row0 + l32 < d_out ? row0 + l32 : d_out - 1;  // rows past the end: unused
-  const uint16_t* eh = Eph + ra * ldep + 8 * lhi;
-  const uint16_t* el = Epl + ra * ldep + 8 * lhi;
-  const int64_t n = c0 + wave * 32 + l32;
-  const uint16_t* bh = Uth + n * ldut + kp0 + 8 * lhi;
-  const uint16_t* bl = Utl + n * ldut + kp0 + 8 * lhi;
-  f32x16_t acc = {};
-  for (int k0 = 0; k0 < kpend; k0 += OB) {
-    bf16x8_t aha[OB / 16], ala[OB / 16], bha[OB / 16], bla[OB / 16];
+  const int64_t eo = split_frag_index(ra, 8 * lhi, EKS);
+  const uint16_t* eh = Efh + eo;
+  const uint16_t* el = Efl + eo;
+  const int64_t uo = split_frag_index(c0 + wave * 32 + l32, kp0 + 8 * lhi, d_in / 16);
+  const uint16_t* bh = Ufh + uo;
+  const uint16_t* bl = Ufl + uo;
+  f32x16_t hh = {}, lh = {}, hl = {};
+  bf16x8_t f0[4][KS / 16], f1[4][KS / 16];  // [eh, el, uh, ul][k step of 16]
+  auto load = [&](bf16x8_t (&f)[4][KS / 16], int k0) {
 #pragma unroll
-    for (int ks = 0; ks < OB / 16; ++ks) {
-      const int kk = k0 + 16 * ks;
-      aha[ks] = *reinterpret_cast<const bf16x8_t*>(eh + kk);
-      ala[ks] = *reinterpret_cast<const bf16x8_t*>(el + kk);
-      bha[ks] = *reinterpret_cast<const bf16x8_t*>(bh + kk);
-      bla[ks] = *reinterpret_cast<const bf16x8_t*>(bl + kk);
+    for (int ks = 0; ks < KS / 16; ++ks) {
+      const int kk = (k0 + 16 * ks) * 32;  // next 16-k unit: 512 elements on
+      f[0][ks] = *reinterpret_cast<const bf16x8_t*>(eh + kk);
+      f[1][ks] = *reinterpret_cast<const bf16x8_t*>(el + kk);
+      f[2][ks] = *reinterpret_cast<const bf16x8_t*>(bh + kk);
+      f[3][ks] = *reinterpret_cast<const bf16x8_t*>(bl + kk);
     }
+  };
+  auto mfmas = [&](const bf16x8_t (&f)[4][KS / 16]) {
 #pragma unroll
-    for (int ks = 0; ks < OB / 16; ++ks) {
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ala[ks], bha[ks], acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aha[ks], bla[ks], acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aha[ks], bha[ks], acc, 0, 0, 0);
+    for (int ks = 0; ks < KS / 16; ++ks) {
+      lh = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[1][ks], f[2][ks], lh, 0, 0, 0);
+      hl = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[0][ks], f[3][ks], hl, 0, 0, 0);
+      hh = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[0][ks], f[2][ks], hh, 0, 0, 0);
     }
+  };
+  // kpend is a multiple of 128: steps in pairs, the loads of each step one step ahead. The
+  // load after the last pair is issued too (it re-reads the last step, in bounds): a skipped
+  // load would make the wait before the second half's MFMAs a full one on every pair.
+  // (The scheduling barriers keep each step's loads ahead of the other step's MFMAs; left to
+  // itself the compiler interleaves them and each MFMA waits for a load issued just before.)
+  load(f0, 0);
+  for (int k0 = 0; k0 < kpend; k0 += 2 * KS) {
+    load(f1, k0 + KS);
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas(f0);
+    __builtin_amdgcn_sched_barrier(0);
+    load(f0, k0 + 2 * KS < kpend ? k0 + 2 * KS : kpend - KS);
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas(f1);
+    __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
-  for (int r = 0; r < 16; ++r) dl[8 * (r >> 2) + 4 * lhi + (r & 3)][wave * 32 + l32] = acc[r];
+  for (int r = 0; r < 16; ++r)
+    dl[8 * (r >> 2) + 4 * lhi + (r & 3)][wave * 32 + l32] = (lh[r] + hl[r]) + hh[r];
 }
 
 template <bool DRIFT, int L>
@@ -289,9 +314,9 @@ __global__ __launch_bounds__(256) void obs_sweep(
     int64_t ldq, float* __restrict__ scales, float* __restrict__ zeros, int64_t ldsz, int64_t gi,
     int given, float* __restrict__ E, int64_t lde, float* __restrict__ Xq, int64_t ldxq,
     float* __restrict__ W_hat, int64_t ldwh, uint16_t* __restrict__ Eh,
-    uint16_t* __restrict__ El, const uint16_t* __restrict__ Eph,
-    const uint16_t* __restrict__ Epl, int64_t ldes, const uint16_t* __restrict__ Uth,
-    const uint16_t* __restrict__ Utl, int64_t ldut, int64_t kp0, int kpend) {
+    uint16_t* __restrict__ El, int64_t ldes, uint16_t* __restrict__ Efh,
+    uint16_t* __restrict__ Efl, const uint16_t* __restrict__ Ufh,
+    const uint16_t* __restrict__ Ufl, int64_t d_in, int64_t kp0, int kpend) {
   __shared__ __attribute__((aligned(16))) float ub[OB * OB];  // U[c0 + j][c0 + k]
   __shared__ __attribute__((aligned(16))) float pb[DRIFT ? OB * OB : 4];  // P[c0 + j][c0 + k]
   __shared__ float rinv[OB];                                   // 1 / U_jj
@@ -306,13 +331,27 @@ __global__ __launch_bounds__(256) void obs_sweep(
   const bool live = row < d_out;
   const int64_t rr = live ? row : d_out - 1;  // rows past the end recompute the last row
 
-  for (int idx = tid; idx < OB * OB / 4; idx += 256) {
-    const int j = idx / (OB / 4), k4 = (idx % (OB / 4)) * 4;
-    *reinterpret_cast<float4*>(ub + j * OB + k4) =
-        *reinterpret_cast<const float4*>(U + (c0 + j) * ldu + c0 + k4);
-    if (DRIFT)
-      *reinterpret_cast<float4*>(pb + j * OB + k4) =
-          *reinterpret_cast<const float4*>(P + (c0 + j) * ldp + c0 + k4);
+  // the U (and P) block: every load requested before the first store (a load-store pair per
+  // iteration would wait out one memory latency per iteration)
+  {
+    constexpr int NV = OB * OB / 4 / 256;
+    float4 uv[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int idx = tid + 256 * i, j = idx / (OB / 4), k4 = (idx % (OB / 4)) * 4;
+      uv[i] = *reinterpret_cast<const float4*>(U + (c0 + j) * ldu + c0 + k4);
+    }
+#pragma unroll
+    for (int i = 0; i < NV; ++i) reinterpret_cast<float4*>(ub)[tid + 256 * i] = uv[i];
+    if (DRIFT) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int idx = tid + 256 * i, j = idx / (OB / 4), k4 = (idx % (OB / 4)) * 4;
+        uv[i] = *reinterpret_cast<const float4*>(P + (c0 + j) * ldp + c0 + k4);
+      }
+#pragma unroll
+      for (int i = 0; i < NV; ++i) reinterpret_cast<float4*>(pb)[tid + 256 * i] = uv[i];
+    }
   }
   if (tid < OB) rinv[tid] = 1.f / U[(c0 + tid) * ldu + c0 + tid];
   float w[CPL];
@@ -323,8 +362,8 @@ __global__ __launch_bounds__(256) void obs_sweep(
   }
   if constexpr (!DRIFT) {
     if (kpend > 0) {  // uniform over the launch
-      pending_update(Eph, Epl, ldes, Uth, Utl, ldut, kp0, kpend, c0, int64_t(blockIdx.x) * RPG,
-                     d_out, wave, lane, dl);
+      pending_update(Efh, Efl, Ufh, Ufl, d_in, kp0, kpend, c0, int64_t(blockIdx.x) * RPG, d_out,
+                     wave, lane, dl);
       __syncthreads();
       const int rl = wave * RPW + lane / LPR;
 #pragma unroll
@@ -390,6 +429,11 @@ __global__ __launch_bounds__(256) void obs_sweep(
       }
       *reinterpret_cast<uint2*>(Eh + row * ldes + cb + 4 * h) = make_uint2(hi[0], hi[1]);
       *reinterpret_cast<uint2*>(El + row * ldes + cb + 4 * h) = make_uint2(lo[0], lo[1]);
+      // and in fragment order for the in-kernel updates of the later blocks of the lazy group
+      // (column kpend + cb + 4 h of the group; four bf16 never straddle an 8-k fragment)
+      const int64_t f = split_frag_index(row, kpend + cb + 4 * h, EKS);
+      *reinterpret_cast<uint2*>(Efh + f) = make_uint2(hi[0], hi[1]);
+      *reinterpret_cast<uint2*>(Efl + f) = make_uint2(lo[0], lo[1]);
     }
     if (DRIFT)
       *reinterpret_cast<float4*>(Xq + row * ldxq + cb + 4 * h) =
@@ -417,7 +461,6 @@ int lazy_blocks(int64_t d_in, int group) {
 // that block starts a lazy group (then every earlier update has been applied to everything after
 // it). So the lazy group divides the quantisation group (up to LZMAX blocks); a group of one
 // block, or the whole row (parameters from the initial row), allows LZMAX.
-constexpr int LZMAX = 4;
 int lazy_blocks_pending(int64_t d_in, int group) {
   if (group < OB || group % OB != 0 || d_in % group != 0) return 0;
   const int m = group / OB;
@@ -434,8 +477,10 @@ int obs_group_ok(int64_t d_in, int group) { return lazy_blocks(d_in, group); }
 size_t obs_ws_bytes(int64_t d_out, int64_t d_in, bool drift) {
   if (d_out <= 0 || d_in <= 0) return 0;
   const size_t split_u = 2 * align256(size_t(d_in) * size_t(d_in) * sizeof(uint16_t));
-  if (!drift)  // split errors of a lazy group, split U^T
-    return 2 * align256(size_t(d_out) * LZMAX * OB * sizeof(uint16_t)) + split_u + 256;
+  if (!drift)  // split errors of a lazy group and split U^T, row-major and in fragment order
+    return 2 * align256(size_t(d_out) * LZMAX * OB * sizeof(uint16_t)) +
+           2 * align256(size_t(cdiv(d_out, 32) * 32) * LZMAX * OB * sizeof(uint16_t)) +
+           2 * split_u + 256;
   // errors and pre-quantisation values of a lazy group, split U^T and -P^T
   return 2 * (align256(size_t(d_out) * GRP * OB * sizeof(float)) + split_u) + 256;
 }
@@ -465,7 +510,12 @@ int obs_launch_pending(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const
   uint16_t* El = cv.take<uint16_t>(size_t(d_out) * ldes);
   uint16_t* Uth = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
   uint16_t* Utl = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
-  KQ_TRY(split_transpose_launch(U, ldu, d_in, Uth, Utl, d_in, s));
+  // the same two, in MFMA-fragment order, for the sweep's in-kernel updates
+  uint16_t* Efh = cv.take<uint16_t>(size_t(cdiv(d_out, 32) * 32) * ldes);
+  uint16_t* Efl = cv.take<uint16_t>(size_t(cdiv(d_out, 32) * 32) * ldes);
+  uint16_t* Ufh = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
+  uint16_t* Ufl = cv.take<uint16_t>(size_t(d_in) * size_t(d_in));
+  KQ_TRY(split_transpose_launch(U, ldu, d_in, Uth, Utl, d_in, s, false, Ufh, Ufl));
   for (int64_t g0 = 0; g0 < nblk; g0 += lz) {
     const int64_t gend = g0 + lz < nblk ? g0 + lz : nblk;
     for (int64_t b = g0; b < gend; ++b) {
@@ -480,9 +530,8 @@ int obs_launch_pending(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const
                     static_cast<const float*>(nullptr), int64_t(0), c0, bits, codes, d_in,
                     scales, zeros, ldsz, gi, given, err ? err + c0 : static_cast<float*>(nullptr),
                     d_in, static_cast<float*>(nullptr), int64_t(0), W_hat, d_in, Eh + eo, El + eo,
-                    static_cast<const uint16_t*>(Eh), static_cast<const uint16_t*>(El), ldes,
-                    static_cast<const uint16_t*>(Uth), static_cast<const uint16_t*>(Utl), d_in,
-                    g0 * OB, int(eo)));
+                    ldes, Efh, Efl, static_cast<const uint16_t*>(Ufh),
+                    static_cast<const uint16_t*>(Ufl), d_in, g0 * OB, int(eo)));
     }
     const int64_t rem = d_in - gend * OB;  // beyond the lazy group
     if (rem > 0) {
@@ -538,10 +587,9 @@ int obs_launch(float* W, int64_t d_out, int64_t d_in, int64_t ldw, const float* 
       KQ_TRY(launch("obs_sweep", obs_sweep<true, 16>, dim3(grid), dim3(256), 0, s, W, d_out, ldw, U,
                     ldu, P, ldp, c0, bits, codes, d_in, scales, zeros, ldsz, gi, given, Eb, lde,
                     Xb, ldx, W_hat, d_in, static_cast<uint16_t*>(nullptr),
+                    static_cast<uint16_t*>(nullptr), int64_t(0), static_cast<uint16_t*>(nullptr),
                     static_cast<uint16_t*>(nullptr), static_cast<const uint16_t*>(nullptr),
-                    static_cast<const uint16_t*>(nullptr), int64_t(0),
-                    static_cast<const uint16_t*>(nullptr), static_cast<const uint16_t*>(nullptr),
-                    int64_t(0), int64_t(0), 0));
+                    static_cast<const uint16_t*>(nullptr), d_in, int64_t(0), 0));
       const int64_t near = (gend - b - 1) * OB;  // rest of the lazy group
       if (near > 0) {
         // W[:, c0+OB : gend*OB] -= E_b U[c0 : c0+OB, c0+OB : gend*OB] - X_b P[...]

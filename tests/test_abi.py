@@ -40,8 +40,10 @@ def test_version_and_workspace_queries():
     assert K.kronq_workspace_bytes(K.OP_CROSS, 0, 4096, 262144) >= 256 * 256 * 256 * 4
     assert K.kronq_workspace_bytes(K.OP_ROTATE_DRIFT, 0, 4096, 0) >= 4096 * 4
     assert K.kronq_workspace_bytes(K.OP_GPTAQ, 0, 4096, 0) >= 4096 * 4096 * 4
-    assert K.kronq_workspace_bytes(K.OP_OBS_DRIFT, 4096, 4096, 0) > K.kronq_workspace_bytes(
-        K.OP_OBS, 4096, 4096, 0)
+    # split U^T (and -P^T with the drift correction), two bf16 planes each; without the drift
+    # correction U^T is kept row-major and in MFMA-fragment order
+    assert K.kronq_workspace_bytes(K.OP_OBS_DRIFT, 4096, 4096, 0) >= 2 * 2 * 4096 * 4096 * 2
+    assert K.kronq_workspace_bytes(K.OP_OBS, 4096, 4096, 0) >= 2 * 2 * 4096 * 4096 * 2
     assert K.kronq_workspace_bytes(99, 1, 1, 1) == 0
     assert K.kronq_workspace_bytes(K.OP_COV, 0, -1, 10) == 0
 

@@ -67,6 +67,22 @@ def test_cov_bf16(n, d):
     assert np.array_equal(h, h.T)
 
 
+@pytest.mark.parametrize("n", [7 * 1024 + 5, 9192, 10000, 12345, 16391, 20000])
+def test_cov_bf16_stage_counts(n):
+    """One 256-channel tile over 7 to 20 whole 32-token stages per slice (slices and their last
+    one of varied length): the steady state of the stage ring with every remainder of stages
+    left to its checked tail, and the loads of a stage split over two half-stages."""
+    d = 256
+    spec = synth.small_spec(d, d, n, seed=n).x
+    X = synth.gen_matrix(spec, DEV)
+    H = torch.full((d, d), float("nan"), device=DEV)
+    note(f"cov bf16 stage counts n={n} d={d}")
+    K.kronq_accumulate_cov(X, H)
+    torch.cuda.synchronize()
+    ref = O.covariance(oracle_view(synth.gen_matrix(spec)))
+    assert rel_frob(to_np(H), ref) < TOL
+
+
 def test_cov_chained_scaled_and_strided():
     n1, n2, d = 1500, 900, 520
     spec = synth.small_spec(d + 8, d + 8, n1 + n2, seed=5).x
