@@ -714,20 +714,6 @@ struct CovPlan {
   bool tail = false;
 };
 
-// compute units of the current device (cached per device; workgroup rounds are counted in them)
-int device_cus() {
-  static int cache[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
-  if (cache[dev] == 0) {
-    int v = 0;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        v <= 0)
-      v = 256;
-    cache[dev] = v;
-  }
-  return cache[dev];
-}
 
 // Token slices S (split-K). Each interior tile x slice is one workgroup holding a whole CU, so
 // the launch runs in ceil(W / CUs) rounds of equal length for W = tiles * S workgroups; the

@@ -485,14 +485,15 @@ __device__ __forceinline__ void emit_digits8(const float (&v)[8], int j0, uint8_
 }
 
 // ---- one vector, 2- and 4-bit codes: the persistent GEMV -------------------------------------
-// A workgroup first puts the digits of x' in LDS, then walks its row blocks (4 * RPW rows each:
-// blockIdx.x, + gridDim.x, ...) in tiles of 128 lane steps, issuing the code, scale and zero
-// loads of the next tile before the dot products of the current one. Every load is issued
-// unconditionally (indices clamped into range), so the wait for a tile's loads counts exactly
-// the next tile's. With FUSE the workgroup computes x' itself: x and the multipliers are
-// requested before the first tile's codes, so the transform (the Sylvester FWHT of a
-// power-of-two d_in, or the scaling alone) runs while the codes are in flight; it is repeated
-// by every workgroup, which costs less than a separate launch at these sizes.
+// A workgroup requests the codes, scales and zeros of its first two tiles, puts the digits of x'
+// in LDS, then walks its row blocks (4 * RPW rows each: blockIdx.x, + gridDim.x, ...) in tiles
+// of 128 lane steps, two tile buffers in turn: a buffer is refilled with the tile two ahead as
+// soon as its dot products are done. Every load is issued unconditionally (indices clamped into
+// range), so the wait for a tile's loads counts exactly the other buffer's. With FUSE the
+// workgroup computes x' itself: x and the multipliers are requested before the tiles' codes, so
+// the transform (the Sylvester FWHT of a power-of-two d_in, or the scaling alone) runs while the
+// codes are in flight; it is repeated by every workgroup, which costs less than a separate launch
+// at these sizes.
 // 8 consecutive activations as loaded (16-byte loads), widened to fp32 later
 template <typename T>
 struct RawX;
@@ -721,8 +722,19 @@ __global__ __launch_bounds__(256) void online_gemv_p(
       mr[2 * k + 1] = mp[1];
     }
   }
+  // tiles in (row block k, base b) order; next() steps to the following tile, clamped to the
+  // last one (a clamped tile is loaded again and never used)
+  auto next = [&](int& kk, int& bb) {
+    if (++bb == nbase) bb = 0, ++kk;
+    if (kk == nrb) kk = nrb - 1, bb = nbase - 1;
+  };
+  // the first two tiles are requested before the prologue, so that their codes stream in while
+  // x' is formed (the prologue is a few microseconds; one tile alone left HBM idle meanwhile)
+  int k = 0, b = 0, k1 = 0, b1 = 0;
+  next(k1, b1);
   TileRegs<BITS, RPW> A, B;
-  load_tile(A, 0, 0, steps, wave, lane, packed, ldp, scales, zeros, ldsz, spg, d_out);
+  load_tile(A, k, b, steps, wave, lane, packed, ldp, scales, zeros, ldsz, spg, d_out);
+  load_tile(B, k1, b1, steps, wave, lane, packed, ldp, scales, zeros, ldsz, spg, d_out);
   if constexpr (FUSE) {
     // the butterflies of strides 1, 2, 4 on each thread's 8 consecutive values, in registers;
     // the other stages in LDS; then the digits, a quad of lanes per 32-column chunk
@@ -767,31 +779,26 @@ __global__ __launch_bounds__(256) void online_gemv_p(
   float acc[RPW];
 #pragma unroll
   for (int r = 0; r < RPW; ++r) acc[r] = 0.f;
-  // tiles in (row block k, base b) order; (k1, b1) is the tile after (k, b), clamped to the last
-  int k = 0, b = 0;
-  auto next = [&](int& kk, int& bb) {
-    if (++bb == nbase) bb = 0, ++kk;
-    if (kk == nrb) kk = nrb - 1, bb = nbase - 1;
-  };
+  // A holds tile (k, b), B the tile after it, (k1, b1); a buffer is refilled with the tile two
+  // ahead as soon as its dot products are done
   for (;;) {
-    int k1 = k, b1 = b;
-    next(k1, b1);
-    load_tile(B, k1, b1, steps, wave, lane, packed, ldp, scales, zeros, ldsz, spg, d_out);
     tile_dots(A, b, steps, lane, sd, se, ss, acc);
     if (b == nbase - 1) flush_rows(acc, k, wave, lane, d_out, yr);
     if (k == nrb - 1 && b == nbase - 1) break;
-    k = k1, b = b1;
+    int k2 = k1, b2 = b1;
+    next(k2, b2);
+    load_tile(A, k2, b2, steps, wave, lane, packed, ldp, scales, zeros, ldsz, spg, d_out);
+    tile_dots(B, b1, steps, lane, sd, se, ss, acc);
+    if (b1 == nbase - 1) flush_rows(acc, k1, wave, lane, d_out, yr);
+    if (k1 == nrb - 1 && b1 == nbase - 1) break;
+    k = k2, b = b2, k1 = k2, b1 = b2;
     next(k1, b1);
-    load_tile(A, k1, b1, steps, wave, lane, packed, ldp, scales, zeros, ldsz, spg, d_out);
-    tile_dots(B, b, steps, lane, sd, se, ss, acc);
-    if (b == nbase - 1) flush_rows(acc, k, wave, lane, d_out, yr);
-    if (k == nrb - 1 && b == nbase - 1) break;
-    k = k1, b = b1;
+    load_tile(B, k1, b1, steps, wave, lane, packed, ldp, scales, zeros, ldsz, spg, d_out);
   }
 }
 
-// the persistent GEMV for one vector: row blocks of 4 * RPW rows dealt to about two workgroups
-// per CU (fewer where the LDS holds less), in equal shares
+// the persistent GEMV for one vector: row blocks of 4 * RPW rows dealt to two workgroups per
+// CU (one where the LDS holds less)
 template <int BITS>
 int gemv_pers(bool fuse, const uint32_t* packed, int64_t ldp, const float* scales,
               const float* zeros, int64_t ldsz, int group, int64_t d_out, int64_t d_in,
@@ -802,8 +809,12 @@ int gemv_pers(bool fuse, const uint32_t* packed, int64_t ldp, const float* scale
   const size_t lds = size_t(nch) * (96 + 8) + (fuse ? size_t(d_in + d_in / 32) * 4 : 0);
   const int64_t per_cu = lds <= 64 * 1024 ? 2 : 1;
   const int64_t nblk = cdiv(d_out, 4 * RPW);
-  const int64_t iters = cdiv(nblk, 256 * per_cu);
-  const dim3 grid(static_cast<unsigned>(cdiv(nblk, iters)));
+  // one workgroup per slot: workgroup w takes row blocks w, w + grid, ..., so the two that share
+  // a CU (w and w + CUs, dispatched in the second round) hold together an equal share; a grid
+  // of nblk / 4 workgroups left a quarter of the CUs with one workgroup and the rest with two,
+  // whose later end set the kernel's time
+  const int64_t slots = int64_t(device_cus()) * per_cu;
+  const dim3 grid(static_cast<unsigned>(nblk < slots ? nblk : slots));
   const float norm = rotate ? float(1.0 / std::sqrt(double(d_in))) : 1.f;
   const uint32_t* dg = reinterpret_cast<const uint32_t*>(dig);
   if (!fuse)
