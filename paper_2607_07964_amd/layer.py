@@ -214,11 +214,11 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
     S_G needs only diag(H_G), which one read of G gives (kronq_cov_diag), so W is rescaled and
     rotated without waiting for the H_G covariance, and the sweep never waits for it either.
     With ``overlap`` diag(H_G) and H_X come first, then the work is split over two streams: the
-    current stream rotates H_X, factors it and runs the sweep; the second stream transforms W
-    as soon as S_X exists, then takes (the drift statistic and) the H_G covariance on
-    ``cov_cus`` CUs (None: the policy of _cov_cus; 0: no cap), whose traces and rotation end
-    the layer. The current stream waits for the second at the end. Both schedules
-    give bit-identical results."""
+    current stream rotates H_X, transforms W, factors H_X and runs the sweep; the second stream
+    takes (the drift statistic and) the H_G covariance on ``cov_cus`` CUs (None: the policy of
+    _cov_cus; 0: no cap) as soon as S_X exists, whose traces and rotation end the layer. The
+    current stream waits for the second at the end. Both schedules give bit-identical
+    results."""
     drift = dX is not None
     if drift and st.D is None:
         raise ValueError("the drift correction needs LayerState.allocate(..., drift=True)")
@@ -250,9 +250,6 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
     # is dispatched as soon as S_X exists rather than after the host has issued them
     with torch.cuda.stream(st.side):
         st.side.wait_event(ev_sx)
-        K.kronq_rotate(W0, st.W, None, st.hgd, rin.sign, rout.sign, rin.q28, rout.q28, st.sx,
-                       st.sg, flags | K.SX_GIVEN | K.HG_DIAG, st.ws_rot)
-        ev_w.record(st.side)
         if drift:  # the drift statistic first: the correction P waits for it
             drift_statistic(st, dX, X)
             ev_d.record(st.side)
@@ -260,6 +257,15 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
         # latency-bound kernels (a covariance workgroup holds its CU for a whole tile)
         K.kronq_accumulate_cov_limited(G, st.HG, cov_cus, 1.0, 0.0, st.ws_cov_g)
         K.kronq_traces(None, st.HG, st.tr_pre)
+    # W's transform on this stream, beside the H_G covariance: the covariance, which ends the
+    # layer, starts as soon as S_X exists
+    K.kronq_rotate(W0, st.W, None, st.hgd, rin.sign, rout.sign, rin.q28, rout.q28, st.sx,
+                   st.sg, flags | K.SX_GIVEN | K.HG_DIAG, st.ws_rot)
+    ev_w.record(main)
+    with torch.cuda.stream(st.side):
+        # the H_G transform uses S_G from W's transform, and the same rotation workspace (the
+        # event is recorded above, before this wait is enqueued)
+        st.side.wait_event(ev_w)
         K.kronq_rotate(None, None, None, st.HG, rin.sign, rout.sign, rin.q28, rout.q28, st.sx,
                        st.sg, flags | K.SX_GIVEN | K.SG_GIVEN, st.ws_rot)
         K.kronq_traces(None, st.HG, st.tr_post)
@@ -269,7 +275,6 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
         main.wait_event(ev_d)
         drift_biip(st, rin, flags)
         K.kronq_gptaq_correction(st.D, st.U, st.P, alpha, st.ws_gptaq)
-    main.wait_event(ev_w)
     if drift:
         K.kronq_obs_quantize_layer_drift(st.W, st.U, st.P, bits, st.codes, st.scales, st.zeros,
                                          st.err, None, group=st.group, ws=st.ws_obs)
