@@ -216,7 +216,7 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
     With ``overlap`` diag(H_G) and H_X come first, then the work is split over two streams: the
     current stream rotates H_X, transforms W, factors H_X and runs the sweep; the second stream
     takes (the drift statistic and) the H_G covariance on ``cov_cus`` CUs (None: the policy of
-    _cov_cus; 0: no cap) as soon as S_X exists, whose traces and rotation end the layer. The
+    _cov_cus; 0: no cap) as soon as H_X is formed, whose traces and rotation end the layer. The
     current stream waits for the second at the end. Both schedules give bit-identical
     results."""
     drift = dX is not None
@@ -241,13 +241,12 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
     K.kronq_cov_diag(G, st.hgd, st.ws_diag)
     if not skip_x:
         K.kronq_accumulate_cov(X, st.HX, 1.0, 0.0, st.ws_cov_x)
+    # (before the side stream starts: the traces kernel rewrites all three slots)
     K.kronq_traces(st.HX, None, st.tr_pre)
-    K.kronq_rotate(W0, None, st.HX, None, rin.sign, None, rin.q28, None, st.sx, st.sg,
-                   flags | K.HX_ONLY, st.ws_rot)
-    K.kronq_traces(st.HX, None, st.tr_post)
+    # the side stream starts once H_X is formed (it needs nothing of H_X): its work is
+    # enqueued before the factorisation's ~160 launches, so that it is dispatched right away
+    # rather than after the host has issued them
     ev_sx.record(main)
-    # the side stream's work is enqueued before the factorisation's ~160 launches, so that it
-    # is dispatched as soon as S_X exists rather than after the host has issued them
     with torch.cuda.stream(st.side):
         st.side.wait_event(ev_sx)
         if drift:  # the drift statistic first: the correction P waits for it
@@ -257,8 +256,10 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
         # latency-bound kernels (a covariance workgroup holds its CU for a whole tile)
         K.kronq_accumulate_cov_limited(G, st.HG, cov_cus, 1.0, 0.0, st.ws_cov_g)
         K.kronq_traces(None, st.HG, st.tr_pre)
-    # W's transform on this stream, beside the H_G covariance: the covariance, which ends the
-    # layer, starts as soon as S_X exists
+    K.kronq_rotate(W0, None, st.HX, None, rin.sign, None, rin.q28, None, st.sx, st.sg,
+                   flags | K.HX_ONLY, st.ws_rot)
+    K.kronq_traces(st.HX, None, st.tr_post)
+    # W's transform on this stream, beside the H_G covariance, which ends the layer
     K.kronq_rotate(W0, st.W, None, st.hgd, rin.sign, rout.sign, rin.q28, rout.q28, st.sx,
                    st.sg, flags | K.SX_GIVEN | K.HG_DIAG, st.ws_rot)
     ev_w.record(main)
