@@ -24,7 +24,7 @@ FLAGS = [
     # no packed fp32 instructions anywhere (v_pk_fma_f32 and friends)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
-SOURCES = ["kq_runtime.cpp", "kronq_api.cpp", "cov.hip", "gemm_f32.hip", "gemm_bf16x3.hip", "rotate.hip",
+SOURCES = ["kq_runtime.cpp", "kronq_api.cpp", "cov.hip", "gemm_f32.hip", "gemm_bf16x3.hip", "gemm_bf16x6.hip", "rotate.hip",
            "chol.hip", "obs.hip", "gptaq.hip", "online.hip", "diag.hip", "loss.hip", "cov_diag.hip", "peaks.hip"]
 
 

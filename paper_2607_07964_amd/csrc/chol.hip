@@ -335,6 +335,27 @@ int64_t chol_scratch(int64_t n) {
   return std::max(chol_scratch(h), r * h + chol_scratch(r));
 }
 
+// Products of at least this many multiply-adds run on the bf16 matrix cores with the six-term
+// split (gemm_f32_split6, as accurate as fp32): the 3584-order and larger products of the top
+// levels of an 8192 or larger factorisation. Below that (2048-order products and smaller, too
+// few 256 x 128 tiles to fill the chip) the fp32 kernels are faster.
+constexpr double SPLIT6_MIN = 3000.0 * 3000.0 * 3000.0;
+
+bool use_split6(int flags, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                const float* B, int64_t ldb) {
+  return double(M) * double(N) * double(K) >= SPLIT6_MIN &&
+         gemm_split6_supports(flags, M, N, K, A, lda, B, ldb);
+}
+
+// one product of the recursion: the split path when it is large enough, else the fp32 kernels
+int chol_gemm(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
+              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
+              hipStream_t s, const char* name) {
+  if (use_split6(flags, M, N, K, A, lda, B, ldb))
+    return gemm_f32_split6(flags, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, s, name);
+  return gemm_f32(flags, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, s, name);
+}
+
 // L and L^-1 of the block [n0, n0 + n) of M; the lower part of the same block of X receives
 // L^-1 (zeros on the upper part of the diagonal leaves). T is scratch of tcap floats (at least
 // chol_scratch(n)).
@@ -352,16 +373,24 @@ int chol_rec(float* M, float* X, float* T, int64_t tcap, int64_t ld, int64_t n0,
   float* X22 = X + (n0 + h) * ld + n0 + h;
   float* M22 = M + (n0 + h) * ld + n0 + h;
   // L21 = M21 X11^T (op(B) = X11^T is upper triangular)
-  KQ_TRY(gemm_f32(GEMM_TB | GEMM_OPB_UPPER, r, h, h, 1.f, M21, ld, X11, ld, 0.f, X21, ld, s,
-                  "chol_trsm"));
-  // in one launch (both need only L21 and X11): M22 -= L21 L21^T (lower tiles only) and
-  // T = L21 X11 (X11 lower triangular)
+  KQ_TRY(chol_gemm(GEMM_TB | GEMM_OPB_UPPER, r, h, h, 1.f, M21, ld, X11, ld, 0.f, X21, ld, s,
+                   "chol_trsm"));
+  // M22 -= L21 L21^T (lower tiles only) and T = L21 X11 (X11 lower triangular); small ones in
+  // one launch (both need only L21 and X11)
   const GemmProb syrk{GEMM_TB | GEMM_LOWER_C, r, r, h, -1.f, X21, ld, X21, ld, 1.f, M22, ld};
   const GemmProb row{GEMM_B_LOWER, r, h, h, 1.f, X21, ld, X11, ld, 0.f, T, h};
-  KQ_TRY(gemm_f32_dual(syrk, row, s, "chol_syrk_trtri_row"));
+  if (use_split6(syrk.flags, r, r, h, X21, ld, X21, ld) &&
+      use_split6(row.flags, r, h, h, X21, ld, X11, ld)) {
+    KQ_TRY(gemm_f32_split6(syrk.flags, r, r, h, -1.f, X21, ld, X21, ld, 1.f, M22, ld, s,
+                           "chol_syrk"));
+    KQ_TRY(gemm_f32_split6(row.flags, r, h, h, 1.f, X21, ld, X11, ld, 0.f, T, h, s,
+                           "chol_trtri_row"));
+  } else {
+    KQ_TRY(gemm_f32_dual(syrk, row, s, "chol_syrk_trtri_row"));
+  }
   KQ_TRY(chol_rec(M, X, T + r * h, tcap - r * h, ld, n0 + h, r, d, info, s));
   // X21 = -X22 T
-  return gemm_f32(GEMM_A_LOWER, r, h, r, -1.f, X22, ld, T, h, 0.f, X21, ld, s, "trtri_update");
+  return chol_gemm(GEMM_A_LOWER, r, h, r, -1.f, X22, ld, T, h, 0.f, X21, ld, s, "trtri_update");
 }
 
 }  // namespace

@@ -215,6 +215,14 @@ int split_transpose_launch(const float* U, int64_t ldu, int64_t d, uint16_t* Th,
 __host__ __device__ inline int64_t split_frag_index(int64_t r, int64_t k, int64_t ksteps) {
   return (((r >> 5) * ksteps + (k >> 4)) * 64 + (r & 31) + 32 * ((k >> 3) & 1)) * 8 + (k & 7);
 }
+// fp32-accurate C = alpha op(A) op(B) + beta C on the bf16 matrix cores (six-term split; the
+// large products of the factorisation). Supported: not GEMM_TA, GEMM_UPPER_C or GEMM_A_UPPER;
+// K, lda, ldb (and N when B is stored [K][N]) multiples of 4; A and B 16-byte aligned.
+bool gemm_split6_supports(int flags, int64_t M, int64_t N, int64_t K, const float* A,
+                          int64_t lda, const float* B, int64_t ldb);
+int gemm_f32_split6(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
+                    int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
+                    hipStream_t s, const char* name);
 int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
              hipStream_t s, const char* name = "gemm_f32_mfma");
