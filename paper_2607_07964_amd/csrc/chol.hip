@@ -375,16 +375,15 @@ int chol_rec(float* M, float* X, float* T, int64_t tcap, int64_t ld, int64_t n0,
   // L21 = M21 X11^T (op(B) = X11^T is upper triangular)
   KQ_TRY(chol_gemm(GEMM_TB | GEMM_OPB_UPPER, r, h, h, 1.f, M21, ld, X11, ld, 0.f, X21, ld, s,
                    "chol_trsm"));
-  // M22 -= L21 L21^T (lower tiles only) and T = L21 X11 (X11 lower triangular); small ones in
-  // one launch (both need only L21 and X11)
+  // M22 -= L21 L21^T (lower tiles only) and T = L21 X11 (X11 lower triangular), in one launch
+  // (both need only L21 and X11)
   const GemmProb syrk{GEMM_TB | GEMM_LOWER_C, r, r, h, -1.f, X21, ld, X21, ld, 1.f, M22, ld};
   const GemmProb row{GEMM_B_LOWER, r, h, h, 1.f, X21, ld, X11, ld, 0.f, T, h};
   if (use_split6(syrk.flags, r, r, h, X21, ld, X21, ld) &&
       use_split6(row.flags, r, h, h, X21, ld, X11, ld)) {
-    KQ_TRY(gemm_f32_split6(syrk.flags, r, r, h, -1.f, X21, ld, X21, ld, 1.f, M22, ld, s,
-                           "chol_syrk"));
-    KQ_TRY(gemm_f32_split6(row.flags, r, h, h, 1.f, X21, ld, X11, ld, 0.f, T, h, s,
-                           "chol_trtri_row"));
+    // the syrk's tiles (all of full K) first, the row product's (K ranges of every length)
+    // after them, filling the last round of workgroups
+    KQ_TRY(gemm_f32_split6_dual(syrk, row, s, "chol_syrk_trtri_row"));
   } else {
     KQ_TRY(gemm_f32_dual(syrk, row, s, "chol_syrk_trtri_row"));
   }

@@ -16,11 +16,11 @@
 //     LDS rows of 64 bytes (m- or n-major planes) are read with ds_read_b128 under an XOR
 //     swizzle of their 16-byte chunks; a k-major op(B) (B stored [K][N]) is kept k-major in LDS
 //     and read with the transposing ds_read_b64_tr_b16.
-//   * Tile order: on large grids the tiles go out in patches of 4 x 8 tiles (1024 x 1024
-//     outputs), one patch per XCD at a time (workgroups are dealt to the 8 XCDs round-robin), so
-//     that the 32 workgroups an XCD runs together share their A rows and B columns in its L2.
+//   * Tile order: row-major, or whole tile columns per XCD in a paired order that balances
+//     triangular work over the 8 XCDs, whichever leaves the busiest XCD the least work.
 //   * Triangular structure limits each tile's K range (GEMM_B_LOWER, GEMM_OPB_UPPER,
 //     GEMM_A_LOWER) or skips the tile (GEMM_LOWER_C), as in the fp32 kernels.
+#include <algorithm>
 #include <type_traits>
 
 #include "kq_common.hpp"
@@ -40,7 +40,6 @@ constexpr int BK = 32;   // K per stage
 constexpr int PA = TM * BK;              // bf16 per A plane per stage
 constexpr int PB = TN * BK;              // bf16 per B plane per stage
 constexpr int STAGE = 3 * (PA + PB);     // bf16 per stage (73,728 bytes)
-constexpr int PATCH_MIN_TILES = 512;     // grids at least this large use the patch order
 constexpr int NT = 512;                  // threads: 8 waves, two per SIMD
 constexpr int NWM = 4, NWN = 2;          // waves along M and N
 constexpr int WTM = TM / NWM, WTN = TN / NWN;  // wave tile: 64 x 64
@@ -96,24 +95,42 @@ __device__ __forceinline__ int clamp_idx(int64_t v) {
 template <int V>
 using ic = std::integral_constant<int, V>;
 
+// one product as the kernel sees it, with its tile grid
+struct Job {
+  int flags;
+  int64_t M, N, K;
+  float alpha;
+  const float* A;
+  int64_t lda;
+  const float* B;
+  int64_t ldb;
+  float beta;
+  float* C;
+  int64_t ldc;
+  int nt_m, nt_n;  // tiles along M and N
+  int vc;          // column order: virtual tile columns per XCD (0: row-major tile order)
+  int blocks;      // workgroups of the launch
+};
+
+// tile b of product J (all workgroup-uniform but the thread index)
 template <bool KMAJ>  // op(B) stored [K][N] (k-major) rather than [N][K]
-__global__ __launch_bounds__(NT) void gemm6(int flags, int64_t M, int64_t N, int64_t K,
-                                             float alpha, const float* __restrict__ A,
-                                             int64_t lda, const float* __restrict__ B,
-                                             int64_t ldb, float beta, float* __restrict__ C,
-                                             int64_t ldc, int nt_m, int nt_n, int npn, int np) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+__device__ __forceinline__ void gemm6_tile(const Job& J, int b, uint16_t* lds) {
+  const int flags = J.flags;
+  const int64_t M = J.M, N = J.N, K = J.K, lda = J.lda, ldb = J.ldb, ldc = J.ldc;
+  const float* __restrict__ A = J.A;
+  const float* __restrict__ B = J.B;
+  float* __restrict__ C = J.C;
+  const float alpha = J.alpha, beta = J.beta;
+  const int nt_m = J.nt_m, nt_n = J.nt_n, vc = J.vc;
   const int tid = threadIdx.x;
   int tm, tn;
-  if (npn > 0) {  // patch order: patch p = 8 (s / 32) + XCD, tile q = s % 32 of it
-    const int x = int(blockIdx.x) & 7, s = int(blockIdx.x) >> 3;
-    const int p = (s >> 5) * 8 + x, q = s & 31;
-    if (p >= np) return;
-    tm = (p / npn) * 4 + (q >> 3);
-    tn = (p % npn) * 8 + (q & 7);
+  if (vc > 0) {  // column order: XCD x = b % 8 owns columns x, 15 - x, 16 + x, 31 - x, ...
+    const int x = b & 7, s = b >> 3, j = s % vc;
+    tm = s / vc;
+    tn = 16 * (j >> 1) + ((j & 1) ? 15 - x : x);
   } else {
-    tm = int(blockIdx.x) / nt_n;
-    tn = int(blockIdx.x) % nt_n;
+    tm = b / nt_n;
+    tn = b % nt_n;
   }
   if (tm >= nt_m || tn >= nt_n) return;
   const int64_t m0 = int64_t(tm) * TM, n0 = int64_t(tn) * TN;
@@ -364,6 +381,66 @@ __global__ __launch_bounds__(NT) void gemm6(int flags, int64_t M, int64_t N, int
       }
 }
 
+template <bool KMAJ>
+__global__ __launch_bounds__(NT) void gemm6(Job J) {
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+  gemm6_tile<KMAJ>(J, int(blockIdx.x), lds);
+}
+
+// two independent products in one launch: the first product's workgroups come first
+template <bool KMAJ0, bool KMAJ1>
+__global__ __launch_bounds__(NT) void gemm6_dual(Job J0, Job J1) {
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+  const int b = int(blockIdx.x);
+  if (b < J0.blocks)
+    gemm6_tile<KMAJ0>(J0, b, lds);
+  else
+    gemm6_tile<KMAJ1>(J1, b - J0.blocks, lds);
+}
+
+// K stages of tile (tm, tn), as the kernel bounds them (-1: tile skipped)
+int tile_stages(const GemmProb& p, int tm, int tn) {
+  const int64_t m0 = int64_t(tm) * TM, n0 = int64_t(tn) * TN;
+  if ((p.flags & GEMM_LOWER_C) && m0 + TM <= n0) return -1;
+  int64_t kbeg = 0, kend = p.K;
+  if ((p.flags & GEMM_B_LOWER) && n0 > kbeg) kbeg = n0;
+  if ((p.flags & GEMM_A_LOWER) && m0 + TM < kend) kend = m0 + TM;
+  if ((p.flags & GEMM_OPB_UPPER) && n0 + TN < kend) kend = n0 + TN;
+  return kend > kbeg ? int((kend - kbeg + BK - 1) / BK) : 0;
+}
+
+// Tile order. Workgroups go to the 8 XCDs round-robin, one at a time per CU here (the LDS
+// stages fill it). Row-major order gives XCD x every 8th tile; the column order gives XCD x
+// whole tile columns x, 15 - x, 16 + x, ... walked row by row, so that the 32 tiles an XCD runs
+// together share a few A row blocks and its B column blocks in its L2, and, pairing column
+// c with 15 - c, evens out work that grows or shrinks along N (triangular K ranges, the lower
+// triangle of GEMM_LOWER_C). The launch takes the order whose busiest XCD has the least work
+// (in K stages, plus a few a tile for its prologue and epilogue).
+Job make_job(const GemmProb& p) {
+  Job j{p.flags, p.M, p.N, p.K, p.alpha, p.A, p.lda, p.B, p.ldb, p.beta, p.C, p.ldc,
+        int(cdiv(p.M, TM)), int(cdiv(p.N, TN)), 0, 0};
+  constexpr int64_t TILE_COST = 4;
+  int64_t row_major[8] = {}, col_order[8] = {};
+  const int vc = int(cdiv(j.nt_n, 8));
+  for (int tm = 0; tm < j.nt_m; ++tm)
+    for (int tn = 0; tn < j.nt_n; ++tn) {
+      const int st = tile_stages(p, tm, tn);
+      if (st < 0) continue;
+      row_major[(int64_t(tm) * j.nt_n + tn) % 8] += st + TILE_COST;
+      // column tn belongs to XCD tn % 16 (< 8) or 15 - tn % 16
+      const int c16 = tn % 16;
+      col_order[c16 < 8 ? c16 : 15 - c16] += st + TILE_COST;
+    }
+  const int64_t rm = *std::max_element(row_major, row_major + 8);
+  const int64_t co = *std::max_element(col_order, col_order + 8);
+  j.blocks = j.nt_m * j.nt_n;
+  if (co < rm) {
+    j.vc = vc;
+    j.blocks = 8 * j.nt_m * vc;
+  }
+  return j;
+}
+
 }  // namespace
 
 bool gemm_split6_supports(int flags, int64_t M, int64_t N, int64_t K, const float* A,
@@ -378,26 +455,38 @@ bool gemm_split6_supports(int flags, int64_t M, int64_t N, int64_t K, const floa
   return (flags & GEMM_TB) || N % 4 == 0;
 }
 
+bool split6_ok(const GemmProb& p) {
+  return gemm_split6_supports(p.flags, p.M, p.N, p.K, p.A, p.lda, p.B, p.ldb);
+}
+
 int gemm_f32_split6(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
                     int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
                     hipStream_t s, const char* name) {
   if (M <= 0 || N <= 0) return KRONQ_OK;
-  KQ_REQUIRE(gemm_split6_supports(flags, M, N, K, A, lda, B, ldb), KRONQ_ERR_UNSUPPORTED,
+  const GemmProb p{flags, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc};
+  KQ_REQUIRE(split6_ok(p), KRONQ_ERR_UNSUPPORTED,
              "gemm_f32_split6: flags %d, shape %lld x %lld x %lld or alignment not supported",
              flags, (long long)M, (long long)N, (long long)K);
-  const int nt_m = int(cdiv(M, TM)), nt_n = int(cdiv(N, TN));
-  int npn = 0, np = 0;
-  unsigned blocks = unsigned(nt_m) * unsigned(nt_n);
-  if (int64_t(nt_m) * nt_n >= PATCH_MIN_TILES) {
-    npn = int(cdiv(nt_n, 8));
-    np = int(cdiv(nt_m, 4)) * npn;
-    blocks = unsigned(cdiv(np, 8)) * 256u;
-  }
+  const Job j = make_job(p);
   if (flags & GEMM_TB)
-    return launch(name, gemm6<false>, dim3(blocks), dim3(NT), 0, s, flags, M, N, K, alpha, A,
-                  lda, B, ldb, beta, C, ldc, nt_m, nt_n, npn, np);
-  return launch(name, gemm6<true>, dim3(blocks), dim3(NT), 0, s, flags, M, N, K, alpha, A, lda,
-                B, ldb, beta, C, ldc, nt_m, nt_n, npn, np);
+    return launch(name, gemm6<false>, dim3(unsigned(j.blocks)), dim3(NT), 0, s, j);
+  return launch(name, gemm6<true>, dim3(unsigned(j.blocks)), dim3(NT), 0, s, j);
+}
+
+int gemm_f32_split6_dual(const GemmProb& p0, const GemmProb& p1, hipStream_t s,
+                         const char* name) {
+  KQ_REQUIRE(p0.M > 0 && p0.N > 0 && p1.M > 0 && p1.N > 0 && split6_ok(p0) && split6_ok(p1),
+             KRONQ_ERR_UNSUPPORTED, "gemm_f32_split6_dual: products not supported");
+  Job j0 = make_job(p0);
+  const Job j1 = make_job(p1);
+  // the second product's XCD assignment assumes its first workgroup lands on XCD 0
+  if (j1.vc > 0) j0.blocks = int(cdiv(j0.blocks, 8)) * 8;
+  const dim3 grid(unsigned(j0.blocks + j1.blocks));
+  const bool t0 = p0.flags & GEMM_TB, t1 = p1.flags & GEMM_TB;
+  if (t0 && t1) return launch(name, gemm6_dual<false, false>, grid, dim3(NT), 0, s, j0, j1);
+  if (t0) return launch(name, gemm6_dual<false, true>, grid, dim3(NT), 0, s, j0, j1);
+  if (t1) return launch(name, gemm6_dual<true, false>, grid, dim3(NT), 0, s, j0, j1);
+  return launch(name, gemm6_dual<true, true>, grid, dim3(NT), 0, s, j0, j1);
 }
 
 }  // namespace kq

@@ -220,9 +220,6 @@ __host__ __device__ inline int64_t split_frag_index(int64_t r, int64_t k, int64_
 // K, lda, ldb (and N when B is stored [K][N]) multiples of 4; A and B 16-byte aligned.
 bool gemm_split6_supports(int flags, int64_t M, int64_t N, int64_t K, const float* A,
                           int64_t lda, const float* B, int64_t ldb);
-int gemm_f32_split6(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
-                    int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
-                    hipStream_t s, const char* name);
 int gemm_f32(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
              int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
              hipStream_t s, const char* name = "gemm_f32_mfma");
@@ -242,6 +239,13 @@ struct GemmProb {
 // two independent products in one launch (small-tile kernel; the outputs must not overlap
 // each other or the inputs)
 int gemm_f32_dual(const GemmProb& p1, const GemmProb& p2, hipStream_t s, const char* name);
+int gemm_f32_split6(int flags, int64_t M, int64_t N, int64_t K, float alpha, const float* A,
+                    int64_t lda, const float* B, int64_t ldb, float beta, float* C, int64_t ldc,
+                    hipStream_t s, const char* name);
+// two independent products of the split path in one launch (the outputs must not overlap);
+// the first product's workgroups are dispatched first
+int gemm_f32_split6_dual(const GemmProb& p0, const GemmProb& p1, hipStream_t s,
+                         const char* name);
 // Cholesky inverse factor
 size_t chol_ws_bytes(int64_t d);
 int chol_launch(float* H, int64_t d, int64_t ldh, float damp_rel, float* U, int64_t ldu,
