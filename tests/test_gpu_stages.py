@@ -225,6 +225,51 @@ def test_rotate_forward(d_out, d_in, flags):
     np.testing.assert_allclose(to_np(sg), ref["sg"], rtol=1e-5)
 
 
+@pytest.mark.parametrize("d_out", [16384, 28 * 1024])
+def test_rotate_long_rows_sampled(d_out):
+    """Output sides of 16384 and 28 * 1024: their row passes hold one workgroup per CU, each
+    walking its rows (64 and 112) with the next row prefetched into registers. H from 64 tokens,
+    so that an entry of U S^-1 H_G S^-1 U^T is a dot product of two rotated token rows (the
+    oracle's rotated rows, as in the full-size sampled test); sampled entries of the rotated W."""
+    d_in, ntok = 256, 64
+    s = synth.small_spec(d_out, d_in, ntok, seed=5, name="long_rows")
+    ax = O.as_f64(oracle_view(synth.gen_matrix(s.x)))
+    ag = O.as_f64(oracle_view(synth.gen_matrix(s.g)))
+    W = synth.gen_matrix(s.w)
+    ri = synth.rotation_params(d_in, 5, "long_rows:in")
+    ro = synth.rotation_params(d_out, 5, "long_rows:out")
+    HX = f32(O.covariance(ax))
+    HG = f32(O.covariance(ag))
+    hx_diag = to_np(torch.diagonal(HX)).astype(np.float64)
+    hg_diag = to_np(torch.diagonal(HG)).astype(np.float64)
+    w = O.as_f64(oracle_view(W))
+    sx, sg = O.rescale_factors(w, hx_diag, hg_diag)
+    Wd = torch.empty(d_out, d_in, device=DEV)
+    sxd = torch.empty(d_in, device=DEV)
+    sgd = torch.empty(d_out, device=DEV)
+    rin, rout = rot_device(ri), rot_device(ro)
+    note(f"rotate long rows {d_out}x{d_in}")
+    K.kronq_rotate(W.to(DEV), Wd, HX, HG, rin.sign, rout.sign, rin.q28, rout.q28, sxd, sgd,
+                   K.BIIP)
+    torch.cuda.synchronize()
+    assert rel_frob(to_np(sgd), sg) < TOL
+    rng = np.random.default_rng(12)
+    sgn, q = rot_oracle(ro)
+    rows = np.sort(rng.choice(d_out, 16, replace=False))
+    Uo = O.rht_rows(d_out, sgn, q, rows)
+    R = (Uo / sg[None, :]) @ ag.T
+    ref = R @ R.T
+    got = to_np(HG[rows][:, rows]).astype(np.float64)
+    scale = np.sqrt(np.outer(np.diag(ref), np.diag(ref)))
+    assert np.max(np.abs(got - ref) / scale) < TOL
+    sgi, qi = rot_oracle(ri)
+    cols = np.sort(rng.choice(d_in, 8, replace=False))
+    Vo = O.rht_rows(d_in, sgi, qi, cols)
+    ref_w = Uo @ (sg[:, None] * w * sx[None, :]) @ Vo.T
+    got_w = to_np(Wd[rows][:, cols]).astype(np.float64)
+    assert rel_frob(got_w, ref_w) < TOL
+
+
 def test_rotate_inverse_and_in_place():
     d_out, d_in = 448, 256
     s, W, hx, hg, ri, ro = _rot_problem(d_out, d_in, 9)
