@@ -151,7 +151,7 @@ __global__ __launch_bounds__(256) void gemm_bf16x3_sub(
 // barrier per stage) and every operand loaded as 16-byte chunks of bf16: the next stage is
 // fetched into registers during the current stage's MFMAs and written to the other buffer.
 template <int TM>
-__global__ __launch_bounds__(256) void gemm3_presplit_sub(
+__global__ __launch_bounds__(256, 2) void gemm3_presplit_sub(
     int64_t M, int64_t N, int64_t K, const uint16_t* __restrict__ Ah,
     const uint16_t* __restrict__ Al, int64_t lda, const uint16_t* __restrict__ Bh,
     const uint16_t* __restrict__ Bl, int64_t ldb, float* __restrict__ C, int64_t ldc) {
@@ -178,6 +178,19 @@ __global__ __launch_bounds__(256) void gemm3_presplit_sub(
   for (int a = 0; a < NB; ++a)
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[a][b] = f32x16_t{};
+  // this lane's elements of the C tile (in the accumulator layout), requested first so that
+  // their latency hides behind the whole K loop instead of ending the tile
+  float cin[NB][NB][16];
+#pragma unroll
+  for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < NB; ++bj)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t gm = m0 + wm * (TM / 2) + bi * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
+        const int64_t gn = n0 + wn * (TM / 2) + bj * 32 + l32;
+        cin[bi][bj][r] = (gm < M && gn < N) ? C[gm * ldc + gn] : 0.f;
+      }
   const int nst = int(K / BK);  // even: K is a multiple of 64
 #define KQ_FETCH(k0)                                                         \
   _Pragma("unroll") for (int v = 0; v < V; ++v) {                            \
@@ -239,7 +252,7 @@ __global__ __launch_bounds__(256) void gemm3_presplit_sub(
       for (int r = 0; r < 16; ++r) {
         const int64_t gm = m0 + wm * (TM / 2) + bi * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
         const int64_t gn = n0 + wn * (TM / 2) + bj * 32 + l32;
-        if (gm < M && gn < N) C[gm * ldc + gn] -= acc[bi][bj][r];
+        if (gm < M && gn < N) C[gm * ldc + gn] = cin[bi][bj][r] - acc[bi][bj][r];
       }
 }
 
