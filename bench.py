@@ -624,7 +624,6 @@ def layer_bench(args, spec, dev, steps: int, warmup: int, cpu_tokens: int,
     L.check(st)
     print(f"[bench] {spec.name}: warmup done ({warmup} steps)", file=sys.stderr, flush=True)
 
-    peaks = None if brief else measured_peaks(X, dev)
     SHARED = "syrk_bf16_mfma_shared"  # the H_G covariance on part of the chip (two streams)
     K.kronq_profile_only(f"{dominant},{SHARED}")
     K.kronq_profile_reset()
@@ -649,6 +648,9 @@ def layer_bench(args, spec, dev, steps: int, warmup: int, cpu_tokens: int,
         0.5 * sum(sorted(per_step)[steps // 2 - 1:steps // 2 + 1])
     print(f"[bench] {spec.name}: timed {steps} steps: {ms_step:.3f} ms/step "
           f"(median {med:.3f})", file=sys.stderr, flush=True)
+    # the chip's measured ceilings, after the timed steps: the register-resident MFMA loop runs
+    # the chip at its power limit, which left the first timed step after it slower
+    peaks = None if brief else measured_peaks(X, dev)
 
     # dominant kernel roofline: algorithmic flops N d (d + 1) per covariance launch (averaged
     # over the covariances run on the whole chip: both, or H_X alone when H_G ran beside the
