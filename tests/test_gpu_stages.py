@@ -305,8 +305,11 @@ def test_rotate_inverse_and_in_place():
 # ------------------------------------------------------------------------------ Cholesky
 # sizes cover one leaf, a ragged last leaf, odd leaf counts (uneven recursive splits) and
 # several levels of the recursion; in 8392 the two largest levels take the split-bf16 path with
-# ragged operand edges (4168 x 4224 products) (fewer tokens there: the oracle's covariance cost)
-@pytest.mark.parametrize("d", [77, 128, 256, 300, 384, 640, 1000, 1024, 2112, 4096, 4200, 8392])
+# ragged operand edges (4168 x 4224 products), in 8193 the top level's first three products do
+# (4097 rows) while its last (K = 4097) falls back to the fp32 kernels (fewer tokens at these
+# sizes: the oracle's covariance cost)
+@pytest.mark.parametrize("d", [77, 128, 256, 300, 384, 640, 1000, 1024, 2112, 4096, 4200, 8193,
+                               8392])
 def test_cholesky_inverse_factor(d):
     h = spd_from_tokens(d, 3 * d if d <= 4200 else d + 512, d)
     H = f32(h)
