@@ -79,7 +79,7 @@ def _ref(codes, scales, zeros, sx, sg, group, ri, ro, flags, x64):
     (448, 384, 2, 384, 2, K.ROT_OUT | K.RESCALE_OUT, torch.bfloat16),
     (200, 640, 4, 128, 1, 0, torch.float32),
     # one vector: the persistent GEMV, with the input transform inside (power-of-two or no
-    # input rotation, d_in <= 8192) or after a separate transform (28 * 2^k, larger d_in);
+    # input rotation, d_in <= 8192) or after a separate transform (larger d_in);
     # several tiles per workgroup, several tiles per row, a ragged last row block
     (9000, 512, 2, 128, 1, K.ROT_IN | K.RESCALE_IN | K.RESCALE_OUT, torch.bfloat16),
     (14336, 256, 4, 128, 1, K.BIIP, torch.float32),
@@ -87,6 +87,13 @@ def _ref(codes, scales, zeros, sx, sg, group, ri, ro, flags, x64):
     (64, 16384, 4, 128, 1, K.BIIP, torch.float32),
     (1024, 8192, 2, 256, 1, K.BIIP, torch.float32),
     (130, 1024, 4, 1024, 1, K.RESCALE_IN | K.RESCALE_OUT, torch.bfloat16),
+    # one vector with a 28 * m input rotation (the separate input transform, then the persistent
+    # GEMV on its digits): m = 64, 256 without an output rotation, 128 with a 28 * m output, and
+    # 1024 (the largest input one vector allows)
+    (300, 1792, 4, 256, 1, K.ROT_IN | K.RESCALE_IN | K.RESCALE_OUT, torch.float32),
+    (130, 7168, 2, 1792, 1, K.ROT_IN | K.RESCALE_IN, torch.bfloat16),
+    (896, 3584, 2, 128, 1, K.BIIP, torch.bfloat16),
+    (64, 28672, 4, 128, 1, K.BIIP, torch.float32),
 ])
 def test_online_matvec(d_out, d_in, bits, group, batch, flags, xdt):
     codes, scales, zeros, sx, sg = quantised_layer(d_out, d_in, bits, group, d_out + d_in)
