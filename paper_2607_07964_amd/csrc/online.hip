@@ -280,31 +280,20 @@ __global__ __launch_bounds__(1024) void seg_transform(
                       : ((__popc(unsigned(a & tid)) & 1) ? -1.f : 1.f);
   __syncthreads();
   if (tid < m) {
-    float v[32];  // all L loads in flight before the first use
-#pragma unroll
-    for (int k = 0; k < 32; ++k)
-      if (k < L) {
-        const int64_t idx = int64_t(k) * m + tid;
-        v[k] = ld_f32(x, idx);
-        if (pre) v[k] *= pre[idx];
-      }
+    // the L segments in an order that starts at this workgroup's own (every workgroup reads
+    // all of them; in one order their requests would queue on the same lines)
     float acc = 0.f;
-#pragma unroll
-    for (int k = 0; k < 32; ++k)
-      if (k < L) acc = fmaf(arow[k], v[k], acc);
+    for (int kk = 0; kk < L; ++kk) {
+      const int k = kk + a < L ? kk + a : kk + a - L;
+      const int64_t idx = int64_t(k) * m + tid;
+      float v = ld_f32(x, idx);
+      if (pre) v *= pre[idx];
+      acc = fmaf(arow[k], v, acc);
+    }
     t[tid] = acc;
   }
   __syncthreads();
-  for (int lh = 0; (1 << lh) < m; ++lh) {  // radix-2 FWHT of the segment, one butterfly/thread
-    const int h = 1 << lh;
-    if (tid < m / 2) {
-      const int i = ((tid >> lh) << (lh + 1)) + (tid & (h - 1));
-      const float u = t[i], w = t[i + h];
-      t[i] = u + w;
-      t[i + h] = u - w;
-    }
-    __syncthreads();
-  }
+  fwht_lds(t, m, m, tid, 1024);  // radix-8 groups of stages; ends with a barrier
   if (tid < m) {
     const int64_t idx = int64_t(a) * m + tid;
     float v = t[tid] * norm;
@@ -768,8 +757,13 @@ __global__ __launch_bounds__(256) void online_gemv_p(
       }
     }
   } else {
-    for (int i = tid; i < nch * 6; i += 256)
-      reinterpret_cast<uint4*>(sd)[i] = reinterpret_cast<const uint4*>(dig)[i];
+    // every workgroup copies the same digits: each starts at its own offset, so that their
+    // requests spread over the L2 channels instead of queueing on one line at a time
+    const int n16 = nch * 6, r16 = int((uint32_t(blockIdx.x) * 97u) % uint32_t(n16));
+    for (int i = tid; i < n16; i += 256) {
+      const int ii = i + r16 < n16 ? i + r16 : i + r16 - n16;
+      reinterpret_cast<uint4*>(sd)[ii] = reinterpret_cast<const uint4*>(dig)[ii];
+    }
     for (int i = tid; i < nch; i += 256) {
       se[i] = dexp[i];
       ss[i] = dsum[i];
