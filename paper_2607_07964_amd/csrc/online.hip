@@ -262,6 +262,34 @@ __device__ __forceinline__ void emit_digits(float v, int64_t col, int lane32, in
   }
 }
 
+// 8 consecutive activations as loaded (16-byte loads), widened to fp32 later
+template <typename T>
+struct RawX;
+template <>
+struct RawX<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = reinterpret_cast<const float4*>(p)[0];
+    b = reinterpret_cast<const float4*>(p)[1];
+  }
+  __device__ __forceinline__ void widen(float* v) const {
+    v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w, v[4] = b.x, v[5] = b.y, v[6] = b.z, v[7] = b.w;
+  }
+};
+template <>
+struct RawX<uint16_t> {
+  uint4 a;
+  __device__ __forceinline__ void load(const uint16_t* p) { a = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ void widen(float* v) const {
+    const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      v[2 * k] = __uint_as_float(w[k] << 16);
+      v[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
+    }
+  }
+};
+
 // Transform of B vectors of order d = L m: out[b] = diag(post) (A (x) H_m) diag(pre) src[b] * norm
 // (A = Q28 or Q28^T when has28, else the Sylvester H_L). Workgroup (a, b): segment a of vector b.
 // With dig != nullptr (and m a multiple of 32) it also writes the digits of the result.
@@ -273,23 +301,44 @@ __global__ __launch_bounds__(1024) void seg_transform(
     float* __restrict__ dsum, int64_t ldc, int bits) {
   __shared__ float t[1024];
   __shared__ float arow[32];
+  extern __shared__ __attribute__((aligned(16))) float xs[];  // L m floats: diag(pre) src[b]
   const int a = blockIdx.x, tid = threadIdx.x;
   const T* x = src + int64_t(blockIdx.y) * lds_;
   if (tid < L)
     arow[tid] = has28 ? (q_trans ? q28[tid * 28 + a] : q28[a * 28 + tid])
                       : ((__popc(unsigned(a & tid)) & 1) ? -1.f : 1.f);
+  // the whole vector, scaled, into LDS with 16-byte loads (8 elements a thread and step), each
+  // workgroup starting at its own offset: every workgroup reads all L segments, and in one
+  // order, or with each thread's L loads in flight at once, their requests queued on the same
+  // lines (a segment read straight from memory by each thread took about 10 us at 28 x 512)
+  const int d = L * m;
+  const bool vec = d % 8 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(pre) & 15) == 0;
+  if (vec) {
+    const int n8 = d / 8, rot = int((uint32_t(a) * 97u + uint32_t(blockIdx.y) * 31u) % uint32_t(n8));
+    for (int i = tid; i < n8; i += 1024) {
+      const int j = 8 * (i + rot < n8 ? i + rot : i + rot - n8);
+      RawX<T> r;
+      r.load(x + j);
+      float v[8];
+      r.widen(v);
+      if (pre) {
+        const float4 p0 = reinterpret_cast<const float4*>(pre + j)[0];
+        const float4 p1 = reinterpret_cast<const float4*>(pre + j)[1];
+        v[0] *= p0.x, v[1] *= p0.y, v[2] *= p0.z, v[3] *= p0.w;
+        v[4] *= p1.x, v[5] *= p1.y, v[6] *= p1.z, v[7] *= p1.w;
+      }
+      float4* o = reinterpret_cast<float4*>(xs + j);
+      o[0] = make_float4(v[0], v[1], v[2], v[3]);
+      o[1] = make_float4(v[4], v[5], v[6], v[7]);
+    }
+  } else {
+    for (int i = tid; i < d; i += 1024) xs[i] = pre ? ld_f32(x, i) * pre[i] : ld_f32(x, i);
+  }
   __syncthreads();
   if (tid < m) {
-    // the L segments in an order that starts at this workgroup's own (every workgroup reads
-    // all of them; in one order their requests would queue on the same lines)
     float acc = 0.f;
-    for (int kk = 0; kk < L; ++kk) {
-      const int k = kk + a < L ? kk + a : kk + a - L;
-      const int64_t idx = int64_t(k) * m + tid;
-      float v = ld_f32(x, idx);
-      if (pre) v *= pre[idx];
-      acc = fmaf(arow[k], v, acc);
-    }
+    for (int k = 0; k < L; ++k) acc = fmaf(arow[k], xs[k * m + tid], acc);
     t[tid] = acc;
   }
   __syncthreads();
@@ -483,34 +532,6 @@ __device__ __forceinline__ void emit_digits8(const float (&v)[8], int j0, uint8_
 // the transform (the Sylvester FWHT of a power-of-two d_in, or the scaling alone) runs while the
 // codes are in flight; it is repeated by every workgroup, which costs less than a separate launch
 // at these sizes.
-// 8 consecutive activations as loaded (16-byte loads), widened to fp32 later
-template <typename T>
-struct RawX;
-template <>
-struct RawX<float> {
-  float4 a, b;
-  __device__ __forceinline__ void load(const float* p) {
-    a = reinterpret_cast<const float4*>(p)[0];
-    b = reinterpret_cast<const float4*>(p)[1];
-  }
-  __device__ __forceinline__ void widen(float* v) const {
-    v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w, v[4] = b.x, v[5] = b.y, v[6] = b.z, v[7] = b.w;
-  }
-};
-template <>
-struct RawX<uint16_t> {
-  uint4 a;
-  __device__ __forceinline__ void load(const uint16_t* p) { a = *reinterpret_cast<const uint4*>(p); }
-  __device__ __forceinline__ void widen(float* v) const {
-    const uint32_t w[4] = {a.x, a.y, a.z, a.w};
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      v[2 * k] = __uint_as_float(w[k] << 16);
-      v[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
-    }
-  }
-};
-
 template <int BITS, int RPW>
 struct TileRegs {
   uint32_t w[2][RPW][4];
@@ -848,13 +869,14 @@ int seg_transform_launch(const void* src, int dtype, int64_t lds_, float* dst, i
                           s));
   } else {
     const dim3 grid(static_cast<unsigned>(L), static_cast<unsigned>(batch));
+    const size_t xs_bytes = size_t(L) * size_t(m) * sizeof(float);  // the staged vector
     uint8_t* dg = fused ? dig : nullptr;
     if (dtype == KRONQ_BF16)
-      KQ_TRY(launch("online_transform", seg_transform<uint16_t>, grid, dim3(1024), 0, s,
+      KQ_TRY(launch("online_transform", seg_transform<uint16_t>, grid, dim3(1024), xs_bytes, s,
                     static_cast<const uint16_t*>(src), lds_, dst, ldd, L, m, pre, post, q28,
                     int(q_trans), has28, norm, dg, dexp, dsum, nch, bits));
     else
-      KQ_TRY(launch("online_transform", seg_transform<float>, grid, dim3(1024), 0, s,
+      KQ_TRY(launch("online_transform", seg_transform<float>, grid, dim3(1024), xs_bytes, s,
                     static_cast<const float*>(src), lds_, dst, ldd, L, m, pre, post, q28,
                     int(q_trans), has28, norm, dg, dexp, dsum, nch, bits));
   }
