@@ -217,8 +217,8 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
     current stream rotates H_X, transforms W, factors H_X and runs the sweep; the second stream
     takes (the drift statistic and) the H_G covariance on ``cov_cus`` CUs (None: the policy of
     _cov_cus; 0: no cap) as soon as H_X is formed, whose traces and rotation end the layer. The
-    current stream waits for the second at the end. Both schedules give bit-identical
-    results."""
+    current stream waits for the second at the end. The two schedules differ only in how the
+    capped H_G covariance splits the tokens into slices (its sums in another order)."""
     drift = dX is not None
     if drift and st.D is None:
         raise ValueError("the drift correction needs LayerState.allocate(..., drift=True)")
