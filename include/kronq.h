@@ -132,8 +132,11 @@ int kronq_accumulate_cov(const void* A, int dtype, int64_t n_rows, int64_t d, in
  * units at once (persistent workgroups, one per CU, rounded down to a multiple of 8; 0: the
  * whole chip). For a caller that runs latency-bound work on another stream meanwhile (the
  * factorisation beside the H_G covariance): a covariance workgroup holds its CU for the whole
- * of its tile, so without a cap the other stream's kernels wait for CUs. Results are identical
- * to kronq_accumulate_cov. max_cus < 0: KRONQ_ERR_INVALID_ARG. */
+ * of its tile, so without a cap the other stream's kernels wait for CUs. The token slices
+ * (split-K) are chosen to fill whole rounds of the capped workgroups, never more slices than
+ * kronq_accumulate_cov takes (so the same workspace serves), so the result equals
+ * kronq_accumulate_cov's up to the order of the fp32 sums, and bit for bit when both choose the
+ * same slices. max_cus < 0: KRONQ_ERR_INVALID_ARG. */
 int kronq_accumulate_cov_limited(const void* A, int dtype, int64_t n_rows, int64_t d,
                                  int64_t lda, float* H, int64_t ldh, float alpha, float beta,
                                  int max_cus, void* ws, size_t ws_bytes, void* stream);
