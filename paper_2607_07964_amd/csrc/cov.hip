@@ -15,9 +15,9 @@
 //     and a ragged token tail (< 32 tokens) go through syrk_bf16_partial, which stages 64
 //     tokens through registers: 8 x 8 bf16 blocks are loaded, transposed with v_perm and
 //     written token-contiguous to LDS so that an MFMA operand is one 16-byte read.
-//   * Partial tiles go to the workspace; a reduction kernel sums the slices, applies
-//     alpha/beta and writes both triangles (the mirror through an LDS transpose), so H is
-//     exactly symmetric; for cross every tile is written as it is.
+//   * Partial tiles go to the workspace in MFMA-fragment order; a reduction kernel sums the
+//     slices, applies alpha/beta and writes both triangles (the mirror through an LDS
+//     transpose), so H is exactly symmetric; for cross every tile is written as it is.
 // fp32 path (small fp32 inputs): a plain LDS-tiled fp32 FMA kernel over the full matrix.
 #include <algorithm>
 #include <cmath>
@@ -87,6 +87,24 @@ __device__ __forceinline__ void store_block_t(uint32_t* __restrict__ lds, const 
     o.w = __builtin_amdgcn_perm(v[7][k], v[6][k], sel);
     *reinterpret_cast<u32x4_t*>(lds + (rowbase + c) * LROW + dw_off) = o;
   }
+}
+
+// Partial tiles are stored in MFMA-fragment order: for wave w (quadrant rows 128 (w % 2), columns
+// 128 (w / 2)), accumulator block (bi, bj) and quarter q, lane l's four values (rows
+// 8 q + 4 (l / 32) + 0..3 of column l % 32 of the block) are 16 consecutive bytes, and a wave's 64
+// lanes one contiguous kilobyte: 64 16-byte stores a lane instead of 256 4-byte ones (the
+// stores of a tile measured 5% of the covariance when row-major).
+__device__ __forceinline__ void store_partial(float* __restrict__ out, const f32x16_t (&acc)[4][4],
+                                              int wave, int lane) {
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 4; ++bj)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        reinterpret_cast<float4*>(out)[((wave * 4 + bi) * 4 + bj) * 256 + q * 64 + lane] =
+            make_float4(acc[bi][bj][4 * q], acc[bi][bj][4 * q + 1], acc[bi][bj][4 * q + 2],
+                        acc[bi][bj][4 * q + 3]);
 }
 
 template <bool CROSS>
@@ -202,19 +220,9 @@ __device__ __forceinline__ void gram_partial(
     __syncthreads();
   }
 
-  // partial tile, row-major 256 x 256 (rows: channels i of the tile, cols: channels j)
+  // the partial tile, in fragment order (store_partial)
   const int64_t npos = CROSS ? int64_t(T) * T : int64_t(T) * (T + 1) / 2;
-  float* out = part + (int64_t(out_slice0 + slice) * npos + pos) * (TT * TT);
-#pragma unroll
-  for (int bi = 0; bi < 4; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 4; ++bj)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = wm * 128 + bi * 32 + (r >> 2) * 8 + lhi * 4 + (r & 3);
-        const int col = wn * 128 + bj * 32 + l32;
-        out[row * TT + col] = acc[bi][bj][r];
-      }
+  store_partial(part + (int64_t(out_slice0 + slice) * npos + pos) * (TT * TT), acc, wave, lane);
 }
 
 
@@ -484,24 +492,16 @@ __device__ __forceinline__ void gram_dma(const uint16_t* __restrict__ A,
     }
   }
   const int64_t npos = CROSS ? int64_t(T) * T : int64_t(T) * (T + 1) / 2;
-  float* out = part + (int64_t(slice) * npos + pos) * (TT * TT);
-  const int l32 = lane & 31, lhi = lane >> 5;
-#pragma unroll
-  for (int bi = 0; bi < 4; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 4; ++bj)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = wm * 128 + bi * 32 + (r >> 2) * 8 + lhi * 4 + (r & 3);
-        const int col = wn * 128 + bj * 32 + l32;
-        out[row * TT + col] = acc[bi][bj][r];
-      }
+  store_partial(part + (int64_t(slice) * npos + pos) * (TT * TT), acc, wave, lane);
   __syncthreads();  // the ring's last reads are done before the next item's loads overwrite it
   }
 }
 
 // Sum the S partial tiles of one 64 x 64 sub-block and write H (and its mirror; cross: the
-// sub-block as it is).
+// sub-block as it is). The sub-block is 2 x 2 accumulator blocks of one wave's quadrant: thread
+// (block b, lane) reads that lane's four 16-byte quarters of each partial tile (a wave's loads of
+// one quarter are one contiguous kilobyte), adds the slices in order, and the sums pass through
+// LDS so that both H and its mirror are written in whole rows.
 template <bool CROSS>
 __device__ __forceinline__ void gram_reduce(const float* __restrict__ part, int n_slices, int T,
                                             int64_t d, float* __restrict__ H, int64_t ldh,
@@ -522,77 +522,75 @@ __device__ __forceinline__ void gram_reduce(const float* __restrict__ part, int 
     J = I + rem;
   }
   const int sr = (sub >> 2) * 64, sc = (sub & 3) * 64;  // sub-block origin inside the tile
+  // below the diagonal of a diagonal tile nothing is written here (the mirror comes from the
+  // sub-block across the diagonal)
+  if (!CROSS && I == J && sr > sc) return;
   const int64_t gi0 = int64_t(I) * TT + sr, gj0 = int64_t(J) * TT + sc;
   const int64_t npos = CROSS ? int64_t(T) * T : int64_t(T) * (T + 1) / 2;
-  const int tid = threadIdx.x;
-  const int c4 = (tid & 15) * 4;
-  const int rb = tid >> 4;
-  // slices added in order; four slices of the four rows (16 loads) in flight at a time
-  float v[4][4];
+  const int tid = threadIdx.x, lane = tid & 63, b = tid >> 6;
+  const int w = (sr >> 7) + 2 * (sc >> 7);  // the wave whose quadrant holds the sub-block
+  const int bi = ((sr & 127) >> 5) + (b >> 1), bj = ((sc & 127) >> 5) + (b & 1);
+  const float4* base = reinterpret_cast<const float4*>(part + int64_t(pos) * (TT * TT)) +
+                       ((w * 4 + bi) * 4 + bj) * 256 + lane;
+  const int64_t slice4 = npos * (TT * TT / 4);
+  // slices added in order; four slices of the four quarters (16 loads) in flight at a time
+  float4 v[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) v[k][0] = v[k][1] = v[k][2] = v[k][3] = 0.f;
-  const float* base = part + int64_t(pos) * (TT * TT) + (sr + rb) * TT + sc + c4;
-  const int64_t slice = npos * (TT * TT);
+  for (int q = 0; q < 4; ++q) v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
   int s = 0;
   for (; s + 4 <= n_slices; s += 4) {
     float4 x[4][4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        x[k][q] = *reinterpret_cast<const float4*>(base + (s + q) * slice + 16 * k * TT);
+      for (int u = 0; u < 4; ++u) x[q][u] = base[(s + u) * slice4 + q * 64];
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        v[k][0] += x[k][q].x;
-        v[k][1] += x[k][q].y;
-        v[k][2] += x[k][q].z;
-        v[k][3] += x[k][q].w;
+      for (int u = 0; u < 4; ++u) {
+        v[q].x += x[q][u].x;
+        v[q].y += x[q][u].y;
+        v[q].z += x[q][u].z;
+        v[q].w += x[q][u].w;
       }
   }
   for (; s < n_slices; ++s) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const float4 x = *reinterpret_cast<const float4*>(base + s * slice + 16 * k * TT);
-      v[k][0] += x.x;
-      v[k][1] += x.y;
-      v[k][2] += x.z;
-      v[k][3] += x.w;
+    for (int q = 0; q < 4; ++q) {
+      const float4 x = base[s * slice4 + q * 64];
+      v[q].x += x.x;
+      v[q].y += x.y;
+      v[q].z += x.z;
+      v[q].w += x.w;
     }
   }
-  if (CROSS) {
+  // quarter q, element e of this lane: row 8 q + 4 (lane / 32) + e, column lane % 32 of its block
+  {
+    const int rl = (b >> 1) * 32 + 4 * (lane >> 5), cl = (b & 1) * 32 + (lane & 31);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int64_t gi = gi0 + rb + 16 * k;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t gj = gj0 + c4 + e;
-        if (gi < d && gj < d) {
-          float* h = H + gi * ldh + gj;
-          *h = beta == 0.f ? alpha * v[k][e] : alpha * v[k][e] + beta * *h;
-        }
-      }
-    }
-    return;
-  }
-  // upper triangle (i <= j) from the sums; the strict lower triangle is its mirror, so H is
-  // exactly symmetric (diagonal tiles included)
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int64_t gi = gi0 + rb + 16 * k;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int64_t gj = gj0 + c4 + e;
-      if (gi < d && gj < d && gi <= gj) {
-        float* h = H + gi * ldh + gj;
-        *h = beta == 0.f ? alpha * v[k][e] : alpha * v[k][e] + beta * *h;
-      }
-      tr[c4 + e][rb + 16 * k] = v[k][e];
+    for (int q = 0; q < 4; ++q) {
+      tr[rl + 8 * q][cl] = v[q].x;
+      tr[rl + 8 * q + 1][cl] = v[q].y;
+      tr[rl + 8 * q + 2][cl] = v[q].z;
+      tr[rl + 8 * q + 3][cl] = v[q].w;
     }
   }
   __syncthreads();
-  // mirror: H[j][i] = value of (i, j) for i < j, coalesced along i
+  // the sub-block in rows (cross: all of it; syrk: the upper triangle, i <= j)
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int idx = tid + 256 * k;
+    const int ii = idx >> 6, jj = idx & 63;
+    const int64_t gi = gi0 + ii, gj = gj0 + jj;
+    if (gi < d && gj < d && (CROSS || gi <= gj)) {
+      float* h = H + gi * ldh + gj;
+      const float x = tr[ii][jj];
+      *h = beta == 0.f ? alpha * x : alpha * x + beta * *h;
+    }
+  }
+  if (CROSS) return;
+  // mirror: H[j][i] = value of (i, j) for i < j, coalesced along i; the strict lower triangle
+  // is the upper one's mirror, so H is exactly symmetric (diagonal tiles included)
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
     const int idx = tid + 256 * k;
@@ -600,7 +598,7 @@ __device__ __forceinline__ void gram_reduce(const float* __restrict__ part, int 
     const int64_t gj = gj0 + jj, gi = gi0 + ii;
     if (gi < d && gj < d && gi < gj) {
       float* h = H + gj * ldh + gi;
-      const float x = tr[jj][ii];
+      const float x = tr[ii][jj];
       *h = beta == 0.f ? alpha * x : alpha * x + beta * *h;
     }
   }
