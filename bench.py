@@ -669,6 +669,12 @@ def layer_bench(args, spec, dev, steps: int, warmup: int, cpu_tokens: int,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic(dominant, wl_key), "kernel": dominant, "launches": dom_n,
             "avg_launch_ms": round(avg_ms, 4)}
+    if args.drift:
+        # the drift statistic holds part of the chip (layer.DRIFT_SHARE) beside the solver
+        ncu = torch.cuda.get_device_properties(dev).multi_processor_count
+        held = max(8, int(ncu * L.DRIFT_SHARE)) // 8 * 8
+        roof["held_cus"] = held
+        roof["frac_of_its_cus"] = round(achieved / (PEAK_BF16_TFLOPS * held / ncu), 4)
     shared = None
     if sh_n:
         cus = cov_cus if cov_cus is not None else L._cov_cus(dev, spec.n_tokens, spec.d_out,

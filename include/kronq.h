@@ -184,6 +184,17 @@ int kronq_accumulate_cross(const void* A, const void* B, int dtype, int64_t n_ro
                            int64_t ld, float* C, int64_t ldc, float alpha, float beta, void* ws,
                            size_t ws_bytes, void* stream);
 
+/* As kronq_accumulate_cross, with the bf16 interior-tile kernel holding at most max_cus compute
+ * units at once (as kronq_accumulate_cov_limited: persistent workgroups, a multiple of 8; 0: the
+ * whole chip), for a caller that runs the factorisation on another stream meanwhile. Token
+ * slices as kronq_accumulate_cov_limited chooses them, so the result equals
+ * kronq_accumulate_cross's up to the order of the fp32 sums (bit for bit when both take the
+ * same slices). max_cus < 0: KRONQ_ERR_INVALID_ARG. */
+int kronq_accumulate_cross_limited(const void* A, const void* B, int dtype, int64_t n_rows,
+                                   int64_t d, int64_t ld, float* C, int64_t ldc, float alpha,
+                                   float beta, int max_cus, void* ws, size_t ws_bytes,
+                                   void* stream);
+
 /* ---- 2. traces and sensitivity (Sec. 4.3 eq. sensitivity) --------------------------------
  * out3[0] = tr H_X, out3[1] = tr H_G, out3[2] = tr H_X * tr H_G, accumulated in fp64.
  * Call before and/or after kronq_rotate (the score of the paper uses post-BiIP traces).

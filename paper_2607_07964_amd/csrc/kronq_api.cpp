@@ -201,7 +201,16 @@ int kronq_probe_mfma_bf16(const void* data, int iters, float* out, int64_t out_l
 int kronq_accumulate_cross(const void* A, const void* B, int dtype, int64_t n_rows, int64_t d,
                            int64_t ld, float* C, int64_t ldc, float alpha, float beta, void* ws,
                            size_t ws_bytes, void* stream) {
+  return kronq_accumulate_cross_limited(A, B, dtype, n_rows, d, ld, C, ldc, alpha, beta, 0, ws,
+                                        ws_bytes, stream);
+}
+
+int kronq_accumulate_cross_limited(const void* A, const void* B, int dtype, int64_t n_rows,
+                                   int64_t d, int64_t ld, float* C, int64_t ldc, float alpha,
+                                   float beta, int max_cus, void* ws, size_t ws_bytes,
+                                   void* stream) {
   kq::clear_error();
+  KQ_REQUIRE(max_cus >= 0, KRONQ_ERR_INVALID_ARG, "max_cus must be >= 0");
   KQ_REQUIRE(valid_dtype(dtype), KRONQ_ERR_INVALID_ARG, "dtype must be KRONQ_BF16 or KRONQ_FP32");
   KQ_REQUIRE(C, KRONQ_ERR_INVALID_ARG, "C is NULL");
   KQ_REQUIRE(n_rows >= 0 && d >= 1 && d <= 65535, KRONQ_ERR_INVALID_ARG,
@@ -218,7 +227,8 @@ int kronq_accumulate_cross(const void* A, const void* B, int dtype, int64_t n_ro
                  "fp32 A and B must be 4-byte aligned");
     KQ_TRY(check_ws(ws, ws_bytes, kq::cov_ws_bytes(dtype, n_rows, d, true)));
   }
-  return kq::cov_launch(A, B, dtype, n_rows, d, ld, C, ldc, alpha, beta, ws, as_stream(stream));
+  return kq::cov_launch(A, B, dtype, n_rows, d, ld, C, ldc, alpha, beta, ws, as_stream(stream),
+                        max_cus);
 }
 
 int kronq_traces(const float* HX, int64_t d_in, int64_t ldx, const float* HG, int64_t d_out,

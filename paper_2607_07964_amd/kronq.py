@@ -36,7 +36,7 @@ EXPORTS = (
     "kronq_rotate_drift",    "kronq_gptaq_correction", "kronq_obs_quantize_layer_drift", "kronq_pack_codes",
     "kronq_online_factors", "kronq_online_matvec", "kronq_matrix_stats", "kronq_eigh",
     "kronq_proxy_loss_factors", "kronq_accumulate_cov_limited", "kronq_cov_diag",
-    "kronq_cov_diag_noalloc", "kronq_probe_mfma_bf16",
+    "kronq_cov_diag_noalloc", "kronq_probe_mfma_bf16", "kronq_accumulate_cross_limited",
 )
 
 
@@ -69,6 +69,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "kronq_cov_diag_noalloc": (I, [P, I, I64, I64, I64, P, I, P]),
         "kronq_probe_mfma_bf16": (I, [P, I, P, I64, P, P]),
         "kronq_accumulate_cross": (I, [P, P, I, I64, I64, I64, P, I64, F, F, P, SZ, P]),
+        "kronq_accumulate_cross_limited": (I, [P, P, I, I64, I64, I64, P, I64, F, F, I, P, SZ,
+                                               P]),
         "kronq_rotate_drift": (I, [P, I64, I64, P, P, P, I, P, SZ, P]),
         "kronq_gptaq_correction": (I, [P, I64, I64, P, I64, F, P, I64, P, SZ, P]),
         "kronq_obs_quantize_layer_drift": (I, [P, I64, I64, I64, P, I64, P, I64, I, I, I, P, P, P,
@@ -293,6 +295,23 @@ def kronq_accumulate_cross(A: torch.Tensor, B: torch.Tensor, C: torch.Tensor, al
                                        _ld(C), alpha, beta, _ptr(ws), ws.numel(),
                                        _stream(C.device))
     _check(rc, "kronq_accumulate_cross")
+    return C
+
+
+def kronq_accumulate_cross_limited(A: torch.Tensor, B: torch.Tensor, C: torch.Tensor,
+                                   max_cus: int, alpha: float = 1.0, beta: float = 0.0,
+                                   ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """kronq_accumulate_cross holding at most ``max_cus`` compute units at once (0: all)."""
+    _dev(A, B, C)
+    n, d = A.shape
+    if B.shape != A.shape or B.dtype != A.dtype or _ld(B) != _ld(A):
+        raise ValueError("A and B must have the same shape, dtype and row stride")
+    if ws is None:
+        ws = workspace(OP_CROSS, 0, d, n, C.device)
+    rc = load().kronq_accumulate_cross_limited(_ptr(A), _ptr(B), _dtype_code(A), n, d, _ld(A),
+                                               _ptr(C), _ld(C), alpha, beta, int(max_cus),
+                                               _ptr(ws), ws.numel(), _stream(C.device))
+    _check(rc, "kronq_accumulate_cross_limited")
     return C
 
 

@@ -124,9 +124,12 @@ def biip(st: LayerState, W0: torch.Tensor, rin: RotParams, rout: RotParams, flag
     K.kronq_traces(st.HX, st.HG, st.tr_post)
 
 
-def drift_statistic(st: LayerState, dX: torch.Tensor, X: torch.Tensor):
-    """Alg. 1 first line, second half: D = dX^T X."""
-    K.kronq_accumulate_cross(dX, X, st.D, 1.0, 0.0, st.ws_cross)
+def drift_statistic(st: LayerState, dX: torch.Tensor, X: torch.Tensor, max_cus: int = 0):
+    """Alg. 1 first line, second half: D = dX^T X (``max_cus`` > 0: on at most that many CUs)."""
+    if max_cus > 0:
+        K.kronq_accumulate_cross_limited(dX, X, st.D, max_cus, 1.0, 0.0, st.ws_cross)
+    else:
+        K.kronq_accumulate_cross(dX, X, st.D, 1.0, 0.0, st.ws_cross)
 
 
 def drift_biip(st: LayerState, rin: RotParams, flags: int = K.BIIP):
@@ -164,6 +167,11 @@ def solve(st: LayerState, bits: int, damp: float = 0.01, alpha: Optional[float] 
 # 20 TFLOP/s for the factorisation.
 FACTOR_SHARE = 0.5
 FACTOR_SHARE_SHORT = 0.125
+# The drift statistic, first on the second stream (before H_G), holds 13/16 of the chip and
+# leaves the rest to the H_X transform and the factorisation's first leaves and products: at
+# q_proj with the drift correction, 18.49-18.56 ms per layer on 208 CUs against 18.85-18.93
+# on 192 and 224, 19.28-19.33 on 176, 20.73-20.75 on 128 and 19.61-19.70 uncapped.
+DRIFT_SHARE = 13.0 / 16.0
 # Measured alternatives (q_proj, alternating with this schedule in one run): H_G started
 # right after H_X with W transformed on the current stream, 11.58 against 11.40 ms; W on a third
 # stream with H_G starting once S_X exists, 11.12 against 11.06 ms; W on the current stream
@@ -250,7 +258,8 @@ def quantize_layer(st: LayerState, X, G, W0, rin: RotParams, rout: RotParams, bi
     with torch.cuda.stream(st.side):
         st.side.wait_event(ev_sx)
         if drift:  # the drift statistic first: the correction P waits for it
-            drift_statistic(st, dX, X)
+            cus_all = torch.cuda.get_device_properties(st.D.device).multi_processor_count
+            drift_statistic(st, dX, X, max(8, int(cus_all * DRIFT_SHARE)))
             ev_d.record(st.side)
         # the H_G covariance leaves part of the chip to the factorisation's and the sweep's
         # latency-bound kernels (a covariance workgroup holds its CU for a whole tile)

@@ -73,6 +73,25 @@ def test_cross_bf16(n, d):
     assert rel_frob(to_np(C), ref) < 1e-4
 
 
+@pytest.mark.parametrize("max_cus", [8, 5, 24])
+def test_cross_limited_matches_uncapped(max_cus):
+    """The drift statistic on at most max_cus CUs (persistent workgroups, several work items
+    each): at d = 1536, N = 8192 every one of these caps keeps the uncapped launch's 8 token
+    slices (36 tiles x 8 slices), so the bits must be the uncapped launch's; and it matches the
+    oracle."""
+    n, d = 8192, 1536
+    spec, X, dX = tokens(d, n, 31)
+    C0 = torch.empty(d, d, device=DEV)
+    C1 = torch.full((d, d), float("nan"), device=DEV)
+    note(f"cross limited max_cus={max_cus}")
+    K.kronq_accumulate_cross(dX.to(DEV), X.to(DEV), C0)
+    K.kronq_accumulate_cross_limited(dX.to(DEV), X.to(DEV), C1, max_cus)
+    torch.cuda.synchronize()
+    assert torch.equal(C0, C1)
+    ref = O.cross_covariance(oracle_view(dX), oracle_view(X))
+    assert rel_frob(to_np(C1), ref) < 1e-4
+
+
 def test_cross_chained_scaled_fp32_and_symmetric_case():
     n1, n2, d = 1500, 900, 520
     spec, X, dX = tokens(d + 8, n1 + n2, 7)
