@@ -92,6 +92,24 @@ def test_cross_limited_matches_uncapped(max_cus):
     assert rel_frob(to_np(C1), ref) < 1e-4
 
 
+@pytest.mark.parametrize("max_cus", [8, 40])
+def test_cross_limited_fewer_slices(max_cus):
+    """At d = 768, N = 20000 the uncapped drift statistic cuts the tokens into 24 slices and a
+    launch capped to 8 or 40 CUs into 8 (whole rounds of its own workgroups): the same sums in
+    another order, so it agrees with the uncapped launch to fp32 rounding and with the oracle."""
+    n, d = 20000, 768
+    spec, X, dX = tokens(d, n, 37)
+    C0 = torch.empty(d, d, device=DEV)
+    C1 = torch.full((d, d), float("nan"), device=DEV)
+    note(f"cross limited, fewer slices, max_cus={max_cus}")
+    K.kronq_accumulate_cross(dX.to(DEV), X.to(DEV), C0)
+    K.kronq_accumulate_cross_limited(dX.to(DEV), X.to(DEV), C1, max_cus)
+    torch.cuda.synchronize()
+    assert rel_frob(to_np(C1), to_np(C0)) < 1e-5
+    ref = O.cross_covariance(oracle_view(dX), oracle_view(X))
+    assert rel_frob(to_np(C1), ref) < 1e-4
+
+
 def test_cross_chained_scaled_fp32_and_symmetric_case():
     n1, n2, d = 1500, 900, 520
     spec, X, dX = tokens(d + 8, n1 + n2, 7)
